@@ -1,0 +1,198 @@
+"""Throughput of the two-axis layer stack (forward + backward) on one MI355X.
+
+One step = forward of every layer of the stack, then backward of every layer, over one batch of
+seeded synthetic tables already resident in HBM.  Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--config 2] [--no-cpu-baseline]
+"""
+
+import argparse
+import json
+import os
+import platform
+import subprocess
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2606_03681_amd import workloads as wl  # noqa: E402
+
+METRIC = "two-axis layer fwd+bwd cells/sec (bf16) + % MFMA peak, 1x MI355X"
+PEAK_TFLOPS = {"mfma_bf16": 2516.6, "mfma_f32": 157.3, "alu_f32": 157.3}
+HBM_PEAK_GBS = 8000.0
+
+
+def step_flops(w):
+    """Algorithmic matmul flops of one launch of each step (per layer), for the whole batch."""
+    R, E, H = w.cfg["R"], w.cfg["E"], w.cfg["H"]
+    lin = kv = fa = ia = 0
+    N = 0
+    for b in range(len(w.n_train)):
+        S = int(np.count_nonzero(w.cell_mask[b]))
+        n = int(w.n_train[b])
+        N += R * S
+        kv += n * S * 4 * E * E
+        fa += R * S * S * 4 * E
+        ia += S * R * n * 4 * E
+    f = {
+        "feat_qkv": 6 * N * E * E, "feat_attn_fwd": fa, "feat_out": 2 * N * E * E,
+        "item_qkv": 2 * N * E * E + kv, "item_attn_fwd": ia, "item_out": 2 * N * E * E,
+        "mlp_up": 2 * N * E * H, "mlp_down": 2 * N * E * H,
+        "feat_attn_bwd": 2 * fa, "item_attn_bwd": 2 * ia,
+        "mlp_down_dx": 2 * N * E * H, "mlp_up_dx": 2 * N * E * H,
+        "item_out_dx": 2 * N * E * E, "item_qkv_dx": 2 * N * E * E + kv,
+        "feat_out_dx": 2 * N * E * E, "feat_qkv_dx": 6 * N * E * E,
+    }
+    return f
+
+
+def git_rev():
+    try:
+        return subprocess.run(["git", "-C", ROOT, "rev-parse", "--short", "HEAD"],
+                              capture_output=True, text=True, timeout=5).stdout.strip() or None
+    except Exception:
+        return None
+
+
+def cpu_baseline(cfg_index, seed):
+    """The float64 oracle, untuned, on a bounded sample of the same workload: one dataset
+    through one layer, forward and backward, at the workload's full per-dataset shape."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        threads = os.cpu_count()
+    w = wl.make_workload(cfg_index, seed=seed, datasets=[0])
+    E, H, heads = w.cfg["E"], w.cfg["H"], w.cfg["heads"]
+    P = oracle.unpack_params(w.params64()[0], E, H)
+    X, dY = w.X64(), w.dY64()
+    t0 = time.perf_counter()
+    _, cache = oracle.layer_forward(X, P, w.n_train, w.cell_mask, heads)
+    oracle.layer_backward(dY, cache)
+    dt = time.perf_counter() - t0
+    cells = int(w.cfg["R"] * np.count_nonzero(w.cell_mask[0]))
+    return {"value": cells / dt, "unit": "cells/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"dataset 0 of the workload, 1 layer fwd+bwd, {cells} active cells, "
+                      f"{dt:.1f} s, host {platform.processor() or platform.machine()} "
+                      f"({os.cpu_count()} logical CPUs)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true",
+                    help="skip the per-step event timing (roofline of the dominant kernel)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} (WORLD_SIZE={world}) is not "
+              "supported: the datasets of a batch are independent, and sharding them across "
+              "GPUs (one all-reduce of the parameter gradients per step) is not built.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_03681_amd import tfm
+    from paper_2606_03681_amd.stack import Stack, to_device
+
+    cfg = wl.get_config(args.config)
+    seed = wl.default_seed(cfg) if args.seed is None else args.seed
+    print(f"[bench] generating {cfg['name']} seed={seed}", file=sys.stderr, flush=True)
+    w = wl.make_workload(args.config, seed=seed)
+    counts = wl.work_counts(w.n_train, w.cell_mask, cfg["R"], cfg["E"], cfg["H"], cfg["layers"])
+    dims = tfm.make_dims(dtype=w.dtype, **{k: v for k, v in w.dims.items() if k != "dtype"})
+    torch.cuda.set_device(0)
+    st = Stack(dims, w.n_train, w.cell_mask, w.params)
+    X = to_device(w.X, w.dtype)
+    dY = to_device(w.dY, w.dtype)
+    del w.X, w.dY
+
+    def step():
+        st.forward(X)
+        st.backward(dY)
+
+    print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    if not args.no_profile:
+        tfm.prof_enable(True)
+    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ev_ms = ev0.elapsed_time(ev1)
+    prof = {}
+    if not args.no_profile:
+        prof = tfm.prof_collect()
+        tfm.prof_enable(False)
+    ms_per_step = ev_ms / args.steps
+    value = counts["cell_layers"] * args.steps / (ev_ms / 1e3)
+    tflops = counts["flops_fwd_bwd"] / (ms_per_step / 1e3) / 1e12
+    peak = PEAK_TFLOPS["mfma_bf16"] if w.dtype == "bf16" else PEAK_TFLOPS["mfma_f32"]
+
+    roof = None
+    steps_out = {}
+    if prof:
+        fl = step_flops(w)
+        for name, (n, ms) in sorted(prof.items(), key=lambda kv: -kv[1][1]):
+            steps_out[name] = {"launches": n, "avg_ms": round(ms / n, 5),
+                               "share": round(ms / (ev_ms or 1), 4)}
+        # step names are "<step>/<unit>", unit in {mfma, valu, hbm}
+        dom = max((k for k in prof if k.split("/")[0] in fl), key=lambda k: prof[k][1],
+                  default=None)
+        if dom is not None:
+            n, ms = prof[dom]
+            avg_s = ms / n / 1e3
+            f = fl[dom.split("/")[0]]
+            achieved = f / avg_s / 1e12
+            mfma = dom.endswith("/mfma")
+            pk = peak if mfma else PEAK_TFLOPS["alu_f32"]
+            roof = {"kernel": dom, "bound": "mfma" if mfma else "alu",
+                    "achieved": round(achieved, 3), "peak": pk, "unit": "TFLOP/s",
+                    "frac": round(achieved / pk, 5), "traffic": None,
+                    "flops_per_launch": f, "avg_launch_ms": round(ms / n, 5)}
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "cells/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": cfg["name"], "B": cfg["B"], "R": cfg["R"],
+                   "n_train": str(cfg["n_train"]), "C": cfg["C"], "E": cfg["E"],
+                   "heads": cfg["heads"], "H": cfg["H"], "layers": cfg["layers"],
+                   "seed": seed, "active_cell_layers": counts["cell_layers"]},
+        "tflops": round(tflops, 3), "mfma_peak_frac": round(tflops / peak, 5),
+        "wall_ms_per_step": round(wall * 1e3 / args.steps, 4),
+        "roofline": roof, "steps_profile": steps_out, "git": git_rev(),
+        "gpu": torch.cuda.get_device_name(0),
+    }
+    del st, X, dY
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(args.config, seed)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

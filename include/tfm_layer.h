@@ -1,0 +1,106 @@
+/*
+ * tfm_layer.h — C ABI of the MI355X (gfx950) two-axis tabular transformer layer.
+ *
+ * The layer (paper "Speedrunning Tabular Foundation Model Pretraining", Sec. 4.1 and the
+ * Fig. 3 caption; Tab. 5 for the baseline sizes) maps a cell tensor X[B, R, C+1, E] — B
+ * datasets (tables), R rows each, C feature cells plus one target cell per row, embedding
+ * width E — to Y of the same shape:
+ *
+ *     H1 = LN1(X  + FeatureAttention(X))    attention across the active cells of each row
+ *     H2 = LN2(H1 + ItemAttention(H1))      attention down each column; every row attends only
+ *                                           to the first n_train[b] (labelled) rows
+ *     Y  = LN3(H2 + W2 GELU(W1 H2 + b1) + b2)
+ *
+ * Post-norm LayerNorms (eps 1e-5, biased variance, affine), exact-erf GELU, attention scale
+ * 1/sqrt(E/heads), two independent attention parameter sets, bias on every linear.
+ *
+ * Memory conventions
+ *   - X, Y, dY, dX: device, row-major [B][R][C+1][E], element type per dims->dtype
+ *     (TFM_F32: float, TFM_BF16: bfloat16 bit patterns).
+ *   - params, grads: device, float32, one packed vector per layer of
+ *     tfm_layer_param_count() floats, in this order (weights row-major [out][in]):
+ *         Wqkv_f[3E][E] bqkv_f[3E] Wo_f[E][E] bo_f[E]       feature-axis attention
+ *         Wqkv_i[3E][E] bqkv_i[3E] Wo_i[E][E] bo_i[E]       item-axis attention
+ *         W1[H][E] b1[H] W2[E][H] b2[E]                     MLP
+ *         g1[E] be1[E] g2[E] be2[E] g3[E] be3[E]            LayerNorm scales and shifts
+ *     Rows [0,E) of Wqkv are Q, [E,2E) K, [2E,3E) V; head j owns rows [j*d, (j+1)*d) of each.
+ *   - n_train: host int32[B], each in [1, R]; rows [0, n_train[b]) of dataset b are its
+ *     train (labelled) rows and the only keys of the item-axis attention.
+ *   - cell_mask: host uint8[B][C+1]; non-zero = active cell column.  The target cell (index
+ *     C) must be active.  Inactive cells are inert: never keys or queries, Y and dX are
+ *     written as 0 there, dY there is ignored, and they add nothing to any gradient.
+ *   - saved: device buffer of tfm_layer_saved_bytes(), written by fwd, read by bwd.
+ *   - workspace: device scratch of tfm_layer_workspace_bytes(); contents are not preserved.
+ *   - stream: a hipStream_t (passed as void*); NULL means the null stream.
+ *
+ * All pointers must be 16-byte aligned.  The caller owns every buffer; the library allocates
+ * no device memory and keeps no state between calls.  Calls are asynchronous on `stream`
+ * and never synchronise the device.  Every entry point validates its arguments before it
+ * launches anything: on error nothing is launched, the return code is negative and
+ * tfm_last_error() describes it.
+ *
+ * Supported envelope: B >= 1, R >= 1, 0 <= C <= 255, heads >= 1, d = E/heads in {16, 32},
+ * 32 <= E <= 256 with E % 32 == 0, 32 <= H <= 1024 with H % 32 == 0.
+ */
+#ifndef TFM_LAYER_H
+#define TFM_LAYER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { TFM_F32 = 0, TFM_BF16 = 1 } tfm_dtype;
+
+/* Problem dimensions.  C counts feature cells; each row has S = C + 1 cells. */
+typedef struct {
+  int32_t B, R, C, E, heads, H;
+  int32_t dtype; /* tfm_dtype */
+} tfm_dims;
+
+/* Return codes. */
+enum {
+  TFM_OK = 0,
+  TFM_ERR_DIMS = -1,      /* dimension outside the supported envelope */
+  TFM_ERR_HEAD_DIM = -2,  /* E % heads != 0 or d = E/heads not supported */
+  TFM_ERR_NTRAIN = -3,    /* some n_train[b] outside [1, R] */
+  TFM_ERR_MASK = -4,      /* target cell of some dataset inactive */
+  TFM_ERR_POINTER = -5,   /* null or misaligned pointer */
+  TFM_ERR_HIP = -6,       /* a HIP launch failed */
+  TFM_ERR_BUFFER = -7     /* saved or workspace buffer smaller than required */
+};
+
+/* Number of float32 parameters of one layer: 8E^2 + 8E + 2EH + H + 7E. 0 on invalid dims. */
+size_t tfm_layer_param_count(const tfm_dims* dims);
+
+/* Bytes of the fwd->bwd state buffer; depends on dims only (sized for all cells active). */
+size_t tfm_layer_saved_bytes(const tfm_dims* dims);
+
+/* Bytes of scratch that fwd and bwd need; depends on dims only. */
+size_t tfm_layer_workspace_bytes(const tfm_dims* dims);
+
+/* Forward pass (Sec. 4.1 / Fig. 3 block).  Reads X and params, writes Y and saved. */
+int tfm_layer_fwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* cell_mask,
+                  const void* X, const float* params, void* Y,
+                  void* saved, size_t saved_bytes, void* workspace, size_t workspace_bytes,
+                  void* stream);
+
+/* Backward pass of the same layer.  X, params, n_train and cell_mask must equal those of the
+ * forward call that wrote `saved`.  Writes dX; writes grads (accumulate == 0) or adds to them
+ * (accumulate != 0).  Parameter gradients are sums over every active cell of every dataset,
+ * reduced in a fixed order (bitwise reproducible). */
+int tfm_layer_bwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* cell_mask,
+                  const void* X, const float* params, const void* saved, size_t saved_bytes,
+                  const void* dY, void* dX, float* grads, int accumulate,
+                  void* workspace, size_t workspace_bytes, void* stream);
+
+/* Message describing the last non-zero return of this thread ("" if none). */
+const char* tfm_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TFM_LAYER_H */

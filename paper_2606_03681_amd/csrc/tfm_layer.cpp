@@ -1,0 +1,484 @@
+// Host side of the C ABI declared in include/tfm_layer.h: argument validation, the
+// active-cell plan, buffer layouts and the launch sequences of the forward and backward pass.
+#include "tfm_layer.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "fast.h"
+#include "prof.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+constexpr size_t kAlign = 256;
+constexpr int64_t kChunk = 8192;  // rows per partial sum of the parameter-gradient reductions
+constexpr int64_t kMaxCells = int64_t(1) << 26;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Dims {
+  int B, R, C, S, E, heads, d, H, dtype;
+  size_t tsz;      // bytes per stored element
+  int64_t Nmax;    // B * R * S
+  int words;       // 32-bit mask words per dataset
+};
+
+int check_dims(const tfm_dims* p, Dims& d) {
+  if (!p) return fail(TFM_ERR_POINTER, "dims is null");
+  d.B = p->B; d.R = p->R; d.C = p->C; d.E = p->E; d.heads = p->heads; d.H = p->H;
+  d.dtype = p->dtype;
+  if (d.dtype != TFM_F32 && d.dtype != TFM_BF16)
+    return fail(TFM_ERR_DIMS, "dtype %d is neither TFM_F32 nor TFM_BF16", d.dtype);
+  if (d.B < 1 || d.R < 1) return fail(TFM_ERR_DIMS, "B=%d and R=%d must be >= 1", d.B, d.R);
+  if (d.C < 0 || d.C > 255) return fail(TFM_ERR_DIMS, "C=%d outside [0, 255]", d.C);
+  if (d.E < 32 || d.E > 256 || d.E % 32)
+    return fail(TFM_ERR_DIMS, "E=%d must be a multiple of 32 in [32, 256]", d.E);
+  if (d.H < 32 || d.H > 1024 || d.H % 32)
+    return fail(TFM_ERR_DIMS, "H=%d must be a multiple of 32 in [32, 1024]", d.H);
+  if (d.heads < 1 || d.E % d.heads)
+    return fail(TFM_ERR_HEAD_DIM, "E=%d is not a multiple of heads=%d", d.E, d.heads);
+  d.d = d.E / d.heads;
+  if (d.d != 16 && d.d != 32)
+    return fail(TFM_ERR_HEAD_DIM, "head dim E/heads=%d not supported (16 or 32)", d.d);
+  d.S = d.C + 1;
+  d.Nmax = (int64_t)d.B * d.R * d.S;
+  if (d.Nmax > kMaxCells)
+    return fail(TFM_ERR_DIMS, "B*R*(C+1)=%lld cells exceeds %lld", (long long)d.Nmax,
+                (long long)kMaxCells);
+  d.tsz = d.dtype == TFM_F32 ? 4 : 2;
+  d.words = (d.S + 31) / 32;
+  return TFM_OK;
+}
+
+// ---- parameter offsets (floats) -------------------------------------------------------------
+struct POff {
+  size_t Wqkv_f, bqkv_f, Wo_f, bo_f, Wqkv_i, bqkv_i, Wo_i, bo_i, W1, b1, W2, b2;
+  size_t g1, be1, g2, be2, g3, be3, total;
+};
+
+POff param_offsets(int E, int H) {
+  POff o;
+  size_t x = 0;
+  auto take = [&](size_t n) { size_t r = x; x += n; return r; };
+  o.Wqkv_f = take((size_t)3 * E * E); o.bqkv_f = take(3 * E);
+  o.Wo_f = take((size_t)E * E); o.bo_f = take(E);
+  o.Wqkv_i = take((size_t)3 * E * E); o.bqkv_i = take(3 * E);
+  o.Wo_i = take((size_t)E * E); o.bo_i = take(E);
+  o.W1 = take((size_t)H * E); o.b1 = take(H);
+  o.W2 = take((size_t)E * H); o.b2 = take(E);
+  o.g1 = take(E); o.be1 = take(E); o.g2 = take(E); o.be2 = take(E);
+  o.g3 = take(E); o.be3 = take(E);
+  o.total = x;
+  return o;
+}
+
+// ---- buffer layouts --------------------------------------------------------------------------
+struct Arena {
+  size_t off = 0;
+  size_t take(size_t bytes) { size_t r = off; off = align_up(off + bytes); return r; }
+};
+
+struct SavedLayout {
+  size_t qkvf, of, lsef, h1, xh1, rs1, qi, ki, vi, oi, lsei, h2, xh2, rs2, g, xh3, rs3, total;
+};
+
+SavedLayout saved_layout(const Dims& d) {
+  SavedLayout L;
+  Arena a;
+  const size_t N = (size_t)d.Nmax, t = d.tsz, E = d.E;
+  L.qkvf = a.take(N * 3 * E * t);
+  L.of = a.take(N * E * t);
+  L.lsef = a.take(N * d.heads * 4);
+  L.h1 = a.take(N * E * t);
+  L.xh1 = a.take(N * E * t);
+  L.rs1 = a.take(N * 4);
+  L.qi = a.take(N * E * t);
+  L.ki = a.take(N * E * t);
+  L.vi = a.take(N * E * t);
+  L.oi = a.take(N * E * t);
+  L.lsei = a.take(N * d.heads * 4);
+  L.h2 = a.take(N * E * t);
+  L.xh2 = a.take(N * E * t);
+  L.rs2 = a.take(N * 4);
+  L.g = a.take(N * d.H * t);
+  L.xh3 = a.take(N * E * t);
+  L.rs3 = a.take(N * 4);
+  L.total = a.off;
+  return L;
+}
+
+struct WsLayout {
+  size_t blob, ds, col_ds, col_c, colmap;
+  size_t xc, ta, tb, tc, td, te, tf, th1, th2, tq, tk, tv, tqkv, D, part, cpart, cpart2;
+  size_t fast;  // region owned by the MFMA path
+  size_t total;
+  int64_t Z;    // partial-sum chunks
+};
+
+WsLayout ws_layout(const Dims& d) {
+  WsLayout L;
+  Arena a;
+  const size_t N = (size_t)d.Nmax, t = d.tsz, E = d.E;
+  L.blob = a.take((size_t)d.B * (3 + d.words) * 4);
+  L.ds = a.take((size_t)d.B * sizeof(tfm::DsInfo));
+  L.col_ds = a.take((size_t)d.B * d.S * 4);
+  L.col_c = a.take((size_t)d.B * d.S * 4);
+  L.colmap = a.take((size_t)d.B * d.S * 4);
+  L.xc = a.take(N * E * t);
+  L.ta = a.take(N * E * t);
+  L.tb = a.take(N * E * t);
+  L.tc = a.take(N * E * t);
+  L.td = a.take(N * E * t);
+  L.te = a.take(N * E * t);
+  L.tf = a.take(N * E * t);
+  L.th1 = a.take(N * d.H * t);
+  L.th2 = a.take(N * d.H * t);
+  L.tq = a.take(N * E * t);
+  L.tk = a.take(N * E * t);
+  L.tv = a.take(N * E * t);
+  L.tqkv = a.take(N * 3 * E * t);
+  L.D = a.take(N * d.heads * 4);
+  L.Z = (d.Nmax + kChunk - 1) / kChunk;
+  size_t maxw = (size_t)3 * E * E;
+  if ((size_t)d.H * E > maxw) maxw = (size_t)d.H * E;
+  L.part = a.take((size_t)L.Z * maxw * 4);
+  size_t maxc = 3 * E > (size_t)d.H ? 3 * E : (size_t)d.H;
+  L.cpart = a.take((size_t)L.Z * maxc * 4);
+  L.cpart2 = a.take((size_t)L.Z * maxc * 4);
+  L.fast = a.take(tfm::fast_workspace_bytes(d.B, d.R, d.S, d.E, d.heads, d.H,
+                                            d.dtype == TFM_BF16));
+  L.total = a.off;
+  return L;
+}
+
+bool aligned(const void* p) { return p && ((uintptr_t)p % 16) == 0; }
+
+// ---- per-call plan ---------------------------------------------------------------------------
+struct Plan {
+  int NC = 0;
+  std::vector<int32_t> blob;
+};
+
+int make_plan(const Dims& d, const int32_t* n_train, const uint8_t* mask, Plan& P) {
+  if (!n_train || !mask) return fail(TFM_ERR_POINTER, "n_train or cell_mask is null");
+  P.blob.assign((size_t)d.B * (3 + d.words), 0);
+  int col = 0;
+  for (int b = 0; b < d.B; ++b) {
+    if (n_train[b] < 1 || n_train[b] > d.R)
+      return fail(TFM_ERR_NTRAIN, "n_train[%d]=%d outside [1, R=%d]", b, n_train[b], d.R);
+    const uint8_t* m = mask + (size_t)b * d.S;
+    if (!m[d.C]) return fail(TFM_ERR_MASK, "target cell (index C=%d) of dataset %d inactive",
+                             d.C, b);
+    int32_t* e = &P.blob[(size_t)b * (3 + d.words)];
+    int cnt = 0;
+    for (int c = 0; c < d.S; ++c)
+      if (m[c]) {
+        ++cnt;
+        e[3 + (c >> 5)] |= (int32_t)(1u << (c & 31));
+      }
+    e[0] = n_train[b];
+    e[1] = col;
+    e[2] = cnt;
+    col += cnt;
+  }
+  P.NC = col;
+  return TFM_OK;
+}
+
+#define HIPCHK(...)                                                                     \
+  do {                                                                                  \
+    hipError_t e_ = (__VA_ARGS__);                                                      \
+    if (e_ != hipSuccess)                                                               \
+      return fail(TFM_ERR_HIP, "%s failed: %s", #__VA_ARGS__, hipGetErrorString(e_));   \
+  } while (0)
+
+#define STEP(name, ...)              \
+  do {                               \
+    tfm::prof_begin(name, s);        \
+    HIPCHK(__VA_ARGS__);             \
+    tfm::prof_end(s);                \
+  } while (0)
+
+int setup_geo(const Dims& d, const Plan& P, char* ws, const WsLayout& W, tfm::Geo& g,
+              hipStream_t s) {
+  int32_t* blob = (int32_t*)(ws + W.blob);
+  g.B = d.B; g.R = d.R; g.S = d.S; g.E = d.E; g.heads = d.heads; g.d = d.d; g.H = d.H;
+  g.NC = P.NC;
+  g.N = (int64_t)P.NC * d.R;
+  g.ds = (const tfm::DsInfo*)(ws + W.ds);
+  g.col_ds = (const int32_t*)(ws + W.col_ds);
+  g.col_c = (const int32_t*)(ws + W.col_c);
+  g.colmap = (const int32_t*)(ws + W.colmap);
+  HIPCHK(tfm::launch_upload(P.blob.data(), (int64_t)P.blob.size(), blob, s));
+  HIPCHK(tfm::launch_expand_meta(blob, d.B, d.S, d.words, (tfm::DsInfo*)(ws + W.ds),
+                                 (int32_t*)(ws + W.col_ds), (int32_t*)(ws + W.col_c),
+                                 (int32_t*)(ws + W.colmap), s));
+  return TFM_OK;
+}
+
+// ---- forward ---------------------------------------------------------------------------------
+template <class T>
+int fwd_simple(const Dims& d, const tfm::Geo& g, const T* X, const float* prm, T* Y, char* sv,
+               const SavedLayout& S, char* ws, const WsLayout& W, hipStream_t s) {
+  using namespace tfm;
+  const POff o = param_offsets(d.E, d.H);
+  const int E = d.E, H = d.H;
+  const int64_t N = g.N;
+  T* xc = (T*)(ws + W.xc);
+  T* ta = (T*)(ws + W.ta);
+  T* tu = (T*)(ws + W.th1);
+  T* qkvf = (T*)(sv + S.qkvf);
+  T* of = (T*)(sv + S.of);
+  T* h1 = (T*)(sv + S.h1);
+  T* h2 = (T*)(sv + S.h2);
+  T* oi = (T*)(sv + S.oi);
+  T* gp = (T*)(sv + S.g);
+  T* yc = (T*)(ws + W.tb);
+  STEP("gather/hbm", launch_gather<T>(g, X, xc, s));
+  STEP("feat_qkv/valu", launch_linear<T, T>(N, 3 * E, E, xc, E, prm + o.Wqkv_f, E, 1, prm + o.bqkv_f, qkvf,
+                             3 * E, s));
+  STEP("feat_attn_fwd/valu", launch_feat_attn_fwd_simple<T>(g, qkvf, of, (float*)(sv + S.lsef), s));
+  STEP("feat_out/valu", launch_linear<T, T>(N, E, E, of, E, prm + o.Wo_f, E, 1, prm + o.bo_f, ta, E, s));
+  STEP("ln1/hbm", launch_add_ln<T>(N, E, xc, ta, prm + o.g1, prm + o.be1, h1, (T*)(sv + S.xh1),
+                          (float*)(sv + S.rs1), s));
+  STEP("item_qkv/valu", launch_linear_item_qkv<T>(g, h1, prm + o.Wqkv_i, prm + o.bqkv_i, (T*)(sv + S.qi),
+                                   (T*)(sv + S.ki), (T*)(sv + S.vi), s));
+  STEP("item_attn_fwd/valu", launch_item_attn_fwd_simple<T>(g, (T*)(sv + S.qi), (T*)(sv + S.ki), (T*)(sv + S.vi),
+                                        oi, (float*)(sv + S.lsei), s));
+  STEP("item_out/valu", launch_linear<T, T>(N, E, E, oi, E, prm + o.Wo_i, E, 1, prm + o.bo_i, ta, E, s));
+  STEP("ln2/hbm", launch_add_ln<T>(N, E, h1, ta, prm + o.g2, prm + o.be2, h2, (T*)(sv + S.xh2),
+                          (float*)(sv + S.rs2), s));
+  STEP("mlp_up/valu", launch_linear<T, T>(N, H, E, h2, E, prm + o.W1, E, 1, prm + o.b1, gp, H, s));
+  STEP("gelu/hbm", launch_gelu<T>(N * H, gp, tu, s));
+  STEP("mlp_down/valu", launch_linear<T, T>(N, E, H, tu, H, prm + o.W2, H, 1, prm + o.b2, ta, E, s));
+  STEP("ln3/hbm", launch_add_ln<T>(N, E, h2, ta, prm + o.g3, prm + o.be3, yc, (T*)(sv + S.xh3),
+                          (float*)(sv + S.rs3), s));
+  STEP("scatter/hbm", launch_scatter<T>(g, yc, (const T*)nullptr, Y, s));
+  return TFM_OK;
+}
+
+// ---- backward --------------------------------------------------------------------------------
+template <class T>
+struct GradSink {
+  const WsLayout& W;
+  char* ws;
+  float* grads;
+  int accumulate;
+  int64_t M;
+  hipStream_t s;
+  // dW[j][i] = sum_m dY[m][j] X[m][i]
+  int wgrad(const T* dY, int Nj, const T* X, int Ki, size_t off) {
+    float* part = (float*)(ws + W.part);
+    int64_t Z = (M + kChunk - 1) / kChunk;
+    if (Z < 1) Z = 1;
+    STEP("wgrad/valu", tfm::launch_wgrad<T>(M, Nj, Ki, dY, Nj, X, Ki, kChunk, part, s));
+    STEP("reduce/hbm", tfm::launch_reduce_partials((int)Z, (int64_t)Nj * Ki, part, grads + off,
+                                               accumulate, s));
+    return TFM_OK;
+  }
+  // g[j] = sum_m A[m][j] (* B[m][j])
+  int colsum(const T* A, const T* B, int Nj, size_t off) {
+    float* part = (float*)(ws + W.cpart);
+    int64_t Z = (M + kChunk - 1) / kChunk;
+    if (Z < 1) Z = 1;
+    STEP("colsum/hbm", tfm::launch_colsum<T>(M, Nj, A, Nj, B, Nj, kChunk, part, s));
+    STEP("reduce/hbm", tfm::launch_reduce_partials((int)Z, Nj, part, grads + off, accumulate, s));
+    return TFM_OK;
+  }
+};
+
+#define CHK(...)                 \
+  do {                           \
+    int c_ = (__VA_ARGS__);      \
+    if (c_ != TFM_OK) return c_; \
+  } while (0)
+
+template <class T>
+int bwd_simple(const Dims& d, const tfm::Geo& g, const T* X, const float* prm, const char* sv,
+               const SavedLayout& S, const T* dY, T* dX, float* grads, int accumulate,
+               char* ws, const WsLayout& W, hipStream_t s) {
+  using namespace tfm;
+  const POff o = param_offsets(d.E, d.H);
+  const int E = d.E, H = d.H;
+  const int64_t N = g.N;
+  GradSink<T> G{W, ws, grads, accumulate, N, s};
+  T* xc = (T*)(ws + W.xc);
+  T* dyc = (T*)(ws + W.ta);
+  T* dz3 = (T*)(ws + W.tb);
+  T* tmp = (T*)(ws + W.tc);
+  T* dh = (T*)(ws + W.td);
+  T* dz2 = (T*)(ws + W.te);
+  T* dz1 = (T*)(ws + W.tf);
+  T* du = (T*)(ws + W.th1);
+  T* uu = (T*)(ws + W.th2);
+  T* dqkv = (T*)(ws + W.tqkv);
+  const T* h1 = (const T*)(sv + S.h1);
+  const T* h2 = (const T*)(sv + S.h2);
+  const T* gp = (const T*)(sv + S.g);
+  STEP("gather/hbm", launch_gather<T>(g, dY, dyc, s));
+  STEP("gather/hbm", launch_gather<T>(g, X, xc, s));
+  // LN3
+  STEP("ln3_bwd/hbm", launch_ln_bwd<T>(N, E, dyc, (const T*)nullptr, (const T*)(sv + S.xh3),
+                          (const float*)(sv + S.rs3), prm + o.g3, dz3, (T*)nullptr, s));
+  CHK(G.colsum(dyc, (const T*)(sv + S.xh3), E, o.g3));
+  CHK(G.colsum(dyc, (const T*)nullptr, E, o.be3));
+  // MLP
+  STEP("mlp_down_dx/valu", launch_linear<T, T>(N, H, E, dz3, E, prm + o.W2, 1, H, nullptr, du, H, s));
+  STEP("gelu/hbm", launch_gelu<T>(N * H, gp, uu, s));
+  CHK(G.wgrad(dz3, E, uu, H, o.W2));
+  CHK(G.colsum(dz3, (const T*)nullptr, E, o.b2));
+  STEP("gelu_bwd/hbm", launch_gelu_bwd<T>(N * H, gp, du, s));
+  CHK(G.wgrad(du, H, h2, E, o.W1));
+  CHK(G.colsum(du, (const T*)nullptr, H, o.b1));
+  STEP("mlp_up_dx/valu", launch_linear<T, T>(N, E, H, du, H, prm + o.W1, 1, E, nullptr, tmp, E, s));
+  // LN2
+  STEP("ln2_bwd/hbm", launch_ln_bwd<T>(N, E, dz3, tmp, (const T*)(sv + S.xh2), (const float*)(sv + S.rs2),
+                          prm + o.g2, dz2, dh, s));
+  CHK(G.colsum(dh, (const T*)(sv + S.xh2), E, o.g2));
+  CHK(G.colsum(dh, (const T*)nullptr, E, o.be2));
+  // item attention
+  T* doi = (T*)(ws + W.tc);
+  STEP("item_out_dx/valu", launch_linear<T, T>(N, E, E, dz2, E, prm + o.Wo_i, 1, E, nullptr, doi, E, s));
+  CHK(G.wgrad(dz2, E, (const T*)(sv + S.oi), E, o.Wo_i));
+  CHK(G.colsum(dz2, (const T*)nullptr, E, o.bo_i));
+  T* dq = (T*)(ws + W.tq);
+  T* dk = (T*)(ws + W.tk);
+  T* dv = (T*)(ws + W.tv);
+  STEP("item_attn_bwd/valu", launch_item_attn_bwd_simple<T>(g, (const T*)(sv + S.qi), (const T*)(sv + S.ki),
+                                        (const T*)(sv + S.vi), (const T*)(sv + S.oi), doi,
+                                        (const float*)(sv + S.lsei), (float*)(ws + W.D), dq, dk,
+                                        dv, s));
+  STEP("item_dqkv_cells/hbm", launch_item_dqkv_to_cells<T>(g, dq, dk, dv, dqkv, s));
+  CHK(G.wgrad(dqkv, 3 * E, h1, E, o.Wqkv_i));
+  CHK(G.colsum(dqkv, (const T*)nullptr, 3 * E, o.bqkv_i));
+  STEP("item_qkv_dx/valu", launch_linear<T, T>(N, E, 3 * E, dqkv, 3 * E, prm + o.Wqkv_i, 1, E, nullptr, tmp, E,
+                             s));
+  // LN1
+  STEP("ln1_bwd/hbm", launch_ln_bwd<T>(N, E, dz2, tmp, (const T*)(sv + S.xh1), (const float*)(sv + S.rs1),
+                          prm + o.g1, dz1, dh, s));
+  CHK(G.colsum(dh, (const T*)(sv + S.xh1), E, o.g1));
+  CHK(G.colsum(dh, (const T*)nullptr, E, o.be1));
+  // feature attention
+  T* dof = (T*)(ws + W.tc);
+  STEP("feat_out_dx/valu", launch_linear<T, T>(N, E, E, dz1, E, prm + o.Wo_f, 1, E, nullptr, dof, E, s));
+  CHK(G.wgrad(dz1, E, (const T*)(sv + S.of), E, o.Wo_f));
+  CHK(G.colsum(dz1, (const T*)nullptr, E, o.bo_f));
+  STEP("feat_attn_bwd/valu", launch_feat_attn_bwd_simple<T>(g, (const T*)(sv + S.qkvf), (const T*)(sv + S.of), dof,
+                                        (const float*)(sv + S.lsef), dqkv, s));
+  CHK(G.wgrad(dqkv, 3 * E, xc, E, o.Wqkv_f));
+  CHK(G.colsum(dqkv, (const T*)nullptr, 3 * E, o.bqkv_f));
+  STEP("feat_qkv_dx/valu", launch_linear<T, T>(N, E, 3 * E, dqkv, 3 * E, prm + o.Wqkv_f, 1, E, nullptr, tmp, E,
+                             s));
+  STEP("scatter/hbm", launch_scatter<T>(g, dz1, tmp, dX, s));
+  return TFM_OK;
+}
+
+}  // namespace
+
+// ============================================================================ C ABI
+extern "C" {
+
+size_t tfm_layer_param_count(const tfm_dims* dims) {
+  Dims d;
+  if (check_dims(dims, d) != TFM_OK) return 0;
+  return param_offsets(d.E, d.H).total;
+}
+
+size_t tfm_layer_saved_bytes(const tfm_dims* dims) {
+  Dims d;
+  if (check_dims(dims, d) != TFM_OK) return 0;
+  return saved_layout(d).total;
+}
+
+size_t tfm_layer_workspace_bytes(const tfm_dims* dims) {
+  Dims d;
+  if (check_dims(dims, d) != TFM_OK) return 0;
+  return ws_layout(d).total;
+}
+
+const char* tfm_last_error(void) { return g_err.c_str(); }
+
+int tfm_layer_fwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* cell_mask,
+                  const void* X, const float* params, void* Y, void* saved, size_t saved_bytes,
+                  void* workspace, size_t workspace_bytes, void* stream) {
+  Dims d;
+  int rc = check_dims(dims, d);
+  if (rc) return rc;
+  if (!aligned(X) || !aligned(params) || !aligned(Y) || !aligned(saved) || !aligned(workspace))
+    return fail(TFM_ERR_POINTER, "X, params, Y, saved and workspace must be non-null and "
+                                 "16-byte aligned");
+  const SavedLayout S = saved_layout(d);
+  const WsLayout W = ws_layout(d);
+  if (saved_bytes < S.total)
+    return fail(TFM_ERR_BUFFER, "saved buffer has %zu bytes, %zu required", saved_bytes, S.total);
+  if (workspace_bytes < W.total)
+    return fail(TFM_ERR_BUFFER, "workspace has %zu bytes, %zu required", workspace_bytes,
+                W.total);
+  Plan P;
+  rc = make_plan(d, n_train, cell_mask, P);
+  if (rc) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  char* sv = (char*)saved;
+  tfm::Geo g;
+  rc = setup_geo(d, P, ws, W, g, s);
+  if (rc) return rc;
+  if (d.dtype == TFM_F32)
+    return fwd_simple<float>(d, g, (const float*)X, params, (float*)Y, sv, S, ws, W, s);
+  return fwd_simple<tfm::bf16>(d, g, (const tfm::bf16*)X, params, (tfm::bf16*)Y, sv, S, ws, W,
+                               s);
+}
+
+int tfm_layer_bwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* cell_mask,
+                  const void* X, const float* params, const void* saved, size_t saved_bytes,
+                  const void* dY, void* dX, float* grads, int accumulate, void* workspace,
+                  size_t workspace_bytes, void* stream) {
+  Dims d;
+  int rc = check_dims(dims, d);
+  if (rc) return rc;
+  if (!aligned(X) || !aligned(params) || !aligned(saved) || !aligned(dY) || !aligned(dX) ||
+      !aligned(grads) || !aligned(workspace))
+    return fail(TFM_ERR_POINTER, "X, params, saved, dY, dX, grads and workspace must be "
+                                 "non-null and 16-byte aligned");
+  const SavedLayout S = saved_layout(d);
+  const WsLayout W = ws_layout(d);
+  if (saved_bytes < S.total)
+    return fail(TFM_ERR_BUFFER, "saved buffer has %zu bytes, %zu required", saved_bytes, S.total);
+  if (workspace_bytes < W.total)
+    return fail(TFM_ERR_BUFFER, "workspace has %zu bytes, %zu required", workspace_bytes,
+                W.total);
+  Plan P;
+  rc = make_plan(d, n_train, cell_mask, P);
+  if (rc) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  tfm::Geo g;
+  rc = setup_geo(d, P, ws, W, g, s);
+  if (rc) return rc;
+  if (d.dtype == TFM_F32)
+    return bwd_simple<float>(d, g, (const float*)X, params, (const char*)saved, S,
+                             (const float*)dY, (float*)dX, grads, accumulate, ws, W, s);
+  return bwd_simple<tfm::bf16>(d, g, (const tfm::bf16*)X, params, (const char*)saved, S,
+                               (const tfm::bf16*)dY, (tfm::bf16*)dX, grads, accumulate, ws, W,
+                               s);
+}
+
+}  // extern "C"

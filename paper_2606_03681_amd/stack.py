@@ -1,0 +1,71 @@
+"""Device-side plumbing around the C ABI: buffers for a stack of layers and the call order of
+their forward and backward passes (forward 0..L-1, backward L-1..0).  Allocation only; all
+arithmetic is in the library."""
+
+import numpy as np
+import torch
+
+from . import tfm
+from .workloads import bf16_bits_to_f32
+
+
+def to_device(a, dtype, device="cuda"):
+    """numpy storage array (float32, or uint16 bfloat16 bits) -> device tensor."""
+    if dtype == "f32":
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(device)
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint16).view(np.int16))
+    return t.to(device).view(torch.bfloat16)
+
+
+def to_host(t, dtype):
+    """device tensor -> numpy float64."""
+    if dtype == "f32":
+        return t.detach().float().cpu().numpy().astype(np.float64)
+    bits = t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    return bf16_bits_to_f32(bits).astype(np.float64)
+
+
+class Stack:
+    """L layers with independent parameters over the same n_train / cell_mask."""
+
+    def __init__(self, dims, n_train, cell_mask, params, device="cuda"):
+        self.dims = dims
+        self.n_train = np.ascontiguousarray(n_train, dtype=np.int32)
+        self.cell_mask = np.ascontiguousarray(cell_mask, dtype=np.uint8)
+        self.device = device
+        self.params = [p if isinstance(p, torch.Tensor) else
+                       torch.from_numpy(np.ascontiguousarray(p, dtype=np.float32)).to(device)
+                       for p in params]
+        self.L = len(self.params)
+        self.elt = torch.float32 if dims.dtype == tfm.TFM_F32 else torch.bfloat16
+        self.shape = (dims.B, dims.R, dims.C + 1, dims.E)
+        sb, wb = tfm.saved_bytes(dims), tfm.workspace_bytes(dims)
+        if sb == 0 or wb == 0:
+            raise tfm.TfmError(-1, tfm.last_error())
+        self.saved = [torch.empty(sb, dtype=torch.uint8, device=device) for _ in range(self.L)]
+        self.workspace = torch.empty(wb, dtype=torch.uint8, device=device)
+        self.acts = [torch.empty(self.shape, dtype=self.elt, device=device)
+                     for _ in range(self.L)]
+        self.grads = [torch.empty_like(p) for p in self.params]
+        self.dxs = [torch.empty(self.shape, dtype=self.elt, device=device) for _ in range(2)]
+        self.inputs = None
+
+    def forward(self, X):
+        """Runs every layer; returns the last layer's output (a buffer owned by the stack)."""
+        self.inputs = [X] + self.acts[:-1]
+        for l in range(self.L):
+            tfm.layer_fwd(self.dims, self.n_train, self.cell_mask, self.inputs[l],
+                          self.params[l], self.acts[l], self.saved[l], self.workspace)
+        return self.acts[-1]
+
+    def backward(self, dY, accumulate=False):
+        """Backward through every layer; returns dX of the first layer.  Parameter gradients
+        land in self.grads."""
+        g = dY
+        for l in range(self.L - 1, -1, -1):
+            out = self.dxs[l % 2]
+            tfm.layer_bwd(self.dims, self.n_train, self.cell_mask, self.inputs[l],
+                          self.params[l], self.saved[l], g, out, self.grads[l], accumulate,
+                          self.workspace)
+            g = out
+        return g

@@ -1,0 +1,156 @@
+"""Thin ctypes binding of libtfmlayer.so (C ABI in include/tfm_layer.h).
+
+Argument marshalling only: every step of the layer runs in the library's HIP kernels.  torch
+supplies device memory and the stream.  There is no fallback: if the library is missing, every
+call raises.
+"""
+
+import ctypes
+import os
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtfmlayer.so")
+_lib = None
+
+TFM_F32, TFM_BF16 = 0, 1
+ERRORS = {
+    -1: "TFM_ERR_DIMS", -2: "TFM_ERR_HEAD_DIM", -3: "TFM_ERR_NTRAIN", -4: "TFM_ERR_MASK",
+    -5: "TFM_ERR_POINTER", -6: "TFM_ERR_HIP", -7: "TFM_ERR_BUFFER",
+}
+EXPORTS = ("tfm_layer_param_count", "tfm_layer_saved_bytes", "tfm_layer_workspace_bytes",
+           "tfm_layer_fwd", "tfm_layer_bwd", "tfm_last_error", "tfm_prof_enable",
+           "tfm_prof_collect", "tfm_prof_step")
+
+
+class TfmError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"{ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+class tfm_dims(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("B", "R", "C", "E", "heads", "H", "dtype")]
+
+
+def make_dims(B, R, C, E, heads, H, dtype):
+    dt = {"f32": TFM_F32, "bf16": TFM_BF16}.get(dtype, dtype)
+    return tfm_dims(int(B), int(R), int(C), int(E), int(heads), int(H), int(dt))
+
+
+def lib():
+    """Loads the library (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is missing: build it with "
+                               "python paper_2606_03681_amd/build.py")
+        L = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.POINTER
+        vp, sz, i32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
+        for name in ("tfm_layer_param_count", "tfm_layer_saved_bytes",
+                     "tfm_layer_workspace_bytes"):
+            getattr(L, name).restype = sz
+            getattr(L, name).argtypes = [P(tfm_dims)]
+        L.tfm_last_error.restype = ctypes.c_char_p
+        L.tfm_last_error.argtypes = []
+        L.tfm_layer_fwd.restype = i32
+        L.tfm_layer_fwd.argtypes = [P(tfm_dims), vp, vp, vp, vp, vp, vp, sz, vp, sz, vp]
+        L.tfm_layer_bwd.restype = i32
+        L.tfm_layer_bwd.argtypes = [P(tfm_dims), vp, vp, vp, vp, vp, sz, vp, vp, vp, i32, vp,
+                                    sz, vp]
+        L.tfm_prof_enable.restype = i32
+        L.tfm_prof_enable.argtypes = [i32]
+        L.tfm_prof_collect.restype = i32
+        L.tfm_prof_collect.argtypes = []
+        L.tfm_prof_step.restype = i32
+        L.tfm_prof_step.argtypes = [i32, P(ctypes.c_char_p), P(ctypes.c_longlong),
+                                    P(ctypes.c_double)]
+        _lib = L
+    return _lib
+
+
+def last_error():
+    return lib().tfm_last_error().decode()
+
+
+def param_count(dims):
+    return lib().tfm_layer_param_count(ctypes.byref(dims))
+
+
+def saved_bytes(dims):
+    return lib().tfm_layer_saved_bytes(ctypes.byref(dims))
+
+
+def workspace_bytes(dims):
+    return lib().tfm_layer_workspace_bytes(ctypes.byref(dims))
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _host(a, dtype):
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a, a.ctypes.data
+
+
+def _check(rc):
+    if rc != 0:
+        raise TfmError(rc, last_error())
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return stream if isinstance(stream, int) else stream.cuda_stream
+
+
+def layer_fwd(dims, n_train, cell_mask, X, params, Y, saved, workspace, stream=None):
+    """tfm_layer_fwd.  n_train: host int32 [B]; cell_mask: host uint8 [B, C+1]; X, Y: device
+    tensors [B, R, C+1, E] (float32 or bfloat16); params: device float32; saved, workspace:
+    device byte tensors of saved_bytes(dims) / workspace_bytes(dims)."""
+    nt, ntp = _host(n_train, np.int32)
+    cm, cmp_ = _host(cell_mask, np.uint8)
+    rc = lib().tfm_layer_fwd(ctypes.byref(dims), ntp, cmp_, _ptr(X), _ptr(params), _ptr(Y),
+                             _ptr(saved), saved.numel() * saved.element_size(),
+                             _ptr(workspace), workspace.numel() * workspace.element_size(),
+                             _stream(stream))
+    _check(rc)
+
+
+def layer_bwd(dims, n_train, cell_mask, X, params, saved, dY, dX, grads, accumulate, workspace,
+              stream=None):
+    """tfm_layer_bwd; grads: device float32 like params, overwritten or accumulated."""
+    nt, ntp = _host(n_train, np.int32)
+    cm, cmp_ = _host(cell_mask, np.uint8)
+    rc = lib().tfm_layer_bwd(ctypes.byref(dims), ntp, cmp_, _ptr(X), _ptr(params), _ptr(saved),
+                             saved.numel() * saved.element_size(), _ptr(dY), _ptr(dX),
+                             _ptr(grads), int(bool(accumulate)), _ptr(workspace),
+                             workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(rc)
+
+
+def prof_enable(on=True):
+    """Turns per-step HIP-event timing of the library's launches on or off (tfm_prof.h)."""
+    _check(lib().tfm_prof_enable(int(bool(on))))
+
+
+def prof_collect():
+    """Waits for the recorded events; returns {step: (launches, total_ms)}."""
+    n = lib().tfm_prof_collect()
+    if n < 0:
+        raise TfmError(n, "profiling events could not be read")
+    out = {}
+    for i in range(n):
+        name = ctypes.c_char_p()
+        cnt = ctypes.c_longlong()
+        ms = ctypes.c_double()
+        lib().tfm_prof_step(i, ctypes.byref(name), ctypes.byref(cnt), ctypes.byref(ms))
+        out[name.value.decode()] = (cnt.value, ms.value)
+    return out

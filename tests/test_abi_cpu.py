@@ -1,0 +1,103 @@
+"""Host-side checks of the C-ABI library that need no GPU: it loads, exports every function
+that include/tfm_layer.h declares, answers the size queries, and rejects invalid arguments with
+the documented codes before launching anything."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2606_03681_amd import tfm
+from paper_2606_03681_amd import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    names = set()
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            text = open(os.path.join(ROOT, "include", fn)).read()
+            text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+            names |= set(re.findall(r"\b(tfm_\w+)\s*\(", text))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    L = tfm.lib()
+    declared = _declared_functions()
+    assert declared >= set(tfm.EXPORTS)
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+def _dims(**kw):
+    base = dict(B=2, R=64, C=8, E=64, heads=4, H=128, dtype="f32")
+    base.update(kw)
+    return tfm.make_dims(**base)
+
+
+def test_param_count_matches_formula():
+    for E, H in ((64, 128), (192, 384), (256, 768)):
+        heads = E // 32
+        d = _dims(E=E, H=H, heads=heads)
+        assert tfm.param_count(d) == 8 * E * E + 8 * E + 2 * E * H + H + 7 * E
+        assert tfm.param_count(d) == wl.param_count(E, H)
+    assert tfm.param_count(_dims(E=192, H=384, heads=6)) == 445632
+
+
+def test_sizes_positive_and_grow_with_batch():
+    d1, d2 = _dims(), _dims(B=4)
+    assert 0 < tfm.saved_bytes(d1) < tfm.saved_bytes(d2)
+    assert 0 < tfm.workspace_bytes(d1) < tfm.workspace_bytes(d2)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=0), -1), (dict(R=0), -1), (dict(C=-1), -1), (dict(C=300), -1),
+    (dict(E=48), -1), (dict(E=512), -1), (dict(H=100), -1), (dict(dtype=7), -1),
+    (dict(heads=3), -2), (dict(E=64, heads=1), -2), (dict(E=256, heads=2), -2),
+])
+def test_invalid_dims_rejected(kw, code):
+    d = _dims(**kw)
+    assert tfm.param_count(d) == 0
+    assert tfm.saved_bytes(d) == 0
+    fake = 1 << 20
+    rc = tfm.lib().tfm_layer_fwd(ctypes.byref(d), None, None, fake, fake, fake, fake, 1 << 40,
+                                 fake, 1 << 40, None)
+    assert rc == code
+    assert tfm.last_error()
+
+
+def _call_fwd(d, n_train, mask, ptr=1 << 20, sb=1 << 40, wb=1 << 40):
+    nt = np.ascontiguousarray(n_train, dtype=np.int32)
+    cm = np.ascontiguousarray(mask, dtype=np.uint8)
+    return tfm.lib().tfm_layer_fwd(ctypes.byref(d), nt.ctypes.data, cm.ctypes.data, ptr, ptr,
+                                   ptr, ptr, sb, ptr, wb, None)
+
+
+def _call_bwd(d, n_train, mask, ptr=1 << 20, sb=1 << 40, wb=1 << 40):
+    nt = np.ascontiguousarray(n_train, dtype=np.int32)
+    cm = np.ascontiguousarray(mask, dtype=np.uint8)
+    return tfm.lib().tfm_layer_bwd(ctypes.byref(d), nt.ctypes.data, cm.ctypes.data, ptr, ptr,
+                                   ptr, sb, ptr, ptr, ptr, 0, ptr, wb, None)
+
+
+@pytest.mark.parametrize("call", [_call_fwd, _call_bwd])
+def test_bad_metadata_and_pointers_rejected_before_launch(call):
+    d = _dims()
+    mask = np.ones((2, 9), np.uint8)
+    assert call(d, [0, 5], mask) == -3
+    assert call(d, [5, 65], mask) == -3
+    assert "n_train" in tfm.last_error()
+    bad = mask.copy()
+    bad[1, 8] = 0
+    assert call(d, [5, 5], bad) == -4
+    assert call(d, [5, 5], mask, ptr=0) == -5
+    assert call(d, [5, 5], mask, ptr=(1 << 20) + 4) == -5
+    assert call(d, [5, 5], mask, sb=16) == -7
+    assert call(d, [5, 5], mask, wb=16) == -7
+    rc = tfm.lib().tfm_layer_fwd(ctypes.byref(d), None, None, 1 << 20, 1 << 20, 1 << 20,
+                                 1 << 20, 1 << 40, 1 << 20, 1 << 40, None)
+    assert rc == -5

@@ -1,0 +1,147 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle, element by element on
+the same seeded inputs.  Tolerance: normwise-max relative error (max|gpu - ref| / max|ref| per
+tensor) <= 1e-4 in float32 mode and <= 2e-2 in bfloat16 mode, on Y, dX and every parameter
+gradient block of every layer.
+
+Small shapes are compared in full.  The full-size workloads run in the benchmark's launch
+configuration (whole batch, all layers) and are compared on sampled rows of sampled datasets,
+layer by layer: the oracle evaluates a layer at a set of query rows from the train rows and
+those rows only (exact by the isolation of test rows), and the backward check drives each layer
+with an upstream gradient supported on those rows only."""
+
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_03681_amd import workloads as wl
+
+from _harness import (TOL, compare_all, gpu_stack, nerr, oracle_params, oracle_rows,
+                      oracle_stack, sample_rows)
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    from paper_2606_03681_amd import tfm
+    tfm.lib()
+
+
+@pytest.mark.parametrize("name", [0, "ragged-small-f32", "ragged-small-bf16", "d16-bf16"])
+def test_parity_full(name):
+    w = wl.make_workload(name)
+    _say(f"[parity] {w.cfg['name']} seed={w.seed}")
+    gpu = gpu_stack(w)
+    errs = compare_all(w, gpu, oracle_stack(w))
+    _say(f"[parity] {w.cfg['name']} worst={max(errs.values()):.3g}")
+
+
+def test_parity_small_bf16_sampled_datasets():
+    """cfg 1 (small bf16 layer): the whole batch on the GPU; the oracle on two datasets."""
+    w = wl.make_workload(1)
+    gpu = gpu_stack(w)
+    sub = [0, 5]
+    ws = wl.make_workload(1, datasets=sub)
+    Y, dX, grads = oracle_stack(ws)
+    tol = TOL["bf16"]
+    assert nerr(gpu["Y"][sub], Y) <= tol
+    assert nerr(gpu["dX"][sub], dX) <= tol
+    # parameter gradients of the two datasets alone, through the library
+    gsub = gpu_stack(ws)
+    compare_all(ws, gsub, (Y, dX, grads))
+
+
+def test_padding_is_inert_under_nan_poison():
+    w = wl.make_workload("ragged-small-bf16")
+    clean = gpu_stack(w, storage=True)
+    X, dY = w.X.copy(), w.dY.copy()
+    for b in range(X.shape[0]):
+        off = w.cell_mask[b] == 0
+        X[b][:, off] = 0x7FC0
+        dY[b][:, off] = 0x7FC0
+    pois = gpu_stack(w, X=X, dY=dY, storage=True)
+    assert np.array_equal(pois["Y"], clean["Y"])
+    assert np.array_equal(pois["dX"], clean["dX"])
+    for a, b in zip(pois["grads"], clean["grads"]):
+        assert np.array_equal(a, b)
+    for b in range(X.shape[0]):
+        off = w.cell_mask[b] == 0
+        assert np.all(clean["Y"][b][:, off] == 0) and np.all(clean["dX"][b][:, off] == 0)
+
+
+def test_bitwise_deterministic():
+    w = wl.make_workload("ragged-small-bf16")
+    a = gpu_stack(w, storage=True)
+    b = gpu_stack(w, storage=True)
+    assert np.array_equal(a["Y"], b["Y"]) and np.array_equal(a["dX"], b["dX"])
+    for x, y in zip(a["grads"], b["grads"]):
+        assert np.array_equal(x, y)
+
+
+def test_test_rows_do_not_change_train_outputs():
+    """Changing every test row leaves the train rows' outputs bit-identical on the GPU."""
+    w = wl.make_workload(1, datasets=[0, 1])
+    a = gpu_stack(w, storage=True)
+    X = w.X.copy()
+    rng = np.random.default_rng(0)
+    for b in range(2):
+        n = w.n_train[b]
+        X[b, n:] = wl.to_storage(rng.normal(0, 3, X[b, n:].shape), "bf16")
+    c = gpu_stack(w, X=X, storage=True)
+    for b in range(2):
+        n = w.n_train[b]
+        assert np.array_equal(a["Y"][b, :n], c["Y"][b, :n])
+
+
+@pytest.mark.parametrize("cfg", [2, 3, 4])
+def test_full_size_sampled_rows(cfg):
+    """Full-size workload in the benchmark's launch configuration, sampled rows per layer."""
+    w = wl.make_workload(cfg)
+    dt, heads, R = w.dtype, w.cfg["heads"], w.cfg["R"]
+    tol = TOL[dt]
+    _say(f"[full] cfg{cfg} {w.cfg['name']}: GPU stack")
+    run = gpu_stack(w, keep_acts=True, storage=True)
+    Ps = oracle_params(w)
+    order = np.argsort(w.n_train * w.cell_mask.sum(1), kind="stable")
+    picks = [int(order[len(order) // 2])]
+    inputs = [w.X] + run["acts"][:-1]
+    for l in range(w.cfg["layers"]):
+        for b in picks:
+            n = int(w.n_train[b])
+            tr, te = sample_rows(n, R, seed=100 * l + b)
+            rows = np.concatenate([tr, te])
+            Xb = wl.storage_to_f64(inputs[l][b], dt)
+            Yq, _, _, act, keep = oracle_rows(Xb, w.cell_mask[b], Ps[l], heads, n, tr, te)
+            Yg = wl.storage_to_f64(run["acts"][l][b][rows][:, act], dt)
+            e = nerr(Yg, Yq)
+            _say(f"[full] cfg{cfg} layer {l} dataset {b} fwd err {e:.3g}")
+            assert e <= tol
+            # backward of this layer alone, upstream gradient only at the sampled rows
+            dY = np.zeros_like(w.dY)
+            dY[b][rows[:, None], act[None, :]] = w.dY[b][rows[:, None], act[None, :]]
+            g = gpu_stack(w, X=inputs[l], dY=dY, params=[w.params[l]], storage=True)
+            dYq = wl.storage_to_f64(dY[b][rows][:, act], dt)
+            _, dz, gr, _, _ = oracle_rows(Xb, w.cell_mask[b], Ps[l], heads, n, tr, te, dYq)
+            dXg = wl.storage_to_f64(g["dX"], dt)
+            e = nerr(dXg[b][keep][:, act], dz)
+            _say(f"[full] cfg{cfg} layer {l} dataset {b} dX err {e:.3g}")
+            assert e <= tol
+            others = np.ones(dXg.shape[0], bool)
+            others[b] = False
+            assert np.all(dXg[others] == 0)
+            rest = np.setdiff1d(np.arange(R), keep)
+            assert np.all(dXg[b][rest] == 0)
+            pg = oracle.unpack_params(g["grads"][0], w.cfg["E"], w.cfg["H"])
+            worst = max(nerr(pg[k], gr[k]) for k in oracle.PARAM_ORDER)
+            _say(f"[full] cfg{cfg} layer {l} dataset {b} grads worst err {worst:.3g}")
+            for k in oracle.PARAM_ORDER:
+                assert nerr(pg[k], gr[k]) <= tol, k
