@@ -1,4 +1,4 @@
-// MFMA (bfloat16) path of the layer: launch sequences for the forward and backward pass.
+// MFMA (bfloat16) kernels of the layer: launch interfaces.
 #pragma once
 
 #include <stddef.h>
@@ -6,6 +6,65 @@
 #include "common.h"
 
 namespace tfm {
+
+// Where rows of an operand live: compact active cells (row m at m * ld) or the native
+// [B][R][S][E] tensor (row m at native_cell(m) * E).
+enum { ROWS_COMPACT = 0, ROWS_NATIVE = 1 };
+
+// Epilogues of the MFMA GEMM.
+enum {
+  EPI_BIAS = 0,      // out = C (+ bias)
+  EPI_GELU_FWD = 1,  // out = C + bias (MLP pre-activation), out2 = GELU(out)
+  EPI_GELU_BWD = 2,  // out = C * GELU'(aux)
+  EPI_ITEM_QKV = 3,  // item Q|K|V + bias, written head-major; K, V for train rows only
+  EPI_LN = 4,        // out = LN(C + bias + resid); xhat, rstd saved
+  EPI_LN_BWD = 5,    // dh = C + resid; out = LN'(dh) with xhat = aux, rstd_in; column partials
+  EPI_DX = 6         // out (native) = C + resid
+};
+
+struct GemmArgs {
+  int64_t M;
+  int N, K, BN, epi;
+  const bf16* A;
+  int64_t lda;
+  int amode;
+  const bf16* Bt;  // [N][K]
+  const float* bias;
+  bf16* out;
+  bf16* out2;
+  bf16* out3;
+  int64_t ldo;
+  int omode;
+  const bf16* resid;
+  int rmode;
+  const float* gamma;
+  const float* beta;
+  bf16* xhat;
+  float* rstd;
+  const float* rstd_in;
+  const bf16* aux;
+  float* part;  // EPI_LN_BWD: [gridDim.x][2][BN] partial sums (dgamma, dbeta)
+  Geo g;
+};
+
+hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
+
+// bf16 copies of the six weight matrices of one layer, as stored ([out][in]) and transposed.
+// Offsets (elements) inside w / wt follow the packed parameter order of the weights:
+// Wqkv_f, Wo_f, Wqkv_i, Wo_i, W1, W2.
+struct WOff {
+  int64_t qkv_f, o_f, qkv_i, o_i, w1, w2, total;
+};
+WOff weight_offsets(int E, int H);
+hipError_t launch_weight_prep(const float* params, int E, int H, bf16* w, bf16* wt,
+                              hipStream_t s);
+
+// grad[i] = (accumulate ? grad[i] : 0) + sum_z part[z * stride + i], z ascending
+hipError_t launch_reduce_strided(int Z, int64_t count, int64_t stride, const float* part,
+                                 float* grad, int accumulate, hipStream_t s);
+
+// Writes 0 to every element of the native tensor that lies in an inactive cell.
+hipError_t launch_zero_inactive(const Geo& g, bf16* native, hipStream_t s);
 
 // Scratch bytes that the MFMA path needs inside the workspace.
 size_t fast_workspace_bytes(int B, int R, int S, int E, int heads, int H, bool bf16);

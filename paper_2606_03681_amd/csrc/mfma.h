@@ -1,0 +1,50 @@
+// CDNA4 (gfx950) matrix-core helpers shared by the MFMA kernels.
+//
+// v_mfma_f32_16x16x32_bf16 operand layout (64-lane wave, g = lane / 16, c = lane % 16):
+//   A (16 x 32): lane holds A[c][8g .. 8g+7]        (8 bf16, 16 bytes)
+//   B (32 x 16): lane holds B[8g .. 8g+7][c]        (8 bf16, 16 bytes)
+//   D (16 x 16): lane holds D[4g .. 4g+3][c]        (4 f32)
+// Any permutation of the 32 k positions that is applied to A and B alike gives the same
+// product, which the attention kernels use to feed a D tile back in as an operand.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "common.h"
+
+namespace tfm {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x4 mfma16(const bf16x8& a, const bf16x8& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x4 zero4() {
+  f32x4 z = {0.f, 0.f, 0.f, 0.f};
+  return z;
+}
+
+// 16-byte loads/stores of 8 bf16 values.
+__device__ __forceinline__ bf16x8 ld8(const bf16* p) {
+  return *reinterpret_cast<const bf16x8*>(p);
+}
+__device__ __forceinline__ uint4 ldu4(const bf16* p) { return *reinterpret_cast<const uint4*>(p); }
+__device__ __forceinline__ void stu4(bf16* p, uint4 v) { *reinterpret_cast<uint4*>(p) = v; }
+
+__device__ __forceinline__ float bf2f(uint16_t u) { return __uint_as_float(((uint32_t)u) << 16); }
+
+// Round-to-nearest-even pack of two floats into two bf16 (low half = a).
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+}
+
+__device__ __forceinline__ float wave_reduce_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+}  // namespace tfm

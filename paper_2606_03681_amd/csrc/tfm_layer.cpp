@@ -97,7 +97,8 @@ struct Arena {
 };
 
 struct SavedLayout {
-  size_t qkvf, of, lsef, h1, xh1, rs1, qi, ki, vi, oi, lsei, h2, xh2, rs2, g, xh3, rs3, total;
+  size_t qkvf, of, lsef, h1, xh1, rs1, qi, ki, vi, oi, lsei, h2, xh2, rs2, g, u, xh3, rs3;
+  size_t total;
 };
 
 SavedLayout saved_layout(const Dims& d) {
@@ -119,6 +120,7 @@ SavedLayout saved_layout(const Dims& d) {
   L.xh2 = a.take(N * E * t);
   L.rs2 = a.take(N * 4);
   L.g = a.take(N * d.H * t);
+  L.u = a.take(N * d.H * t);
   L.xh3 = a.take(N * E * t);
   L.rs3 = a.take(N * 4);
   L.total = a.off;
@@ -391,6 +393,191 @@ int bwd_simple(const Dims& d, const tfm::Geo& g, const T* X, const float* prm, c
   return TFM_OK;
 }
 
+// ---- MFMA path (bfloat16) -------------------------------------------------------------------
+bool fast_eligible(const Dims& d) {
+  return d.dtype == TFM_BF16 && (d.E == 64 || d.E == 128 || d.E == 192 || d.E == 256) &&
+         d.H % d.E == 0;
+}
+
+struct FastWs {
+  tfm::bf16* w;
+  tfm::bf16* wt;
+  float* lnpart;
+  tfm::WOff wo;
+};
+
+FastWs fast_ws(const Dims& d, char* ws, const WsLayout& W) {
+  FastWs f;
+  f.wo = tfm::weight_offsets(d.E, d.H);
+  char* p = ws + W.fast;
+  f.w = (tfm::bf16*)p;
+  p += align_up((size_t)f.wo.total * 2);
+  f.wt = (tfm::bf16*)p;
+  p += align_up((size_t)f.wo.total * 2);
+  f.lnpart = (float*)p;
+  return f;
+}
+
+tfm::GemmArgs gemm_base(const tfm::Geo& g, int64_t M, int N, int K, int epi) {
+  tfm::GemmArgs a{};
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  a.BN = g.E;
+  a.epi = epi;
+  a.g = g;
+  return a;
+}
+
+int fwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* prm,
+             tfm::bf16* Y, char* sv, const SavedLayout& S, char* ws, const WsLayout& W,
+             hipStream_t s) {
+  using namespace tfm;
+  typedef tfm::bf16 T;
+  const POff o = param_offsets(d.E, d.H);
+  const FastWs f = fast_ws(d, ws, W);
+  const int E = d.E, H = d.H;
+  const int64_t N = g.N;
+  STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, s));
+  T* qkvf = (T*)(sv + S.qkvf);
+  T* of = (T*)(sv + S.of);
+  T* h1 = (T*)(sv + S.h1);
+  T* h2 = (T*)(sv + S.h2);
+  T* oi = (T*)(sv + S.oi);
+  // feature Q|K|V from the native cells
+  GemmArgs a = gemm_base(g, N, 3 * E, E, EPI_BIAS);
+  a.A = X; a.amode = ROWS_NATIVE; a.lda = E;
+  a.Bt = f.w + f.wo.qkv_f; a.bias = prm + o.bqkv_f; a.out = qkvf; a.ldo = 3 * E;
+  STEP("feat_qkv/mfma", launch_gemm(a, s));
+  STEP("feat_attn_fwd/valu", launch_feat_attn_fwd_simple<T>(g, qkvf, of, (float*)(sv + S.lsef), s));
+  // H1 = LN1(X + O_f Wo_f^T + bo_f)
+  a = gemm_base(g, N, E, E, EPI_LN);
+  a.A = of; a.lda = E; a.Bt = f.w + f.wo.o_f; a.bias = prm + o.bo_f;
+  a.resid = X; a.rmode = ROWS_NATIVE; a.gamma = prm + o.g1; a.beta = prm + o.be1;
+  a.out = h1; a.omode = ROWS_COMPACT; a.xhat = (T*)(sv + S.xh1); a.rstd = (float*)(sv + S.rs1);
+  STEP("feat_out_ln1/mfma", launch_gemm(a, s));
+  // item Q (all rows), K, V (train rows), head-major
+  a = gemm_base(g, N, 3 * E, E, EPI_ITEM_QKV);
+  a.A = h1; a.lda = E; a.Bt = f.w + f.wo.qkv_i; a.bias = prm + o.bqkv_i;
+  a.out = (T*)(sv + S.qi); a.out2 = (T*)(sv + S.ki); a.out3 = (T*)(sv + S.vi);
+  STEP("item_qkv/mfma", launch_gemm(a, s));
+  STEP("item_attn_fwd/valu", launch_item_attn_fwd_simple<T>(g, (T*)(sv + S.qi), (T*)(sv + S.ki),
+                                                            (T*)(sv + S.vi), oi,
+                                                            (float*)(sv + S.lsei), s));
+  // H2 = LN2(H1 + O_i Wo_i^T + bo_i)
+  a = gemm_base(g, N, E, E, EPI_LN);
+  a.A = oi; a.lda = E; a.Bt = f.w + f.wo.o_i; a.bias = prm + o.bo_i;
+  a.resid = h1; a.rmode = ROWS_COMPACT; a.gamma = prm + o.g2; a.beta = prm + o.be2;
+  a.out = h2; a.omode = ROWS_COMPACT; a.xhat = (T*)(sv + S.xh2); a.rstd = (float*)(sv + S.rs2);
+  STEP("item_out_ln2/mfma", launch_gemm(a, s));
+  // G = H2 W1^T + b1, U = GELU(G)
+  a = gemm_base(g, N, H, E, EPI_GELU_FWD);
+  a.A = h2; a.lda = E; a.Bt = f.w + f.wo.w1; a.bias = prm + o.b1;
+  a.out = (T*)(sv + S.g); a.out2 = (T*)(sv + S.u); a.ldo = H;
+  STEP("mlp_up/mfma", launch_gemm(a, s));
+  // Y = LN3(H2 + U W2^T + b2), written to the native layout
+  a = gemm_base(g, N, E, H, EPI_LN);
+  a.A = (T*)(sv + S.u); a.lda = H; a.Bt = f.w + f.wo.w2; a.bias = prm + o.b2;
+  a.resid = h2; a.rmode = ROWS_COMPACT; a.gamma = prm + o.g3; a.beta = prm + o.be3;
+  a.out = Y; a.omode = ROWS_NATIVE; a.xhat = (T*)(sv + S.xh3); a.rstd = (float*)(sv + S.rs3);
+  STEP("mlp_down_ln3/mfma", launch_gemm(a, s));
+  STEP("zero_inactive/hbm", launch_zero_inactive(g, Y, s));
+  return TFM_OK;
+}
+
+int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* prm,
+             const char* sv, const SavedLayout& S, const tfm::bf16* dY, tfm::bf16* dX,
+             float* grads, int accumulate, char* ws, const WsLayout& W, hipStream_t s) {
+  using namespace tfm;
+  typedef tfm::bf16 T;
+  const POff o = param_offsets(d.E, d.H);
+  const FastWs f = fast_ws(d, ws, W);
+  const int E = d.E, H = d.H;
+  const int64_t N = g.N;
+  const int tiles = (int)((N + 127) / 128);
+  GradSink<T> G{W, ws, grads, accumulate, N, s};
+  STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, s));
+  T* xc = (T*)(ws + W.xc);
+  T* dyc = (T*)(ws + W.ta);
+  T* dz3 = (T*)(ws + W.tb);
+  T* dz2 = (T*)(ws + W.te);
+  T* dz1 = (T*)(ws + W.tf);
+  T* dgb = (T*)(ws + W.th1);
+  T* dqkv = (T*)(ws + W.tqkv);
+  const T* h1 = (const T*)(sv + S.h1);
+  const T* h2 = (const T*)(sv + S.h2);
+  // LN3
+  STEP("gather/hbm", launch_gather<T>(g, dY, dyc, s));
+  STEP("ln3_bwd/hbm", launch_ln_bwd<T>(N, E, dyc, (const T*)nullptr, (const T*)(sv + S.xh3),
+                                       (const float*)(sv + S.rs3), prm + o.g3, dz3, (T*)nullptr,
+                                       s));
+  CHK(G.colsum(dyc, (const T*)(sv + S.xh3), E, o.g3));
+  CHK(G.colsum(dyc, (const T*)nullptr, E, o.be3));
+  // MLP: dG = (dZ3 W2) * GELU'(G)
+  GemmArgs a = gemm_base(g, N, H, E, EPI_GELU_BWD);
+  a.A = dz3; a.lda = E; a.Bt = f.wt + f.wo.w2; a.out = dgb; a.ldo = H;
+  a.aux = (const T*)(sv + S.g);
+  STEP("mlp_down_dx/mfma", launch_gemm(a, s));
+  CHK(G.wgrad(dz3, E, (const T*)(sv + S.u), H, o.W2));
+  CHK(G.colsum(dz3, (const T*)nullptr, E, o.b2));
+  CHK(G.wgrad(dgb, H, h2, E, o.W1));
+  CHK(G.colsum(dgb, (const T*)nullptr, H, o.b1));
+  // dZ2 = LN2'(dZ3 + dG W1)
+  a = gemm_base(g, N, E, H, EPI_LN_BWD);
+  a.A = dgb; a.lda = H; a.Bt = f.wt + f.wo.w1; a.resid = dz3; a.aux = (const T*)(sv + S.xh2);
+  a.rstd_in = (const float*)(sv + S.rs2); a.gamma = prm + o.g2; a.out = dz2; a.part = f.lnpart;
+  STEP("mlp_up_dx_ln2/mfma", launch_gemm(a, s));
+  STEP("reduce/hbm", launch_reduce_strided(tiles, E, 2 * E, f.lnpart, grads + o.g2, accumulate, s));
+  STEP("reduce/hbm", launch_reduce_strided(tiles, E, 2 * E, f.lnpart + E, grads + o.be2,
+                                           accumulate, s));
+  // item attention
+  T* doi = (T*)(ws + W.tc);
+  a = gemm_base(g, N, E, E, EPI_BIAS);
+  a.A = dz2; a.lda = E; a.Bt = f.wt + f.wo.o_i; a.out = doi; a.ldo = E;
+  STEP("item_out_dx/mfma", launch_gemm(a, s));
+  CHK(G.wgrad(dz2, E, (const T*)(sv + S.oi), E, o.Wo_i));
+  CHK(G.colsum(dz2, (const T*)nullptr, E, o.bo_i));
+  T* dq = (T*)(ws + W.tq);
+  T* dk = (T*)(ws + W.tk);
+  T* dv = (T*)(ws + W.tv);
+  STEP("item_attn_bwd/valu",
+       launch_item_attn_bwd_simple<T>(g, (const T*)(sv + S.qi), (const T*)(sv + S.ki),
+                                      (const T*)(sv + S.vi), (const T*)(sv + S.oi), doi,
+                                      (const float*)(sv + S.lsei), (float*)(ws + W.D), dq, dk,
+                                      dv, s));
+  STEP("item_dqkv_cells/hbm", launch_item_dqkv_to_cells<T>(g, dq, dk, dv, dqkv, s));
+  CHK(G.wgrad(dqkv, 3 * E, h1, E, o.Wqkv_i));
+  CHK(G.colsum(dqkv, (const T*)nullptr, 3 * E, o.bqkv_i));
+  // dZ1 = LN1'(dZ2 + dQKV_i Wqkv_i)
+  a = gemm_base(g, N, E, 3 * E, EPI_LN_BWD);
+  a.A = dqkv; a.lda = 3 * E; a.Bt = f.wt + f.wo.qkv_i; a.resid = dz2;
+  a.aux = (const T*)(sv + S.xh1); a.rstd_in = (const float*)(sv + S.rs1); a.gamma = prm + o.g1;
+  a.out = dz1; a.part = f.lnpart;
+  STEP("item_qkv_dx_ln1/mfma", launch_gemm(a, s));
+  STEP("reduce/hbm", launch_reduce_strided(tiles, E, 2 * E, f.lnpart, grads + o.g1, accumulate, s));
+  STEP("reduce/hbm", launch_reduce_strided(tiles, E, 2 * E, f.lnpart + E, grads + o.be1,
+                                           accumulate, s));
+  // feature attention
+  T* dof = (T*)(ws + W.tc);
+  a = gemm_base(g, N, E, E, EPI_BIAS);
+  a.A = dz1; a.lda = E; a.Bt = f.wt + f.wo.o_f; a.out = dof; a.ldo = E;
+  STEP("feat_out_dx/mfma", launch_gemm(a, s));
+  CHK(G.wgrad(dz1, E, (const T*)(sv + S.of), E, o.Wo_f));
+  CHK(G.colsum(dz1, (const T*)nullptr, E, o.bo_f));
+  STEP("feat_attn_bwd/valu",
+       launch_feat_attn_bwd_simple<T>(g, (const T*)(sv + S.qkvf), (const T*)(sv + S.of), dof,
+                                      (const float*)(sv + S.lsef), dqkv, s));
+  STEP("gather/hbm", launch_gather<T>(g, X, xc, s));
+  CHK(G.wgrad(dqkv, 3 * E, xc, E, o.Wqkv_f));
+  CHK(G.colsum(dqkv, (const T*)nullptr, 3 * E, o.bqkv_f));
+  // dX = dZ1 + dQKV_f Wqkv_f, native layout
+  a = gemm_base(g, N, E, 3 * E, EPI_DX);
+  a.A = dqkv; a.lda = 3 * E; a.Bt = f.wt + f.wo.qkv_f; a.resid = dz1; a.out = dX;
+  STEP("feat_qkv_dx/mfma", launch_gemm(a, s));
+  STEP("zero_inactive/hbm", launch_zero_inactive(g, dX, s));
+  return TFM_OK;
+}
+
 }  // namespace
 
 // ============================================================================ C ABI
@@ -443,6 +630,8 @@ int tfm_layer_fwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* c
   if (rc) return rc;
   if (d.dtype == TFM_F32)
     return fwd_simple<float>(d, g, (const float*)X, params, (float*)Y, sv, S, ws, W, s);
+  if (fast_eligible(d))
+    return fwd_fast(d, g, (const tfm::bf16*)X, params, (tfm::bf16*)Y, sv, S, ws, W, s);
   return fwd_simple<tfm::bf16>(d, g, (const tfm::bf16*)X, params, (tfm::bf16*)Y, sv, S, ws, W,
                                s);
 }
@@ -476,6 +665,9 @@ int tfm_layer_bwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* c
   if (d.dtype == TFM_F32)
     return bwd_simple<float>(d, g, (const float*)X, params, (const char*)saved, S,
                              (const float*)dY, (float*)dX, grads, accumulate, ws, W, s);
+  if (fast_eligible(d))
+    return bwd_fast(d, g, (const tfm::bf16*)X, params, (const char*)saved, S,
+                    (const tfm::bf16*)dY, (tfm::bf16*)dX, grads, accumulate, ws, W, s);
   return bwd_simple<tfm::bf16>(d, g, (const tfm::bf16*)X, params, (const char*)saved, S,
                                (const tfm::bf16*)dY, (tfm::bf16*)dX, grads, accumulate, ws, W,
                                s);
