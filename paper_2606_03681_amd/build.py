@@ -23,14 +23,22 @@ FLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
     # packed fp32 VALU forms are kept out of every kernel
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in ordinary VGPRs, so softmax/epilogue arithmetic needs no AGPR copies
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
     "-Wall", "-Wno-unused-function",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
 
 
+# attention kernels: no NaN reaches them (padding is never loaded), which lets max chains
+# lower to v_max3_f32 without canonicalising moves
+EXTRA = {"attn_item.hip": ["-fno-honor-nans"], "attn_item_bwd.hip": ["-fno-honor-nans"],
+         "attn_feat.hip": ["-fno-honor-nans"]}
+
+
 def _compile(src):
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC] + FLAGS + ["-c", src, "-o", obj]
+    cmd = [HIPCC] + FLAGS + EXTRA.get(os.path.basename(src), []) + ["-c", src, "-o", obj]
     if src.endswith(".hip"):
         cmd[1:1] = ["-x", "hip"]
     p = subprocess.run(cmd, capture_output=True, text=True)

@@ -1,0 +1,14 @@
+// MFMA attention kernels of the layer: launch interfaces.
+#pragma once
+
+#include "common.h"
+
+namespace tfm {
+
+// Item-axis attention forward.  q/k/v head-major [col][head][R][d] (k, v valid for train
+// rows), o cell-major [cell][E], lse [col][head][R] (natural log of the softmax denominator
+// including the 1/sqrt(d) scale).
+hipError_t launch_item_attn_fwd(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
+                                bf16* o, float* lse, hipStream_t s);
+
+}  // namespace tfm

@@ -1,0 +1,257 @@
+// Item-axis (down each column) flash attention on bf16 MFMA, forward pass.
+//
+// Problem (column g, head h): queries are all R rows of the column, keys and values are the
+// first n_train rows (the train prefix).  The prefix is a loop bound over key tiles — scores
+// are never materialised and the only masking is inside the last, partial key tile.
+//
+// One workgroup = 4 waves = 128 queries of one problem; each wave owns 32 queries (two 16-query
+// MFMA blocks).  Key tiles of 64 keys are staged in LDS (K as [key][d], V transposed as [d][key])
+// with double buffering and shared by the 4 waves.  Per tile a wave computes S^T = K Q^T
+// (keys x queries, so that a lane holds 4 keys of one query), the online softmax in the exp2
+// domain with the scale folded into one FMA, and O^T += V^T P^T where the D tile of S^T is
+// reused directly as the B operand (the k positions of V^T are permuted to match).
+//
+// Workgroups are numbered so that all query tiles of one problem land on the same XCD (the
+// hardware deals consecutive workgroup ids round-robin over the 8 XCDs), keeping the problem's
+// keys and values in that XCD's L2.
+#include <math.h>
+
+#include "attn.h"
+#include "mfma.h"
+
+namespace tfm {
+
+namespace {
+
+constexpr int KT = 64;   // keys per tile
+constexpr int QWV = 32;  // queries per wave
+constexpr int QWG = 128; // queries per workgroup
+constexpr float LOG2E = 1.4426950408889634f;
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+template <int D>
+struct QK;
+
+// S^T block = K (16 keys x 32 dims) * Q^T (32 dims x 16 queries)
+template <>
+struct QK<32> {
+  typedef bf16x8 frag;
+  static __device__ __forceinline__ frag load(const bf16* row, int lg) { return ld8(row + lg * 8); }
+  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, zero4(), 0, 0, 0);
+  }
+};
+
+// d = 16: v_mfma_f32_16x16x16_bf16, lane holds A[c][4g .. 4g+3]
+template <>
+struct QK<16> {
+  typedef s16x4 frag;
+  static __device__ __forceinline__ frag load(const bf16* row, int lg) {
+    return *reinterpret_cast<const s16x4*>(row + lg * 4);
+  }
+  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b) {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, zero4(), 0, 0, 0);
+  }
+};
+
+__device__ __forceinline__ uint32_t pk_bf16(float a, float b) { return pack2(a, b); }
+
+}  // namespace
+
+template <int D>
+__global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __restrict__ q,
+                                                       const bf16* __restrict__ k,
+                                                       const bf16* __restrict__ v,
+                                                       bf16* __restrict__ o,
+                                                       float* __restrict__ lse, int QT) {
+  constexpr int KS = D + 8;   // LDS row stride of K (elements)
+  constexpr int VS = KT + 8;  // LDS row stride of V^T
+  constexpr int DB = D / 16;  // 16-wide dim blocks
+  constexpr int CPR = D / 8;  // 16-byte chunks per key row
+  __shared__ __attribute__((aligned(16))) bf16 Ks[2][KT * KS];
+  __shared__ __attribute__((aligned(16))) bf16 Vt[2][D * VS];
+
+  const int bid = blockIdx.x;
+  const int64_t prob = (int64_t)((bid >> 3) / QT) * 8 + (bid & 7);
+  const int qt = (bid >> 3) % QT;
+  if (prob >= (int64_t)g.NC * g.heads) return;
+  const int64_t col = prob / g.heads;
+  const int head = (int)(prob - col * g.heads);
+  const int n = g.ds[g.col_ds[col]].n_train;
+  const int R = g.R;
+  const bf16* Qp = q + prob * R * D;
+  const bf16* Kp = k + prob * R * D;
+  const bf16* Vp = v + prob * R * D;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = lane & 15, lg = lane >> 4;
+  const int qw0 = qt * QWG + wave * QWV;
+
+  // Q^T fragments (B operand): lane holds query qw0 + qb*16 + c
+  typename QK<D>::frag qf[2];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    int qq = qw0 + qb * 16 + c;
+    if (qq < R) {
+      qf[qb] = QK<D>::load(Qp + (int64_t)qq * D, lg);
+    } else {
+      qf[qb] = typename QK<D>::frag{};
+    }
+  }
+
+  // staging: thread -> (key, 16-byte chunk of its dims)
+  const int skey = tid / CPR, sch = (tid % CPR) * 8;
+  const bool stager = tid < KT * CPR;
+  uint4 rk = make_uint4(0, 0, 0, 0), rv = make_uint4(0, 0, 0, 0);
+  auto gload = [&](int t0) {
+    int t = t0 + skey;
+    if (stager && t < n) {
+      rk = ldu4(Kp + (int64_t)t * D + sch);
+      rv = ldu4(Vp + (int64_t)t * D + sch);
+    } else {
+      rk = make_uint4(0, 0, 0, 0);
+      rv = make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto sstore = [&](int buf) {
+    if (!stager) return;
+    stu4(&Ks[buf][skey * KS + sch], rk);
+    const uint16_t* pv = reinterpret_cast<const uint16_t*>(&rv);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) Vt[buf][(sch + j) * VS + skey] = pv[j];
+  };
+
+  const float c2 = LOG2E / sqrtf((float)D);
+  // Running reference of the exponent, per query block, in raw-score units.  It is raised
+  // only when a tile's maximum exceeds it by more than 8 (log2 units), so the probabilities
+  // stay below 2^8 and the rescale of the accumulators is rare.
+  float m[2] = {-INFINITY, -INFINITY};
+  const float slack = 8.0f / c2;
+  // O^T accumulators: DB blocks of V^T rows plus one block whose first row is all ones, so
+  // that row accumulates the softmax denominator with the same rescaling as O.
+  f32x4 oacc[DB + 1][2];
+#pragma unroll
+  for (int db = 0; db <= DB; ++db)
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) oacc[db][qb] = zero4();
+  bf16x8 ones;
+  {
+    const uint32_t w = c == 0 ? 0x3f803f80u : 0u;  // bf16 1.0 pairs in row 0 only
+    uint4 u = make_uint4(w, w, w, w);
+    ones = *reinterpret_cast<bf16x8*>(&u);
+  }
+
+  auto tile = [&](const int cur, const int t0, const bool tail) {
+    // S^T = K Q^T for 4 key blocks x 2 query blocks
+    f32x4 sc[4][2];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      typename QK<D>::frag kf = QK<D>::load(&Ks[cur][(kb * 16 + c) * KS], lg);
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) sc[kb][qb] = QK<D>::mma(kf, qf[qb]);
+    }
+    if (tail) {
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (t0 + kb * 16 + lg * 4 + i >= n) {
+            sc[kb][0][i] = -INFINITY;
+            sc[kb][1][i] = -INFINITY;
+          }
+    }
+    bf16x8 pf[2][2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      float mx = fmaxf(fmaxf(sc[0][qb][0], sc[0][qb][1]), fmaxf(sc[0][qb][2], sc[0][qb][3]));
+#pragma unroll
+      for (int kb = 1; kb < 4; ++kb)
+        mx = fmaxf(mx, fmaxf(fmaxf(sc[kb][qb][0], sc[kb][qb][1]),
+                             fmaxf(sc[kb][qb][2], sc[kb][qb][3])));
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      if (__any(mx > m[qb] + slack)) {
+        const float mnew = fmaxf(m[qb], mx);
+        const float corr = exp2_hw((m[qb] - mnew) * c2);
+        m[qb] = mnew;
+#pragma unroll
+        for (int db = 0; db <= DB; ++db) oacc[db][qb] *= corr;
+      }
+      const float mb = -m[qb] * c2;
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        f32x4 a0 = sc[2 * ks][qb], a1 = sc[2 * ks + 1][qb];
+        uint4 u;
+        u.x = pk_bf16(exp2_hw(fmaf(a0[0], c2, mb)), exp2_hw(fmaf(a0[1], c2, mb)));
+        u.y = pk_bf16(exp2_hw(fmaf(a0[2], c2, mb)), exp2_hw(fmaf(a0[3], c2, mb)));
+        u.z = pk_bf16(exp2_hw(fmaf(a1[0], c2, mb)), exp2_hw(fmaf(a1[1], c2, mb)));
+        u.w = pk_bf16(exp2_hw(fmaf(a1[2], c2, mb)), exp2_hw(fmaf(a1[3], c2, mb)));
+        pf[qb][ks] = *reinterpret_cast<bf16x8*>(&u);
+      }
+    }
+    // O^T += V^T P^T (and the ones row += sum of P)
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const bf16* vr = &Vt[cur][(db * 16 + c) * VS + ks * 32 + lg * 4];
+        uint2 lo = *reinterpret_cast<const uint2*>(vr);
+        uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
+        uint4 u = make_uint4(lo.x, lo.y, hi.x, hi.y);
+        bf16x8 vf = *reinterpret_cast<bf16x8*>(&u);
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) oacc[db][qb] = mfma16(vf, pf[qb][ks], oacc[db][qb]);
+      }
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) oacc[DB][qb] = mfma16(ones, pf[qb][ks], oacc[DB][qb]);
+    }
+  };
+
+  const int NT = (n + KT - 1) / KT;
+  const int NF = n / KT;  // full tiles; a partial tail tile follows if NT > NF
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int it = 0; it < NF; ++it) {
+    const int cur = it & 1;
+    if (it + 1 < NT) gload((it + 1) * KT);
+    tile(cur, it * KT, false);
+    if (it + 1 < NT) sstore(cur ^ 1);
+    __syncthreads();
+  }
+  if (NF < NT) tile(NF & 1, NF * KT, true);
+
+  // normalise and write O (cell-major) and the natural-log LSE
+  const float tau = 1.0f / sqrtf((float)D);
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    const float lt = __shfl(oacc[DB][qb][0], c, 64);  // row 0 of the ones block, lane (0, c)
+    const int qq = qw0 + qb * 16 + c;
+    if (qq >= R) continue;
+    const float inv = 1.0f / lt;
+    bf16* orow = o + (col * R + qq) * (int64_t)g.E + head * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      uint2 u;
+      u.x = pk_bf16(oacc[db][qb][0] * inv, oacc[db][qb][1] * inv);
+      u.y = pk_bf16(oacc[db][qb][2] * inv, oacc[db][qb][3] * inv);
+      *reinterpret_cast<uint2*>(orow + db * 16 + lg * 4) = u;
+    }
+    if (lg == 0) lse[prob * R + qq] = m[qb] * tau + logf(lt);
+  }
+}
+
+hipError_t launch_item_attn_fwd(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
+                                bf16* o, float* lse, hipStream_t s) {
+  const int QT = (g.R + QWG - 1) / QWG;
+  const int64_t P = (int64_t)g.NC * g.heads;
+  const int64_t grid = (P + 7) / 8 * 8 * QT;
+  if (g.d == 16)
+    k_item_attn_fwd<16><<<(unsigned)grid, 256, 0, s>>>(g, q, k, v, o, lse, QT);
+  else
+    k_item_attn_fwd<32><<<(unsigned)grid, 256, 0, s>>>(g, q, k, v, o, lse, QT);
+  return hipGetLastError();
+}
+
+}  // namespace tfm

@@ -36,10 +36,22 @@ __device__ __forceinline__ void stu4(bf16* p, uint4 v) { *reinterpret_cast<uint4
 
 __device__ __forceinline__ float bf2f(uint16_t u) { return __uint_as_float(((uint32_t)u) << 16); }
 
-// Round-to-nearest-even pack of two floats into two bf16 (low half = a).
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Round-to-nearest-even pack of two floats into two bf16 (low half = a): v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
-  return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+  f32x2 v = {a, b};
+  bf16x2 r = __builtin_convertvector(v, bf16x2);
+  return *reinterpret_cast<uint32_t*>(&r);
 }
+
+// One bf16 from a float (round to nearest even) through the hardware convert.
+__device__ __forceinline__ uint16_t to_bf16(float a) { return (uint16_t)(pack2(a, 0.f) & 0xffffu); }
+
+// 2^x on the transcendental unit (v_exp_f32), without the library's range handling; the
+// callers pass arguments <= 0 whose results below the float range may flush to 0.
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __device__ __forceinline__ float wave_reduce_sum(float v) {
 #pragma unroll

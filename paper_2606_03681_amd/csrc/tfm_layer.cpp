@@ -11,6 +11,7 @@
 #include <vector>
 
 #include "kernels.h"
+#include "attn.h"
 #include "fast.h"
 #include "prof.h"
 
@@ -461,9 +462,9 @@ int fwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   a.A = h1; a.lda = E; a.Bt = f.w + f.wo.qkv_i; a.bias = prm + o.bqkv_i;
   a.out = (T*)(sv + S.qi); a.out2 = (T*)(sv + S.ki); a.out3 = (T*)(sv + S.vi);
   STEP("item_qkv/mfma", launch_gemm(a, s));
-  STEP("item_attn_fwd/valu", launch_item_attn_fwd_simple<T>(g, (T*)(sv + S.qi), (T*)(sv + S.ki),
-                                                            (T*)(sv + S.vi), oi,
-                                                            (float*)(sv + S.lsei), s));
+  STEP("item_attn_fwd/mfma", launch_item_attn_fwd(g, (T*)(sv + S.qi), (T*)(sv + S.ki),
+                                                   (T*)(sv + S.vi), oi, (float*)(sv + S.lsei),
+                                                   s));
   // H2 = LN2(H1 + O_i Wo_i^T + bo_i)
   a = gemm_base(g, N, E, E, EPI_LN);
   a.A = oi; a.lda = E; a.Bt = f.w + f.wo.o_i; a.bias = prm + o.bo_i;
