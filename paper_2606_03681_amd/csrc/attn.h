@@ -11,4 +11,9 @@ namespace tfm {
 hipError_t launch_item_attn_fwd(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
                                 bf16* o, float* lse, hipStream_t s);
 
+// Item-axis attention backward: dq, dk, dv head-major (dk, dv for train rows only).
+hipError_t launch_item_attn_bwd(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
+                                const bf16* o, const bf16* dout, const float* lse, bf16* dq,
+                                bf16* dk, bf16* dv, hipStream_t s);
+
 }  // namespace tfm

@@ -117,9 +117,8 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
   auto sstore = [&](int buf) {
     if (!stager) return;
     stu4(&Ks[buf][skey * KS + sch], rk);
-    const uint16_t* pv = reinterpret_cast<const uint16_t*>(&rv);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) Vt[buf][(sch + j) * VS + skey] = pv[j];
+    for (int j = 0; j < 8; ++j) Vt[buf][(sch + j) * VS + skey] = u4_elem(rv, j);
   };
 
   const float c2 = LOG2E / sqrtf((float)D);
@@ -212,13 +211,13 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
   const int NF = n / KT;  // full tiles; a partial tail tile follows if NT > NF
   gload(0);
   sstore(0);
-  __syncthreads();
+  lds_barrier();
   for (int it = 0; it < NF; ++it) {
     const int cur = it & 1;
     if (it + 1 < NT) gload((it + 1) * KT);
     tile(cur, it * KT, false);
     if (it + 1 < NT) sstore(cur ^ 1);
-    __syncthreads();
+    lds_barrier();
   }
   if (NF < NT) tile(NF & 1, NF * KT, true);
 

@@ -1,0 +1,411 @@
+// Item-axis flash attention on bf16 MFMA, backward pass, as two kernels that each recompute
+// the probabilities from the saved log-sum-exp:
+//
+//   dK/dV kernel (key-major): a workgroup owns 64 train rows (4 waves x 16 keys) of one problem
+//     and streams all query rows in chunks of 64 through LDS:
+//       S = Q K^T, dP = dO V^T            (D tiles: a lane holds 4 queries of one key)
+//       P = exp2(S tau log2e - lse log2e),  dS = P (dP - D),  D = rowsum(dO o O)
+//       dV^T += dO^T P,  dK^T += Q^T dS   (the S-layout tiles are used directly as B operands)
+//
+//   dQ kernel (query-major, shaped like the forward pass): a workgroup owns 128 query rows
+//     (4 waves x 32) and streams the train prefix in key tiles of 64 through LDS:
+//       S^T = K Q^T, dP^T = V dO^T        (a lane holds 4 keys of one query)
+//       dS^T = P^T (dP^T - D),  dQ^T += K^T dS^T
+//
+// Both accumulate in registers only, so each output element is summed in a fixed order
+// (bitwise reproducible), and neither needs more than ~40 KB of LDS, which keeps several
+// workgroups resident per CU.  Workgroups of one problem are numbered onto the same XCD.
+#include <math.h>
+
+#include "attn.h"
+#include "mfma.h"
+
+namespace tfm {
+
+namespace {
+
+constexpr float LOG2E = 1.4426950408889634f;
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// Products over the head dimension: A (16 rows x D) times B (D x 16 cols).
+template <int D>
+struct Dot;
+
+template <>
+struct Dot<32> {
+  typedef bf16x8 frag;
+  static constexpr int FB = 16;  // bytes of a fragment per lane
+  static __device__ __forceinline__ frag lds(const bf16* row, int lg) { return ld8(row + lg * 8); }
+  static __device__ __forceinline__ frag buf(rsrc_t r, uint32_t off) {
+    uint4 u = bload16(r, off);
+    return *reinterpret_cast<bf16x8*>(&u);
+  }
+  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, zero4(), 0, 0, 0);
+  }
+  // sum over the lane's 8 elements of a * b
+  static __device__ __forceinline__ float dot(const frag& a, const frag& b) {
+    const uint4 ua = *reinterpret_cast<const uint4*>(&a);
+    const uint4 ub = *reinterpret_cast<const uint4*>(&b);
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s = fmaf(bf2f(u4_elem(ua, j)), bf2f(u4_elem(ub, j)), s);
+    return s;
+  }
+};
+
+template <>
+struct Dot<16> {
+  typedef s16x4 frag;
+  static constexpr int FB = 8;
+  static __device__ __forceinline__ frag lds(const bf16* row, int lg) {
+    return *reinterpret_cast<const s16x4*>(row + lg * 4);
+  }
+  static __device__ __forceinline__ frag buf(rsrc_t r, uint32_t off) {
+    uint2 u = bload8(r, off);
+    return *reinterpret_cast<s16x4*>(&u);
+  }
+  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b) {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, zero4(), 0, 0, 0);
+  }
+  static __device__ __forceinline__ float dot(const frag& a, const frag& b) {
+    const uint2 ua = *reinterpret_cast<const uint2*>(&a);
+    const uint2 ub = *reinterpret_cast<const uint2*>(&b);
+    const uint4 wa = make_uint4(ua.x, ua.y, 0, 0), wb = make_uint4(ub.x, ub.y, 0, 0);
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) s = fmaf(bf2f(u4_elem(wa, j)), bf2f(u4_elem(wb, j)), s);
+    return s;
+  }
+};
+
+__device__ __forceinline__ bf16x8 cat8(uint2 lo, uint2 hi) {
+  uint4 u = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  return *reinterpret_cast<bf16x8*>(&u);
+}
+
+// 8 k positions from two 4-element runs 16 apart (the S / S^T tile permutation of k).
+__device__ __forceinline__ bf16x8 ld_perm(const bf16* p) {
+  return cat8(*reinterpret_cast<const uint2*>(p), *reinterpret_cast<const uint2*>(p + 16));
+}
+
+__device__ __forceinline__ bf16x8 pack8(const f32x4& a, const f32x4& b) {
+  uint4 u = make_uint4(pack2(a[0], a[1]), pack2(a[2], a[3]), pack2(b[0], b[1]),
+                       pack2(b[2], b[3]));
+  return *reinterpret_cast<bf16x8*>(&u);
+}
+
+}  // namespace
+
+// =============================================================================== dK / dV
+template <int D>
+__global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __restrict__ q,
+                                                        const bf16* __restrict__ k,
+                                                        const bf16* __restrict__ v,
+                                                        const bf16* __restrict__ o,
+                                                        const bf16* __restrict__ dout,
+                                                        const float* __restrict__ lse,
+                                                        bf16* __restrict__ dk,
+                                                        bf16* __restrict__ dv, int KT) {
+  constexpr int QC = 64;          // queries per chunk
+  constexpr int DB = D / 16;
+  constexpr int CPR = D / 8;      // 16-byte chunks per row of d values
+  constexpr int NIT = QC * CPR / 128;  // staging items per thread (128 threads per tensor)
+  constexpr int RS = D + 8;       // LDS row stride of row-major Q / dO (elements)
+  constexpr int TS = QC + 4;      // LDS row stride of Q^T / dO^T
+  __shared__ __attribute__((aligned(16))) bf16 Qs[2][QC * RS];
+  __shared__ __attribute__((aligned(16))) bf16 dOs[2][QC * RS];
+  __shared__ __attribute__((aligned(16))) bf16 QTs[2][D * TS];
+  __shared__ __attribute__((aligned(16))) bf16 dOTs[2][D * TS];
+  __shared__ __attribute__((aligned(16))) float Dq[2][QC];
+  __shared__ __attribute__((aligned(16))) float Lq[2][QC];
+
+  const int bid = blockIdx.x;
+  const int64_t prob = (int64_t)((bid >> 3) / KT) * 8 + (bid & 7);
+  const int kt = (bid >> 3) % KT;
+  if (prob >= (int64_t)g.NC * g.heads) return;
+  const int64_t col = prob / g.heads;
+  const int head = (int)(prob - col * g.heads);
+  const int n = g.ds[g.col_ds[col]].n_train;
+  const int t0 = kt * 64;
+  if (t0 >= n) return;
+  const int R = g.R, E = g.E;
+
+  const uint32_t rowQ = D * 2, rowO = (uint32_t)E * 2;
+  const rsrc_t rQ = make_rsrc(q + prob * R * D, (uint32_t)R * rowQ);
+  const rsrc_t rK = make_rsrc(k + prob * R * D, (uint32_t)n * rowQ);
+  const rsrc_t rV = make_rsrc(v + prob * R * D, (uint32_t)n * rowQ);
+  const uint32_t obytes = (uint32_t)(R - 1) * rowO + rowQ;
+  const rsrc_t rO = make_rsrc(o + col * R * (int64_t)E + head * D, obytes);
+  const rsrc_t rdO = make_rsrc(dout + col * R * (int64_t)E + head * D, obytes);
+  const rsrc_t rL = make_rsrc(lse + prob * R, (uint32_t)R * 4);
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int c = lane & 15, lg = lane >> 4;
+  const float c2 = LOG2E / sqrtf((float)D);
+  const float tau = 1.0f / sqrtf((float)D);
+
+  const int key = t0 + w * 16 + c;  // this lane's key column in the S layout
+  const typename Dot<D>::frag kf = Dot<D>::buf(rK, (uint32_t)key * rowQ + lg * Dot<D>::FB);
+  const typename Dot<D>::frag vf = Dot<D>::buf(rV, (uint32_t)key * rowQ + lg * Dot<D>::FB);
+
+  // staging: threads 0-127 move Q, threads 128-255 move dO (and O for D, and the LSE); each
+  // handles NIT (query, 16-byte chunk) items; item it -> query it / CPR, dims (it % CPR) * 8
+  const int half = tid >> 7, st = tid & 127;
+  uint4 ru[NIT], ro[NIT];
+  float rl[NIT];
+  auto gload = [&](int qc0) {
+#pragma unroll
+    for (int h = 0; h < NIT; ++h) {
+      const int it = st + h * 128;
+      const uint32_t qg = (uint32_t)(qc0 + it / CPR), d0 = (it % CPR) * 8;
+      if (half == 0) {
+        ru[h] = bload16(rQ, qg * rowQ + d0 * 2);
+      } else {
+        ru[h] = bload16(rdO, qg * rowO + d0 * 2);
+        ro[h] = bload16(rO, qg * rowO + d0 * 2);
+        rl[h] = bloadf(rL, qg * 4);
+      }
+    }
+  };
+  auto sstore = [&](int b) {
+#pragma unroll
+    for (int h = 0; h < NIT; ++h) {
+      const int it = st + h * 128;
+      const int qq = it / CPR, d0 = (it % CPR) * 8;
+      bf16* rm = half == 0 ? Qs[b] : dOs[b];
+      bf16* tr = half == 0 ? QTs[b] : dOTs[b];
+      stu4(&rm[qq * RS + d0], ru[h]);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) tr[(d0 + j) * TS + qq] = u4_elem(ru[h], j);
+      if (half == 1) {
+        float dot = 0.f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          dot = fmaf(bf2f(u4_elem(ru[h], j)), bf2f(u4_elem(ro[h], j)), dot);
+#pragma unroll
+        for (int off = 1; off < CPR; off <<= 1) dot += __shfl_xor(dot, off, 64);
+        if ((it % CPR) == 0) {
+          Dq[b][qq] = dot;
+          Lq[b][qq] = -rl[h] * LOG2E;  // queries past R read lse = 0: P = 1, but dO = 0
+        }
+      }
+    }
+  };
+
+  f32x4 dkt[DB], dvt[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) dkt[db] = dvt[db] = zero4();
+
+  // Keys past n have K = V = 0 here and their dK, dV are never written, so no key masking.
+  const int NCH = (R + QC - 1) / QC;
+  gload(0);
+  sstore(0);
+  lds_barrier();
+  for (int ic = 0; ic < NCH; ++ic) {
+    const int b = ic & 1;
+    if (ic + 1 < NCH) gload((ic + 1) * QC);
+    // S = Q K^T, dP = dO V^T for 4 query blocks (lane: queries qb*16 + 4*lg + i of `key`)
+    uint32_t pw[4][2], sw[4][2];
+#pragma unroll
+    for (int qb = 0; qb < 4; ++qb) {
+      const f32x4 s = Dot<D>::mma(Dot<D>::lds(&Qs[b][(qb * 16 + c) * RS], lg), kf);
+      const f32x4 dp = Dot<D>::mma(Dot<D>::lds(&dOs[b][(qb * 16 + c) * RS], lg), vf);
+      const float4 d4 = *reinterpret_cast<const float4*>(&Dq[b][qb * 16 + lg * 4]);
+      const float4 l4 = *reinterpret_cast<const float4*>(&Lq[b][qb * 16 + lg * 4]);
+      const float p0 = exp2_hw(fmaf(s[0], c2, l4.x)), p1 = exp2_hw(fmaf(s[1], c2, l4.y));
+      const float p2 = exp2_hw(fmaf(s[2], c2, l4.z)), p3 = exp2_hw(fmaf(s[3], c2, l4.w));
+      pw[qb][0] = pack2(p0, p1);
+      pw[qb][1] = pack2(p2, p3);
+      sw[qb][0] = pack2(p0 * (dp[0] - d4.x), p1 * (dp[1] - d4.y));
+      sw[qb][1] = pack2(p2 * (dp[2] - d4.z), p3 * (dp[3] - d4.w));
+    }
+    // dV^T += dO^T P, dK^T += Q^T dS over the chunk's 64 queries (two k steps of 32)
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const bf16x8 pf = cat8(make_uint2(pw[2 * ks][0], pw[2 * ks][1]),
+                             make_uint2(pw[2 * ks + 1][0], pw[2 * ks + 1][1]));
+      const bf16x8 sf = cat8(make_uint2(sw[2 * ks][0], sw[2 * ks][1]),
+                             make_uint2(sw[2 * ks + 1][0], sw[2 * ks + 1][1]));
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const int row = (db * 16 + c) * TS + ks * 32 + lg * 4;
+        dvt[db] = mfma16(ld_perm(&dOTs[b][row]), pf, dvt[db]);
+        dkt[db] = mfma16(ld_perm(&QTs[b][row]), sf, dkt[db]);
+      }
+    }
+    if (ic + 1 < NCH) sstore(b ^ 1);
+    lds_barrier();
+  }
+  // lane: dims db*16 + 4*lg + i of key `key`
+  if (key < n) {
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const uint2 a = make_uint2(pack2(dkt[db][0] * tau, dkt[db][1] * tau),
+                                 pack2(dkt[db][2] * tau, dkt[db][3] * tau));
+      const uint2 bb = make_uint2(pack2(dvt[db][0], dvt[db][1]), pack2(dvt[db][2], dvt[db][3]));
+      *reinterpret_cast<uint2*>(dk + (prob * R + key) * D + db * 16 + lg * 4) = a;
+      *reinterpret_cast<uint2*>(dv + (prob * R + key) * D + db * 16 + lg * 4) = bb;
+    }
+  }
+}
+
+// =============================================================================== dQ
+template <int D>
+__global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restrict__ q,
+                                                      const bf16* __restrict__ k,
+                                                      const bf16* __restrict__ v,
+                                                      const bf16* __restrict__ o,
+                                                      const bf16* __restrict__ dout,
+                                                      const float* __restrict__ lse,
+                                                      bf16* __restrict__ dq, int QT) {
+  constexpr int KTL = 64;         // keys per tile
+  constexpr int DB = D / 16;
+  constexpr int CPR = D / 8;
+  constexpr int KS = D + 8;       // LDS row stride of K, V ([key][d])
+  constexpr int TS = KTL + 8;     // LDS row stride of K^T ([d][key])
+  __shared__ __attribute__((aligned(16))) bf16 Ks[2][KTL * KS];
+  __shared__ __attribute__((aligned(16))) bf16 Vs[2][KTL * KS];
+  __shared__ __attribute__((aligned(16))) bf16 KTs[2][D * TS];
+
+  const int bid = blockIdx.x;
+  const int64_t prob = (int64_t)((bid >> 3) / QT) * 8 + (bid & 7);
+  const int qt = (bid >> 3) % QT;
+  if (prob >= (int64_t)g.NC * g.heads) return;
+  const int64_t col = prob / g.heads;
+  const int head = (int)(prob - col * g.heads);
+  const int n = g.ds[g.col_ds[col]].n_train;
+  const int R = g.R, E = g.E;
+
+  const uint32_t rowQ = D * 2, rowO = (uint32_t)E * 2;
+  const rsrc_t rQ = make_rsrc(q + prob * R * D, (uint32_t)R * rowQ);
+  const rsrc_t rK = make_rsrc(k + prob * R * D, (uint32_t)n * rowQ);
+  const rsrc_t rV = make_rsrc(v + prob * R * D, (uint32_t)n * rowQ);
+  const uint32_t obytes = (uint32_t)(R - 1) * rowO + rowQ;
+  const rsrc_t rO = make_rsrc(o + col * R * (int64_t)E + head * D, obytes);
+  const rsrc_t rdO = make_rsrc(dout + col * R * (int64_t)E + head * D, obytes);
+  const rsrc_t rL = make_rsrc(lse + prob * R, (uint32_t)R * 4);
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int c = lane & 15, lg = lane >> 4;
+  const int qw0 = qt * 128 + w * 32;
+  const float c2 = LOG2E / sqrtf((float)D);
+  const float tau = 1.0f / sqrtf((float)D);
+
+  // per query block: Q^T and dO^T fragments (B operands), D = rowsum(dO o O), -lse log2(e);
+  // queries past R read as zero (their results are not written)
+  typename Dot<D>::frag qf[2], df[2];
+  float Dv[2], nb[2];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    const uint32_t qq = (uint32_t)(qw0 + qb * 16 + c);
+    qf[qb] = Dot<D>::buf(rQ, qq * rowQ + lg * Dot<D>::FB);
+    df[qb] = Dot<D>::buf(rdO, qq * rowO + lg * Dot<D>::FB);
+    const typename Dot<D>::frag of = Dot<D>::buf(rO, qq * rowO + lg * Dot<D>::FB);
+    float dot = Dot<D>::dot(df[qb], of);
+    dot += __shfl_xor(dot, 16, 64);
+    dot += __shfl_xor(dot, 32, 64);
+    Dv[qb] = dot;
+    nb[qb] = -bloadf(rL, qq * 4) * LOG2E;
+  }
+
+  // key tile staging: thread -> (key, 16-byte chunk of its d values); keys past n read 0
+  const int skey = tid / CPR, sch = (tid % CPR) * 8;
+  const bool stager = tid < KTL * CPR;
+  uint4 rk = make_uint4(0, 0, 0, 0), rv = make_uint4(0, 0, 0, 0);
+  auto gload = [&](int t0) {
+    if (stager) {
+      rk = bload16(rK, (uint32_t)(t0 + skey) * rowQ + sch * 2);
+      rv = bload16(rV, (uint32_t)(t0 + skey) * rowQ + sch * 2);
+    }
+  };
+  auto sstore = [&](int b) {
+    if (!stager) return;
+    stu4(&Ks[b][skey * KS + sch], rk);
+    stu4(&Vs[b][skey * KS + sch], rv);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) KTs[b][(sch + j) * TS + skey] = u4_elem(rk, j);
+  };
+
+  f32x4 acc[DB][2];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) acc[db][0] = acc[db][1] = zero4();
+
+  auto tile = [&](const int b, const int t0, const bool tail) {
+    f32x4 dsv[4][2];
+#pragma unroll
+    for (int kb = 0; kb < 4; ++kb) {
+      const typename Dot<D>::frag kfr = Dot<D>::lds(&Ks[b][(kb * 16 + c) * KS], lg);
+      const typename Dot<D>::frag vfr = Dot<D>::lds(&Vs[b][(kb * 16 + c) * KS], lg);
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) {
+        const f32x4 s = Dot<D>::mma(kfr, qf[qb]);
+        const f32x4 dp = Dot<D>::mma(vfr, df[qb]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float p = exp2_hw(fmaf(s[i], c2, nb[qb]));
+          if (tail && t0 + kb * 16 + lg * 4 + i >= n) p = 0.f;
+          dsv[kb][qb][i] = p * (dp[i] - Dv[qb]);
+        }
+      }
+    }
+    // dQ^T += K^T dS^T  (k = keys, permuted to match the S^T layout)
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) {
+        const bf16x8 sf = pack8(dsv[2 * ks][qb], dsv[2 * ks + 1][qb]);
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          acc[db][qb] = mfma16(ld_perm(&KTs[b][(db * 16 + c) * TS + ks * 32 + lg * 4]), sf,
+                               acc[db][qb]);
+      }
+  };
+
+  const int NT = (n + KTL - 1) / KTL;
+  const int NF = n / KTL;
+  gload(0);
+  sstore(0);
+  lds_barrier();
+  for (int it = 0; it < NF; ++it) {
+    const int b = it & 1;
+    if (it + 1 < NT) gload((it + 1) * KTL);
+    tile(b, it * KTL, false);
+    if (it + 1 < NT) sstore(b ^ 1);
+    lds_barrier();
+  }
+  if (NF < NT) tile(NF & 1, NF * KTL, true);
+
+  // lane: dims db*16 + 4*lg + i of query qw0 + qb*16 + c
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    const int qq = qw0 + qb * 16 + c;
+    if (qq >= R) continue;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const uint2 u = make_uint2(pack2(acc[db][qb][0] * tau, acc[db][qb][1] * tau),
+                                 pack2(acc[db][qb][2] * tau, acc[db][qb][3] * tau));
+      *reinterpret_cast<uint2*>(dq + (prob * R + qq) * D + db * 16 + lg * 4) = u;
+    }
+  }
+}
+
+hipError_t launch_item_attn_bwd(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
+                                const bf16* o, const bf16* dout, const float* lse, bf16* dq,
+                                bf16* dk, bf16* dv, hipStream_t s) {
+  const int64_t P = (int64_t)g.NC * g.heads;
+  const int KT = (g.R + 63) / 64;
+  const int QT = (g.R + 127) / 128;
+  const unsigned grid_kv = (unsigned)((P + 7) / 8 * 8 * KT);
+  const unsigned grid_q = (unsigned)((P + 7) / 8 * 8 * QT);
+  if (g.d == 16) {
+    k_item_attn_dkdv<16><<<grid_kv, 256, 0, s>>>(g, q, k, v, o, dout, lse, dk, dv, KT);
+    k_item_attn_dq<16><<<grid_q, 256, 0, s>>>(g, q, k, v, o, dout, lse, dq, QT);
+  } else {
+    k_item_attn_dkdv<32><<<grid_kv, 256, 0, s>>>(g, q, k, v, o, dout, lse, dk, dv, KT);
+    k_item_attn_dq<32><<<grid_q, 256, 0, s>>>(g, q, k, v, o, dout, lse, dq, QT);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace tfm

@@ -53,6 +53,42 @@ __device__ __forceinline__ uint16_t to_bf16(float a) { return (uint16_t)(pack2(a
 // callers pass arguments <= 0 whose results below the float range may flush to 0.
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Buffer resources: 32-bit offsets from an SGPR descriptor; loads at offsets >= bytes return 0
+// (the hardware range check of raw buffers), which the kernels use for ragged tails.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+__device__ __forceinline__ uint4 bload16(rsrc_t r, uint32_t off) {
+  u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ uint2 bload8(rsrc_t r, uint32_t off) {
+  u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+  return make_uint2(v.x, v.y);
+}
+__device__ __forceinline__ float bloadf(rsrc_t r, uint32_t off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+
+// Workgroup barrier that waits only for this wave's LDS traffic (lgkmcnt), not for global
+// loads still in flight, so that prefetches issued before it keep overlapping compute.
+// The memory clobber keeps the compiler from moving memory accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Element j (0..7) of 8 bf16 values held in a uint4, as raw bits (j must be a constant after
+// unrolling; no memory round trip).
+__device__ __forceinline__ uint16_t u4_elem(const uint4& u, int j) {
+  const uint32_t w = j < 2 ? u.x : (j < 4 ? u.y : (j < 6 ? u.z : u.w));
+  return (uint16_t)((j & 1) ? (w >> 16) : (w & 0xffffu));
+}
+
 __device__ __forceinline__ float wave_reduce_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

@@ -541,11 +541,10 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   T* dq = (T*)(ws + W.tq);
   T* dk = (T*)(ws + W.tk);
   T* dv = (T*)(ws + W.tv);
-  STEP("item_attn_bwd/valu",
-       launch_item_attn_bwd_simple<T>(g, (const T*)(sv + S.qi), (const T*)(sv + S.ki),
-                                      (const T*)(sv + S.vi), (const T*)(sv + S.oi), doi,
-                                      (const float*)(sv + S.lsei), (float*)(ws + W.D), dq, dk,
-                                      dv, s));
+  STEP("item_attn_bwd/mfma",
+       launch_item_attn_bwd(g, (const T*)(sv + S.qi), (const T*)(sv + S.ki),
+                            (const T*)(sv + S.vi), (const T*)(sv + S.oi), doi,
+                            (const float*)(sv + S.lsei), dq, dk, dv, s));
   STEP("item_dqkv_cells/hbm", launch_item_dqkv_to_cells<T>(g, dq, dk, dv, dqkv, s));
   CHK(G.wgrad(dqkv, 3 * E, h1, E, o.Wqkv_i));
   CHK(G.colsum(dqkv, (const T*)nullptr, 3 * E, o.bqkv_i));
