@@ -66,6 +66,35 @@ hipError_t launch_reduce_strided(int Z, int64_t count, int64_t stride, const flo
 // Writes 0 to every element of the native tensor that lies in an inactive cell.
 hipError_t launch_zero_inactive(const Geo& g, bf16* native, hipStream_t s);
 
+// Weight gradient dW[n][k] = sum_m dY[m][n] X[m][k] (+ db[n] = sum_m dY[m][n]) over M cells,
+// split into chunks of WGRAD_CHUNK cells; partials land in part [Z][N][K] and bpart [Z][N].
+constexpr int WGRAD_CHUNK = 4096;
+struct WgradArgs {
+  int64_t M;
+  int N, K;
+  const bf16* dY;  // compact rows, leading dimension ldy
+  int64_t ldy;
+  const bf16* X;   // rows per xmode (compact with ldx, or the native cell tensor)
+  int64_t ldx;
+  int xmode;
+  float* part;
+  float* bpart;    // may be null: no bias gradient
+  int64_t chunk;
+  Geo g;
+};
+int wgrad_chunks(int64_t M);
+hipError_t launch_wgrad_mfma(const WgradArgs& a, hipStream_t s);
+// out[i] = (accumulate ? out[i] : 0) + sum_z part[z * stride + i], fixed summation order
+hipError_t launch_reduce_z(int Z, int64_t count, int64_t stride, const float* part, float* out,
+                           int accumulate, hipStream_t s);
+
+// Backward of the last LayerNorm from the native upstream gradient: dz = LN3'(dY) at active
+// cells (compact), plus per-block partial column sums of dY * xhat and dY into
+// part [blocks][2][E].  Returns the number of blocks through *nblocks.
+hipError_t launch_ln_out_bwd(const Geo& g, const bf16* dY, const bf16* xhat, const float* rstd,
+                             const float* gamma, bf16* dz, float* part, int* nblocks,
+                             hipStream_t s);
+
 // Scratch bytes that the MFMA path needs inside the workspace.
 size_t fast_workspace_bytes(int B, int R, int S, int E, int heads, int H, bool bf16);
 

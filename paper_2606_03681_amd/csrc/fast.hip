@@ -1,5 +1,6 @@
 // Small kernels of the MFMA path: weight casts, strided reductions, zero fill.
 #include "fast.h"
+#include "mfma.h"
 
 namespace tfm {
 
@@ -84,6 +85,80 @@ hipError_t launch_zero_inactive(const Geo& g, bf16* native, hipStream_t s) {
   return hipGetLastError();
 }
 
+// One wave per cell, 8 waves per block, LN_CELLS cells per block; each lane holds up to 4 of
+// the E <= 256 values of a cell and keeps running column sums across the block's cells.
+constexpr int LN_CELLS = 256;
+
+__global__ __launch_bounds__(512) void k_ln_out_bwd(Geo g, const bf16* __restrict__ dY,
+                                                    const bf16* __restrict__ xhat,
+                                                    const float* __restrict__ rstd,
+                                                    const float* __restrict__ gamma,
+                                                    bf16* __restrict__ dz,
+                                                    float* __restrict__ part) {
+  __shared__ float red[8][2][256];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int E = g.E;
+  float cs1[4] = {0.f, 0.f, 0.f, 0.f}, cs2[4] = {0.f, 0.f, 0.f, 0.f};
+  float gm[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) gm[i] = lane + 64 * i < E ? gamma[lane + 64 * i] : 0.f;
+  const int64_t c0 = (int64_t)blockIdx.x * LN_CELLS;
+  for (int cc = w; cc < LN_CELLS; cc += 8) {
+    const int64_t p = c0 + cc;
+    if (p >= g.N) break;
+    const int64_t src = native_cell(g, p) * E;
+    float dy[4], xv[4];
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = lane + 64 * i;
+      dy[i] = 0.f;
+      xv[i] = 0.f;
+      if (e < E) {
+        dy[i] = bf2f(dY[src + e]);
+        xv[i] = bf2f(xhat[p * E + e]);
+        cs1[i] += dy[i] * xv[i];
+        cs2[i] += dy[i];
+        s1 += dy[i] * gm[i];
+        s2 += dy[i] * gm[i] * xv[i];
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      s1 += __shfl_xor(s1, o, 64);
+      s2 += __shfl_xor(s2, o, 64);
+    }
+    const float m1 = s1 / E, m2 = s2 / E, rs = rstd[p];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int e = lane + 64 * i;
+      if (e < E) dz[p * E + e] = f2bf(rs * (dy[i] * gm[i] - m1 - xv[i] * m2));
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    red[w][0][lane + 64 * i] = cs1[i];
+    red[w][1][lane + 64 * i] = cs2[i];
+  }
+  __syncthreads();
+  if (threadIdx.x < 2 * E) {
+    const int t = threadIdx.x / E, e = threadIdx.x % E;
+    float s = 0.f;
+#pragma unroll
+    for (int ww = 0; ww < 8; ++ww) s += red[ww][t][e];
+    part[(int64_t)blockIdx.x * 2 * E + t * E + e] = s;
+  }
+}
+
+hipError_t launch_ln_out_bwd(const Geo& g, const bf16* dY, const bf16* xhat, const float* rstd,
+                             const float* gamma, bf16* dz, float* part, int* nblocks,
+                             hipStream_t s) {
+  const int64_t nb = (g.N + LN_CELLS - 1) / LN_CELLS;
+  *nblocks = (int)nb;
+  k_ln_out_bwd<<<(unsigned)nb, 512, 0, s>>>(g, dY, xhat, rstd, gamma, dz, part);
+  return hipGetLastError();
+}
+
 size_t fast_workspace_bytes(int B, int R, int S, int E, int heads, int H, bool bf16) {
   (void)heads;
   if (!bf16) return 0;
@@ -91,6 +166,12 @@ size_t fast_workspace_bytes(int B, int R, int S, int E, int heads, int H, bool b
   int64_t tiles = ((int64_t)B * R * S + 127) / 128;
   size_t bytes = 2 * (size_t)wo.total * 2 + 1024;   // w and wt
   bytes += (size_t)tiles * 2 * E * 4 + 256;         // LN-backward column partials
+  const int64_t cells = (int64_t)B * R * S;
+  const int64_t zw = (cells + WGRAD_CHUNK - 1) / WGRAD_CHUNK;
+  const int64_t maxw = 3LL * E * E > (int64_t)H * E ? 3LL * E * E : (int64_t)H * E;
+  const int64_t maxn = 3LL * E > H ? 3LL * E : H;
+  bytes += (size_t)zw * maxw * 4 + 256;                // weight-gradient partials
+  bytes += (size_t)zw * maxn * 4 + 256;                // bias-gradient partials
   return bytes;
 }
 

@@ -404,6 +404,8 @@ struct FastWs {
   tfm::bf16* w;
   tfm::bf16* wt;
   float* lnpart;
+  float* wpart;
+  float* bpart;
   tfm::WOff wo;
 };
 
@@ -416,6 +418,12 @@ FastWs fast_ws(const Dims& d, char* ws, const WsLayout& W) {
   f.wt = (tfm::bf16*)p;
   p += align_up((size_t)f.wo.total * 2);
   f.lnpart = (float*)p;
+  p += align_up((size_t)((d.Nmax + 127) / 128) * 2 * d.E * 4 + 256);
+  const int64_t zw = (d.Nmax + tfm::WGRAD_CHUNK - 1) / tfm::WGRAD_CHUNK;
+  const int64_t maxw = 3LL * d.E * d.E > (int64_t)d.H * d.E ? 3LL * d.E * d.E : (int64_t)d.H * d.E;
+  f.wpart = (float*)p;
+  p += align_up((size_t)zw * maxw * 4 + 256);
+  f.bpart = (float*)p;
   return f;
 }
 
@@ -486,6 +494,27 @@ int fwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   return TFM_OK;
 }
 
+// Weight and bias gradients of one linear on the MFMA path (split over cells, fixed-order sums).
+struct FastGrads {
+  const FastWs& f;
+  const tfm::Geo& g;
+  float* grads;
+  int accumulate;
+  hipStream_t s;
+  int run(const tfm::bf16* dY, int N, const tfm::bf16* X, int K, int xmode, size_t offW,
+          size_t offb) {
+    tfm::WgradArgs a{};
+    a.M = g.N; a.N = N; a.K = K; a.dY = dY; a.ldy = N; a.X = X; a.ldx = K; a.xmode = xmode;
+    a.part = f.wpart; a.bpart = f.bpart; a.g = g;
+    const int Z = tfm::wgrad_chunks(g.N);
+    STEP("wgrad/mfma", tfm::launch_wgrad_mfma(a, s));
+    STEP("reduce/hbm", tfm::launch_reduce_z(Z, (int64_t)N * K, (int64_t)N * K, f.wpart,
+                                            grads + offW, accumulate, s));
+    STEP("reduce/hbm", tfm::launch_reduce_z(Z, N, N, f.bpart, grads + offb, accumulate, s));
+    return TFM_OK;
+  }
+};
+
 int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* prm,
              const char* sv, const SavedLayout& S, const tfm::bf16* dY, tfm::bf16* dX,
              float* grads, int accumulate, char* ws, const WsLayout& W, hipStream_t s) {
@@ -496,10 +525,8 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   const int E = d.E, H = d.H;
   const int64_t N = g.N;
   const int tiles = (int)((N + 127) / 128);
-  GradSink<T> G{W, ws, grads, accumulate, N, s};
+  FastGrads G{f, g, grads, accumulate, s};
   STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, s));
-  T* xc = (T*)(ws + W.xc);
-  T* dyc = (T*)(ws + W.ta);
   T* dz3 = (T*)(ws + W.tb);
   T* dz2 = (T*)(ws + W.te);
   T* dz1 = (T*)(ws + W.tf);
@@ -507,37 +534,32 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   T* dqkv = (T*)(ws + W.tqkv);
   const T* h1 = (const T*)(sv + S.h1);
   const T* h2 = (const T*)(sv + S.h2);
-  // LN3
-  STEP("gather/hbm", launch_gather<T>(g, dY, dyc, s));
-  STEP("ln3_bwd/hbm", launch_ln_bwd<T>(N, E, dyc, (const T*)nullptr, (const T*)(sv + S.xh3),
-                                       (const float*)(sv + S.rs3), prm + o.g3, dz3, (T*)nullptr,
-                                       s));
-  CHK(G.colsum(dyc, (const T*)(sv + S.xh3), E, o.g3));
-  CHK(G.colsum(dyc, (const T*)nullptr, E, o.be3));
+  // LN3 (from the native dY), with its gamma/beta column sums
+  int nb = 0;
+  STEP("ln3_bwd/hbm", launch_ln_out_bwd(g, dY, (const T*)(sv + S.xh3), (const float*)(sv + S.rs3),
+                                        prm + o.g3, dz3, f.lnpart, &nb, s));
+  STEP("reduce/hbm", launch_reduce_z(nb, E, 2 * E, f.lnpart, grads + o.g3, accumulate, s));
+  STEP("reduce/hbm", launch_reduce_z(nb, E, 2 * E, f.lnpart + E, grads + o.be3, accumulate, s));
   // MLP: dG = (dZ3 W2) * GELU'(G)
   GemmArgs a = gemm_base(g, N, H, E, EPI_GELU_BWD);
   a.A = dz3; a.lda = E; a.Bt = f.wt + f.wo.w2; a.out = dgb; a.ldo = H;
   a.aux = (const T*)(sv + S.g);
   STEP("mlp_down_dx/mfma", launch_gemm(a, s));
-  CHK(G.wgrad(dz3, E, (const T*)(sv + S.u), H, o.W2));
-  CHK(G.colsum(dz3, (const T*)nullptr, E, o.b2));
-  CHK(G.wgrad(dgb, H, h2, E, o.W1));
-  CHK(G.colsum(dgb, (const T*)nullptr, H, o.b1));
+  CHK(G.run(dz3, E, (const T*)(sv + S.u), H, ROWS_COMPACT, o.W2, o.b2));
+  CHK(G.run(dgb, H, h2, E, ROWS_COMPACT, o.W1, o.b1));
   // dZ2 = LN2'(dZ3 + dG W1)
   a = gemm_base(g, N, E, H, EPI_LN_BWD);
   a.A = dgb; a.lda = H; a.Bt = f.wt + f.wo.w1; a.resid = dz3; a.aux = (const T*)(sv + S.xh2);
   a.rstd_in = (const float*)(sv + S.rs2); a.gamma = prm + o.g2; a.out = dz2; a.part = f.lnpart;
   STEP("mlp_up_dx_ln2/mfma", launch_gemm(a, s));
-  STEP("reduce/hbm", launch_reduce_strided(tiles, E, 2 * E, f.lnpart, grads + o.g2, accumulate, s));
-  STEP("reduce/hbm", launch_reduce_strided(tiles, E, 2 * E, f.lnpart + E, grads + o.be2,
-                                           accumulate, s));
+  STEP("reduce/hbm", launch_reduce_z(tiles, E, 2 * E, f.lnpart, grads + o.g2, accumulate, s));
+  STEP("reduce/hbm", launch_reduce_z(tiles, E, 2 * E, f.lnpart + E, grads + o.be2, accumulate, s));
   // item attention
   T* doi = (T*)(ws + W.tc);
   a = gemm_base(g, N, E, E, EPI_BIAS);
   a.A = dz2; a.lda = E; a.Bt = f.wt + f.wo.o_i; a.out = doi; a.ldo = E;
   STEP("item_out_dx/mfma", launch_gemm(a, s));
-  CHK(G.wgrad(dz2, E, (const T*)(sv + S.oi), E, o.Wo_i));
-  CHK(G.colsum(dz2, (const T*)nullptr, E, o.bo_i));
+  CHK(G.run(dz2, E, (const T*)(sv + S.oi), E, ROWS_COMPACT, o.Wo_i, o.bo_i));
   T* dq = (T*)(ws + W.tq);
   T* dk = (T*)(ws + W.tk);
   T* dv = (T*)(ws + W.tv);
@@ -546,30 +568,25 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
                             (const T*)(sv + S.vi), (const T*)(sv + S.oi), doi,
                             (const float*)(sv + S.lsei), dq, dk, dv, s));
   STEP("item_dqkv_cells/hbm", launch_item_dqkv_to_cells<T>(g, dq, dk, dv, dqkv, s));
-  CHK(G.wgrad(dqkv, 3 * E, h1, E, o.Wqkv_i));
-  CHK(G.colsum(dqkv, (const T*)nullptr, 3 * E, o.bqkv_i));
+  CHK(G.run(dqkv, 3 * E, h1, E, ROWS_COMPACT, o.Wqkv_i, o.bqkv_i));
   // dZ1 = LN1'(dZ2 + dQKV_i Wqkv_i)
   a = gemm_base(g, N, E, 3 * E, EPI_LN_BWD);
   a.A = dqkv; a.lda = 3 * E; a.Bt = f.wt + f.wo.qkv_i; a.resid = dz2;
   a.aux = (const T*)(sv + S.xh1); a.rstd_in = (const float*)(sv + S.rs1); a.gamma = prm + o.g1;
   a.out = dz1; a.part = f.lnpart;
   STEP("item_qkv_dx_ln1/mfma", launch_gemm(a, s));
-  STEP("reduce/hbm", launch_reduce_strided(tiles, E, 2 * E, f.lnpart, grads + o.g1, accumulate, s));
-  STEP("reduce/hbm", launch_reduce_strided(tiles, E, 2 * E, f.lnpart + E, grads + o.be1,
-                                           accumulate, s));
+  STEP("reduce/hbm", launch_reduce_z(tiles, E, 2 * E, f.lnpart, grads + o.g1, accumulate, s));
+  STEP("reduce/hbm", launch_reduce_z(tiles, E, 2 * E, f.lnpart + E, grads + o.be1, accumulate, s));
   // feature attention
   T* dof = (T*)(ws + W.tc);
   a = gemm_base(g, N, E, E, EPI_BIAS);
   a.A = dz1; a.lda = E; a.Bt = f.wt + f.wo.o_f; a.out = dof; a.ldo = E;
   STEP("feat_out_dx/mfma", launch_gemm(a, s));
-  CHK(G.wgrad(dz1, E, (const T*)(sv + S.of), E, o.Wo_f));
-  CHK(G.colsum(dz1, (const T*)nullptr, E, o.bo_f));
+  CHK(G.run(dz1, E, (const T*)(sv + S.of), E, ROWS_COMPACT, o.Wo_f, o.bo_f));
   STEP("feat_attn_bwd/valu",
        launch_feat_attn_bwd_simple<T>(g, (const T*)(sv + S.qkvf), (const T*)(sv + S.of), dof,
                                       (const float*)(sv + S.lsef), dqkv, s));
-  STEP("gather/hbm", launch_gather<T>(g, X, xc, s));
-  CHK(G.wgrad(dqkv, 3 * E, xc, E, o.Wqkv_f));
-  CHK(G.colsum(dqkv, (const T*)nullptr, 3 * E, o.bqkv_f));
+  CHK(G.run(dqkv, 3 * E, X, E, ROWS_NATIVE, o.Wqkv_f, o.bqkv_f));
   // dX = dZ1 + dQKV_f Wqkv_f, native layout
   a = gemm_base(g, N, E, 3 * E, EPI_DX);
   a.A = dqkv; a.lda = 3 * E; a.Bt = f.wt + f.wo.qkv_f; a.resid = dz1; a.out = dX;

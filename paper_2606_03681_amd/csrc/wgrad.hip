@@ -1,0 +1,203 @@
+// Weight gradients on bf16 MFMA: dW[n][k] = sum over active cells m of dY[m][n] X[m][k], with
+// the bias gradient db[n] = sum_m dY[m][n] formed from the same staged tiles.
+//
+// The reduction runs over the cells (1.6 M at eval scale) while the output is one E x E tile
+// of the weight, so the cells are split into chunks (split-K): workgroup (n-tile, k-tile, z)
+// sums chunk z into a float32 partial, and a second kernel adds the partials in a fixed order
+// (bitwise reproducible).  The MFMA contraction index is the cell, which is the slow index in
+// memory for both operands, so 32-cell slices of dY and X are staged transposed in LDS
+// ([n][cell] and [k][cell]); consecutive lanes take consecutive cells so that the transposed
+// 16-bit writes of a wave fall on distinct banks.
+#include "fast.h"
+#include "mfma.h"
+
+namespace tfm {
+
+namespace {
+constexpr int MS = 32;       // cells per MFMA step
+constexpr int LS = MS + 8;   // LDS row stride (elements)
+}  // namespace
+
+// 512 threads = 8 waves in a 2 (n) x 4 (k) arrangement; tile BT x BT with BT = E.
+template <int BT>
+__global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
+  constexpr int NBW = BT / 32;   // 16-row blocks per wave along n (BT/2 rows)
+  constexpr int KBW = BT / 64;   // 16-col blocks per wave along k (BT/4 cols)
+  constexpr int CH = 4 * BT;     // 16-byte chunks per operand slice (MS x BT)
+  constexpr int CPT = CH / 256;  // chunks per staging thread (256 threads per operand)
+  __shared__ __attribute__((aligned(16))) bf16 As[2][BT * LS];
+  __shared__ __attribute__((aligned(16))) bf16 Bs[2][BT * LS];
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int c = lane & 15, lg = lane >> 4;
+  const int wn = w >> 2, wk = w & 3;
+  const int n0 = blockIdx.x * BT, k0 = blockIdx.y * BT;
+  const int64_t mb = (int64_t)blockIdx.z * a.chunk;
+  const int64_t me = mb + a.chunk < a.M ? mb + a.chunk : a.M;
+  const Geo& g = a.g;
+
+  // staging: threads 0-255 stage dY columns [n0, n0+BT), threads 256-511 stage X columns
+  // [k0, k0+BT); chunk ch -> cell offset ch % 32, column block (ch / 32) * 8
+  const int op = tid >> 8, st = tid & 255;
+  const bf16* src = op == 0 ? a.dY : a.X;
+  const int64_t ld = op == 0 ? a.ldy : a.ldx;
+  const int mode = op == 0 ? ROWS_COMPACT : a.xmode;
+  const int cb = op == 0 ? n0 : k0;
+  bf16* dst0 = op == 0 ? As[0] : Bs[0];
+  bf16* dst1 = op == 0 ? As[1] : Bs[1];
+  const bool bsum = op == 0 && a.bpart && blockIdx.y == 0;
+  float csum[CPT][8];
+#pragma unroll
+  for (int i = 0; i < CPT; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) csum[i][j] = 0.f;
+
+  uint4 r[CPT];
+  auto gload = [&](int64_t m0) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int ch = st + 256 * i;
+      const int64_t m = m0 + (ch & 31);
+      const int col = cb + (ch >> 5) * 8;
+      r[i] = make_uint4(0, 0, 0, 0);
+      if (m < me) {
+        const int64_t base = mode == ROWS_NATIVE ? native_cell(g, m) * g.E : m * ld;
+        r[i] = ldu4(src + base + col);
+      }
+    }
+  };
+  auto sstore = [&](int b) {
+    bf16* d = b ? dst1 : dst0;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int ch = st + 256 * i;
+      const int mm = ch & 31, cc = (ch >> 5) * 8;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) d[(cc + j) * LS + mm] = u4_elem(r[i], j);
+      if (bsum) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) csum[i][j] += bf2f(u4_elem(r[i], j));
+      }
+    }
+  };
+
+  f32x4 acc[NBW][KBW];
+#pragma unroll
+  for (int i = 0; i < NBW; ++i)
+#pragma unroll
+    for (int j = 0; j < KBW; ++j) acc[i][j] = zero4();
+
+  const int64_t steps = (me - mb + MS - 1) / MS;
+  if (steps > 0) {
+    gload(mb);
+    sstore(0);
+  }
+  lds_barrier();
+  for (int64_t s = 0; s < steps; ++s) {
+    const int b = (int)(s & 1);
+    if (s + 1 < steps) gload(mb + (s + 1) * MS);
+    const bf16* A = b ? As[1] : As[0];
+    const bf16* B = b ? Bs[1] : Bs[0];
+    bf16x8 af[NBW], bfr[KBW];
+#pragma unroll
+    for (int i = 0; i < NBW; ++i) af[i] = ld8(&A[(wn * (BT / 2) + i * 16 + c) * LS + lg * 8]);
+#pragma unroll
+    for (int j = 0; j < KBW; ++j) bfr[j] = ld8(&B[(wk * (BT / 4) + j * 16 + c) * LS + lg * 8]);
+#pragma unroll
+    for (int i = 0; i < NBW; ++i)
+#pragma unroll
+      for (int j = 0; j < KBW; ++j) acc[i][j] = mfma16(af[i], bfr[j], acc[i][j]);
+    if (s + 1 < steps) sstore(b ^ 1);
+    lds_barrier();
+  }
+
+  // partial tile: lane holds rows n = wn*BT/2 + i*16 + 4*lg + q, column k = wk*BT/4 + j*16 + c
+  float* out = a.part + (int64_t)blockIdx.z * a.N * a.K;
+#pragma unroll
+  for (int i = 0; i < NBW; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int n = n0 + wn * (BT / 2) + i * 16 + lg * 4 + q;
+#pragma unroll
+      for (int j = 0; j < KBW; ++j) out[(int64_t)n * a.K + k0 + wk * (BT / 4) + j * 16 + c] = acc[i][j][q];
+    }
+  if (bsum) {
+    // the 32 lanes of a half-wave share a column block; sum over them in a fixed pattern
+#pragma unroll
+    for (int i = 0; i < CPT; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        float v = csum[i][j];
+#pragma unroll
+        for (int off = 1; off < 32; off <<= 1) v += __shfl_xor(v, off, 64);
+        csum[i][j] = v;
+      }
+    if ((st & 31) == 0) {
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) {
+        const int ch = st + 256 * i;
+        float* bp = a.bpart + (int64_t)blockIdx.z * a.N + n0 + (ch >> 5) * 8;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) bp[j] = csum[i][j];
+      }
+    }
+  }
+}
+
+// out[i] = (accumulate ? out[i] : 0) + sum_z part[z * stride + i]; four interleaved z groups
+// per output summed in a fixed order, then combined in order.
+__global__ __launch_bounds__(256) void k_reduce_z(int Z, int64_t count, int64_t stride,
+                                                  const float* __restrict__ part,
+                                                  float* __restrict__ out, int accumulate) {
+  __shared__ float red[4][64];
+  const int o = threadIdx.x & 63, gz = threadIdx.x >> 6;
+  const int64_t i = (int64_t)blockIdx.x * 64 + o;
+  float s = 0.f;
+  if (i < count) {
+    float s0 = 0.f, s1 = 0.f;
+    int z = gz;
+    for (; z + 4 < Z; z += 8) {
+      s0 += part[(int64_t)z * stride + i];
+      s1 += part[(int64_t)(z + 4) * stride + i];
+    }
+    if (z < Z) s0 += part[(int64_t)z * stride + i];
+    s = s0 + s1;
+  }
+  red[gz][o] = s;
+  __syncthreads();
+  if (gz == 0 && i < count) {
+    const float t = ((red[0][o] + red[1][o]) + red[2][o]) + red[3][o];
+    out[i] = (accumulate ? out[i] : 0.f) + t;
+  }
+}
+
+int wgrad_chunks(int64_t M) {
+  int64_t z = (M + WGRAD_CHUNK - 1) / WGRAD_CHUNK;
+  return (int)(z < 1 ? 1 : z);
+}
+
+hipError_t launch_wgrad_mfma(const WgradArgs& a, hipStream_t s) {
+  const int Z = wgrad_chunks(a.M);
+  const int BT = a.g.E;
+  if (a.N % BT || a.K % BT) return hipErrorInvalidValue;
+  dim3 grid((unsigned)(a.N / BT), (unsigned)(a.K / BT), (unsigned)Z);
+  WgradArgs b = a;
+  b.chunk = WGRAD_CHUNK;
+  switch (BT) {
+    case 64: k_wgrad<64><<<grid, 512, 0, s>>>(b); break;
+    case 128: k_wgrad<128><<<grid, 512, 0, s>>>(b); break;
+    case 192: k_wgrad<192><<<grid, 512, 0, s>>>(b); break;
+    case 256: k_wgrad<256><<<grid, 512, 0, s>>>(b); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_z(int Z, int64_t count, int64_t stride, const float* part, float* out,
+                           int accumulate, hipStream_t s) {
+  k_reduce_z<<<(unsigned)((count + 63) / 64), 256, 0, s>>>(Z, count, stride, part, out,
+                                                          accumulate);
+  return hipGetLastError();
+}
+
+}  // namespace tfm
