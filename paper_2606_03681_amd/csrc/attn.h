@@ -16,4 +16,13 @@ hipError_t launch_item_attn_bwd(const Geo& g, const bf16* q, const bf16* k, cons
                                 const bf16* o, const bf16* dout, const float* lse, bf16* dq,
                                 bf16* dk, bf16* dv, hipStream_t s);
 
+// Feature-axis attention (cells of a row, per head).  qkv cell-major [cell][3E]; o, dout
+// cell-major [cell][E]; lse [cell][heads]; dqkv cell-major [cell][3E].  Requires
+// feat_attn_mfma_ok(g) (at most 128 active cells per row, 32-bit row offsets).
+bool feat_attn_mfma_ok(const Geo& g);
+hipError_t launch_feat_attn_fwd(const Geo& g, const bf16* qkv, bf16* o, float* lse,
+                                hipStream_t s);
+hipError_t launch_feat_attn_bwd(const Geo& g, const bf16* qkv, const bf16* o, const bf16* dout,
+                                const float* lse, bf16* dqkv, hipStream_t s);
+
 }  // namespace tfm

@@ -1,0 +1,401 @@
+// Feature-axis attention on bf16 MFMA: within each row (b, r), every active cell attends to
+// every active cell of that row, per head.  S_b <= 128 active cells per row.
+//
+// One wave owns one (row, head) pair.  The cells of row (b, r) are the compact cells
+// p = (col0 + k) * R + r, so they are R * 3E elements apart in the Q|K|V buffer; a buffer
+// resource based at the row's first cell with S_b cells in range returns zeros past the last
+// active cell, which pads the cell count to whole 16-cell MFMA blocks.
+//
+// Forward, per 16-query block: S^T = K Q^T (keys x queries; K fragments stay in registers for
+// the whole row), a softmax over all keys at once (no online rescaling: the row fits), and
+// O^T = V^T P^T with V^T staged once per row in the wave's LDS.
+//
+// Backward, two sweeps (probabilities recomputed from the saved log-sum-exp):
+//   query-major:  dS^T = P^T (dP^T - D),  dQ^T = K^T dS^T             (K^T staged in LDS)
+//   key-major:    dS = P (dP - D),  dV^T += dO^T P,  dK^T += Q^T dS    (Q^T, dO^T in LDS)
+// so that every product's fragment comes from the lane's own registers or a 16-byte /
+// 8-byte LDS read.
+#include <math.h>
+
+#include "attn.h"
+#include "mfma.h"
+
+namespace tfm {
+
+namespace {
+
+constexpr float LOG2E = 1.4426950408889634f;
+constexpr int SMAX = 128;       // cells per row handled here
+constexpr int NKB = SMAX / 16;  // 16-cell blocks
+constexpr int TSF = SMAX + 8;   // LDS row stride of the transposed tiles (elements)
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+template <int D>
+struct FDot;
+
+template <>
+struct FDot<32> {
+  typedef bf16x8 frag;
+  static constexpr int FB = 16;
+  static __device__ __forceinline__ frag buf(rsrc_t r, uint32_t off) {
+    uint4 u = bload16(r, off);
+    return *reinterpret_cast<bf16x8*>(&u);
+  }
+  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, zero4(), 0, 0, 0);
+  }
+  static __device__ __forceinline__ float dot(const frag& a, const frag& b) {
+    const uint4 ua = *reinterpret_cast<const uint4*>(&a);
+    const uint4 ub = *reinterpret_cast<const uint4*>(&b);
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s = fmaf(bf2f(u4_elem(ua, j)), bf2f(u4_elem(ub, j)), s);
+    return s;
+  }
+};
+
+template <>
+struct FDot<16> {
+  typedef s16x4 frag;
+  static constexpr int FB = 8;
+  static __device__ __forceinline__ frag buf(rsrc_t r, uint32_t off) {
+    uint2 u = bload8(r, off);
+    return *reinterpret_cast<s16x4*>(&u);
+  }
+  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b) {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, zero4(), 0, 0, 0);
+  }
+  static __device__ __forceinline__ float dot(const frag& a, const frag& b) {
+    const uint2 ua = *reinterpret_cast<const uint2*>(&a);
+    const uint2 ub = *reinterpret_cast<const uint2*>(&b);
+    const uint4 wa = make_uint4(ua.x, ua.y, 0, 0), wb = make_uint4(ub.x, ub.y, 0, 0);
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) s = fmaf(bf2f(u4_elem(wa, j)), bf2f(u4_elem(wb, j)), s);
+    return s;
+  }
+};
+
+// Makes this wave's LDS writes visible to its own later LDS reads (no workgroup barrier: each
+// wave owns its LDS region).
+__device__ __forceinline__ void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+__device__ __forceinline__ bf16x8 cat8(uint2 lo, uint2 hi) {
+  uint4 u = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  return *reinterpret_cast<bf16x8*>(&u);
+}
+
+__device__ __forceinline__ bf16x8 ld_perm(const bf16* p) {
+  return cat8(*reinterpret_cast<const uint2*>(p), *reinterpret_cast<const uint2*>(p + 16));
+}
+
+__device__ __forceinline__ bf16x8 pack8(const f32x4& a, const f32x4& b) {
+  uint4 u = make_uint4(pack2(a[0], a[1]), pack2(a[2], a[3]), pack2(b[0], b[1]),
+                       pack2(b[2], b[3]));
+  return *reinterpret_cast<bf16x8*>(&u);
+}
+
+// Row (b, r) and head of the pair handled by this wave; false if past the last pair.
+struct Pair {
+  int64_t cell0;   // compact cell of the row's first active column
+  int S;           // active cells of the row
+  int head;
+};
+
+__device__ __forceinline__ bool pair_of(const Geo& g, int64_t t, Pair& p) {
+  if (t >= (int64_t)g.B * g.R * g.heads) return false;
+  p.head = (int)(t % g.heads);
+  const int64_t rho = t / g.heads;
+  const int b = (int)(rho / g.R), r = (int)(rho % g.R);
+  const DsInfo di = g.ds[b];
+  p.S = di.S;
+  p.cell0 = (int64_t)di.col0 * g.R + r;
+  return true;
+}
+
+// Stage rows of a [S][d] operand (cell stride `stride` bytes, head offset applied in `off0`)
+// transposed into dst[d][TSF]; cells past S (out of range) read as zero.
+template <int D>
+__device__ __forceinline__ void stage_t(rsrc_t r, uint32_t stride, uint32_t off0, int nkb,
+                                        int lane, bf16* dst) {
+  constexpr int CPR = D / 8;
+  for (int ch = lane; ch < nkb * 16 * CPR; ch += 64) {
+    const int kk = ch / CPR, d0 = (ch % CPR) * 8;
+    const uint4 u = bload16(r, (uint32_t)kk * stride + off0 + d0 * 2);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) dst[(d0 + j) * TSF + kk] = u4_elem(u, j);
+  }
+}
+
+}  // namespace
+
+// ================================================================================ forward
+template <int D>
+__global__ __launch_bounds__(256) void k_feat_attn_fwd(Geo g, const bf16* __restrict__ qkv,
+                                                       bf16* __restrict__ o,
+                                                       float* __restrict__ lse) {
+  constexpr int DB = D / 16;
+  __shared__ __attribute__((aligned(16))) bf16 Vt[4][D * TSF];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int c = lane & 15, lg = lane >> 4;
+  Pair pr;
+  if (!pair_of(g, (int64_t)blockIdx.x * 4 + w, pr)) return;
+  const int E = g.E, S = pr.S;
+  const int nkb = (S + 15) / 16;
+  const uint32_t cs = (uint32_t)g.R * 3 * E * 2;  // bytes between cells of the row
+  const rsrc_t rq = make_rsrc(qkv + pr.cell0 * 3 * E, (uint32_t)(S - 1) * cs + 3 * E * 2);
+  const uint32_t oq = pr.head * D * 2, ok = (E + pr.head * D) * 2, ov = (2 * E + pr.head * D) * 2;
+  const float c2 = LOG2E / sqrtf((float)D);
+
+  bf16* vt = Vt[w];
+  const int nks = (nkb + 1) & ~1;  // staged blocks: whole pairs of 16-cell blocks
+  stage_t<D>(rq, cs, ov, nks, lane, vt);
+  typename FDot<D>::frag kf[NKB];
+#pragma unroll
+  for (int kb = 0; kb < NKB; ++kb)
+    if (kb < nkb) kf[kb] = FDot<D>::buf(rq, (uint32_t)(kb * 16 + c) * cs + ok + lg * FDot<D>::FB);
+  wave_lds_sync();
+
+  const uint32_t ocs = (uint32_t)g.R * E * 2;  // bytes between cells in O
+  bf16* orow = o + pr.cell0 * E + pr.head * D;
+  float* lrow = lse + pr.cell0 * g.heads + pr.head;
+  for (int qb = 0; qb < nkb; ++qb) {
+    const typename FDot<D>::frag qf =
+        FDot<D>::buf(rq, (uint32_t)(qb * 16 + c) * cs + oq + lg * FDot<D>::FB);
+    f32x4 s[NKB];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) {
+      if (kb < nkb) {
+        s[kb] = FDot<D>::mma(kf[kb], qf);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (kb * 16 + lg * 4 + i >= S) s[kb][i] = -INFINITY;
+          mx = fmaxf(mx, s[kb][i]);
+        }
+      }
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mb = -mx * c2;
+    float l = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+      if (kb < nkb) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          s[kb][i] = exp2_hw(fmaf(s[kb][i], c2, mb));
+          l += s[kb][i];
+        }
+      } else {
+        s[kb] = zero4();
+      }
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    f32x4 oacc[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) oacc[db] = zero4();
+#pragma unroll
+    for (int ks = 0; ks < NKB / 2; ++ks) {
+      if (2 * ks < nkb) {
+        const bf16x8 pf = pack8(s[2 * ks], s[2 * ks + 1]);
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          oacc[db] = mfma16(ld_perm(&vt[(db * 16 + c) * TSF + ks * 32 + lg * 4]), pf, oacc[db]);
+      }
+    }
+    const int qq = qb * 16 + c;
+    if (qq < S) {
+      const float inv = 1.0f / l;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const uint2 u = make_uint2(pack2(oacc[db][0] * inv, oacc[db][1] * inv),
+                                   pack2(oacc[db][2] * inv, oacc[db][3] * inv));
+        *reinterpret_cast<uint2*>((char*)orow + (uint64_t)qq * ocs + (db * 16 + lg * 4) * 2) = u;
+      }
+      if (lg == 0) lrow[(int64_t)qq * g.R * g.heads] = mx / sqrtf((float)D) + logf(l);
+    }
+  }
+}
+
+// ================================================================================ backward
+template <int D>
+__global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __restrict__ qkv,
+                                                       const bf16* __restrict__ o,
+                                                       const bf16* __restrict__ dout,
+                                                       const float* __restrict__ lse,
+                                                       bf16* __restrict__ dqkv) {
+  constexpr int DB = D / 16;
+  // per wave: sweep 1 uses [0, D*TSF) for K^T; sweep 2 uses Q^T then dO^T
+  __shared__ __attribute__((aligned(16))) bf16 T[4][2 * D * TSF];
+  __shared__ __attribute__((aligned(16))) float Lr[4][SMAX];
+  __shared__ __attribute__((aligned(16))) float Dr[4][SMAX];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int c = lane & 15, lg = lane >> 4;
+  Pair pr;
+  if (!pair_of(g, (int64_t)blockIdx.x * 4 + w, pr)) return;
+  const int E = g.E, S = pr.S;
+  const int nkb = (S + 15) / 16;
+  const uint32_t cs = (uint32_t)g.R * 3 * E * 2;  // Q|K|V cell stride (bytes)
+  const uint32_t ecs = (uint32_t)g.R * E * 2;     // O / dO cell stride (bytes)
+  const rsrc_t rq = make_rsrc(qkv + pr.cell0 * 3 * E, (uint32_t)(S - 1) * cs + 3 * E * 2);
+  const rsrc_t ro = make_rsrc(o + pr.cell0 * E, (uint32_t)(S - 1) * ecs + E * 2);
+  const rsrc_t rdo = make_rsrc(dout + pr.cell0 * E, (uint32_t)(S - 1) * ecs + E * 2);
+  const uint32_t hq = pr.head * D * 2, hk = (E + pr.head * D) * 2, hv = (2 * E + pr.head * D) * 2;
+  const float c2 = LOG2E / sqrtf((float)D);
+  const float tau = 1.0f / sqrtf((float)D);
+  bf16* t0 = T[w];
+  bf16* t1 = T[w] + D * TSF;
+  bf16* drow = dqkv + pr.cell0 * 3 * E + pr.head * D;
+  const uint64_t dcs = (uint64_t)g.R * 3 * E;  // elements between cells in dQKV
+
+  // K and V fragments of every key block (row role: lane = key c)
+  typename FDot<D>::frag kf[NKB], vf[NKB];
+#pragma unroll
+  for (int kb = 0; kb < NKB; ++kb)
+    if (kb < nkb) {
+      kf[kb] = FDot<D>::buf(rq, (uint32_t)(kb * 16 + c) * cs + hk + lg * FDot<D>::FB);
+      vf[kb] = FDot<D>::buf(rq, (uint32_t)(kb * 16 + c) * cs + hv + lg * FDot<D>::FB);
+    }
+  const int nks = (nkb + 1) & ~1;  // staged blocks: whole pairs of 16-cell blocks
+  for (int i = lane; i < SMAX; i += 64) {
+    Lr[w][i] = 0.f;
+    Dr[w][i] = 0.f;
+  }
+  stage_t<D>(rq, cs, hk, nks, lane, t0);  // K^T
+  wave_lds_sync();
+
+  // ---- sweep 1 (query-major): dQ^T = K^T dS^T; also D and -lse log2e per query -> LDS
+  for (int qb = 0; qb < nkb; ++qb) {
+    const uint32_t qrow = (uint32_t)(qb * 16 + c);
+    const typename FDot<D>::frag qf = FDot<D>::buf(rq, qrow * cs + hq + lg * FDot<D>::FB);
+    const typename FDot<D>::frag df = FDot<D>::buf(rdo, qrow * ecs + hq + lg * FDot<D>::FB);
+    const typename FDot<D>::frag of = FDot<D>::buf(ro, qrow * ecs + hq + lg * FDot<D>::FB);
+    float Dq = FDot<D>::dot(df, of);
+    Dq += __shfl_xor(Dq, 16, 64);
+    Dq += __shfl_xor(Dq, 32, 64);
+    const int qq = qb * 16 + c;
+    const float nb = qq < S ? -lse[(pr.cell0 + (int64_t)qq * g.R) * g.heads + pr.head] * LOG2E
+                            : 0.f;
+    if (lg == 0) {
+      Lr[w][qq] = nb;
+      Dr[w][qq] = Dq;
+    }
+    f32x4 ds[NKB];
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) {
+      if (kb < nkb) {
+        const f32x4 s = FDot<D>::mma(kf[kb], qf);
+        const f32x4 dp = FDot<D>::mma(vf[kb], df);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float p = exp2_hw(fmaf(s[i], c2, nb));
+          if (kb * 16 + lg * 4 + i >= S) p = 0.f;
+          ds[kb][i] = p * (dp[i] - Dq);
+        }
+      } else {
+        ds[kb] = zero4();
+      }
+    }
+    f32x4 acc[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) acc[db] = zero4();
+#pragma unroll
+    for (int ks = 0; ks < NKB / 2; ++ks)
+      if (2 * ks < nkb) {
+        const bf16x8 sf = pack8(ds[2 * ks], ds[2 * ks + 1]);
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          acc[db] = mfma16(ld_perm(&t0[(db * 16 + c) * TSF + ks * 32 + lg * 4]), sf, acc[db]);
+      }
+    if (qq < S) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const uint2 u = make_uint2(pack2(acc[db][0] * tau, acc[db][1] * tau),
+                                   pack2(acc[db][2] * tau, acc[db][3] * tau));
+        *reinterpret_cast<uint2*>(drow + qq * dcs + db * 16 + lg * 4) = u;
+      }
+    }
+  }
+  wave_lds_sync();
+  // ---- sweep 2 (key-major): dV^T += dO^T P, dK^T += Q^T dS over all query blocks
+  stage_t<D>(rq, cs, hq, nks, lane, t0);     // Q^T
+  stage_t<D>(rdo, ecs, hq, nks, lane, t1);   // dO^T
+  wave_lds_sync();
+  for (int kb = 0; kb < nkb; ++kb) {
+    f32x4 dvt[DB], dkt[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) dvt[db] = dkt[db] = zero4();
+#pragma unroll
+    for (int ks = 0; ks < NKB / 2; ++ks) {
+      if (2 * ks < nkb) {
+        f32x4 p[2], dsv[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int qb = 2 * ks + h;
+          const uint32_t qrow = (uint32_t)(qb * 16 + c);
+          const typename FDot<D>::frag qf = FDot<D>::buf(rq, qrow * cs + hq + lg * FDot<D>::FB);
+          const typename FDot<D>::frag df = FDot<D>::buf(rdo, qrow * ecs + hq + lg * FDot<D>::FB);
+          const f32x4 s = FDot<D>::mma(qf, kf[kb]);
+          const f32x4 dp = FDot<D>::mma(df, vf[kb]);
+          const float4 l4 = *reinterpret_cast<const float4*>(&Lr[w][qb * 16 + lg * 4]);
+          const float4 d4 = *reinterpret_cast<const float4*>(&Dr[w][qb * 16 + lg * 4]);
+          const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dv4[4] = {d4.x, d4.y, d4.z, d4.w};
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const bool qok = qb * 16 + lg * 4 + i < S;
+            p[h][i] = qok ? exp2_hw(fmaf(s[i], c2, lv[i])) : 0.f;
+            dsv[h][i] = p[h][i] * (dp[i] - dv4[i]);
+          }
+        }
+        const bf16x8 pf = pack8(p[0], p[1]);
+        const bf16x8 sf = pack8(dsv[0], dsv[1]);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const int row = (db * 16 + c) * TSF + ks * 32 + lg * 4;
+          dvt[db] = mfma16(ld_perm(&t1[row]), pf, dvt[db]);
+          dkt[db] = mfma16(ld_perm(&t0[row]), sf, dkt[db]);
+        }
+      }
+    }
+    const int kk = kb * 16 + c;
+    if (kk < S) {
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        const uint2 uk = make_uint2(pack2(dkt[db][0] * tau, dkt[db][1] * tau),
+                                    pack2(dkt[db][2] * tau, dkt[db][3] * tau));
+        const uint2 uv = make_uint2(pack2(dvt[db][0], dvt[db][1]), pack2(dvt[db][2], dvt[db][3]));
+        *reinterpret_cast<uint2*>(drow + kk * dcs + E + db * 16 + lg * 4) = uk;
+        *reinterpret_cast<uint2*>(drow + kk * dcs + 2 * E + db * 16 + lg * 4) = uv;
+      }
+    }
+  }
+}
+
+bool feat_attn_mfma_ok(const Geo& g) {
+  return g.S <= SMAX && (int64_t)g.R * g.S * 3 * g.E * 2 < (int64_t(1) << 31);
+}
+
+hipError_t launch_feat_attn_fwd(const Geo& g, const bf16* qkv, bf16* o, float* lse,
+                                hipStream_t s) {
+  const int64_t pairs = (int64_t)g.B * g.R * g.heads;
+  const unsigned grid = (unsigned)((pairs + 3) / 4);
+  if (g.d == 16)
+    k_feat_attn_fwd<16><<<grid, 256, 0, s>>>(g, qkv, o, lse);
+  else
+    k_feat_attn_fwd<32><<<grid, 256, 0, s>>>(g, qkv, o, lse);
+  return hipGetLastError();
+}
+
+hipError_t launch_feat_attn_bwd(const Geo& g, const bf16* qkv, const bf16* o, const bf16* dout,
+                                const float* lse, bf16* dqkv, hipStream_t s) {
+  const int64_t pairs = (int64_t)g.B * g.R * g.heads;
+  const unsigned grid = (unsigned)((pairs + 3) / 4);
+  if (g.d == 16)
+    k_feat_attn_bwd<16><<<grid, 256, 0, s>>>(g, qkv, o, dout, lse, dqkv);
+  else
+    k_feat_attn_bwd<32><<<grid, 256, 0, s>>>(g, qkv, o, dout, lse, dqkv);
+  return hipGetLastError();
+}
+
+}  // namespace tfm

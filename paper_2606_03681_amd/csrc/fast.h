@@ -9,7 +9,20 @@ namespace tfm {
 
 // Where rows of an operand live: compact active cells (row m at m * ld) or the native
 // [B][R][S][E] tensor (row m at native_cell(m) * E).
-enum { ROWS_COMPACT = 0, ROWS_NATIVE = 1 };
+// ROWS_ITEM_HM: the item-axis Q|K|V gradients, head-major [col][head][R][d] in three arrays
+// (Q, K, V); row m = cell, column k in [0, 3E); K and V read as 0 at non-train rows.
+enum { ROWS_COMPACT = 0, ROWS_NATIVE = 1, ROWS_ITEM_HM = 2 };
+
+// Element offset of (cell m, column k) in the head-major item Q|K|V arrays; part receives
+// 0 (Q), 1 (K) or 2 (V); returns -1 where K/V do not exist (non-train rows).
+__device__ __forceinline__ int64_t item_hm_offset(const Geo& g, int64_t col, int r, int k,
+                                                  int* part) {
+  const int p = k / g.E, within = k - p * g.E;
+  const int head = within / g.d, j = within - head * g.d;
+  *part = p;
+  if (p > 0 && r >= g.ds[g.col_ds[col]].n_train) return -1;
+  return ((col * g.heads + head) * g.R + r) * g.d + j;
+}
 
 // Epilogues of the MFMA GEMM.
 enum {
@@ -26,6 +39,8 @@ struct GemmArgs {
   int64_t M;
   int N, K, BN, epi;
   const bf16* A;
+  const bf16* A2;  // ROWS_ITEM_HM: K and V arrays (A is Q)
+  const bf16* A3;
   int64_t lda;
   int amode;
   const bf16* Bt;  // [N][K]
@@ -72,8 +87,11 @@ constexpr int WGRAD_CHUNK = 4096;
 struct WgradArgs {
   int64_t M;
   int N, K;
-  const bf16* dY;  // compact rows, leading dimension ldy
+  const bf16* dY;  // compact rows, leading dimension ldy, or ROWS_ITEM_HM (dY, dY2, dY3)
+  const bf16* dY2;
+  const bf16* dY3;
   int64_t ldy;
+  int ymode;
   const bf16* X;   // rows per xmode (compact with ldx, or the native cell tensor)
   int64_t ldx;
   int xmode;

@@ -83,7 +83,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
     akc[i] = (c & 3) * 8;
     int64_t m = m0 + arow[i];
     aval[i] = m < a.M;
-    aoff[i] = aval[i] ? row_addr(g, a.amode, m, a.lda) : 0;
+    aoff[i] = aval[i] && a.amode != ROWS_ITEM_HM ? row_addr(g, a.amode, m, a.lda) : 0;
   }
   int brow[BCH], bkc[BCH];
 #pragma unroll
@@ -95,10 +95,29 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   const bf16* Bt = a.Bt + (int64_t)n0 * a.K;
 
   uint4 ra[2], rb[BCH];
+  // head-major item gradients: per row, the column (global active column) and the row index
+  int64_t hcol[2];
+  int hr[2];
+  if (a.amode == ROWS_ITEM_HM) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int64_t m = m0 + arow[i];
+      hcol[i] = m / g.R;
+      hr[i] = (int)(m - hcol[i] * g.R);
+    }
+  }
   auto gload = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
-      ra[i] = aval[i] ? ldu4(a.A + aoff[i] + k0 + akc[i]) : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < 2; ++i) {
+      if (a.amode == ROWS_ITEM_HM) {
+        int part = 0;
+        const int64_t off = aval[i] ? item_hm_offset(g, hcol[i], hr[i], k0 + akc[i], &part) : -1;
+        const bf16* base = part == 0 ? a.A : (part == 1 ? a.A2 : a.A3);
+        ra[i] = off >= 0 ? ldu4(base + off) : make_uint4(0, 0, 0, 0);
+      } else {
+        ra[i] = aval[i] ? ldu4(a.A + aoff[i] + k0 + akc[i]) : make_uint4(0, 0, 0, 0);
+      }
+    }
 #pragma unroll
     for (int i = 0; i < BCH; ++i) rb[i] = ldu4(Bt + (int64_t)brow[i] * a.K + k0 + bkc[i]);
   };

@@ -458,7 +458,11 @@ int fwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   a.A = X; a.amode = ROWS_NATIVE; a.lda = E;
   a.Bt = f.w + f.wo.qkv_f; a.bias = prm + o.bqkv_f; a.out = qkvf; a.ldo = 3 * E;
   STEP("feat_qkv/mfma", launch_gemm(a, s));
-  STEP("feat_attn_fwd/valu", launch_feat_attn_fwd_simple<T>(g, qkvf, of, (float*)(sv + S.lsef), s));
+  if (feat_attn_mfma_ok(g))
+    STEP("feat_attn_fwd/mfma", launch_feat_attn_fwd(g, qkvf, of, (float*)(sv + S.lsef), s));
+  else
+    STEP("feat_attn_fwd/valu",
+         launch_feat_attn_fwd_simple<T>(g, qkvf, of, (float*)(sv + S.lsef), s));
   // H1 = LN1(X + O_f Wo_f^T + bo_f)
   a = gemm_base(g, N, E, E, EPI_LN);
   a.A = of; a.lda = E; a.Bt = f.w + f.wo.o_f; a.bias = prm + o.bo_f;
@@ -502,9 +506,10 @@ struct FastGrads {
   int accumulate;
   hipStream_t s;
   int run(const tfm::bf16* dY, int N, const tfm::bf16* X, int K, int xmode, size_t offW,
-          size_t offb) {
+          size_t offb, const tfm::bf16* dY2 = nullptr, const tfm::bf16* dY3 = nullptr) {
     tfm::WgradArgs a{};
     a.M = g.N; a.N = N; a.K = K; a.dY = dY; a.ldy = N; a.X = X; a.ldx = K; a.xmode = xmode;
+    a.dY2 = dY2; a.dY3 = dY3; a.ymode = dY2 ? tfm::ROWS_ITEM_HM : tfm::ROWS_COMPACT;
     a.part = f.wpart; a.bpart = f.bpart; a.g = g;
     const int Z = tfm::wgrad_chunks(g.N);
     STEP("wgrad/mfma", tfm::launch_wgrad_mfma(a, s));
@@ -567,11 +572,11 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
        launch_item_attn_bwd(g, (const T*)(sv + S.qi), (const T*)(sv + S.ki),
                             (const T*)(sv + S.vi), (const T*)(sv + S.oi), doi,
                             (const float*)(sv + S.lsei), dq, dk, dv, s));
-  STEP("item_dqkv_cells/hbm", launch_item_dqkv_to_cells<T>(g, dq, dk, dv, dqkv, s));
-  CHK(G.run(dqkv, 3 * E, h1, E, ROWS_COMPACT, o.Wqkv_i, o.bqkv_i));
-  // dZ1 = LN1'(dZ2 + dQKV_i Wqkv_i)
+  CHK(G.run(dq, 3 * E, h1, E, ROWS_COMPACT, o.Wqkv_i, o.bqkv_i, dk, dv));
+  // dZ1 = LN1'(dZ2 + dQKV_i Wqkv_i), the gradients read head-major in place
   a = gemm_base(g, N, E, 3 * E, EPI_LN_BWD);
-  a.A = dqkv; a.lda = 3 * E; a.Bt = f.wt + f.wo.qkv_i; a.resid = dz2;
+  a.A = dq; a.A2 = dk; a.A3 = dv; a.amode = ROWS_ITEM_HM; a.lda = 3 * E;
+  a.Bt = f.wt + f.wo.qkv_i; a.resid = dz2;
   a.aux = (const T*)(sv + S.xh1); a.rstd_in = (const float*)(sv + S.rs1); a.gamma = prm + o.g1;
   a.out = dz1; a.part = f.lnpart;
   STEP("item_qkv_dx_ln1/mfma", launch_gemm(a, s));
@@ -583,9 +588,14 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   a.A = dz1; a.lda = E; a.Bt = f.wt + f.wo.o_f; a.out = dof; a.ldo = E;
   STEP("feat_out_dx/mfma", launch_gemm(a, s));
   CHK(G.run(dz1, E, (const T*)(sv + S.of), E, ROWS_COMPACT, o.Wo_f, o.bo_f));
-  STEP("feat_attn_bwd/valu",
-       launch_feat_attn_bwd_simple<T>(g, (const T*)(sv + S.qkvf), (const T*)(sv + S.of), dof,
-                                      (const float*)(sv + S.lsef), dqkv, s));
+  if (feat_attn_mfma_ok(g))
+    STEP("feat_attn_bwd/mfma",
+         launch_feat_attn_bwd(g, (const T*)(sv + S.qkvf), (const T*)(sv + S.of), dof,
+                              (const float*)(sv + S.lsef), dqkv, s));
+  else
+    STEP("feat_attn_bwd/valu",
+         launch_feat_attn_bwd_simple<T>(g, (const T*)(sv + S.qkvf), (const T*)(sv + S.of), dof,
+                                        (const float*)(sv + S.lsef), dqkv, s));
   CHK(G.run(dqkv, 3 * E, X, E, ROWS_NATIVE, o.Wqkv_f, o.bqkv_f));
   // dX = dZ1 + dQKV_f Wqkv_f, native layout
   a = gemm_base(g, N, E, 3 * E, EPI_DX);

@@ -41,7 +41,7 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
   const int op = tid >> 8, st = tid & 255;
   const bf16* src = op == 0 ? a.dY : a.X;
   const int64_t ld = op == 0 ? a.ldy : a.ldx;
-  const int mode = op == 0 ? ROWS_COMPACT : a.xmode;
+  const int mode = op == 0 ? a.ymode : a.xmode;
   const int cb = op == 0 ? n0 : k0;
   bf16* dst0 = op == 0 ? As[0] : Bs[0];
   bf16* dst1 = op == 0 ? As[1] : Bs[1];
@@ -61,8 +61,16 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
       const int col = cb + (ch >> 5) * 8;
       r[i] = make_uint4(0, 0, 0, 0);
       if (m < me) {
-        const int64_t base = mode == ROWS_NATIVE ? native_cell(g, m) * g.E : m * ld;
-        r[i] = ldu4(src + base + col);
+        if (mode == ROWS_ITEM_HM) {
+          const int64_t gc = m / g.R;
+          int part = 0;
+          const int64_t off = item_hm_offset(g, gc, (int)(m - gc * g.R), col, &part);
+          const bf16* base = part == 0 ? a.dY : (part == 1 ? a.dY2 : a.dY3);
+          if (off >= 0) r[i] = ldu4(base + off);
+        } else {
+          const int64_t base = mode == ROWS_NATIVE ? native_cell(g, m) * g.E : m * ld;
+          r[i] = ldu4(src + base + col);
+        }
       }
     }
   };
@@ -144,30 +152,58 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
   }
 }
 
-// out[i] = (accumulate ? out[i] : 0) + sum_z part[z * stride + i]; four interleaved z groups
-// per output summed in a fixed order, then combined in order.
+// out[i] = (accumulate ? out[i] : 0) + sum_z part[z * stride + i].  A block owns 32 groups of
+// four consecutive outputs; 8 z-groups of threads each sum z = zg, zg + 8, ... with four
+// independent accumulators, combined in a fixed order (bitwise reproducible).
 __global__ __launch_bounds__(256) void k_reduce_z(int Z, int64_t count, int64_t stride,
                                                   const float* __restrict__ part,
                                                   float* __restrict__ out, int accumulate) {
-  __shared__ float red[4][64];
-  const int o = threadIdx.x & 63, gz = threadIdx.x >> 6;
-  const int64_t i = (int64_t)blockIdx.x * 64 + o;
-  float s = 0.f;
-  if (i < count) {
-    float s0 = 0.f, s1 = 0.f;
-    int z = gz;
-    for (; z + 4 < Z; z += 8) {
-      s0 += part[(int64_t)z * stride + i];
-      s1 += part[(int64_t)(z + 4) * stride + i];
+  __shared__ float4 red[8][32];
+  const int o = threadIdx.x & 31, zg = threadIdx.x >> 5;
+  const int64_t i4 = ((int64_t)blockIdx.x * 32 + o) * 4;
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (i4 < count) {
+    float4 a[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) a[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+    const bool full = i4 + 4 <= count && (stride & 3) == 0;
+    int z = zg;
+    for (; z < Z; z += 32) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int zz = z + 8 * u;
+        if (zz < Z) {
+          const float* p = part + (int64_t)zz * stride + i4;
+          float4 v;
+          if (full) {
+            v = *reinterpret_cast<const float4*>(p);
+          } else {
+            v.x = p[0];
+            v.y = i4 + 1 < count ? p[1] : 0.f;
+            v.z = i4 + 2 < count ? p[2] : 0.f;
+            v.w = i4 + 3 < count ? p[3] : 0.f;
+          }
+          a[u].x += v.x; a[u].y += v.y; a[u].z += v.z; a[u].w += v.w;
+        }
+      }
     }
-    if (z < Z) s0 += part[(int64_t)z * stride + i];
-    s = s0 + s1;
+    s.x = (a[0].x + a[1].x) + (a[2].x + a[3].x);
+    s.y = (a[0].y + a[1].y) + (a[2].y + a[3].y);
+    s.z = (a[0].z + a[1].z) + (a[2].z + a[3].z);
+    s.w = (a[0].w + a[1].w) + (a[2].w + a[3].w);
   }
-  red[gz][o] = s;
+  red[zg][o] = s;
   __syncthreads();
-  if (gz == 0 && i < count) {
-    const float t = ((red[0][o] + red[1][o]) + red[2][o]) + red[3][o];
-    out[i] = (accumulate ? out[i] : 0.f) + t;
+  if (zg == 0 && i4 < count) {
+    float4 t = red[0][o];
+#pragma unroll
+    for (int k = 1; k < 8; ++k) {
+      t.x += red[k][o].x; t.y += red[k][o].y; t.z += red[k][o].z; t.w += red[k][o].w;
+    }
+    const float tv[4] = {t.x, t.y, t.z, t.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (i4 + k < count) out[i4 + k] = (accumulate ? out[i4 + k] : 0.f) + tv[k];
   }
 }
 
@@ -195,8 +231,8 @@ hipError_t launch_wgrad_mfma(const WgradArgs& a, hipStream_t s) {
 
 hipError_t launch_reduce_z(int Z, int64_t count, int64_t stride, const float* part, float* out,
                            int accumulate, hipStream_t s) {
-  k_reduce_z<<<(unsigned)((count + 63) / 64), 256, 0, s>>>(Z, count, stride, part, out,
-                                                          accumulate);
+  k_reduce_z<<<(unsigned)((count + 127) / 128), 256, 0, s>>>(Z, count, stride, part, out,
+                                                            accumulate);
   return hipGetLastError();
 }
 
