@@ -64,6 +64,10 @@ struct GemmArgs {
 
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
 
+// Cells per block tile of the MFMA GEMM; EPI_LN_BWD writes one partial row per tile.
+constexpr int GEMM_BM = 64;
+inline int64_t gemm_row_tiles(int64_t M) { return (M + GEMM_BM - 1) / GEMM_BM; }
+
 // bf16 copies of the six weight matrices of one layer, as stored ([out][in]) and transposed.
 // Offsets (elements) inside w / wt follow the packed parameter order of the weights:
 // Wqkv_f, Wo_f, Wqkv_i, Wo_i, W1, W2.
@@ -102,8 +106,10 @@ struct WgradArgs {
 };
 int wgrad_chunks(int64_t M);
 hipError_t launch_wgrad_mfma(const WgradArgs& a, hipStream_t s);
-// out[i] = (accumulate ? out[i] : 0) + sum_z part[z * stride + i], fixed summation order
-hipError_t launch_reduce_z(int Z, int64_t count, int64_t stride, const float* part, float* out,
+// out[i] = (accumulate ? out[i] : 0) + sum_z part[z * stride + i], fixed summation order.
+// With many partials and few outputs the sum runs in two passes, the first of which
+// overwrites part (it is scratch).
+hipError_t launch_reduce_z(int Z, int64_t count, int64_t stride, float* part, float* out,
                            int accumulate, hipStream_t s);
 
 // Backward of the last LayerNorm from the native upstream gradient: dz = LN3'(dY) at active

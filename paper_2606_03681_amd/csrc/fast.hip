@@ -163,7 +163,7 @@ size_t fast_workspace_bytes(int B, int R, int S, int E, int heads, int H, bool b
   (void)heads;
   if (!bf16) return 0;
   WOff wo = weight_offsets(E, H);
-  int64_t tiles = ((int64_t)B * R * S + 127) / 128;
+  const int64_t tiles = gemm_row_tiles((int64_t)B * R * S);
   size_t bytes = 2 * (size_t)wo.total * 2 + 1024;   // w and wt
   bytes += (size_t)tiles * 2 * E * 4 + 256;         // LN-backward column partials
   const int64_t cells = (int64_t)B * R * S;

@@ -2,10 +2,10 @@
 //
 //   C[m, n] = sum_k A[m, k] * Bt[n, k]        (A: cells x K, Bt: [N][K] bf16 weights)
 //
-// Block tile 128 x BN (BN = E, the embedding width, so that one block owns whole cell rows and
+// Block tile 64 x BN (BN = E, the embedding width, so that one block owns whole cell rows and
 // LayerNorm can run in the epilogue), K streamed through LDS in steps of 32 with double
-// buffering.  Four waves in a 2 x 2 arrangement; each wave owns a 64 x BN/2 sub-tile held as
-// 4 x (BN/32) accumulators of v_mfma_f32_16x16x32_bf16.
+// buffering.  Four waves in a 2 x 2 arrangement; each wave owns a 32 x BN/2 sub-tile held as
+// 2 x (BN/32) accumulators of v_mfma_f32_16x16x32_bf16.
 #include <math.h>
 
 #include "fast.h"
@@ -15,7 +15,8 @@ namespace tfm {
 
 namespace {
 
-constexpr int BM = 128;
+constexpr int BM = GEMM_BM;
+constexpr int MI = BM / 32;  // 16-row blocks per wave (2 x 2 waves, each BM/2 rows)
 constexpr int BK = 32;
 constexpr int LDS_STRIDE = BK + 8;  // bf16 elements per LDS row (16-byte pad)
 
@@ -47,10 +48,17 @@ template <int BN, int EPI>
 __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   constexpr int NB = BN / 32;          // 16-wide column blocks per wave
   constexpr int BCH = BN * 4 / 256;    // 16-byte chunks of the B tile per thread
-  __shared__ __attribute__((aligned(16))) bf16 As[2][BM * LDS_STRIDE];
-  __shared__ __attribute__((aligned(16))) bf16 Bs[2][BN * LDS_STRIDE];
+  constexpr int TS = BN + 8;  // epilogue tile row stride (elements)
+  constexpr int MAIN_BYTES = 2 * (BM + BN) * LDS_STRIDE * 2;
+  constexpr int TILE_BYTES = BM * TS * 2;
+  __shared__ __attribute__((aligned(16))) char smem[MAIN_BYTES > TILE_BYTES ? MAIN_BYTES : TILE_BYTES];
+  bf16 (*As)[BM * LDS_STRIDE] = reinterpret_cast<bf16 (*)[BM * LDS_STRIDE]>(smem);
+  bf16 (*Bs)[BN * LDS_STRIDE] =
+      reinterpret_cast<bf16 (*)[BN * LDS_STRIDE]>(smem + 2 * BM * LDS_STRIDE * 2);
+  bf16* tile = reinterpret_cast<bf16*>(smem);  // epilogue: [BM][TS], after the main loop
   __shared__ float red[2][BM];
   __shared__ float cred[2][2][BN];
+  __shared__ int64_t rbase[BM];  // epilogue: per-row element offset for the current mode
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -73,11 +81,12 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   }
 
   // ---- global -> register staging assignment
-  int64_t aoff[2];
-  bool aval[2];
-  int arow[2], akc[2];
+  constexpr int ACH = BM * 4 / 256;  // 16-byte chunks of the A tile per thread
+  int64_t aoff[ACH];
+  bool aval[ACH];
+  int arow[ACH], akc[ACH];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < ACH; ++i) {
     int c = tid + 256 * i;
     arow[i] = c >> 2;
     akc[i] = (c & 3) * 8;
@@ -94,13 +103,13 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   }
   const bf16* Bt = a.Bt + (int64_t)n0 * a.K;
 
-  uint4 ra[2], rb[BCH];
+  uint4 ra[ACH], rb[BCH];
   // head-major item gradients: per row, the column (global active column) and the row index
-  int64_t hcol[2];
-  int hr[2];
+  int64_t hcol[ACH];
+  int hr[ACH];
   if (a.amode == ROWS_ITEM_HM) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < ACH; ++i) {
       const int64_t m = m0 + arow[i];
       hcol[i] = m / g.R;
       hr[i] = (int)(m - hcol[i] * g.R);
@@ -108,7 +117,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   }
   auto gload = [&](int k0) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < ACH; ++i) {
       if (a.amode == ROWS_ITEM_HM) {
         int part = 0;
         const int64_t off = aval[i] ? item_hm_offset(g, hcol[i], hr[i], k0 + akc[i], &part) : -1;
@@ -123,14 +132,14 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   };
   auto sstore = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) stu4(&As[buf][arow[i] * LDS_STRIDE + akc[i]], ra[i]);
+    for (int i = 0; i < ACH; ++i) stu4(&As[buf][arow[i] * LDS_STRIDE + akc[i]], ra[i]);
 #pragma unroll
     for (int i = 0; i < BCH; ++i) stu4(&Bs[buf][brow[i] * LDS_STRIDE + bkc[i]], rb[i]);
   };
 
-  f32x4 acc[4][NB];
+  f32x4 acc[MI][NB];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < MI; ++i)
 #pragma unroll
     for (int j = 0; j < NB; ++j) acc[i][j] = zero4();
 
@@ -141,15 +150,15 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   for (int kt = 0; kt < KT; ++kt) {
     const int cur = kt & 1;
     if (kt + 1 < KT) gload((kt + 1) * BK);
-    bf16x8 af[4], bfr[NB];
+    bf16x8 af[MI], bfr[NB];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      af[i] = ld8(&As[cur][(wm * 64 + i * 16 + lr) * LDS_STRIDE + lg * 8]);
+    for (int i = 0; i < MI; ++i)
+      af[i] = ld8(&As[cur][(wm * (BM / 2) + i * 16 + lr) * LDS_STRIDE + lg * 8]);
 #pragma unroll
     for (int j = 0; j < NB; ++j)
       bfr[j] = ld8(&Bs[cur][(wn * (BN / 2) + j * 16 + lr) * LDS_STRIDE + lg * 8]);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
       for (int j = 0; j < NB; ++j) acc[i][j] = mfma16(af[i], bfr[j], acc[i][j]);
     if (kt + 1 < KT) sstore(cur ^ 1);
@@ -157,68 +166,144 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   }
 
   // ---- epilogues.  acc[i][j][q] is C[row, col] with
-  //   row = m0 + wm*64 + i*16 + lg*4 + q,  col = n0 + wn*BN/2 + j*16 + lr
+  //   row = m0 + wm*BM/2 + i*16 + lg*4 + q,  col = n0 + wn*BN/2 + j*16 + lr
+  // Global traffic goes through the LDS tile [BM][TS] in 16-byte row chunks: residual / x-hat
+  // inputs are loaded into it, outputs are written into it and copied out row by row.
   const int colb = wn * (BN / 2) + lr;  // column within the tile for j = 0
+  constexpr int CPRW = BN / 8;          // 16-byte chunks per tile row
+  auto rloc = [&](int i, int q) { return wm * (BM / 2) + i * 16 + lg * 4 + q; };
 
-  if (EPI == EPI_BIAS || EPI == EPI_GELU_FWD || EPI == EPI_GELU_BWD) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        int64_t m = m0 + wm * 64 + i * 16 + lg * 4 + q;
-        if (m >= a.M) continue;
-#pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          int n = n0 + colb + j * 16;
-          float v = acc[i][j][q];
-          if (a.bias) v += a.bias[n];
-          int64_t o = m * a.ldo + n;
-          if (EPI == EPI_GELU_BWD) v *= gelu_grad_f(bf2f(a.aux[o]));
-          a.out[o] = f2bf(v);
-          if (EPI == EPI_GELU_FWD) a.out2[o] = f2bf(gelu_f(bf2f(a.out[o])));
+  // per-row element offsets: ROWS_COMPACT with leading dimension ld, ROWS_NATIVE, or the
+  // head-major item layout (offset of row m's (head 0, dim 0); -1 where K/V do not exist)
+  auto set_rows = [&](int mode, int64_t ld, int hm_part) {
+    if (tid < BM) {
+      const int64_t m = m0 + tid;
+      int64_t off = -1;
+      if (m < a.M) {
+        if (hm_part >= 0) {
+          const int64_t col = m / g.R;
+          const int r = (int)(m - col * g.R);
+          if (hm_part == 0 || r < g.ds[g.col_ds[col]].n_train)
+            off = (col * g.heads * g.R + r) * (int64_t)g.d;
+        } else {
+          off = mode == ROWS_NATIVE ? native_cell(g, m) * g.E : m * ld;
         }
       }
+      rbase[tid] = off;
+    }
+  };
+  // tile <- rows of src (columns [c0, c0 + BN)); rows without an offset read as 0
+  auto load_tile = [&](const bf16* src, int c0) {
+    for (int ch = tid; ch < BM * CPRW; ch += 256) {
+      const int row = ch / CPRW, cc = (ch % CPRW) * 8;
+      const int64_t off = rbase[row];
+      stu4(&tile[row * TS + cc], off >= 0 ? ldu4(src + off + c0 + cc) : make_uint4(0, 0, 0, 0));
+    }
+  };
+  // rows of dst <- tile (columns [c0, c0 + BN)); head-major destinations when hm is set
+  auto store_tile = [&](bf16* dst, int c0, bool hm) {
+    for (int ch = tid; ch < BM * CPRW; ch += 256) {
+      const int row = ch / CPRW, cc = (ch % CPRW) * 8;
+      const int64_t off = rbase[row];
+      if (off < 0) continue;
+      int64_t o = off + c0 + cc;
+      if (hm) {
+        const int head = cc / g.d, jj = cc - head * g.d;
+        o = off + (int64_t)head * g.R * g.d + jj;
+      }
+      stu4(dst + o, ldu4(&tile[row * TS + cc]));
+    }
+  };
+  auto tile_at = [&](int i, int j, int q) -> float {
+    return bf2f(tile[rloc(i, q) * TS + colb + j * 16]);
+  };
+  auto put = [&](int i, int j, int q, float v) { tile[rloc(i, q) * TS + colb + j * 16] = to_bf16(v); };
+
+  if (EPI == EPI_BIAS || EPI == EPI_GELU_FWD || EPI == EPI_ITEM_QKV) {
+    if (EPI == EPI_ITEM_QKV)
+      set_rows(ROWS_COMPACT, 0, blockIdx.y);
+    else
+      set_rows(ROWS_COMPACT, a.ldo, -1);
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const float b = a.bias ? a.bias[n0 + colb + j * 16] : 0.f;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) put(i, j, q, acc[i][j][q] + b);
+      }
+    lds_barrier();
+    if (EPI == EPI_ITEM_QKV) {
+      bf16* dst = blockIdx.y == 0 ? a.out : (blockIdx.y == 1 ? a.out2 : a.out3);
+      store_tile(dst, 0, true);
+      return;
+    }
+    store_tile(a.out, n0, false);
+    if (EPI == EPI_GELU_FWD) {
+      // U = GELU of the stored (bf16) pre-activation, computed in place of the accumulators
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) acc[i][j][q] = gelu_f(tile_at(i, j, q));
+      lds_barrier();
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) put(i, j, q, acc[i][j][q]);
+      lds_barrier();
+      store_tile(a.out2, n0, false);
+    }
     return;
   }
 
-  if (EPI == EPI_ITEM_QKV) {
-    const int part = blockIdx.y;  // 0 = Q, 1 = K, 2 = V
-    bf16* dst = part == 0 ? a.out : (part == 1 ? a.out2 : a.out3);
+  if (EPI == EPI_GELU_BWD) {
+    set_rows(ROWS_COMPACT, a.ldo, -1);
+    lds_barrier();
+    load_tile(a.aux, n0);
+    lds_barrier();
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        int64_t m = m0 + wm * 64 + i * 16 + lg * 4 + q;
-        if (m >= a.M) continue;
-        int64_t col = m / g.R;
-        int r = (int)(m - col * g.R);
-        if (part > 0 && r >= g.ds[g.col_ds[col]].n_train) continue;
+      for (int j = 0; j < NB; ++j)
 #pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          int within = colb + j * 16;
-          int head = within / g.d, jj = within - head * g.d;
-          float v = acc[i][j][q] + a.bias[n0 + within];
-          dst[((col * g.heads + head) * g.R + r) * g.d + jj] = f2bf(v);
-        }
-      }
+        for (int q = 0; q < 4; ++q) acc[i][j][q] *= gelu_grad_f(tile_at(i, j, q));
+    lds_barrier();
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) put(i, j, q, acc[i][j][q]);
+    lds_barrier();
+    store_tile(a.out, n0, false);
     return;
   }
 
   if (EPI == EPI_DX) {
+    set_rows(ROWS_COMPACT, BN, -1);
+    lds_barrier();
+    load_tile(a.resid, 0);
+    lds_barrier();
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        int64_t m = m0 + wm * 64 + i * 16 + lg * 4 + q;
-        if (m >= a.M) continue;
-        int64_t ro = m * (int64_t)BN;
-        int64_t oo = native_cell(g, m) * BN;
+      for (int j = 0; j < NB; ++j)
 #pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          int n = colb + j * 16;
-          a.out[oo + n] = f2bf(acc[i][j][q] + bf2f(a.resid[ro + n]));
-        }
-      }
+        for (int q = 0; q < 4; ++q) acc[i][j][q] += tile_at(i, j, q);
+    lds_barrier();
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) put(i, j, q, acc[i][j][q]);
+    set_rows(ROWS_NATIVE, 0, -1);
+    lds_barrier();
+    store_tile(a.out, 0, false);
     return;
   }
 
@@ -230,108 +315,114 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   for (int j = 0; j < NB; ++j) gam[j] = a.gamma[colb + j * 16];
 
   if (EPI == EPI_LN) {
+    set_rows(a.rmode, BN, -1);
+    lds_barrier();
+    load_tile(a.resid, 0);
+    lds_barrier();
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        int64_t m = m0 + wm * 64 + i * 16 + lg * 4 + q;
-        bool ok = m < a.M;
-        int64_t ro = ok ? row_addr(g, a.rmode, m, BN) : 0;
+      for (int j = 0; j < NB; ++j) {
+        const float b = a.bias[colb + j * 16];
 #pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          int n = colb + j * 16;
-          val[i][j][q] = ok ? acc[i][j][q] + a.bias[n] + bf2f(a.resid[ro + n]) : 0.f;
-        }
+        for (int q = 0; q < 4; ++q) val[i][j][q] = acc[i][j][q] + b + tile_at(i, j, q);
       }
     // mean
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        float s = 0.f;
+        float sm = 0.f;
 #pragma unroll
-        for (int j = 0; j < NB; ++j) s += val[i][j][q];
-        s = sum16(s);
-        if (lr == 0) red[wn][wm * 64 + i * 16 + lg * 4 + q] = s;
+        for (int j = 0; j < NB; ++j) sm += val[i][j][q];
+        sm = sum16(sm);
+        if (lr == 0) red[wn][rloc(i, q)] = sm;
       }
-    __syncthreads();
-    float mean[4][4];
+    lds_barrier();
+    float mean[MI][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        int rl = wm * 64 + i * 16 + lg * 4 + q;
+        const int rl = rloc(i, q);
         mean[i][q] = (red[0][rl] + red[1][rl]) * (1.0f / BN);
       }
-    __syncthreads();
+    lds_barrier();
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        float s = 0.f;
+        float sm = 0.f;
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
-          float dv = val[i][j][q] - mean[i][q];
-          s += dv * dv;
+          const float dv = val[i][j][q] - mean[i][q];
+          sm += dv * dv;
         }
-        s = sum16(s);
-        if (lr == 0) red[wn][wm * 64 + i * 16 + lg * 4 + q] = s;
+        sm = sum16(sm);
+        if (lr == 0) red[wn][rloc(i, q)] = sm;
       }
-    __syncthreads();
+    lds_barrier();
     float bet[NB];
 #pragma unroll
     for (int j = 0; j < NB; ++j) bet[j] = a.beta[colb + j * 16];
+    // x-hat in place of val; rstd per row
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        int rl = wm * 64 + i * 16 + lg * 4 + q;
-        int64_t m = m0 + rl;
-        if (m >= a.M) continue;
-        float rs = 1.0f / sqrtf((red[0][rl] + red[1][rl]) * (1.0f / BN) + 1e-5f);
-        int64_t oo = row_addr(g, a.omode, m, BN);
-        int64_t co = m * (int64_t)BN;
+        const int rl = rloc(i, q);
+        const float rs = 1.0f / sqrtf((red[0][rl] + red[1][rl]) * (1.0f / BN) + 1e-5f);
 #pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          int n = colb + j * 16;
-          float xh = (val[i][j][q] - mean[i][q]) * rs;
-          a.out[oo + n] = f2bf(fmaf(gam[j], xh, bet[j]));
-          a.xhat[co + n] = f2bf(xh);
-        }
-        if (wn == 0 && lr == 0) a.rstd[m] = rs;
+        for (int j = 0; j < NB; ++j) val[i][j][q] = (val[i][j][q] - mean[i][q]) * rs;
+        if (wn == 0 && lr == 0 && m0 + rl < a.M) a.rstd[m0 + rl] = rs;
       }
+    // h = gamma * x-hat + beta -> out (omode); x-hat -> xhat (compact)
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) put(i, j, q, fmaf(gam[j], val[i][j][q], bet[j]));
+    set_rows(a.omode, BN, -1);
+    lds_barrier();
+    store_tile(a.out, 0, false);
+    lds_barrier();
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) put(i, j, q, val[i][j][q]);
+    set_rows(ROWS_COMPACT, BN, -1);
+    lds_barrier();
+    store_tile(a.xhat, 0, false);
     return;
   }
 
   if (EPI == EPI_LN_BWD) {
-    // dh = acc + resid; du = rstd * (g - mean(g) - xhat * mean(g * xhat)), g = dh * gamma.
-    // xhat (aux) is re-read from memory in each pass to keep register pressure down.
-    auto xv_at = [&](int i, int j, int q) -> float {
-      int64_t m = m0 + wm * 64 + i * 16 + lg * 4 + q;
-      return m < a.M ? bf2f(a.aux[m * (int64_t)BN + colb + j * 16]) : 0.f;
-    };
+    // dh = acc + resid; du = rstd * (g - mean(g) - xhat * mean(g * xhat)), g = dh * gamma;
+    // column partial sums of dh * xhat (dgamma) and dh (dbeta) per workgroup
+    set_rows(ROWS_COMPACT, BN, -1);
+    lds_barrier();
+    load_tile(a.resid, 0);
+    lds_barrier();
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        int64_t m = m0 + wm * 64 + i * 16 + lg * 4 + q;
-        bool ok = m < a.M;
-        int64_t ro = m * (int64_t)BN;
+      for (int j = 0; j < NB; ++j)
 #pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          int n = colb + j * 16;
-          val[i][j][q] = ok ? acc[i][j][q] + bf2f(a.resid[ro + n]) : 0.f;
-        }
-      }
-    // column partial sums for dgamma (sum dh * xhat) and dbeta (sum dh)
+        for (int q = 0; q < 4; ++q) val[i][j][q] = acc[i][j][q] + tile_at(i, j, q);
+    lds_barrier();
+    load_tile(a.aux, 0);  // x-hat stays in the tile for the rest of the epilogue
+    lds_barrier();
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
       float s1 = 0.f, s2 = 0.f;
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < MI; ++i)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          s1 += val[i][j][q] * xv_at(i, j, q);
+          s1 += val[i][j][q] * tile_at(i, j, q);
           s2 += val[i][j][q];
         }
       s1 += __shfl_xor(s1, 16, 64);
@@ -343,59 +434,62 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
         cred[1][wm][colb + j * 16] = s2;
       }
     }
-    float m1[4][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        float s = 0.f;
+        float sm = 0.f;
 #pragma unroll
-        for (int j = 0; j < NB; ++j) s += val[i][j][q] * gam[j];
-        s = sum16(s);
-        if (lr == 0) red[wn][wm * 64 + i * 16 + lg * 4 + q] = s;
+        for (int j = 0; j < NB; ++j) sm += val[i][j][q] * gam[j];
+        sm = sum16(sm);
+        if (lr == 0) red[wn][rloc(i, q)] = sm;
       }
-    __syncthreads();
+    lds_barrier();
     if (tid < BN) {
       float* pg = a.part + (int64_t)blockIdx.x * 2 * BN;
       pg[tid] = cred[0][0][tid] + cred[0][1][tid];
       pg[BN + tid] = cred[1][0][tid] + cred[1][1][tid];
     }
+    float m1[MI][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        int rl = wm * 64 + i * 16 + lg * 4 + q;
+        const int rl = rloc(i, q);
         m1[i][q] = (red[0][rl] + red[1][rl]) * (1.0f / BN);
       }
-    __syncthreads();
+    lds_barrier();
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        float s = 0.f;
-#pragma unroll
-        for (int j = 0; j < NB; ++j) s += val[i][j][q] * gam[j] * xv_at(i, j, q);
-        s = sum16(s);
-        if (lr == 0) red[wn][wm * 64 + i * 16 + lg * 4 + q] = s;
-      }
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < MI; ++i)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        int rl = wm * 64 + i * 16 + lg * 4 + q;
-        int64_t m = m0 + rl;
-        if (m >= a.M) continue;
-        float m2 = (red[0][rl] + red[1][rl]) * (1.0f / BN);
-        float rs = a.rstd_in[m];
-        int64_t co = m * (int64_t)BN;
+        float sm = 0.f;
 #pragma unroll
-        for (int j = 0; j < NB; ++j) {
-          int n = colb + j * 16;
-          float gg = val[i][j][q] * gam[j];
-          a.out[co + n] = f2bf(rs * (gg - m1[i][q] - xv_at(i, j, q) * m2));
-        }
+        for (int j = 0; j < NB; ++j) sm += val[i][j][q] * gam[j] * tile_at(i, j, q);
+        sm = sum16(sm);
+        if (lr == 0) red[wn][rloc(i, q)] = sm;
       }
+    lds_barrier();
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int rl = rloc(i, q);
+        const float m2 = (red[0][rl] + red[1][rl]) * (1.0f / BN);
+        const float rs = m0 + rl < a.M ? a.rstd_in[m0 + rl] : 0.f;
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+          val[i][j][q] = rs * (val[i][j][q] * gam[j] - m1[i][q] - tile_at(i, j, q) * m2);
+      }
+    lds_barrier();
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) put(i, j, q, val[i][j][q]);
+    lds_barrier();
+    store_tile(a.out, 0, false);
     return;
   }
 }

@@ -418,7 +418,7 @@ FastWs fast_ws(const Dims& d, char* ws, const WsLayout& W) {
   f.wt = (tfm::bf16*)p;
   p += align_up((size_t)f.wo.total * 2);
   f.lnpart = (float*)p;
-  p += align_up((size_t)((d.Nmax + 127) / 128) * 2 * d.E * 4 + 256);
+  p += align_up((size_t)tfm::gemm_row_tiles(d.Nmax) * 2 * d.E * 4 + 256);
   const int64_t zw = (d.Nmax + tfm::WGRAD_CHUNK - 1) / tfm::WGRAD_CHUNK;
   const int64_t maxw = 3LL * d.E * d.E > (int64_t)d.H * d.E ? 3LL * d.E * d.E : (int64_t)d.H * d.E;
   f.wpart = (float*)p;
@@ -529,7 +529,7 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   const FastWs f = fast_ws(d, ws, W);
   const int E = d.E, H = d.H;
   const int64_t N = g.N;
-  const int tiles = (int)((N + 127) / 128);
+  const int tiles = (int)tfm::gemm_row_tiles(N);
   FastGrads G{f, g, grads, accumulate, s};
   STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, s));
   T* dz3 = (T*)(ws + W.tb);
@@ -543,8 +543,8 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   int nb = 0;
   STEP("ln3_bwd/hbm", launch_ln_out_bwd(g, dY, (const T*)(sv + S.xh3), (const float*)(sv + S.rs3),
                                         prm + o.g3, dz3, f.lnpart, &nb, s));
-  STEP("reduce/hbm", launch_reduce_z(nb, E, 2 * E, f.lnpart, grads + o.g3, accumulate, s));
-  STEP("reduce/hbm", launch_reduce_z(nb, E, 2 * E, f.lnpart + E, grads + o.be3, accumulate, s));
+  // gamma and beta gradients are adjacent in the packed order: one sum over 2E columns
+  STEP("reduce/hbm", launch_reduce_z(nb, 2 * E, 2 * E, f.lnpart, grads + o.g3, accumulate, s));
   // MLP: dG = (dZ3 W2) * GELU'(G)
   GemmArgs a = gemm_base(g, N, H, E, EPI_GELU_BWD);
   a.A = dz3; a.lda = E; a.Bt = f.wt + f.wo.w2; a.out = dgb; a.ldo = H;
@@ -557,8 +557,7 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   a.A = dgb; a.lda = H; a.Bt = f.wt + f.wo.w1; a.resid = dz3; a.aux = (const T*)(sv + S.xh2);
   a.rstd_in = (const float*)(sv + S.rs2); a.gamma = prm + o.g2; a.out = dz2; a.part = f.lnpart;
   STEP("mlp_up_dx_ln2/mfma", launch_gemm(a, s));
-  STEP("reduce/hbm", launch_reduce_z(tiles, E, 2 * E, f.lnpart, grads + o.g2, accumulate, s));
-  STEP("reduce/hbm", launch_reduce_z(tiles, E, 2 * E, f.lnpart + E, grads + o.be2, accumulate, s));
+  STEP("reduce/hbm", launch_reduce_z(tiles, 2 * E, 2 * E, f.lnpart, grads + o.g2, accumulate, s));
   // item attention
   T* doi = (T*)(ws + W.tc);
   a = gemm_base(g, N, E, E, EPI_BIAS);
@@ -580,8 +579,7 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   a.aux = (const T*)(sv + S.xh1); a.rstd_in = (const float*)(sv + S.rs1); a.gamma = prm + o.g1;
   a.out = dz1; a.part = f.lnpart;
   STEP("item_qkv_dx_ln1/mfma", launch_gemm(a, s));
-  STEP("reduce/hbm", launch_reduce_z(tiles, E, 2 * E, f.lnpart, grads + o.g1, accumulate, s));
-  STEP("reduce/hbm", launch_reduce_z(tiles, E, 2 * E, f.lnpart + E, grads + o.be1, accumulate, s));
+  STEP("reduce/hbm", launch_reduce_z(tiles, 2 * E, 2 * E, f.lnpart, grads + o.g1, accumulate, s));
   // feature attention
   T* dof = (T*)(ws + W.tc);
   a = gemm_base(g, N, E, E, EPI_BIAS);

@@ -152,27 +152,33 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
   }
 }
 
-// out[i] = (accumulate ? out[i] : 0) + sum_z part[z * stride + i].  A block owns 32 groups of
-// four consecutive outputs; 8 z-groups of threads each sum z = zg, zg + 8, ... with four
-// independent accumulators, combined in a fixed order (bitwise reproducible).
-__global__ __launch_bounds__(256) void k_reduce_z(int Z, int64_t count, int64_t stride,
-                                                  const float* __restrict__ part,
-                                                  float* __restrict__ out, int accumulate) {
+// out[i] = (accumulate ? out[i] : 0) + sum over z in [z0, z1) of part[z * stride + i], with
+// z0 = blockIdx.y * zc, z1 = min(Z, z0 + zc), and out advanced by blockIdx.y * out_ystride.  A
+// block owns 32 groups of four consecutive outputs; 8 z-groups of threads each sum z = z0 + zg,
+// z0 + zg + 8, ... with four independent accumulators, combined in a fixed order (bitwise
+// reproducible).  out may be the first partial row of the block's own range (the first pass of
+// a two-pass sum): every read of the range precedes the barrier, every write follows it, and no
+// other block touches the range.
+__global__ __launch_bounds__(256) void k_reduce_z(int Z, int zc, int64_t count, int64_t stride,
+                                                  const float* part, float* out,
+                                                  int64_t out_ystride, int accumulate) {
   __shared__ float4 red[8][32];
   const int o = threadIdx.x & 31, zg = threadIdx.x >> 5;
   const int64_t i4 = ((int64_t)blockIdx.x * 32 + o) * 4;
+  const int z0 = (int)blockIdx.y * zc;
+  const int z1 = z0 + zc < Z ? z0 + zc : Z;
+  out += (int64_t)blockIdx.y * out_ystride;
   float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
   if (i4 < count) {
     float4 a[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) a[u] = make_float4(0.f, 0.f, 0.f, 0.f);
     const bool full = i4 + 4 <= count && (stride & 3) == 0;
-    int z = zg;
-    for (; z < Z; z += 32) {
+    for (int z = z0 + zg; z < z1; z += 32) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int zz = z + 8 * u;
-        if (zz < Z) {
+        if (zz < z1) {
           const float* p = part + (int64_t)zz * stride + i4;
           float4 v;
           if (full) {
@@ -229,10 +235,21 @@ hipError_t launch_wgrad_mfma(const WgradArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_reduce_z(int Z, int64_t count, int64_t stride, const float* part, float* out,
+hipError_t launch_reduce_z(int Z, int64_t count, int64_t stride, float* part, float* out,
                            int accumulate, hipStream_t s) {
-  k_reduce_z<<<(unsigned)((count + 127) / 128), 256, 0, s>>>(Z, count, stride, part, out,
-                                                            accumulate);
+  if (Z <= 0 || count <= 0) return hipSuccess;
+  const unsigned bx = (unsigned)((count + 127) / 128);
+  // Few output blocks and many partials: first fold groups of ZC partials into the first row
+  // of each group, leaving ceil(Z / ZC) partials ZC rows apart.
+  constexpr int ZC = 64;
+  if (bx < 512 && Z > 2 * ZC) {
+    const unsigned groups = (unsigned)((Z + ZC - 1) / ZC);
+    k_reduce_z<<<dim3(bx, groups), 256, 0, s>>>(Z, ZC, count, stride, part, part,
+                                                 (int64_t)ZC * stride, 0);
+    Z = (int)groups;
+    stride *= ZC;
+  }
+  k_reduce_z<<<dim3(bx, 1), 256, 0, s>>>(Z, Z, count, stride, part, out, 0, accumulate);
   return hipGetLastError();
 }
 
