@@ -4,17 +4,17 @@
 // One wave owns one (row, head) pair.  The cells of row (b, r) are the compact cells
 // p = (col0 + k) * R + r, so they are R * 3E elements apart in the Q|K|V buffer; a buffer
 // resource based at the row's first cell with S_b cells in range returns zeros past the last
-// active cell, which pads the cell count to whole 16-cell MFMA blocks.
+// active cell, which pads the cell count to whole 16-cell MFMA blocks.  Every operand fragment
+// of the pair is loaded once, at the start (a single memory round trip per wave); the
+// transposed LDS tiles the products need are written from those registers.
 //
-// Forward, per 16-query block: S^T = K Q^T (keys x queries; K fragments stay in registers for
-// the whole row), a softmax over all keys at once (no online rescaling: the row fits), and
-// O^T = V^T P^T with V^T staged once per row in the wave's LDS.
+// Forward, per 16-query block: S^T = K Q^T (keys x queries), a softmax over all keys at once
+// (no online rescaling: the row fits), and O^T = V^T P^T with V^T in the wave's LDS.
 //
 // Backward, two sweeps (probabilities recomputed from the saved log-sum-exp):
-//   query-major:  dS^T = P^T (dP^T - D),  dQ^T = K^T dS^T             (K^T staged in LDS)
+//   query-major:  dS^T = P^T (dP^T - D),  dQ^T = K^T dS^T             (K^T in LDS)
 //   key-major:    dS = P (dP - D),  dV^T += dO^T P,  dK^T += Q^T dS    (Q^T, dO^T in LDS)
-// so that every product's fragment comes from the lane's own registers or a 16-byte /
-// 8-byte LDS read.
+// so that every product's fragment comes from the lane's own registers or an 8-byte LDS read.
 #include <math.h>
 
 #include "attn.h"
@@ -113,18 +113,22 @@ __device__ __forceinline__ bool pair_of(const Geo& g, int64_t t, Pair& p) {
   return true;
 }
 
-// Stage rows of a [S][d] operand (cell stride `stride` bytes, head offset applied in `off0`)
-// transposed into dst[d][TSF]; cells past S (out of range) read as zero.
+// Write the row-role fragments fr[kb] (lane: cell kb*16 + c, dims lg*EPL .. lg*EPL + EPL-1)
+// transposed into dst[d][TSF] for the first nks 16-cell blocks.
 template <int D>
-__device__ __forceinline__ void stage_t(rsrc_t r, uint32_t stride, uint32_t off0, int nkb,
-                                        int lane, bf16* dst) {
-  constexpr int CPR = D / 8;
-  for (int ch = lane; ch < nkb * 16 * CPR; ch += 64) {
-    const int kk = ch / CPR, d0 = (ch % CPR) * 8;
-    const uint4 u = bload16(r, (uint32_t)kk * stride + off0 + d0 * 2);
+__device__ __forceinline__ void stage_frag(const typename FDot<D>::frag* fr, int nks, int c,
+                                           int lg, bf16* dst) {
+  constexpr int EPL = FDot<D>::FB / 2;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) dst[(d0 + j) * TSF + kk] = u4_elem(u, j);
-  }
+  for (int kb = 0; kb < NKB; ++kb)
+    if (kb < nks) {
+      const uint2* u = reinterpret_cast<const uint2*>(&fr[kb]);
+#pragma unroll
+      for (int j = 0; j < EPL; ++j) {
+        const uint32_t wd = j < 4 ? (j < 2 ? u[0].x : u[0].y) : (j < 6 ? u[1].x : u[1].y);
+        dst[(lg * EPL + j) * TSF + kb * 16 + c] = (bf16)(j & 1 ? wd >> 16 : wd & 0xffff);
+      }
+    }
 }
 
 }  // namespace
@@ -149,25 +153,34 @@ __global__ __launch_bounds__(256) void k_feat_attn_fwd(Geo g, const bf16* __rest
 
   bf16* vt = Vt[w];
   const int nks = (nkb + 1) & ~1;  // staged blocks: whole pairs of 16-cell blocks
-  stage_t<D>(rq, cs, ov, nks, lane, vt);
-  typename FDot<D>::frag kf[NKB];
+  typedef typename FDot<D>::frag frag;
+  frag kf[NKB], qf[NKB];
+  {
+    frag vf[NKB];
 #pragma unroll
-  for (int kb = 0; kb < NKB; ++kb)
-    if (kb < nkb) kf[kb] = FDot<D>::buf(rq, (uint32_t)(kb * 16 + c) * cs + ok + lg * FDot<D>::FB);
+    for (int kb = 0; kb < NKB; ++kb)
+      if (kb < nks) {
+        const uint32_t row = (uint32_t)(kb * 16 + c) * cs + lg * FDot<D>::FB;
+        kf[kb] = FDot<D>::buf(rq, row + ok);
+        vf[kb] = FDot<D>::buf(rq, row + ov);
+        qf[kb] = FDot<D>::buf(rq, row + oq);
+      }
+    stage_frag<D>(vf, nks, c, lg, vt);
+  }
   wave_lds_sync();
 
   const uint32_t ocs = (uint32_t)g.R * E * 2;  // bytes between cells in O
   bf16* orow = o + pr.cell0 * E + pr.head * D;
   float* lrow = lse + pr.cell0 * g.heads + pr.head;
-  for (int qb = 0; qb < nkb; ++qb) {
-    const typename FDot<D>::frag qf =
-        FDot<D>::buf(rq, (uint32_t)(qb * 16 + c) * cs + oq + lg * FDot<D>::FB);
+#pragma unroll
+  for (int qb = 0; qb < NKB; ++qb) {
+    if (qb >= nkb) break;
     f32x4 s[NKB];
     float mx = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb) {
       if (kb < nkb) {
-        s[kb] = FDot<D>::mma(kf[kb], qf);
+        s[kb] = FDot<D>::mma(kf[kb], qf[qb]);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           if (kb * 16 + lg * 4 + i >= S) s[kb][i] = -INFINITY;
@@ -249,49 +262,53 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
   bf16* drow = dqkv + pr.cell0 * 3 * E + pr.head * D;
   const uint64_t dcs = (uint64_t)g.R * 3 * E;  // elements between cells in dQKV
 
-  // K and V fragments of every key block (row role: lane = key c)
-  typename FDot<D>::frag kf[NKB], vf[NKB];
+  // every fragment of the pair in the row role (lane: cell kb*16 + c), loaded up front
+  typedef typename FDot<D>::frag frag;
+  const int nks = (nkb + 1) & ~1;  // staged blocks: whole pairs of 16-cell blocks
+  frag kf[NKB], vf[NKB], qf[NKB], df[NKB];
+  float nbq[NKB], dq[NKB];  // per query kb*16 + c: -lse * log2(e) and D = rowsum(dO * O)
 #pragma unroll
   for (int kb = 0; kb < NKB; ++kb)
-    if (kb < nkb) {
-      kf[kb] = FDot<D>::buf(rq, (uint32_t)(kb * 16 + c) * cs + hk + lg * FDot<D>::FB);
-      vf[kb] = FDot<D>::buf(rq, (uint32_t)(kb * 16 + c) * cs + hv + lg * FDot<D>::FB);
+    if (kb < nks) {
+      const uint32_t rr = (uint32_t)(kb * 16 + c);
+      const uint32_t fo = lg * FDot<D>::FB;
+      kf[kb] = FDot<D>::buf(rq, rr * cs + hk + fo);
+      vf[kb] = FDot<D>::buf(rq, rr * cs + hv + fo);
+      qf[kb] = FDot<D>::buf(rq, rr * cs + hq + fo);
+      df[kb] = FDot<D>::buf(rdo, rr * ecs + hq + fo);
+      dq[kb] = FDot<D>::dot(df[kb], FDot<D>::buf(ro, rr * ecs + hq + fo));
+      nbq[kb] = (int)rr < S ? -lse[(pr.cell0 + (int64_t)rr * g.R) * g.heads + pr.head] * LOG2E
+                            : 0.f;
     }
-  const int nks = (nkb + 1) & ~1;  // staged blocks: whole pairs of 16-cell blocks
-  for (int i = lane; i < SMAX; i += 64) {
-    Lr[w][i] = 0.f;
-    Dr[w][i] = 0.f;
-  }
-  stage_t<D>(rq, cs, hk, nks, lane, t0);  // K^T
+#pragma unroll
+  for (int kb = 0; kb < NKB; ++kb)
+    if (kb < nks) {
+      dq[kb] += __shfl_xor(dq[kb], 16, 64);
+      dq[kb] += __shfl_xor(dq[kb], 32, 64);
+      if (lg == 0) {
+        Lr[w][kb * 16 + c] = nbq[kb];
+        Dr[w][kb * 16 + c] = dq[kb];
+      }
+    }
+  stage_frag<D>(kf, nks, c, lg, t0);  // K^T
   wave_lds_sync();
 
-  // ---- sweep 1 (query-major): dQ^T = K^T dS^T; also D and -lse log2e per query -> LDS
-  for (int qb = 0; qb < nkb; ++qb) {
-    const uint32_t qrow = (uint32_t)(qb * 16 + c);
-    const typename FDot<D>::frag qf = FDot<D>::buf(rq, qrow * cs + hq + lg * FDot<D>::FB);
-    const typename FDot<D>::frag df = FDot<D>::buf(rdo, qrow * ecs + hq + lg * FDot<D>::FB);
-    const typename FDot<D>::frag of = FDot<D>::buf(ro, qrow * ecs + hq + lg * FDot<D>::FB);
-    float Dq = FDot<D>::dot(df, of);
-    Dq += __shfl_xor(Dq, 16, 64);
-    Dq += __shfl_xor(Dq, 32, 64);
+  // ---- sweep 1 (query-major): dQ^T = K^T dS^T
+#pragma unroll
+  for (int qb = 0; qb < NKB; ++qb) {
+    if (qb >= nkb) break;
     const int qq = qb * 16 + c;
-    const float nb = qq < S ? -lse[(pr.cell0 + (int64_t)qq * g.R) * g.heads + pr.head] * LOG2E
-                            : 0.f;
-    if (lg == 0) {
-      Lr[w][qq] = nb;
-      Dr[w][qq] = Dq;
-    }
     f32x4 ds[NKB];
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb) {
       if (kb < nkb) {
-        const f32x4 s = FDot<D>::mma(kf[kb], qf);
-        const f32x4 dp = FDot<D>::mma(vf[kb], df);
+        const f32x4 s = FDot<D>::mma(kf[kb], qf[qb]);
+        const f32x4 dp = FDot<D>::mma(vf[kb], df[qb]);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          float p = exp2_hw(fmaf(s[i], c2, nb));
+          float p = exp2_hw(fmaf(s[i], c2, nbq[qb]));
           if (kb * 16 + lg * 4 + i >= S) p = 0.f;
-          ds[kb][i] = p * (dp[i] - Dq);
+          ds[kb][i] = p * (dp[i] - dq[qb]);
         }
       } else {
         ds[kb] = zero4();
@@ -319,10 +336,12 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
   }
   wave_lds_sync();
   // ---- sweep 2 (key-major): dV^T += dO^T P, dK^T += Q^T dS over all query blocks
-  stage_t<D>(rq, cs, hq, nks, lane, t0);     // Q^T
-  stage_t<D>(rdo, ecs, hq, nks, lane, t1);   // dO^T
+  stage_frag<D>(qf, nks, c, lg, t0);  // Q^T
+  stage_frag<D>(df, nks, c, lg, t1);  // dO^T
   wave_lds_sync();
-  for (int kb = 0; kb < nkb; ++kb) {
+#pragma unroll
+  for (int kb = 0; kb < NKB; ++kb) {
+    if (kb >= nkb) break;
     f32x4 dvt[DB], dkt[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db) dvt[db] = dkt[db] = zero4();
@@ -333,11 +352,8 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const int qb = 2 * ks + h;
-          const uint32_t qrow = (uint32_t)(qb * 16 + c);
-          const typename FDot<D>::frag qf = FDot<D>::buf(rq, qrow * cs + hq + lg * FDot<D>::FB);
-          const typename FDot<D>::frag df = FDot<D>::buf(rdo, qrow * ecs + hq + lg * FDot<D>::FB);
-          const f32x4 s = FDot<D>::mma(qf, kf[kb]);
-          const f32x4 dp = FDot<D>::mma(df, vf[kb]);
+          const f32x4 s = FDot<D>::mma(qf[qb], kf[kb]);
+          const f32x4 dp = FDot<D>::mma(df[qb], vf[kb]);
           const float4 l4 = *reinterpret_cast<const float4*>(&Lr[w][qb * 16 + lg * 4]);
           const float4 d4 = *reinterpret_cast<const float4*>(&Dr[w][qb * 16 + lg * 4]);
           const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dv4[4] = {d4.x, d4.y, d4.z, d4.w};
