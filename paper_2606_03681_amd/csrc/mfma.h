@@ -36,6 +36,16 @@ __device__ __forceinline__ void stu4(bf16* p, uint4 v) { *reinterpret_cast<uint4
 
 __device__ __forceinline__ float bf2f(uint16_t u) { return __uint_as_float(((uint32_t)u) << 16); }
 
+// LDS transpose read (ds_read_b64_tr_b16).  Every lane names an 8-byte LDS address (four
+// bf16); within each group of 16 lanes, lane i receives as its element j the element i % 4 of
+// the four named by lane 4j + i / 4.  So if lane L of a group names row L / 4, columns
+// c0 + 4 (L % 4) .. +3 of a row-major tile, lane i receives column c0 + i of rows 0..3: a
+// 4-deep slice of an MFMA operand whose contraction index runs down the tile's rows.
+__device__ __forceinline__ bf16x4 lds_read_tr16(const bf16* p) {
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p));
+}
+
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 

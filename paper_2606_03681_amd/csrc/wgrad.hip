@@ -1,92 +1,176 @@
 // Weight gradients on bf16 MFMA: dW[n][k] = sum over active cells m of dY[m][n] X[m][k], with
-// the bias gradient db[n] = sum_m dY[m][n] formed from the same staged tiles.
+// the bias gradient db[n] = sum_m dY[m][n] formed from the same staged data.
 //
 // The reduction runs over the cells (1.6 M at eval scale) while the output is one E x E tile
 // of the weight, so the cells are split into chunks (split-K): workgroup (n-tile, k-tile, z)
 // sums chunk z into a float32 partial, and a second kernel adds the partials in a fixed order
-// (bitwise reproducible).  The MFMA contraction index is the cell, which is the slow index in
-// memory for both operands, so 32-cell slices of dY and X are staged transposed in LDS
-// ([n][cell] and [k][cell]); consecutive lanes take consecutive cells so that the transposed
-// 16-bit writes of a wave fall on distinct banks.
+// (bitwise reproducible).  The MFMA contraction index is the cell, the slow index in memory
+// for both operands: 32-cell slices of dY and X are copied row-major into LDS with 16-byte
+// stores and read back transposed with ds_read_b64_tr_b16.  Slot t of a lane's 8-element
+// fragment (lane group g = lane / 16) holds cell 16 (t / 4) + 4 g + t % 4 of the slice, for A
+// and B alike, so each half-wave transpose read touches 8 consecutive rows; with a row stride
+// of an odd multiple of 32 bytes those rows fall on disjoint LDS banks.
 #include "fast.h"
 #include "mfma.h"
 
 namespace tfm {
 
 namespace {
-constexpr int MS = 32;       // cells per MFMA step
-constexpr int LS = MS + 8;   // LDS row stride (elements)
+constexpr int MS = 32;  // cells per step
+
+// One staged 16-byte chunk of an operand: features [f, f + 8) of the cell `off` rows into each
+// slice.  The cursor moves one slice (MS cells) per load without division; the layout MODE
+// (compact, native, head-major item gradients) selects which fields are used.
+struct Cursor {
+  int64_t addr;  // element offset of the chunk for the next slice to load
+  int rem;       // cells left in the workgroup's range from this chunk's cell (<= 0: done)
+  int col, r;    // active column and row of that cell (ROWS_NATIVE, ROWS_ITEM_HM)
+  int ntr;       // train-prefix length of the column (ROWS_ITEM_HM)
+  int hmo;       // ROWS_ITEM_HM: head * R * d + offset in head
+  int part;      // ROWS_ITEM_HM: 0, 1, 2 for Q, K, V
+};
+
+template <int MODE>
+__device__ __forceinline__ void cur_init(Cursor& c, const Geo& g, int64_t m, int64_t me, int f,
+                                         int64_t ld) {
+  c.rem = (int)(me - m);
+  c.col = (int)(m / g.R);
+  c.r = (int)(m - (int64_t)c.col * g.R);
+  c.ntr = 0;
+  c.part = 0;
+  c.hmo = 0;
+  if (MODE == ROWS_COMPACT) {
+    c.addr = m * ld + f;
+  } else if (MODE == ROWS_NATIVE) {
+    c.addr = c.rem > 0 ? native_cell(g, m) * g.E + f : 0;
+  } else {
+    c.part = f / g.E;
+    const int within = f - c.part * g.E;
+    const int head = within / g.d;
+    c.hmo = head * g.R * g.d + (within - head * g.d);
+    c.addr = 0;
+    if (c.rem > 0) {
+      c.ntr = g.ds[g.col_ds[c.col]].n_train;
+      c.addr = ((int64_t)c.col * g.heads * g.R + c.r) * g.d + c.hmo;
+    }
+  }
+}
+
+template <int MODE>
+__device__ __forceinline__ uint4 cur_load(const Cursor& c, const bf16* p0, const bf16* p1,
+                                          const bf16* p2) {
+  uint4 v = make_uint4(0, 0, 0, 0);
+  if (c.rem > 0) {
+    if (MODE == ROWS_ITEM_HM) {
+      const bf16* base = c.part == 0 ? p0 : (c.part == 1 ? p1 : p2);
+      if (c.part == 0 || c.r < c.ntr) v = ldu4(base + c.addr);
+    } else {
+      v = ldu4(p0 + c.addr);
+    }
+  }
+  return v;
+}
+
+template <int MODE>
+__device__ __forceinline__ void cur_advance(Cursor& c, const Geo& g, int64_t ld, int f) {
+  c.rem -= MS;
+  if (MODE == ROWS_COMPACT) {
+    c.addr += MS * ld;
+    return;
+  }
+  c.r += MS;
+  if (c.r < g.R) {
+    c.addr += (MODE == ROWS_NATIVE ? (int64_t)g.S * g.E : (int64_t)g.d) * MS;
+    return;
+  }
+  while (c.r >= g.R) {
+    c.r -= g.R;
+    ++c.col;
+  }
+  if (c.rem <= 0) return;
+  if (MODE == ROWS_NATIVE) {
+    c.addr = (((int64_t)g.col_ds[c.col] * g.R + c.r) * g.S + g.col_c[c.col]) * g.E + f;
+  } else {
+    c.ntr = g.ds[g.col_ds[c.col]].n_train;
+    c.addr = ((int64_t)c.col * g.heads * g.R + c.r) * g.d + c.hmo;
+  }
+}
 }  // namespace
 
-// 512 threads = 8 waves in a 2 (n) x 4 (k) arrangement; tile BT x BT with BT = E.
-template <int BT>
+// 512 threads = 8 waves in a 2 (n) x 4 (k) arrangement; tile BN x BK.  dY is in layout YM
+// (compact or head-major item gradients), X in layout XM (compact or native).
+template <int BN, int BK, int YM, int XM>
 __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
-  constexpr int NBW = BT / 32;   // 16-row blocks per wave along n (BT/2 rows)
-  constexpr int KBW = BT / 64;   // 16-col blocks per wave along k (BT/4 cols)
-  constexpr int CH = 4 * BT;     // 16-byte chunks per operand slice (MS x BT)
-  constexpr int CPT = CH / 256;  // chunks per staging thread (256 threads per operand)
-  __shared__ __attribute__((aligned(16))) bf16 As[2][BT * LS];
-  __shared__ __attribute__((aligned(16))) bf16 Bs[2][BT * LS];
+  constexpr int NBW = BN / 32;      // 16-row blocks per wave along n (BN/2 rows)
+  constexpr int KBW = BK / 64;      // 16-col blocks per wave along k (BK/4 cols)
+  constexpr int LSA = BN + 16;      // LDS row strides (elements): odd multiples of 32 bytes
+  constexpr int LSB = BK + 16;
+  constexpr int CPA = BN / 64;      // 16-byte chunks per staging thread and slice (dY)
+  constexpr int CPB = BK / 64;      // (X)
+  __shared__ __attribute__((aligned(16))) bf16 As[2][MS * LSA];
+  __shared__ __attribute__((aligned(16))) bf16 Bs[2][MS * LSB];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int c = lane & 15, lg = lane >> 4;
+  const int lg = lane >> 4, c = lane & 15;
   const int wn = w >> 2, wk = w & 3;
-  const int n0 = blockIdx.x * BT, k0 = blockIdx.y * BT;
+  const int n0 = blockIdx.x * BN, k0 = blockIdx.y * BK;
   const int64_t mb = (int64_t)blockIdx.z * a.chunk;
   const int64_t me = mb + a.chunk < a.M ? mb + a.chunk : a.M;
   const Geo& g = a.g;
 
-  // staging: threads 0-255 stage dY columns [n0, n0+BT), threads 256-511 stage X columns
-  // [k0, k0+BT); chunk ch -> cell offset ch % 32, column block (ch / 32) * 8
-  const int op = tid >> 8, st = tid & 255;
-  const bf16* src = op == 0 ? a.dY : a.X;
-  const int64_t ld = op == 0 ? a.ldy : a.ldx;
-  const int mode = op == 0 ? a.ymode : a.xmode;
-  const int cb = op == 0 ? n0 : k0;
-  bf16* dst0 = op == 0 ? As[0] : Bs[0];
-  bf16* dst1 = op == 0 ? As[1] : Bs[1];
-  const bool bsum = op == 0 && a.bpart && blockIdx.y == 0;
-  float csum[CPT][8];
+  // staging: threads 0-255 stage dY features [n0, n0+BN), threads 256-511 X features
+  // [k0, k0+BK); chunk ch -> cell ch / (width/8) of the slice, features (ch % (width/8)) * 8
+  const bool opa = tid < 256;
+  const int st = tid & 255;
+  constexpr int CPM = CPA > CPB ? CPA : CPB;
+  Cursor cu[CPM];  // one array for both roles (a select between two arrays would not stay in
+                   // registers)
 #pragma unroll
-  for (int i = 0; i < CPT; ++i)
+  for (int i = 0; i < CPM; ++i) {
+    const int ch = st + 256 * i;
+    if (opa) {
+      if (i < CPA) cur_init<YM>(cu[i], g, mb + ch / (BN / 8), me, n0 + (ch % (BN / 8)) * 8, a.ldy);
+    } else {
+      if (i < CPB) cur_init<XM>(cu[i], g, mb + ch / (BK / 8), me, k0 + (ch % (BK / 8)) * 8, a.ldx);
+    }
+  }
+  auto gload = [&](uint4* r) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) csum[i][j] = 0.f;
-
-  uint4 r[CPT];
-  auto gload = [&](int64_t m0) {
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
+    for (int i = 0; i < CPM; ++i) {
       const int ch = st + 256 * i;
-      const int64_t m = m0 + (ch & 31);
-      const int col = cb + (ch >> 5) * 8;
-      r[i] = make_uint4(0, 0, 0, 0);
-      if (m < me) {
-        if (mode == ROWS_ITEM_HM) {
-          const int64_t gc = m / g.R;
-          int part = 0;
-          const int64_t off = item_hm_offset(g, gc, (int)(m - gc * g.R), col, &part);
-          const bf16* base = part == 0 ? a.dY : (part == 1 ? a.dY2 : a.dY3);
-          if (off >= 0) r[i] = ldu4(base + off);
-        } else {
-          const int64_t base = mode == ROWS_NATIVE ? native_cell(g, m) * g.E : m * ld;
-          r[i] = ldu4(src + base + col);
+      if (opa) {
+        if (i < CPA) {
+          r[i] = cur_load<YM>(cu[i], a.dY, a.dY2, a.dY3);
+          cur_advance<YM>(cu[i], g, a.ldy, n0 + (ch % (BN / 8)) * 8);
+        }
+      } else {
+        if (i < CPB) {
+          r[i] = cur_load<XM>(cu[i], a.X, nullptr, nullptr);
+          cur_advance<XM>(cu[i], g, a.ldx, k0 + (ch % (BK / 8)) * 8);
         }
       }
     }
   };
-  auto sstore = [&](int b) {
-    bf16* d = b ? dst1 : dst0;
+  auto sstore = [&](const uint4* r, int b) {
+    if (opa) {
 #pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int ch = st + 256 * i;
-      const int mm = ch & 31, cc = (ch >> 5) * 8;
+      for (int i = 0; i < CPA; ++i) {
+        const int ch = st + 256 * i;
+        stu4(&As[b][(ch / (BN / 8)) * LSA + (ch % (BN / 8)) * 8], r[i]);
+      }
+    } else {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) d[(cc + j) * LS + mm] = u4_elem(r[i], j);
-      if (bsum) {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) csum[i][j] += bf2f(u4_elem(r[i], j));
+      for (int i = 0; i < CPB; ++i) {
+        const int ch = st + 256 * i;
+        stu4(&Bs[b][(ch / (BK / 8)) * LSB + (ch % (BK / 8)) * 8], r[i]);
       }
     }
+  };
+  // fragment of the 16 columns starting at c0: slots 0-3 from rows 0-15, 4-7 from rows 16-31
+  auto frag = [&](const bf16* T, int ls, int c0) -> bf16x8 {
+    const bf16* p = T + (lane >> 2) * ls + c0 + 4 * (lane & 3);
+    const bf16x4 lo = lds_read_tr16(p), hi = lds_read_tr16(p + 16 * ls);
+    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   };
 
   f32x4 acc[NBW][KBW];
@@ -94,60 +178,74 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
   for (int i = 0; i < NBW; ++i)
 #pragma unroll
     for (int j = 0; j < KBW; ++j) acc[i][j] = zero4();
+  // bias gradient: the k-tile-0 waves with wk == 0 sum the dY fragments they already hold
+  const bool bsum = a.bpart && blockIdx.y == 0 && wk == 0;  // wave-uniform
+  float bacc[NBW];
+#pragma unroll
+  for (int i = 0; i < NBW; ++i) bacc[i] = 0.f;
 
-  const int64_t steps = (me - mb + MS - 1) / MS;
-  if (steps > 0) {
-    gload(mb);
-    sstore(0);
-  }
-  lds_barrier();
-  for (int64_t s = 0; s < steps; ++s) {
-    const int b = (int)(s & 1);
-    if (s + 1 < steps) gload(mb + (s + 1) * MS);
-    const bf16* A = b ? As[1] : As[0];
-    const bf16* B = b ? Bs[1] : Bs[0];
+  auto compute = [&](int b) {
     bf16x8 af[NBW], bfr[KBW];
 #pragma unroll
-    for (int i = 0; i < NBW; ++i) af[i] = ld8(&A[(wn * (BT / 2) + i * 16 + c) * LS + lg * 8]);
+    for (int i = 0; i < NBW; ++i) af[i] = frag(As[b], LSA, wn * (BN / 2) + i * 16);
 #pragma unroll
-    for (int j = 0; j < KBW; ++j) bfr[j] = ld8(&B[(wk * (BT / 4) + j * 16 + c) * LS + lg * 8]);
+    for (int j = 0; j < KBW; ++j) bfr[j] = frag(Bs[b], LSB, wk * (BK / 4) + j * 16);
 #pragma unroll
     for (int i = 0; i < NBW; ++i)
 #pragma unroll
       for (int j = 0; j < KBW; ++j) acc[i][j] = mfma16(af[i], bfr[j], acc[i][j]);
-    if (s + 1 < steps) sstore(b ^ 1);
+    if (bsum) {
+#pragma unroll
+      for (int i = 0; i < NBW; ++i) {
+        float t = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) t += (float)af[i][e];
+        bacc[i] += t;
+      }
+    }
+  };
+
+  // Two register sets: slice s + 2 is loaded while slice s is multiplied, and slice s + 1
+  // (loaded one step earlier) goes to LDS at the end of step s.
+  const int64_t steps = (me - mb + MS - 1) / MS;
+  uint4 r0[CPM], r1[CPM];
+  if (steps > 0) gload(r0);
+  if (steps > 1) gload(r1);
+  if (steps > 0) sstore(r0, 0);
+  lds_barrier();
+  for (int64_t s = 0; s < steps; s += 2) {
+    // even step s: compute buffer 0; r0 refills with slice s + 2; r1 (slice s + 1) -> buffer 1
+    if (s + 2 < steps) gload(r0);
+    compute(0);
+    if (s + 1 < steps) sstore(r1, 1);
+    lds_barrier();
+    if (s + 1 >= steps) break;
+    // odd step s + 1: compute buffer 1; r1 refills with slice s + 3; r0 (slice s + 2) -> 0
+    if (s + 3 < steps) gload(r1);
+    compute(1);
+    if (s + 2 < steps) sstore(r0, 0);
     lds_barrier();
   }
 
-  // partial tile: lane holds rows n = wn*BT/2 + i*16 + 4*lg + q, column k = wk*BT/4 + j*16 + c
+  // partial tile: lane holds rows n = wn*BN/2 + i*16 + 4*lg + q, column k = wk*BK/4 + j*16 + c
   float* out = a.part + (int64_t)blockIdx.z * a.N * a.K;
 #pragma unroll
   for (int i = 0; i < NBW; ++i)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int n = n0 + wn * (BT / 2) + i * 16 + lg * 4 + q;
+      const int n = n0 + wn * (BN / 2) + i * 16 + lg * 4 + q;
 #pragma unroll
-      for (int j = 0; j < KBW; ++j) out[(int64_t)n * a.K + k0 + wk * (BT / 4) + j * 16 + c] = acc[i][j][q];
+      for (int j = 0; j < KBW; ++j)
+        out[(int64_t)n * a.K + k0 + wk * (BK / 4) + j * 16 + c] = acc[i][j][q];
     }
   if (bsum) {
-    // the 32 lanes of a half-wave share a column block; sum over them in a fixed pattern
+    // lane (lg, c) summed 8 cells of feature n = wn*BN/2 + i*16 + c; add the four lane groups
 #pragma unroll
-    for (int i = 0; i < CPT; ++i)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        float v = csum[i][j];
-#pragma unroll
-        for (int off = 1; off < 32; off <<= 1) v += __shfl_xor(v, off, 64);
-        csum[i][j] = v;
-      }
-    if ((st & 31) == 0) {
-#pragma unroll
-      for (int i = 0; i < CPT; ++i) {
-        const int ch = st + 256 * i;
-        float* bp = a.bpart + (int64_t)blockIdx.z * a.N + n0 + (ch >> 5) * 8;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) bp[j] = csum[i][j];
-      }
+    for (int i = 0; i < NBW; ++i) {
+      float t = bacc[i];
+      t += __shfl_xor(t, 16, 64);
+      t += __shfl_xor(t, 32, 64);
+      if (lg == 0) a.bpart[(int64_t)blockIdx.z * a.N + n0 + wn * (BN / 2) + i * 16 + c] = t;
     }
   }
 }
@@ -218,21 +316,36 @@ int wgrad_chunks(int64_t M) {
   return (int)(z < 1 ? 1 : z);
 }
 
+template <int BN, int BK>
+static hipError_t wgrad_modes(const WgradArgs& b, dim3 grid, hipStream_t s) {
+  const bool yhm = b.ymode == ROWS_ITEM_HM, xnat = b.xmode == ROWS_NATIVE;
+  if (b.ymode != ROWS_COMPACT && !yhm) return hipErrorInvalidValue;
+  if (b.xmode != ROWS_COMPACT && !xnat) return hipErrorInvalidValue;
+  if (yhm && xnat)
+    k_wgrad<BN, BK, ROWS_ITEM_HM, ROWS_NATIVE><<<grid, 512, 0, s>>>(b);
+  else if (yhm)
+    k_wgrad<BN, BK, ROWS_ITEM_HM, ROWS_COMPACT><<<grid, 512, 0, s>>>(b);
+  else if (xnat)
+    k_wgrad<BN, BK, ROWS_COMPACT, ROWS_NATIVE><<<grid, 512, 0, s>>>(b);
+  else
+    k_wgrad<BN, BK, ROWS_COMPACT, ROWS_COMPACT><<<grid, 512, 0, s>>>(b);
+  return hipGetLastError();
+}
+
 hipError_t launch_wgrad_mfma(const WgradArgs& a, hipStream_t s) {
   const int Z = wgrad_chunks(a.M);
-  const int BT = a.g.E;
-  if (a.N % BT || a.K % BT) return hipErrorInvalidValue;
-  dim3 grid((unsigned)(a.N / BT), (unsigned)(a.K / BT), (unsigned)Z);
+  const int BN = a.g.E, BK = a.g.E > 192 ? 128 : a.g.E;
+  if (a.N % BN || a.K % BK) return hipErrorInvalidValue;
+  dim3 grid((unsigned)(a.N / BN), (unsigned)(a.K / BK), (unsigned)Z);
   WgradArgs b = a;
   b.chunk = WGRAD_CHUNK;
-  switch (BT) {
-    case 64: k_wgrad<64><<<grid, 512, 0, s>>>(b); break;
-    case 128: k_wgrad<128><<<grid, 512, 0, s>>>(b); break;
-    case 192: k_wgrad<192><<<grid, 512, 0, s>>>(b); break;
-    case 256: k_wgrad<256><<<grid, 512, 0, s>>>(b); break;
+  switch (BN) {
+    case 64: return wgrad_modes<64, 64>(b, grid, s);
+    case 128: return wgrad_modes<128, 128>(b, grid, s);
+    case 192: return wgrad_modes<192, 192>(b, grid, s);
+    case 256: return wgrad_modes<256, 128>(b, grid, s);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 hipError_t launch_reduce_z(int Z, int64_t count, int64_t stride, float* part, float* out,
