@@ -65,12 +65,12 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
                                                        const bf16* __restrict__ v,
                                                        bf16* __restrict__ o,
                                                        float* __restrict__ lse, int QT) {
-  constexpr int KS = D + 8;   // LDS row stride of K (elements)
-  constexpr int VS = KT + 8;  // LDS row stride of V^T
+  constexpr int KS = D + 8;   // LDS row stride of K (elements; conflict-free 16-byte reads)
+  constexpr int VS = 48;      // LDS row stride of V (96 bytes: conflict-free transpose reads)
   constexpr int DB = D / 16;  // 16-wide dim blocks
   constexpr int CPR = D / 8;  // 16-byte chunks per key row
   __shared__ __attribute__((aligned(16))) bf16 Ks[2][KT * KS];
-  __shared__ __attribute__((aligned(16))) bf16 Vt[2][D * VS];
+  __shared__ __attribute__((aligned(16))) bf16 Vs[2][KT * VS];
 
   const int bid = blockIdx.x;
   const int64_t prob = (int64_t)((bid >> 3) / QT) * 8 + (bid & 7);
@@ -117,8 +117,7 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
   auto sstore = [&](int buf) {
     if (!stager) return;
     stu4(&Ks[buf][skey * KS + sch], rk);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) Vt[buf][(sch + j) * VS + skey] = u4_elem(rv, j);
+    stu4(&Vs[buf][skey * VS + sch], rv);
   };
 
   const float c2 = LOG2E / sqrtf((float)D);
@@ -194,11 +193,7 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
     for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const bf16* vr = &Vt[cur][(db * 16 + c) * VS + ks * 32 + lg * 4];
-        uint2 lo = *reinterpret_cast<const uint2*>(vr);
-        uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
-        uint4 u = make_uint4(lo.x, lo.y, hi.x, hi.y);
-        bf16x8 vf = *reinterpret_cast<bf16x8*>(&u);
+        const bf16x8 vf = ld_tr8(&Vs[cur][ks * 32 * VS], VS, db * 16, lane);
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) oacc[db][qb] = mfma16(vf, pf[qb][ks], oacc[db][qb]);
       }

@@ -1,8 +1,8 @@
 // Item-axis flash attention on bf16 MFMA, backward pass, as two kernels that each recompute
 // the probabilities from the saved log-sum-exp:
 //
-//   dK/dV kernel (key-major): a workgroup owns 64 train rows (4 waves x 16 keys) of one problem
-//     and streams all query rows in chunks of 64 through LDS:
+//   dK/dV kernel (key-major): a workgroup owns 128 train rows (4 waves x 32 keys) of one
+//     problem and streams all query rows in chunks of 64 through LDS:
 //       S = Q K^T, dP = dO V^T            (D tiles: a lane holds 4 queries of one key)
 //       P = exp2(S tau log2e - lse log2e),  dS = P (dP - D),  D = rowsum(dO o O)
 //       dV^T += dO^T P,  dK^T += Q^T dS   (the S-layout tiles are used directly as B operands)
@@ -13,8 +13,10 @@
 //       dS^T = P^T (dP^T - D),  dQ^T += K^T dS^T
 //
 // Both accumulate in registers only, so each output element is summed in a fixed order
-// (bitwise reproducible), and neither needs more than ~40 KB of LDS, which keeps several
-// workgroups resident per CU.  Workgroups of one problem are numbered onto the same XCD.
+// (bitwise reproducible), and neither needs more than ~30 KB of LDS, which keeps several
+// workgroups resident per CU.  Tiles are staged row-major with 16-byte stores; the
+// transposed operands (Q^T, dO^T, K^T) come from LDS transpose reads.  Workgroups of one
+// problem are numbered onto the same XCD.
 #include <math.h>
 
 #include "attn.h"
@@ -84,11 +86,6 @@ __device__ __forceinline__ bf16x8 cat8(uint2 lo, uint2 hi) {
   return *reinterpret_cast<bf16x8*>(&u);
 }
 
-// 8 k positions from two 4-element runs 16 apart (the S / S^T tile permutation of k).
-__device__ __forceinline__ bf16x8 ld_perm(const bf16* p) {
-  return cat8(*reinterpret_cast<const uint2*>(p), *reinterpret_cast<const uint2*>(p + 16));
-}
-
 __device__ __forceinline__ bf16x8 pack8(const f32x4& a, const f32x4& b) {
   uint4 u = make_uint4(pack2(a[0], a[1]), pack2(a[2], a[3]), pack2(b[0], b[1]),
                        pack2(b[2], b[3]));
@@ -108,15 +105,13 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
                                                         bf16* __restrict__ dk,
                                                         bf16* __restrict__ dv, int KT) {
   constexpr int QC = 64;          // queries per chunk
+  constexpr int KW = 32;          // keys per wave (two 16-key blocks)
   constexpr int DB = D / 16;
   constexpr int CPR = D / 8;      // 16-byte chunks per row of d values
   constexpr int NIT = QC * CPR / 128;  // staging items per thread (128 threads per tensor)
-  constexpr int RS = D + 8;       // LDS row stride of row-major Q / dO (elements)
-  constexpr int TS = QC + 4;      // LDS row stride of Q^T / dO^T
+  constexpr int RS = 48;          // LDS row stride of Q / dO (96 bytes: see ld_tr8)
   __shared__ __attribute__((aligned(16))) bf16 Qs[2][QC * RS];
   __shared__ __attribute__((aligned(16))) bf16 dOs[2][QC * RS];
-  __shared__ __attribute__((aligned(16))) bf16 QTs[2][D * TS];
-  __shared__ __attribute__((aligned(16))) bf16 dOTs[2][D * TS];
   __shared__ __attribute__((aligned(16))) float Dq[2][QC];
   __shared__ __attribute__((aligned(16))) float Lq[2][QC];
 
@@ -127,7 +122,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
   const int64_t col = prob / g.heads;
   const int head = (int)(prob - col * g.heads);
   const int n = g.ds[g.col_ds[col]].n_train;
-  const int t0 = kt * 64;
+  const int t0 = kt * 4 * KW;
   if (t0 >= n) return;
   const int R = g.R, E = g.E;
 
@@ -145,9 +140,16 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
   const float c2 = LOG2E / sqrtf((float)D);
   const float tau = 1.0f / sqrtf((float)D);
 
-  const int key = t0 + w * 16 + c;  // this lane's key column in the S layout
-  const typename Dot<D>::frag kf = Dot<D>::buf(rK, (uint32_t)key * rowQ + lg * Dot<D>::FB);
-  const typename Dot<D>::frag vf = Dot<D>::buf(rV, (uint32_t)key * rowQ + lg * Dot<D>::FB);
+  // this lane's key column of key block kb in the S layout: t0 + w*32 + kb*16 + c; keys past
+  // n read K = V = 0 here and their dK, dV are never written, so no key masking is needed
+  const int kw0 = t0 + w * KW;
+  typename Dot<D>::frag kf[2], vf[2];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    const uint32_t key = (uint32_t)(kw0 + kb * 16 + c);
+    kf[kb] = Dot<D>::buf(rK, key * rowQ + lg * Dot<D>::FB);
+    vf[kb] = Dot<D>::buf(rV, key * rowQ + lg * Dot<D>::FB);
+  }
 
   // staging: threads 0-127 move Q, threads 128-255 move dO (and O for D, and the LSE); each
   // handles NIT (query, 16-byte chunk) items; item it -> query it / CPR, dims (it % CPR) * 8
@@ -173,11 +175,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
     for (int h = 0; h < NIT; ++h) {
       const int it = st + h * 128;
       const int qq = it / CPR, d0 = (it % CPR) * 8;
-      bf16* rm = half == 0 ? Qs[b] : dOs[b];
-      bf16* tr = half == 0 ? QTs[b] : dOTs[b];
-      stu4(&rm[qq * RS + d0], ru[h]);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) tr[(d0 + j) * TS + qq] = u4_elem(ru[h], j);
+      stu4(&(half == 0 ? Qs[b] : dOs[b])[qq * RS + d0], ru[h]);
       if (half == 1) {
         float dot = 0.f;
 #pragma unroll
@@ -193,11 +191,12 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
     }
   };
 
-  f32x4 dkt[DB], dvt[DB];
+  f32x4 dkt[2][DB], dvt[2][DB];
 #pragma unroll
-  for (int db = 0; db < DB; ++db) dkt[db] = dvt[db] = zero4();
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int db = 0; db < DB; ++db) dkt[kb][db] = dvt[kb][db] = zero4();
 
-  // Keys past n have K = V = 0 here and their dK, dV are never written, so no key masking.
   const int NCH = (R + QC - 1) / QC;
   gload(0);
   sstore(0);
@@ -205,45 +204,58 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
   for (int ic = 0; ic < NCH; ++ic) {
     const int b = ic & 1;
     if (ic + 1 < NCH) gload((ic + 1) * QC);
-    // S = Q K^T, dP = dO V^T for 4 query blocks (lane: queries qb*16 + 4*lg + i of `key`)
-    uint32_t pw[4][2], sw[4][2];
+    // S = Q K^T, dP = dO V^T per (query block, key block); lane: queries qb*16 + 4*lg + i
+    uint32_t pw[2][4][2], sw[2][4][2];
 #pragma unroll
     for (int qb = 0; qb < 4; ++qb) {
-      const f32x4 s = Dot<D>::mma(Dot<D>::lds(&Qs[b][(qb * 16 + c) * RS], lg), kf);
-      const f32x4 dp = Dot<D>::mma(Dot<D>::lds(&dOs[b][(qb * 16 + c) * RS], lg), vf);
+      const typename Dot<D>::frag qa = Dot<D>::lds(&Qs[b][(qb * 16 + c) * RS], lg);
+      const typename Dot<D>::frag da = Dot<D>::lds(&dOs[b][(qb * 16 + c) * RS], lg);
       const float4 d4 = *reinterpret_cast<const float4*>(&Dq[b][qb * 16 + lg * 4]);
       const float4 l4 = *reinterpret_cast<const float4*>(&Lq[b][qb * 16 + lg * 4]);
-      const float p0 = exp2_hw(fmaf(s[0], c2, l4.x)), p1 = exp2_hw(fmaf(s[1], c2, l4.y));
-      const float p2 = exp2_hw(fmaf(s[2], c2, l4.z)), p3 = exp2_hw(fmaf(s[3], c2, l4.w));
-      pw[qb][0] = pack2(p0, p1);
-      pw[qb][1] = pack2(p2, p3);
-      sw[qb][0] = pack2(p0 * (dp[0] - d4.x), p1 * (dp[1] - d4.y));
-      sw[qb][1] = pack2(p2 * (dp[2] - d4.z), p3 * (dp[3] - d4.w));
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const f32x4 s = Dot<D>::mma(qa, kf[kb]);
+        const f32x4 dp = Dot<D>::mma(da, vf[kb]);
+        const float p0 = exp2_hw(fmaf(s[0], c2, l4.x)), p1 = exp2_hw(fmaf(s[1], c2, l4.y));
+        const float p2 = exp2_hw(fmaf(s[2], c2, l4.z)), p3 = exp2_hw(fmaf(s[3], c2, l4.w));
+        pw[kb][qb][0] = pack2(p0, p1);
+        pw[kb][qb][1] = pack2(p2, p3);
+        sw[kb][qb][0] = pack2(p0 * (dp[0] - d4.x), p1 * (dp[1] - d4.y));
+        sw[kb][qb][1] = pack2(p2 * (dp[2] - d4.z), p3 * (dp[3] - d4.w));
+      }
     }
     // dV^T += dO^T P, dK^T += Q^T dS over the chunk's 64 queries (two k steps of 32)
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      const bf16x8 pf = cat8(make_uint2(pw[2 * ks][0], pw[2 * ks][1]),
-                             make_uint2(pw[2 * ks + 1][0], pw[2 * ks + 1][1]));
-      const bf16x8 sf = cat8(make_uint2(sw[2 * ks][0], sw[2 * ks][1]),
-                             make_uint2(sw[2 * ks + 1][0], sw[2 * ks + 1][1]));
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const int row = (db * 16 + c) * TS + ks * 32 + lg * 4;
-        dvt[db] = mfma16(ld_perm(&dOTs[b][row]), pf, dvt[db]);
-        dkt[db] = mfma16(ld_perm(&QTs[b][row]), sf, dkt[db]);
+        const bf16x8 dot_ = ld_tr8(&dOs[b][ks * 32 * RS], RS, db * 16, lane);
+        const bf16x8 qt_ = ld_tr8(&Qs[b][ks * 32 * RS], RS, db * 16, lane);
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          const bf16x8 pf = cat8(make_uint2(pw[kb][2 * ks][0], pw[kb][2 * ks][1]),
+                                 make_uint2(pw[kb][2 * ks + 1][0], pw[kb][2 * ks + 1][1]));
+          const bf16x8 sf = cat8(make_uint2(sw[kb][2 * ks][0], sw[kb][2 * ks][1]),
+                                 make_uint2(sw[kb][2 * ks + 1][0], sw[kb][2 * ks + 1][1]));
+          dvt[kb][db] = mfma16(dot_, pf, dvt[kb][db]);
+          dkt[kb][db] = mfma16(qt_, sf, dkt[kb][db]);
+        }
       }
     }
     if (ic + 1 < NCH) sstore(b ^ 1);
     lds_barrier();
   }
-  // lane: dims db*16 + 4*lg + i of key `key`
-  if (key < n) {
+  // lane: dims db*16 + 4*lg + i of key kw0 + kb*16 + c
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    const int key = kw0 + kb * 16 + c;
+    if (key >= n) continue;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      const uint2 a = make_uint2(pack2(dkt[db][0] * tau, dkt[db][1] * tau),
-                                 pack2(dkt[db][2] * tau, dkt[db][3] * tau));
-      const uint2 bb = make_uint2(pack2(dvt[db][0], dvt[db][1]), pack2(dvt[db][2], dvt[db][3]));
+      const uint2 a = make_uint2(pack2(dkt[kb][db][0] * tau, dkt[kb][db][1] * tau),
+                                 pack2(dkt[kb][db][2] * tau, dkt[kb][db][3] * tau));
+      const uint2 bb = make_uint2(pack2(dvt[kb][db][0], dvt[kb][db][1]),
+                                  pack2(dvt[kb][db][2], dvt[kb][db][3]));
       *reinterpret_cast<uint2*>(dk + (prob * R + key) * D + db * 16 + lg * 4) = a;
       *reinterpret_cast<uint2*>(dv + (prob * R + key) * D + db * 16 + lg * 4) = bb;
     }
@@ -262,11 +274,10 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
   constexpr int KTL = 64;         // keys per tile
   constexpr int DB = D / 16;
   constexpr int CPR = D / 8;
-  constexpr int KS = D + 8;       // LDS row stride of K, V ([key][d])
-  constexpr int TS = KTL + 8;     // LDS row stride of K^T ([d][key])
+  constexpr int KS = 48;          // LDS row stride of K ([key][d]; 96 bytes: see ld_tr8)
+  constexpr int VS = D + 8;       // LDS row stride of V (conflict-free 16-byte row reads)
   __shared__ __attribute__((aligned(16))) bf16 Ks[2][KTL * KS];
-  __shared__ __attribute__((aligned(16))) bf16 Vs[2][KTL * KS];
-  __shared__ __attribute__((aligned(16))) bf16 KTs[2][D * TS];
+  __shared__ __attribute__((aligned(16))) bf16 Vs[2][KTL * VS];
 
   const int bid = blockIdx.x;
   const int64_t prob = (int64_t)((bid >> 3) / QT) * 8 + (bid & 7);
@@ -322,9 +333,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
   auto sstore = [&](int b) {
     if (!stager) return;
     stu4(&Ks[b][skey * KS + sch], rk);
-    stu4(&Vs[b][skey * KS + sch], rv);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) KTs[b][(sch + j) * TS + skey] = u4_elem(rk, j);
+    stu4(&Vs[b][skey * VS + sch], rv);
   };
 
   f32x4 acc[DB][2];
@@ -336,7 +345,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       const typename Dot<D>::frag kfr = Dot<D>::lds(&Ks[b][(kb * 16 + c) * KS], lg);
-      const typename Dot<D>::frag vfr = Dot<D>::lds(&Vs[b][(kb * 16 + c) * KS], lg);
+      const typename Dot<D>::frag vfr = Dot<D>::lds(&Vs[b][(kb * 16 + c) * VS], lg);
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
         const f32x4 s = Dot<D>::mma(kfr, qf[qb]);
@@ -349,16 +358,15 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
         }
       }
     }
-    // dQ^T += K^T dS^T  (k = keys, permuted to match the S^T layout)
+    // dQ^T += K^T dS^T  (k = keys, in the S^T tile order)
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        const bf16x8 sf = pack8(dsv[2 * ks][qb], dsv[2 * ks + 1][qb]);
+      for (int db = 0; db < DB; ++db) {
+        const bf16x8 kt_ = ld_tr8(&Ks[b][ks * 32 * KS], KS, db * 16, lane);
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
-          acc[db][qb] = mfma16(ld_perm(&KTs[b][(db * 16 + c) * TS + ks * 32 + lg * 4]), sf,
-                               acc[db][qb]);
+        for (int qb = 0; qb < 2; ++qb)
+          acc[db][qb] = mfma16(kt_, pack8(dsv[2 * ks][qb], dsv[2 * ks + 1][qb]), acc[db][qb]);
       }
   };
 
@@ -394,7 +402,7 @@ hipError_t launch_item_attn_bwd(const Geo& g, const bf16* q, const bf16* k, cons
                                 const bf16* o, const bf16* dout, const float* lse, bf16* dq,
                                 bf16* dk, bf16* dv, hipStream_t s) {
   const int64_t P = (int64_t)g.NC * g.heads;
-  const int KT = (g.R + 63) / 64;
+  const int KT = (g.R + 127) / 128;
   const int QT = (g.R + 127) / 128;
   const unsigned grid_kv = (unsigned)((P + 7) / 8 * 8 * KT);
   const unsigned grid_q = (unsigned)((P + 7) / 8 * 8 * QT);

@@ -46,6 +46,17 @@ __device__ __forceinline__ bf16x4 lds_read_tr16(const bf16* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(p));
 }
 
+// MFMA fragment whose k positions run down the rows of a row-major LDS tile T (row stride ls
+// elements): lane (g, c) receives column c0 + c of rows 4g .. 4g+3 (slots 0-3) and
+// 16 + 4g .. 16 + 4g + 3 (slots 4-7).  That is the k order of two 16-row D tiles packed
+// side by side, so an S tile can meet the transposed operand it multiplies.  Conflict-free
+// when ls * 2 bytes is an odd multiple of 32.
+__device__ __forceinline__ bf16x8 ld_tr8(const bf16* T, int ls, int c0, int lane) {
+  const bf16* p = T + (lane >> 2) * ls + c0 + 4 * (lane & 3);
+  const bf16x4 lo = lds_read_tr16(p), hi = lds_read_tr16(p + 16 * ls);
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 

@@ -166,12 +166,8 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
       }
     }
   };
-  // fragment of the 16 columns starting at c0: slots 0-3 from rows 0-15, 4-7 from rows 16-31
-  auto frag = [&](const bf16* T, int ls, int c0) -> bf16x8 {
-    const bf16* p = T + (lane >> 2) * ls + c0 + 4 * (lane & 3);
-    const bf16x4 lo = lds_read_tr16(p), hi = lds_read_tr16(p + 16 * ls);
-    return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-  };
+  // fragment of the 16 columns starting at c0 (k positions: the slice's 32 cells)
+  auto frag = [&](const bf16* T, int ls, int c0) -> bf16x8 { return ld_tr8(T, ls, c0, lane); };
 
   f32x4 acc[NBW][KBW];
 #pragma unroll
