@@ -19,9 +19,27 @@ namespace {
 
 constexpr int BM = GEMM_BM;
 constexpr int MI = BM / 32;  // 16-row blocks per wave (2 x 2 waves, each BM/2 rows)
-constexpr int BK = 32;
-constexpr int LDS_STRIDE = BK + 8;  // bf16 elements per LDS row (16-byte pad)
-constexpr int CPRK = BK / 8;        // 16-byte chunks per staged row
+constexpr int BK = 32;       // k per pipeline stage: one 64-byte LDS row per operand row
+
+// Source of the 16-byte loads of rows that do not exist (past M, or K/V rows of test cells).
+__device__ __attribute__((aligned(16))) const uint4 kZeroChunk = {0u, 0u, 0u, 0u};
+
+// Slot of 16-byte k chunk kc (0..3) in LDS row r: rows are 64 bytes, so 4 consecutive rows
+// span the 64 banks; rotating the chunks by (r / 4) % 4 lets 16 consecutive rows read the same
+// kc without bank conflicts.
+__device__ __forceinline__ int kslot(int r, int kc) { return kc ^ ((r >> 2) & 3); }
+
+// 16 bytes per lane from global memory into LDS at lds_dst + 16 * lane (lds_dst wave-uniform).
+// Issued through inline assembly so that the compiler does not add its own conservative
+// vmcnt waits before later LDS reads: the pipeline waits for these loads explicitly.
+__device__ __forceinline__ void lds_dma16(const void* src, bf16* lds_dst) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds_dst);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(m0v), "v"(src)
+               : "memory", "m0");
+}
 
 // Normal CDF Phi(x) = (1 + erf(x / sqrt 2)) / 2 with erf from Abramowitz & Stegun 7.1.26
 // (|error| <= 1.5e-7): erf(z) = 1 - t (a1 + t (a2 + ... + t a5)) exp(-z^2), t = 1 / (1 + p z)
@@ -81,14 +99,15 @@ __device__ __forceinline__ f32x4 unpack4(uint2 u) {
 template <int BN, int EPI>
 __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   constexpr int NB = BN / 32;          // 16-wide column blocks per wave
-  constexpr int BCH = BN * CPRK / 256; // 16-byte chunks of the B tile per thread
-  constexpr int TS = BN + 8;  // epilogue tile row stride (elements)
-  constexpr int MAIN_BYTES = 2 * (BM + BN) * LDS_STRIDE * 2;
+  constexpr int TS = BN + 8;           // epilogue tile row stride (elements)
+  constexpr int S = BN > 192 ? 3 : 4;  // pipeline stages in the LDS ring
+  constexpr int A_EL = BM * BK;        // elements of one stage's A rows
+  constexpr int STAGE_EL = (BM + BN) * BK;
+  constexpr int NBB = BN / 64;         // 1 KB blocks of B per wave and stage
+  constexpr int RING_BYTES = S * STAGE_EL * 2;
   constexpr int TILE_BYTES = BM * TS * 2;
-  __shared__ __attribute__((aligned(16))) char smem[MAIN_BYTES > TILE_BYTES ? MAIN_BYTES : TILE_BYTES];
-  bf16 (*As)[BM * LDS_STRIDE] = reinterpret_cast<bf16 (*)[BM * LDS_STRIDE]>(smem);
-  bf16 (*Bs)[BN * LDS_STRIDE] =
-      reinterpret_cast<bf16 (*)[BN * LDS_STRIDE]>(smem + 2 * BM * LDS_STRIDE * 2);
+  __shared__ __attribute__((aligned(16))) char smem[RING_BYTES > TILE_BYTES ? RING_BYTES : TILE_BYTES];
+  bf16* ring = reinterpret_cast<bf16*>(smem);  // stage slot s: A at s*STAGE_EL, B after A
   bf16* tile = reinterpret_cast<bf16*>(smem);  // epilogue: [BM][TS], after the main loop
   __shared__ float red[2][BM];
   __shared__ float cred[2][2][BN];
@@ -99,11 +118,20 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   const int lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int lr = lane & 15, lg = lane >> 4;
-  const int64_t m0 = (int64_t)blockIdx.x * BM;
-  const int n0 = blockIdx.y * BN;
+  // Workgroup -> (row tile bx, column tile by).  The hardware deals consecutive workgroups
+  // round-robin over the 8 XCDs; all column tiles of a row tile are given consecutive slots
+  // of one XCD so that the row tile's A rows are fetched from memory once and then hit that
+  // XCD's L2.
+  const int NY = a.N / BN;
+  const int idx = (int)(blockIdx.x >> 3), xcd = (int)(blockIdx.x & 7);
+  const int64_t bx = (int64_t)(idx / NY) * 8 + xcd;
+  const int by = idx % NY;
+  const int64_t m0 = bx * BM;
+  if (m0 >= a.M) return;
+  const int n0 = by * BN;
   const Geo& g = a.g;
 
-  if (EPI == EPI_ITEM_QKV && blockIdx.y > 0) {
+  if (EPI == EPI_ITEM_QKV && by > 0) {
     // K and V exist for train rows only: skip tiles made of test rows alone
     int64_t last = m0 + BM - 1 < a.M ? m0 + BM - 1 : a.M - 1;
     int64_t c0 = m0 / g.R, c1 = last / g.R;
@@ -115,61 +143,51 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
     if (!any) return;
   }
 
-  // ---- global -> register staging assignment
-  constexpr int ACH = BM * CPRK / 256;  // 16-byte chunks of the A tile per thread
-  int64_t aoff[ACH];
-  bool aval[ACH];
-  int arow[ACH], akc[ACH];
-#pragma unroll
-  for (int i = 0; i < ACH; ++i) {
-    int c = tid + 256 * i;
-    arow[i] = c / CPRK;
-    akc[i] = (c % CPRK) * 8;
-    int64_t m = m0 + arow[i];
-    aval[i] = m < a.M;
-    aoff[i] = aval[i] && a.amode != ROWS_ITEM_HM ? row_addr(g, a.amode, m, a.lda) : 0;
-  }
-  int brow[BCH], bkc[BCH];
-#pragma unroll
-  for (int i = 0; i < BCH; ++i) {
-    int c = tid + 256 * i;
-    brow[i] = c / CPRK;
-    bkc[i] = (c % CPRK) * 8;
-  }
-  const bf16* Bt = a.Bt + (int64_t)n0 * a.K;
-
-  uint4 ra[ACH], rb[BCH];
-  // head-major item gradients: per row, the column (global active column) and the row index
-  int64_t hcol[ACH];
-  int hr[ACH];
+  // ---- operand streaming.  Every stage moves A rows [m0, m0+64) and B rows [n0, n0+BN), k in
+  // [k0, k0+32), straight from memory into the stage's LDS slot (global_load_lds: lane L of a
+  // wave fills bytes 16L..16L+15 of the wave's 1 KB block).  LDS position p (16-byte units)
+  // holds row p / 4, k chunk kslot^-1(p % 4); this lane's A position is wave*64 + lane.
+  const int ar = (wave * 64 + lane) >> 2;
+  const int akc = kslot(ar, lane & 3);
+  const int64_t am = m0 + ar;
+  const bool arow_ok = am < a.M;
+  const bf16* zero = reinterpret_cast<const bf16*>(&kZeroChunk);
+  const bf16* aptr = zero;  // row address + chunk, for compact / native rows
+  int64_t hcol = 0;
+  int hr = 0, hntr = 0;
   if (a.amode == ROWS_ITEM_HM) {
-#pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      const int64_t m = m0 + arow[i];
-      hcol[i] = m / g.R;
-      hr[i] = (int)(m - hcol[i] * g.R);
+    if (arow_ok) {
+      hcol = am / g.R;
+      hr = (int)(am - hcol * g.R);
+      hntr = g.ds[g.col_ds[hcol]].n_train;
     }
+  } else if (arow_ok) {
+    aptr = a.A + row_addr(g, a.amode, am, a.lda) + akc * 8;
   }
-  auto gload = [&](int k0) {
+  const bf16* bptr[NBB];
 #pragma unroll
-    for (int i = 0; i < ACH; ++i) {
-      if (a.amode == ROWS_ITEM_HM) {
-        int part = 0;
-        const int64_t off = aval[i] ? item_hm_offset(g, hcol[i], hr[i], k0 + akc[i], &part) : -1;
-        const bf16* base = part == 0 ? a.A : (part == 1 ? a.A2 : a.A3);
-        ra[i] = off >= 0 ? ldu4(base + off) : make_uint4(0, 0, 0, 0);
-      } else {
-        ra[i] = aval[i] ? ldu4(a.A + aoff[i] + k0 + akc[i]) : make_uint4(0, 0, 0, 0);
-      }
+  for (int t = 0; t < NBB; ++t) {
+    const int p = (wave + 4 * t) * 64 + lane;
+    const int n = p >> 2;
+    bptr[t] = a.Bt + (int64_t)(n0 + n) * a.K + kslot(n, p & 3) * 8;
+  }
+  auto issue = [&](int st) {
+    bf16* sa = ring + (st % S) * STAGE_EL;
+    const int k0 = st * BK;
+    const bf16* src = arow_ok ? aptr + k0 : zero;
+    if (a.amode == ROWS_ITEM_HM) {
+      // k -> part (Q, K, V), head, offset in head; K and V rows exist for train rows only
+      const int k = k0 + akc * 8;
+      const int part = k / BN, within = k - part * BN;
+      const int head = within / g.d, jj = within - head * g.d;
+      const bf16* base = part == 0 ? a.A : (part == 1 ? a.A2 : a.A3);
+      src = arow_ok && (part == 0 || hr < hntr)
+                ? base + ((hcol * g.heads + head) * g.R + hr) * (int64_t)g.d + jj
+                : zero;
     }
+    lds_dma16(src, sa + wave * 512);
 #pragma unroll
-    for (int i = 0; i < BCH; ++i) rb[i] = ldu4(Bt + (int64_t)brow[i] * a.K + k0 + bkc[i]);
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < ACH; ++i) stu4(&As[buf][arow[i] * LDS_STRIDE + akc[i]], ra[i]);
-#pragma unroll
-    for (int i = 0; i < BCH; ++i) stu4(&Bs[buf][brow[i] * LDS_STRIDE + bkc[i]], rb[i]);
+    for (int t = 0; t < NBB; ++t) lds_dma16(bptr[t] + k0, sa + A_EL + (wave + 4 * t) * 512);
   };
 
   // per-column epilogue parameters of this column tile, staged once
@@ -179,43 +197,83 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
     if (EPI == EPI_LN) cpar[2][tid] = a.beta[tid];
   }
 
+  // ---- epilogue inputs (residual, x-hat, pre-activation) do not depend on the product: their
+  // rows are fetched into registers now, so that they travel with the first stages instead of
+  // costing a memory round trip after the main loop.
+  constexpr int CPRW = BN / 8;              // 16-byte chunks per tile row
+  constexpr int NCH = BM * CPRW / 256;      // chunks per thread of one tile
+  constexpr bool IN0 = EPI == EPI_GELU_BWD || EPI == EPI_DX || EPI == EPI_LN || EPI == EPI_LN_BWD;
+  constexpr bool IN1 = EPI == EPI_LN_BWD;
+  uint4 pin0[IN0 ? NCH : 1], pin1[IN1 ? NCH : 1];
+  if (IN0) {
+    if (tid < BM) {
+      const int64_t m = m0 + tid;
+      int64_t off = -1;
+      if (m < a.M) {
+        if (EPI == EPI_GELU_BWD) off = m * a.ldo;
+        else if (EPI == EPI_LN) off = row_addr(g, a.rmode, m, BN);
+        else off = m * BN;
+      }
+      rbase[tid] = off;
+    }
+    lds_barrier();
+    const bf16* src0 = EPI == EPI_GELU_BWD ? a.aux + n0 : a.resid;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int ch = tid + 256 * c;
+      const int64_t off = rbase[ch / CPRW];
+      const int cc = (ch % CPRW) * 8;
+      pin0[c] = off >= 0 ? ldu4(src0 + off + cc) : make_uint4(0, 0, 0, 0);
+      if (IN1) pin1[c] = off >= 0 ? ldu4(a.aux + off + cc) : make_uint4(0, 0, 0, 0);
+    }
+  }
+
   f32x4 acc[MI][NB];
 #pragma unroll
   for (int i = 0; i < MI; ++i)
 #pragma unroll
     for (int j = 0; j < NB; ++j) acc[i][j] = zero4();
 
+  // Stage kt is consumed at iteration kt; S - 1 stages are in flight ahead of it.  Each wave
+  // waits for its own loads of stage kt (vmcnt counts in issue order; a stage is 1 + NBB
+  // loads), then the barrier makes every wave's part visible and frees the slot of stage
+  // kt - 1, which stage kt + S - 1 refills.
   const int KT = a.K / BK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
+#pragma unroll
+  for (int st = 0; st < S - 1; ++st)
+    if (st < KT) issue(st);
   for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < KT) gload((kt + 1) * BK);
-#pragma unroll
-    for (int ks = 0; ks < BK / 32; ++ks) {
-      bf16x8 af[MI], bfr[NB];
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-        af[i] = ld8(&As[cur][(wm * (BM / 2) + i * 16 + lr) * LDS_STRIDE + ks * 32 + lg * 8]);
-#pragma unroll
-      for (int j = 0; j < NB; ++j)
-        bfr[j] = ld8(&Bs[cur][(wn * (BN / 2) + j * 16 + lr) * LDS_STRIDE + ks * 32 + lg * 8]);
-#pragma unroll
-      for (int i = 0; i < MI; ++i)
-#pragma unroll
-        for (int j = 0; j < NB; ++j) acc[i][j] = mfma16(bfr[j], af[i], acc[i][j]);
+    if (kt + S - 2 < KT) {
+      asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"((S - 2) * (1 + NBB)) : "memory");
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
     }
-    if (kt + 1 < KT) sstore(cur ^ 1);
-    __syncthreads();
+    if (kt + S - 1 < KT) issue(kt + S - 1);
+    const bf16* sa = ring + (kt % S) * STAGE_EL;
+    const bf16* sb = sa + A_EL;
+    bf16x8 af[MI], bfr[NB];
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+      const int r = wm * (BM / 2) + i * 16 + lr;
+      af[i] = ld8(&sa[r * BK + kslot(r, lg) * 8]);
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int n = wn * (BN / 2) + j * 16 + lr;
+      bfr[j] = ld8(&sb[n * BK + kslot(n, lg) * 8]);
+    }
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j) acc[i][j] = mfma16(bfr[j], af[i], acc[i][j]);
   }
+  lds_barrier();  // every wave is done with the ring before the epilogue tile reuses it
 
   // ---- epilogues.  acc[i][j][q] is C[row, col] with
   //   row = m0 + wm*BM/2 + i*16 + lr,  col = n0 + wn*BN/2 + j*16 + lg*4 + q
   // Global traffic goes through the LDS tile [BM][TS] in 16-byte row chunks: residual / x-hat
   // inputs are loaded into it, outputs are written into it and copied out row by row.
   const int cb0 = wn * (BN / 2) + lg * 4;  // tile column of q = 0 for j = 0
-  constexpr int CPRW = BN / 8;             // 16-byte chunks per tile row
   auto rloc = [&](int i) { return wm * (BM / 2) + i * 16 + lr; };
 
   // per-row element offsets: ROWS_COMPACT with leading dimension ld, ROWS_NATIVE, or the
@@ -237,12 +295,12 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
       rbase[tid] = off;
     }
   };
-  // tile <- rows of src (columns [c0, c0 + BN)); rows without an offset read as 0
-  auto load_tile = [&](const bf16* src, int c0) {
-    for (int ch = tid; ch < BM * CPRW; ch += 256) {
-      const int row = ch / CPRW, cc = (ch % CPRW) * 8;
-      const int64_t off = rbase[row];
-      stu4(&tile[row * TS + cc], off >= 0 ? ldu4(src + off + c0 + cc) : make_uint4(0, 0, 0, 0));
+  // tile <- prefetched rows
+  auto fill_tile = [&](const uint4* pin) {
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int ch = tid + 256 * c;
+      stu4(&tile[(ch / CPRW) * TS + (ch % CPRW) * 8], pin[c]);
     }
   };
   // rows of dst <- tile (columns [c0, c0 + BN)); head-major destinations when hm is set
@@ -276,7 +334,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
 
   if (EPI == EPI_BIAS || EPI == EPI_GELU_FWD || EPI == EPI_ITEM_QKV) {
     if (EPI == EPI_ITEM_QKV)
-      set_rows(ROWS_COMPACT, 0, blockIdx.y);
+      set_rows(ROWS_COMPACT, 0, by);
     else
       set_rows(ROWS_COMPACT, a.ldo, -1);
 #pragma unroll
@@ -287,7 +345,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
     }
     lds_barrier();
     if (EPI == EPI_ITEM_QKV) {
-      bf16* dst = blockIdx.y == 0 ? a.out : (blockIdx.y == 1 ? a.out2 : a.out3);
+      bf16* dst = by == 0 ? a.out : (by == 1 ? a.out2 : a.out3);
       store_tile(dst, 0, true);
       return;
     }
@@ -314,9 +372,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   }
 
   if (EPI == EPI_GELU_BWD) {
-    set_rows(ROWS_COMPACT, a.ldo, -1);
-    lds_barrier();
-    load_tile(a.aux, n0);
+    fill_tile(pin0);  // rbase still holds the compact rows (leading dimension ldo)
     lds_barrier();
 #pragma unroll
     for (int i = 0; i < MI; ++i)
@@ -337,9 +393,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   }
 
   if (EPI == EPI_DX) {
-    set_rows(ROWS_COMPACT, BN, -1);
-    lds_barrier();
-    load_tile(a.resid, 0);
+    fill_tile(pin0);
     lds_barrier();
 #pragma unroll
     for (int i = 0; i < MI; ++i)
@@ -379,9 +433,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   };
 
   if (EPI == EPI_LN) {
-    set_rows(a.rmode, BN, -1);
-    lds_barrier();
-    load_tile(a.resid, 0);
+    fill_tile(pin0);
     lds_barrier();
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
@@ -427,16 +479,14 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   if (EPI == EPI_LN_BWD) {
     // dh = acc + resid; du = rstd * (g - mean(g) - xhat * mean(g * xhat)), g = dh * gamma;
     // column partial sums of dh * xhat (dgamma) and dh (dbeta) per workgroup
-    set_rows(ROWS_COMPACT, BN, -1);
-    lds_barrier();
-    load_tile(a.resid, 0);
+    fill_tile(pin0);  // rbase still holds the compact rows
     lds_barrier();
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
       for (int j = 0; j < NB; ++j) val[i][j] = acc[i][j] + tile4(i, j);
     lds_barrier();
-    load_tile(a.aux, 0);  // x-hat stays in the tile for the rest of the epilogue
+    fill_tile(pin1);  // x-hat stays in the tile for the rest of the epilogue
     lds_barrier();
     // column sums over the wave's rows: within the lane over i, then over the 16 row lanes
 #pragma unroll
@@ -459,7 +509,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
     float m1[MI], m2[MI];
     row_sum([&](int i, int j) { return val[i][j] * par4(1, j); }, m1);
     if (tid < BN) {
-      float* pg = a.part + (int64_t)blockIdx.x * 2 * BN;
+      float* pg = a.part + bx * 2 * BN;
       pg[tid] = cred[0][0][tid] + cred[0][1][tid];
       pg[BN + tid] = cred[1][0][tid] + cred[1][1][tid];
     }
@@ -484,7 +534,8 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
 
 template <int BN>
 static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
-  dim3 grid((unsigned)((a.M + BM - 1) / BM), (unsigned)(a.N / BN));
+  const int64_t mt = (a.M + BM - 1) / BM;
+  const dim3 grid((unsigned)((mt + 7) / 8 * 8 * (a.N / BN)));
   switch (a.epi) {
     case EPI_BIAS: k_gemm<BN, EPI_BIAS><<<grid, 256, 0, s>>>(a); break;
     case EPI_GELU_FWD: k_gemm<BN, EPI_GELU_FWD><<<grid, 256, 0, s>>>(a); break;

@@ -113,8 +113,17 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lg = lane >> 4, c = lane & 15;
   const int wn = w >> 2, wk = w & 3;
-  const int n0 = blockIdx.x * BN, k0 = blockIdx.y * BK;
-  const int64_t mb = (int64_t)blockIdx.z * a.chunk;
+  // Workgroup -> (cell chunk z, n-tile, k-tile).  The hardware deals consecutive workgroups
+  // round-robin over the 8 XCDs; all tiles of one chunk get consecutive slots of one XCD, so
+  // the chunk's rows come from memory once and are then served by that XCD's L2.
+  const int NX = a.N / BN, NT = NX * (a.K / BK);
+  const int idx = (int)(blockIdx.x >> 3), xcd = (int)(blockIdx.x & 7);
+  const int64_t zb = (int64_t)(idx / NT) * 8 + xcd;
+  const int tl = idx % NT;
+  const int tx = tl % NX, ty = tl / NX;
+  const int64_t mb = zb * a.chunk;
+  if (mb >= a.M) return;
+  const int n0 = tx * BN, k0 = ty * BK;
   const int64_t me = mb + a.chunk < a.M ? mb + a.chunk : a.M;
   const Geo& g = a.g;
 
@@ -175,7 +184,7 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
 #pragma unroll
     for (int j = 0; j < KBW; ++j) acc[i][j] = zero4();
   // bias gradient: the k-tile-0 waves with wk == 0 sum the dY fragments they already hold
-  const bool bsum = a.bpart && blockIdx.y == 0 && wk == 0;  // wave-uniform
+  const bool bsum = a.bpart && ty == 0 && wk == 0;  // wave-uniform
   float bacc[NBW];
 #pragma unroll
   for (int i = 0; i < NBW; ++i) bacc[i] = 0.f;
@@ -224,7 +233,7 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
   }
 
   // partial tile: lane holds rows n = wn*BN/2 + i*16 + 4*lg + q, column k = wk*BK/4 + j*16 + c
-  float* out = a.part + (int64_t)blockIdx.z * a.N * a.K;
+  float* out = a.part + zb * a.N * a.K;
 #pragma unroll
   for (int i = 0; i < NBW; ++i)
 #pragma unroll
@@ -241,7 +250,7 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
       float t = bacc[i];
       t += __shfl_xor(t, 16, 64);
       t += __shfl_xor(t, 32, 64);
-      if (lg == 0) a.bpart[(int64_t)blockIdx.z * a.N + n0 + wn * (BN / 2) + i * 16 + c] = t;
+      if (lg == 0) a.bpart[zb * a.N + n0 + wn * (BN / 2) + i * 16 + c] = t;
     }
   }
 }
@@ -332,7 +341,7 @@ hipError_t launch_wgrad_mfma(const WgradArgs& a, hipStream_t s) {
   const int Z = wgrad_chunks(a.M);
   const int BN = a.g.E, BK = a.g.E > 192 ? 128 : a.g.E;
   if (a.N % BN || a.K % BK) return hipErrorInvalidValue;
-  dim3 grid((unsigned)(a.N / BN), (unsigned)(a.K / BK), (unsigned)Z);
+  const dim3 grid((unsigned)(((int64_t)Z + 7) / 8 * 8 * (a.N / BN) * (a.K / BK)));
   WgradArgs b = a;
   b.chunk = WGRAD_CHUNK;
   switch (BN) {
