@@ -293,38 +293,39 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
   stage_frag<D>(kf, nks, c, lg, t0);  // K^T
   wave_lds_sync();
 
-  // ---- sweep 1 (query-major): dQ^T = K^T dS^T
+  // ---- sweep 1 (query-major): dQ^T = K^T dS^T, one pair of key blocks (32 keys) at a time
 #pragma unroll
   for (int qb = 0; qb < NKB; ++qb) {
     if (qb >= nkb) break;
     const int qq = qb * 16 + c;
-    f32x4 ds[NKB];
-#pragma unroll
-    for (int kb = 0; kb < NKB; ++kb) {
-      if (kb < nkb) {
-        const f32x4 s = FDot<D>::mma(kf[kb], qf[qb]);
-        const f32x4 dp = FDot<D>::mma(vf[kb], df[qb]);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float p = exp2_hw(fmaf(s[i], c2, nbq[qb]));
-          if (kb * 16 + lg * 4 + i >= S) p = 0.f;
-          ds[kb][i] = p * (dp[i] - dq[qb]);
-        }
-      } else {
-        ds[kb] = zero4();
-      }
-    }
     f32x4 acc[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db) acc[db] = zero4();
 #pragma unroll
-    for (int ks = 0; ks < NKB / 2; ++ks)
-      if (2 * ks < nkb) {
-        const bf16x8 sf = pack8(ds[2 * ks], ds[2 * ks + 1]);
+    for (int ks = 0; ks < NKB / 2; ++ks) {
+      if (2 * ks >= nkb) break;
+      f32x4 ds[2];
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
-          acc[db] = mfma16(ld_perm(&t0[(db * 16 + c) * TSF + ks * 32 + lg * 4]), sf, acc[db]);
+      for (int h = 0; h < 2; ++h) {
+        const int kb = 2 * ks + h;
+        if (kb < nkb) {
+          const f32x4 s = FDot<D>::mma(kf[kb], qf[qb]);
+          const f32x4 dp = FDot<D>::mma(vf[kb], df[qb]);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            float p = exp2_hw(fmaf(s[i], c2, nbq[qb]));
+            if (kb * 16 + lg * 4 + i >= S) p = 0.f;
+            ds[h][i] = p * (dp[i] - dq[qb]);
+          }
+        } else {
+          ds[h] = zero4();
+        }
       }
+      const bf16x8 sf = pack8(ds[0], ds[1]);
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        acc[db] = mfma16(ld_perm(&t0[(db * 16 + c) * TSF + ks * 32 + lg * 4]), sf, acc[db]);
+    }
     if (qq < S) {
 #pragma unroll
       for (int db = 0; db < DB; ++db) {

@@ -1,16 +1,16 @@
 // Item-axis flash attention on bf16 MFMA, backward pass, as two kernels that each recompute
 // the probabilities from the saved log-sum-exp:
 //
-//   dK/dV kernel (key-major): a workgroup owns 128 train rows (4 waves x 32 keys) of one
-//     problem and streams all query rows in chunks of 64 through LDS:
-//       S = Q K^T, dP = dO V^T            (D tiles: a lane holds 4 queries of one key)
-//       P = exp2(S tau log2e - lse log2e),  dS = P (dP - D),  D = rowsum(dO o O)
-//       dV^T += dO^T P,  dK^T += Q^T dS   (the S-layout tiles are used directly as B operands)
-//
-//   dQ kernel (query-major, shaped like the forward pass): a workgroup owns 128 query rows
-//     (4 waves x 32) and streams the train prefix in key tiles of 64 through LDS:
+//   dQ kernel first (query-major, shaped like the forward pass): a workgroup owns 128 query
+//     rows (4 waves x 32) and streams the train prefix in key tiles of 64 through LDS:
 //       S^T = K Q^T, dP^T = V dO^T        (a lane holds 4 keys of one query)
-//       dS^T = P^T (dP^T - D),  dQ^T += K^T dS^T
+//       dS^T = P^T (dP^T - D),  dQ^T += K^T dS^T,  D = rowsum(dO o O) also written out
+//
+//   dK/dV kernel (key-major): a workgroup owns 128 train rows (4 waves x 32 keys) of one
+//     problem and streams all query rows (Q, dO, D, lse) in chunks of 64 through LDS:
+//       S = Q K^T, dP = dO V^T            (D tiles: a lane holds 4 queries of one key)
+//       P = exp2(S tau log2e - lse log2e),  dS = P (dP - D)
+//       dV^T += dO^T P,  dK^T += Q^T dS   (the S-layout tiles are used directly as B operands)
 //
 // Both accumulate in registers only, so each output element is summed in a fixed order
 // (bitwise reproducible), and neither needs more than ~30 KB of LDS, which keeps several
@@ -102,6 +102,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
                                                         const bf16* __restrict__ o,
                                                         const bf16* __restrict__ dout,
                                                         const float* __restrict__ lse,
+                                                        const float* __restrict__ Dbuf,
                                                         bf16* __restrict__ dk,
                                                         bf16* __restrict__ dv, int KT) {
   constexpr int QC = 64;          // queries per chunk
@@ -134,6 +135,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
   const rsrc_t rO = make_rsrc(o + col * R * (int64_t)E + head * D, obytes);
   const rsrc_t rdO = make_rsrc(dout + col * R * (int64_t)E + head * D, obytes);
   const rsrc_t rL = make_rsrc(lse + prob * R, (uint32_t)R * 4);
+  const rsrc_t rD = make_rsrc(Dbuf + prob * R, (uint32_t)R * 4);
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int c = lane & 15, lg = lane >> 4;
@@ -151,11 +153,12 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
     vf[kb] = Dot<D>::buf(rV, key * rowQ + lg * Dot<D>::FB);
   }
 
-  // staging: threads 0-127 move Q, threads 128-255 move dO (and O for D, and the LSE); each
-  // handles NIT (query, 16-byte chunk) items; item it -> query it / CPR, dims (it % CPR) * 8
+  // staging: threads 0-127 move Q, threads 128-255 move dO (and D and the LSE); each handles
+  // NIT (query, 16-byte chunk) items; item it -> query it / CPR, dims (it % CPR) * 8.  Queries
+  // past R read Q = dO = D = lse = 0: their P is 1 but dO and dS vanish.
   const int half = tid >> 7, st = tid & 127;
-  uint4 ru[NIT], ro[NIT];
-  float rl[NIT];
+  uint4 ru[NIT];
+  float rd[NIT], rl[NIT];
   auto gload = [&](int qc0) {
 #pragma unroll
     for (int h = 0; h < NIT; ++h) {
@@ -165,8 +168,10 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
         ru[h] = bload16(rQ, qg * rowQ + d0 * 2);
       } else {
         ru[h] = bload16(rdO, qg * rowO + d0 * 2);
-        ro[h] = bload16(rO, qg * rowO + d0 * 2);
-        rl[h] = bloadf(rL, qg * 4);
+        if ((it % CPR) == 0) {
+          rd[h] = bloadf(rD, qg * 4);
+          rl[h] = bloadf(rL, qg * 4);
+        }
       }
     }
   };
@@ -176,17 +181,9 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
       const int it = st + h * 128;
       const int qq = it / CPR, d0 = (it % CPR) * 8;
       stu4(&(half == 0 ? Qs[b] : dOs[b])[qq * RS + d0], ru[h]);
-      if (half == 1) {
-        float dot = 0.f;
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-          dot = fmaf(bf2f(u4_elem(ru[h], j)), bf2f(u4_elem(ro[h], j)), dot);
-#pragma unroll
-        for (int off = 1; off < CPR; off <<= 1) dot += __shfl_xor(dot, off, 64);
-        if ((it % CPR) == 0) {
-          Dq[b][qq] = dot;
-          Lq[b][qq] = -rl[h] * LOG2E;  // queries past R read lse = 0: P = 1, but dO = 0
-        }
+      if (half == 1 && (it % CPR) == 0) {
+        Dq[b][qq] = rd[h];
+        Lq[b][qq] = -rl[h] * LOG2E;
       }
     }
   };
@@ -270,6 +267,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
                                                       const bf16* __restrict__ o,
                                                       const bf16* __restrict__ dout,
                                                       const float* __restrict__ lse,
+                                                      float* __restrict__ Dbuf,
                                                       bf16* __restrict__ dq, int QT) {
   constexpr int KTL = 64;         // keys per tile
   constexpr int DB = D / 16;
@@ -318,6 +316,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
     dot += __shfl_xor(dot, 32, 64);
     Dv[qb] = dot;
     nb[qb] = -bloadf(rL, qq * 4) * LOG2E;
+    if (lg == 0 && (int)qq < R) Dbuf[prob * R + qq] = dot;
   }
 
   // key tile staging: thread -> (key, 16-byte chunk of its d values); keys past n read 0
@@ -399,19 +398,20 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
 }
 
 hipError_t launch_item_attn_bwd(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
-                                const bf16* o, const bf16* dout, const float* lse, bf16* dq,
-                                bf16* dk, bf16* dv, hipStream_t s) {
+                                const bf16* o, const bf16* dout, const float* lse, float* Dbuf,
+                                bf16* dq, bf16* dk, bf16* dv, hipStream_t s) {
   const int64_t P = (int64_t)g.NC * g.heads;
   const int KT = (g.R + 127) / 128;
   const int QT = (g.R + 127) / 128;
   const unsigned grid_kv = (unsigned)((P + 7) / 8 * 8 * KT);
   const unsigned grid_q = (unsigned)((P + 7) / 8 * 8 * QT);
+  // dQ first: it also writes D = rowsum(dO o O), which the dK/dV kernel reads
   if (g.d == 16) {
-    k_item_attn_dkdv<16><<<grid_kv, 256, 0, s>>>(g, q, k, v, o, dout, lse, dk, dv, KT);
-    k_item_attn_dq<16><<<grid_q, 256, 0, s>>>(g, q, k, v, o, dout, lse, dq, QT);
+    k_item_attn_dq<16><<<grid_q, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dq, QT);
+    k_item_attn_dkdv<16><<<grid_kv, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dk, dv, KT);
   } else {
-    k_item_attn_dkdv<32><<<grid_kv, 256, 0, s>>>(g, q, k, v, o, dout, lse, dk, dv, KT);
-    k_item_attn_dq<32><<<grid_q, 256, 0, s>>>(g, q, k, v, o, dout, lse, dq, QT);
+    k_item_attn_dq<32><<<grid_q, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dq, QT);
+    k_item_attn_dkdv<32><<<grid_kv, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dk, dv, KT);
   }
   return hipGetLastError();
 }
