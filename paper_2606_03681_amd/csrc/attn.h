@@ -12,10 +12,14 @@ hipError_t launch_item_attn_fwd(const Geo& g, const bf16* q, const bf16* k, cons
                                 bf16* o, float* lse, hipStream_t s);
 
 // Item-axis attention backward: dq, dk, dv head-major (dk, dv for train rows only).
-// Dbuf: [problem][R] float32 scratch, receives D = rowsum(dO o O) per query row.
-hipError_t launch_item_attn_bwd(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
-                                const bf16* o, const bf16* dout, const float* lse, float* Dbuf,
-                                bf16* dq, bf16* dk, bf16* dv, hipStream_t s);
+// Backward in two launches, dQ first: it also writes Dbuf ([problem][R] float32) with
+// D = rowsum(dO o O) per query row, which the dK/dV launch reads.
+hipError_t launch_item_attn_dq(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
+                               const bf16* o, const bf16* dout, const float* lse, float* Dbuf,
+                               bf16* dq, hipStream_t s);
+hipError_t launch_item_attn_dkdv(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
+                                 const bf16* o, const bf16* dout, const float* lse,
+                                 const float* Dbuf, bf16* dk, bf16* dv, hipStream_t s);
 
 // Feature-axis attention (cells of a row, per head).  qkv cell-major [cell][3E]; o, dout
 // cell-major [cell][E]; lse [cell][heads]; dqkv cell-major [cell][3E].  Requires

@@ -397,22 +397,29 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
   }
 }
 
-hipError_t launch_item_attn_bwd(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
-                                const bf16* o, const bf16* dout, const float* lse, float* Dbuf,
-                                bf16* dq, bf16* dk, bf16* dv, hipStream_t s) {
+hipError_t launch_item_attn_dq(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
+                               const bf16* o, const bf16* dout, const float* lse, float* Dbuf,
+                               bf16* dq, hipStream_t s) {
+  const int64_t P = (int64_t)g.NC * g.heads;
+  const int QT = (g.R + 127) / 128;
+  const unsigned grid = (unsigned)((P + 7) / 8 * 8 * QT);
+  if (g.d == 16)
+    k_item_attn_dq<16><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dq, QT);
+  else
+    k_item_attn_dq<32><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dq, QT);
+  return hipGetLastError();
+}
+
+hipError_t launch_item_attn_dkdv(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
+                                 const bf16* o, const bf16* dout, const float* lse,
+                                 const float* Dbuf, bf16* dk, bf16* dv, hipStream_t s) {
   const int64_t P = (int64_t)g.NC * g.heads;
   const int KT = (g.R + 127) / 128;
-  const int QT = (g.R + 127) / 128;
-  const unsigned grid_kv = (unsigned)((P + 7) / 8 * 8 * KT);
-  const unsigned grid_q = (unsigned)((P + 7) / 8 * 8 * QT);
-  // dQ first: it also writes D = rowsum(dO o O), which the dK/dV kernel reads
-  if (g.d == 16) {
-    k_item_attn_dq<16><<<grid_q, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dq, QT);
-    k_item_attn_dkdv<16><<<grid_kv, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dk, dv, KT);
-  } else {
-    k_item_attn_dq<32><<<grid_q, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dq, QT);
-    k_item_attn_dkdv<32><<<grid_kv, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dk, dv, KT);
-  }
+  const unsigned grid = (unsigned)((P + 7) / 8 * 8 * KT);
+  if (g.d == 16)
+    k_item_attn_dkdv<16><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dk, dv, KT);
+  else
+    k_item_attn_dkdv<32><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dk, dv, KT);
   return hipGetLastError();
 }
 

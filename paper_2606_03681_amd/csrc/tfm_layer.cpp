@@ -567,10 +567,14 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   T* dq = (T*)(ws + W.tq);
   T* dk = (T*)(ws + W.tk);
   T* dv = (T*)(ws + W.tv);
-  STEP("item_attn_bwd/mfma",
-       launch_item_attn_bwd(g, (const T*)(sv + S.qi), (const T*)(sv + S.ki),
-                            (const T*)(sv + S.vi), (const T*)(sv + S.oi), doi,
-                            (const float*)(sv + S.lsei), (float*)(ws + W.D), dq, dk, dv, s));
+  const T* qi = (const T*)(sv + S.qi);
+  const T* ki = (const T*)(sv + S.ki);
+  const T* vi = (const T*)(sv + S.vi);
+  const T* oi = (const T*)(sv + S.oi);
+  const float* lsei = (const float*)(sv + S.lsei);
+  float* Dq = (float*)(ws + W.D);
+  STEP("item_attn_dq/mfma", launch_item_attn_dq(g, qi, ki, vi, oi, doi, lsei, Dq, dq, s));
+  STEP("item_attn_dkdv/mfma", launch_item_attn_dkdv(g, qi, ki, vi, oi, doi, lsei, Dq, dk, dv, s));
   CHK(G.run(dq, 3 * E, h1, E, ROWS_COMPACT, o.Wqkv_i, o.bqkv_i, dk, dv));
   // dZ1 = LN1'(dZ2 + dQKV_i Wqkv_i), the gradients read head-major in place
   a = gemm_base(g, N, E, 3 * E, EPI_LN_BWD);
