@@ -100,7 +100,7 @@ template <int BN, int EPI>
 __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   constexpr int NB = BN / 32;          // 16-wide column blocks per wave
   constexpr int TS = BN + 8;           // epilogue tile row stride (elements)
-  constexpr int S = BN > 192 ? 3 : 4;  // pipeline stages in the LDS ring
+  constexpr int S = 3;  // pipeline stages in the LDS ring (48 KB at E = 192: 3 workgroups per CU)
   constexpr int A_EL = BM * BK;        // elements of one stage's A rows
   constexpr int STAGE_EL = (BM + BN) * BK;
   constexpr int NBB = BN / 64;         // 1 KB blocks of B per wave and stage
