@@ -85,9 +85,12 @@ hipError_t launch_zero_inactive(const Geo& g, bf16* native, hipStream_t s) {
   return hipGetLastError();
 }
 
-// One wave per cell, 8 waves per block, LN_CELLS cells per block; each lane holds up to 4 of
-// the E <= 256 values of a cell and keeps running column sums across the block's cells.
+// LN3 backward from the native dY: 512 threads = 16 half-waves; a half-wave owns one cell at a
+// time, lane l holding features 8l .. 8l+7 (E <= 256) in 16-byte pieces.  A block covers
+// LN_CELLS consecutive compact cells; half-wave h takes cells h, h + 16, ..., four per batch
+// with all their loads in flight, and keeps running column sums of dY * xhat and dY.
 constexpr int LN_CELLS = 256;
+constexpr int LN_BATCH = 4;
 
 __global__ __launch_bounds__(512) void k_ln_out_bwd(Geo g, const bf16* __restrict__ dY,
                                                     const bf16* __restrict__ xhat,
@@ -95,58 +98,86 @@ __global__ __launch_bounds__(512) void k_ln_out_bwd(Geo g, const bf16* __restric
                                                     const float* __restrict__ gamma,
                                                     bf16* __restrict__ dz,
                                                     float* __restrict__ part) {
-  __shared__ float red[8][2][256];
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  __shared__ float red[16][2][256];
+  const int tid = threadIdx.x, hw = tid >> 5, l = tid & 31;
   const int E = g.E;
-  float cs1[4] = {0.f, 0.f, 0.f, 0.f}, cs2[4] = {0.f, 0.f, 0.f, 0.f};
-  float gm[4];
+  const bool act = 8 * l < E;
+  float gm[8], cs1[8], cs2[8];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) gm[i] = lane + 64 * i < E ? gamma[lane + 64 * i] : 0.f;
+  for (int j = 0; j < 8; ++j) {
+    gm[j] = act ? gamma[8 * l + j] : 0.f;
+    cs1[j] = cs2[j] = 0.f;
+  }
   const int64_t c0 = (int64_t)blockIdx.x * LN_CELLS;
-  for (int cc = w; cc < LN_CELLS; cc += 8) {
-    const int64_t p = c0 + cc;
-    if (p >= g.N) break;
-    const int64_t src = native_cell(g, p) * E;
-    float dy[4], xv[4];
-    float s1 = 0.f, s2 = 0.f;
+  const int col0 = (int)(c0 / g.R), r0 = (int)(c0 - (int64_t)col0 * g.R);
+  for (int base = hw; base < LN_CELLS; base += 16 * LN_BATCH) {
+    uint4 dyv[LN_BATCH], xv[LN_BATCH];
+    float rs[LN_BATCH];
+    int64_t pc[LN_BATCH];
+    bool ok[LN_BATCH];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int e = lane + 64 * i;
-      dy[i] = 0.f;
-      xv[i] = 0.f;
-      if (e < E) {
-        dy[i] = bf2f(dY[src + e]);
-        xv[i] = bf2f(xhat[p * E + e]);
-        cs1[i] += dy[i] * xv[i];
-        cs2[i] += dy[i];
-        s1 += dy[i] * gm[i];
-        s2 += dy[i] * gm[i] * xv[i];
+    for (int u = 0; u < LN_BATCH; ++u) {
+      const int cc = base + 16 * u;
+      const int64_t p = c0 + cc;
+      pc[u] = p;
+      ok[u] = cc < LN_CELLS && p < g.N;
+      dyv[u] = xv[u] = make_uint4(0, 0, 0, 0);
+      rs[u] = 0.f;
+      if (ok[u]) {
+        int col = col0, r = r0 + cc;
+        while (r >= g.R) {
+          r -= g.R;
+          ++col;
+        }
+        const int64_t nat = ((int64_t)g.col_ds[col] * g.R + r) * g.S + g.col_c[col];
+        rs[u] = rstd[p];
+        if (act) {
+          dyv[u] = ldu4(dY + nat * E + 8 * l);
+          xv[u] = ldu4(xhat + p * E + 8 * l);
+        }
       }
     }
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      s1 += __shfl_xor(s1, o, 64);
-      s2 += __shfl_xor(s2, o, 64);
-    }
-    const float m1 = s1 / E, m2 = s2 / E, rs = rstd[p];
+    for (int u = 0; u < LN_BATCH; ++u) {
+      float dy[8], x[8];
+      float s1 = 0.f, s2 = 0.f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int e = lane + 64 * i;
-      if (e < E) dz[p * E + e] = f2bf(rs * (dy[i] * gm[i] - m1 - xv[i] * m2));
+      for (int j = 0; j < 8; ++j) {
+        dy[j] = bf2f(u4_elem(dyv[u], j));
+        x[j] = bf2f(u4_elem(xv[u], j));
+        cs1[j] += dy[j] * x[j];
+        cs2[j] += dy[j];
+        s1 += dy[j] * gm[j];
+        s2 += dy[j] * gm[j] * x[j];
+      }
+#pragma unroll
+      for (int o = 1; o < 32; o <<= 1) {
+        s1 += __shfl_xor(s1, o, 64);
+        s2 += __shfl_xor(s2, o, 64);
+      }
+      const float m1 = s1 / E, m2 = s2 / E;
+      if (ok[u] && act) {
+        uint4 o;
+        o.x = pack2(rs[u] * (dy[0] * gm[0] - m1 - x[0] * m2), rs[u] * (dy[1] * gm[1] - m1 - x[1] * m2));
+        o.y = pack2(rs[u] * (dy[2] * gm[2] - m1 - x[2] * m2), rs[u] * (dy[3] * gm[3] - m1 - x[3] * m2));
+        o.z = pack2(rs[u] * (dy[4] * gm[4] - m1 - x[4] * m2), rs[u] * (dy[5] * gm[5] - m1 - x[5] * m2));
+        o.w = pack2(rs[u] * (dy[6] * gm[6] - m1 - x[6] * m2), rs[u] * (dy[7] * gm[7] - m1 - x[7] * m2));
+        stu4(dz + pc[u] * E + 8 * l, o);
+      }
     }
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    red[w][0][lane + 64 * i] = cs1[i];
-    red[w][1][lane + 64 * i] = cs2[i];
+  for (int j = 0; j < 8; ++j) {
+    red[hw][0][8 * l + j] = cs1[j];
+    red[hw][1][8 * l + j] = cs2[j];
   }
   __syncthreads();
-  if (threadIdx.x < 2 * E) {
-    const int t = threadIdx.x / E, e = threadIdx.x % E;
-    float s = 0.f;
+  if (tid < 2 * E) {
+    const int t = tid / E, e = tid % E;
+    float sm = 0.f;
 #pragma unroll
-    for (int ww = 0; ww < 8; ++ww) s += red[ww][t][e];
-    part[(int64_t)blockIdx.x * 2 * E + t * E + e] = s;
+    for (int h = 0; h < 16; ++h) sm += red[h][t][e];
+    part[(int64_t)blockIdx.x * 2 * E + t * E + e] = sm;
   }
 }
 
