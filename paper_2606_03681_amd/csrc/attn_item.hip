@@ -26,7 +26,6 @@ namespace {
 constexpr int KT = 64;   // keys per tile
 constexpr int QWV = 32;  // queries per wave
 constexpr int QWG = 128; // queries per workgroup
-constexpr float LOG2E = 1.4426950408889634f;
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
@@ -38,8 +37,8 @@ template <>
 struct QK<32> {
   typedef bf16x8 frag;
   static __device__ __forceinline__ frag load(const bf16* row, int lg) { return ld8(row + lg * 8); }
-  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, zero4(), 0, 0, 0);
+  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b, const f32x4& c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
   }
 };
 
@@ -50,8 +49,8 @@ struct QK<16> {
   static __device__ __forceinline__ frag load(const bf16* row, int lg) {
     return *reinterpret_cast<const s16x4*>(row + lg * 4);
   }
-  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b) {
-    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, zero4(), 0, 0, 0);
+  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b, const f32x4& c) {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
   }
 };
 
@@ -120,12 +119,13 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
     stu4(&Vs[buf][skey * VS + sch], rv);
   };
 
-  const float c2 = LOG2E / sqrtf((float)D);
-  // Running reference of the exponent, per query block, in raw-score units.  It is raised
-  // only when a tile's maximum exceeds it by more than 8 (log2 units), so the probabilities
-  // stay below 2^8 and the rescale of the accumulators is rare.
-  float m[2] = {-INFINITY, -INFINITY};
-  const float slack = 8.0f / c2;
+  // K arrives pre-multiplied by log2(e)/sqrt(d), so S^T = K Q^T is in the exp2 domain.  The MFMA
+  // accumulators start at -ref, a running reference of the exponent per query, so they return
+  // S^T - ref and p = exp2(acc) needs no further arithmetic.  The reference is set by the first
+  // tile and raised only when a tile's maximum exceeds it by more than 8, which keeps every p
+  // below 2^8 and makes the shift-and-rescale rare.
+  float ref[2] = {-INFINITY, -INFINITY};
+  constexpr float slack = 8.0f;
   // O^T accumulators: DB blocks of V^T rows plus one block whose first row is all ones, so
   // that row accumulates the softmax denominator with the same rescaling as O.
   f32x4 oacc[DB + 1][2];
@@ -141,13 +141,19 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
   }
 
   auto tile = [&](const int cur, const int t0, const bool tail) {
-    // S^T = K Q^T for 4 key blocks x 2 query blocks
+    // S^T - ref for 4 key blocks x 2 query blocks
     f32x4 sc[4][2];
+    f32x4 init[2];
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      const float r0 = ref[qb] == -INFINITY ? 0.f : -ref[qb];
+      init[qb][0] = init[qb][1] = init[qb][2] = init[qb][3] = r0;
+    }
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
       typename QK<D>::frag kf = QK<D>::load(&Ks[cur][(kb * 16 + c) * KS], lg);
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) sc[kb][qb] = QK<D>::mma(kf, qf[qb]);
+      for (int qb = 0; qb < 2; ++qb) sc[kb][qb] = QK<D>::mma(kf, qf[qb], init[qb]);
     }
     if (tail) {
 #pragma unroll
@@ -169,22 +175,25 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
                              fmaxf(sc[kb][qb][2], sc[kb][qb][3])));
       mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
       mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      if (__any(mx > m[qb] + slack)) {
-        const float mnew = fmaxf(m[qb], mx);
-        const float corr = exp2_hw((m[qb] - mnew) * c2);
-        m[qb] = mnew;
+      // first tile: ref = the tile maximum; later: raise ref by the excess when it is large
+      const bool first = ref[qb] == -INFINITY;
+      if (__any(first || mx > slack)) {
+        const float delta = first ? mx : fmaxf(mx, 0.f);
+        ref[qb] = first ? mx : ref[qb] + delta;
+        const float corr = exp2_hw(-delta);
 #pragma unroll
         for (int db = 0; db <= DB; ++db) oacc[db][qb] *= corr;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) sc[kb][qb] -= delta;
       }
-      const float mb = -m[qb] * c2;
 #pragma unroll
       for (int ks = 0; ks < 2; ++ks) {
         f32x4 a0 = sc[2 * ks][qb], a1 = sc[2 * ks + 1][qb];
         uint4 u;
-        u.x = pk_bf16(exp2_hw(fmaf(a0[0], c2, mb)), exp2_hw(fmaf(a0[1], c2, mb)));
-        u.y = pk_bf16(exp2_hw(fmaf(a0[2], c2, mb)), exp2_hw(fmaf(a0[3], c2, mb)));
-        u.z = pk_bf16(exp2_hw(fmaf(a1[0], c2, mb)), exp2_hw(fmaf(a1[1], c2, mb)));
-        u.w = pk_bf16(exp2_hw(fmaf(a1[2], c2, mb)), exp2_hw(fmaf(a1[3], c2, mb)));
+        u.x = pk_bf16(exp2_hw(a0[0]), exp2_hw(a0[1]));
+        u.y = pk_bf16(exp2_hw(a0[2]), exp2_hw(a0[3]));
+        u.z = pk_bf16(exp2_hw(a1[0]), exp2_hw(a1[1]));
+        u.w = pk_bf16(exp2_hw(a1[2]), exp2_hw(a1[3]));
         pf[qb][ks] = *reinterpret_cast<bf16x8*>(&u);
       }
     }
@@ -216,8 +225,7 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
   }
   if (NF < NT) tile(NF & 1, NF * KT, true);
 
-  // normalise and write O (cell-major) and the natural-log LSE
-  const float tau = 1.0f / sqrtf((float)D);
+  // normalise and write O (cell-major) and the natural-log LSE = ln 2 * (ref + log2 l)
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
     const float lt = __shfl(oacc[DB][qb][0], c, 64);  // row 0 of the ones block, lane (0, c)
@@ -232,7 +240,7 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
       u.y = pk_bf16(oacc[db][qb][2] * inv, oacc[db][qb][3] * inv);
       *reinterpret_cast<uint2*>(orow + db * 16 + lg * 4) = u;
     }
-    if (lg == 0) lse[prob * R + qq] = m[qb] * tau + logf(lt);
+    if (lg == 0) lse[prob * R + qq] = (ref[qb] + log2f(lt)) * 0.69314718055994531f;
   }
 }
 

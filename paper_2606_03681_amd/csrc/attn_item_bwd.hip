@@ -12,6 +12,10 @@
 //       P = exp2(S tau log2e - lse log2e),  dS = P (dP - D)
 //       dV^T += dO^T P,  dK^T += Q^T dS   (the S-layout tiles are used directly as B operands)
 //
+// K arrives pre-multiplied by log2(e)/sqrt(d) (see the item Q|K|V projection), so Q K^T is in
+// the exp2 domain.  The S accumulators start at -lse log2(e) and the dP accumulators at -D, so
+// the MFMA returns the exponent of P and dP - D directly: P = exp2(acc), dS = P (dP - D).
+//
 // Both accumulate in registers only, so each output element is summed in a fixed order
 // (bitwise reproducible), and neither needs more than ~30 KB of LDS, which keeps several
 // workgroups resident per CU.  Tiles are staged row-major with 16-byte stores; the
@@ -42,8 +46,8 @@ struct Dot<32> {
     uint4 u = bload16(r, off);
     return *reinterpret_cast<bf16x8*>(&u);
   }
-  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, zero4(), 0, 0, 0);
+  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b, const f32x4& c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
   }
   // sum over the lane's 8 elements of a * b
   static __device__ __forceinline__ float dot(const frag& a, const frag& b) {
@@ -67,8 +71,8 @@ struct Dot<16> {
     uint2 u = bload8(r, off);
     return *reinterpret_cast<s16x4*>(&u);
   }
-  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b) {
-    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, zero4(), 0, 0, 0);
+  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b, const f32x4& c) {
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
   }
   static __device__ __forceinline__ float dot(const frag& a, const frag& b) {
     const uint2 ua = *reinterpret_cast<const uint2*>(&a);
@@ -139,7 +143,6 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int c = lane & 15, lg = lane >> 4;
-  const float c2 = LOG2E / sqrtf((float)D);
   const float tau = 1.0f / sqrtf((float)D);
 
   // this lane's key column of key block kb in the S layout: t0 + w*32 + kb*16 + c; keys past
@@ -182,7 +185,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
       const int qq = it / CPR, d0 = (it % CPR) * 8;
       stu4(&(half == 0 ? Qs[b] : dOs[b])[qq * RS + d0], ru[h]);
       if (half == 1 && (it % CPR) == 0) {
-        Dq[b][qq] = rd[h];
+        Dq[b][qq] = -rd[h];
         Lq[b][qq] = -rl[h] * LOG2E;
       }
     }
@@ -207,18 +210,19 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
     for (int qb = 0; qb < 4; ++qb) {
       const typename Dot<D>::frag qa = Dot<D>::lds(&Qs[b][(qb * 16 + c) * RS], lg);
       const typename Dot<D>::frag da = Dot<D>::lds(&dOs[b][(qb * 16 + c) * RS], lg);
-      const float4 d4 = *reinterpret_cast<const float4*>(&Dq[b][qb * 16 + lg * 4]);
-      const float4 l4 = *reinterpret_cast<const float4*>(&Lq[b][qb * 16 + lg * 4]);
+      // seeds: -lse log2(e) and -D of the lane's 4 query rows
+      const f32x4 nl = *reinterpret_cast<const f32x4*>(&Lq[b][qb * 16 + lg * 4]);
+      const f32x4 nd = *reinterpret_cast<const f32x4*>(&Dq[b][qb * 16 + lg * 4]);
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        const f32x4 s = Dot<D>::mma(qa, kf[kb]);
-        const f32x4 dp = Dot<D>::mma(da, vf[kb]);
-        const float p0 = exp2_hw(fmaf(s[0], c2, l4.x)), p1 = exp2_hw(fmaf(s[1], c2, l4.y));
-        const float p2 = exp2_hw(fmaf(s[2], c2, l4.z)), p3 = exp2_hw(fmaf(s[3], c2, l4.w));
+        const f32x4 s = Dot<D>::mma(qa, kf[kb], nl);     // S log2(e) - lse log2(e)
+        const f32x4 dp = Dot<D>::mma(da, vf[kb], nd);    // dP - D
+        const float p0 = exp2_hw(s[0]), p1 = exp2_hw(s[1]);
+        const float p2 = exp2_hw(s[2]), p3 = exp2_hw(s[3]);
         pw[kb][qb][0] = pack2(p0, p1);
         pw[kb][qb][1] = pack2(p2, p3);
-        sw[kb][qb][0] = pack2(p0 * (dp[0] - d4.x), p1 * (dp[1] - d4.y));
-        sw[kb][qb][1] = pack2(p2 * (dp[2] - d4.z), p3 * (dp[3] - d4.w));
+        sw[kb][qb][0] = pack2(p0 * dp[0], p1 * dp[1]);
+        sw[kb][qb][1] = pack2(p2 * dp[2], p3 * dp[3]);
       }
     }
     // dV^T += dO^T P, dK^T += Q^T dS over the chunk's 64 queries (two k steps of 32)
@@ -298,9 +302,6 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int c = lane & 15, lg = lane >> 4;
   const int qw0 = qt * 128 + w * 32;
-  const float c2 = LOG2E / sqrtf((float)D);
-  const float tau = 1.0f / sqrtf((float)D);
-
   // per query block: Q^T and dO^T fragments (B operands), D = rowsum(dO o O), -lse log2(e);
   // queries past R read as zero (their results are not written)
   typename Dot<D>::frag qf[2], df[2];
@@ -339,6 +340,13 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
 #pragma unroll
   for (int db = 0; db < DB; ++db) acc[db][0] = acc[db][1] = zero4();
 
+  // seeds: -lse log2(e) and -D of the lane's query (one query per lane in the S^T layout)
+  f32x4 snl[2], snd[2];
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    snl[qb][0] = snl[qb][1] = snl[qb][2] = snl[qb][3] = nb[qb];
+    snd[qb][0] = snd[qb][1] = snd[qb][2] = snd[qb][3] = -Dv[qb];
+  }
   auto tile = [&](const int b, const int t0, const bool tail) {
     f32x4 dsv[4][2];
 #pragma unroll
@@ -347,13 +355,13 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
       const typename Dot<D>::frag vfr = Dot<D>::lds(&Vs[b][(kb * 16 + c) * VS], lg);
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
-        const f32x4 s = Dot<D>::mma(kfr, qf[qb]);
-        const f32x4 dp = Dot<D>::mma(vfr, df[qb]);
+        const f32x4 s = Dot<D>::mma(kfr, qf[qb], snl[qb]);    // exponent of P^T
+        const f32x4 dp = Dot<D>::mma(vfr, df[qb], snd[qb]);   // dP^T - D
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          float p = exp2_hw(fmaf(s[i], c2, nb[qb]));
+          float p = exp2_hw(s[i]);
           if (tail && t0 + kb * 16 + lg * 4 + i >= n) p = 0.f;
-          dsv[kb][qb][i] = p * (dp[i] - Dv[qb]);
+          dsv[kb][qb][i] = p * dp[i];
         }
       }
     }
@@ -383,15 +391,17 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
   }
   if (NF < NT) tile(NF & 1, NF * KTL, true);
 
-  // lane: dims db*16 + 4*lg + i of query qw0 + qb*16 + c
+  // lane: dims db*16 + 4*lg + i of query qw0 + qb*16 + c.  dQ = tau dS K, and the staged K
+  // is log2(e) tau K, so the factor left is 1 / log2(e) = ln 2.
+  constexpr float kLn2 = 0.69314718055994531f;
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
     const int qq = qw0 + qb * 16 + c;
     if (qq >= R) continue;
 #pragma unroll
     for (int db = 0; db < DB; ++db) {
-      const uint2 u = make_uint2(pack2(acc[db][qb][0] * tau, acc[db][qb][1] * tau),
-                                 pack2(acc[db][qb][2] * tau, acc[db][qb][3] * tau));
+      const uint2 u = make_uint2(pack2(acc[db][qb][0] * kLn2, acc[db][qb][1] * kLn2),
+                                 pack2(acc[db][qb][2] * kLn2, acc[db][qb][3] * kLn2));
       *reinterpret_cast<uint2*>(dq + (prob * R + qq) * D + db * 16 + lg * 4) = u;
     }
   }

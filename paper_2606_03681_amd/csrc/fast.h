@@ -29,7 +29,8 @@ enum {
   EPI_BIAS = 0,      // out = C (+ bias)
   EPI_GELU_FWD = 1,  // out = C + bias (MLP pre-activation), out2 = GELU(out)
   EPI_GELU_BWD = 2,  // out = C * GELU'(aux)
-  EPI_ITEM_QKV = 3,  // item Q|K|V + bias, written head-major; K, V for train rows only
+  EPI_ITEM_QKV = 3,  // item Q|K|V + bias, written head-major; K, V for train rows only; K is
+                     // stored times log2(e)/sqrt(d)
   EPI_LN = 4,        // out = LN(C + bias + resid); xhat, rstd saved
   EPI_LN_BWD = 5,    // dh = C + resid; out = LN'(dh) with xhat = aux, rstd_in; column partials
   EPI_DX = 6         // out (native) = C + resid

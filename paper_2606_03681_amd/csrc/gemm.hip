@@ -337,11 +337,15 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
       set_rows(ROWS_COMPACT, 0, by);
     else
       set_rows(ROWS_COMPACT, a.ldo, -1);
+    // item K is stored pre-multiplied by log2(e)/sqrt(d) (in fp32, before the bf16 rounding):
+    // the attention kernels then get scores in the exp2 domain straight from the MFMA
+    const float ksc =
+        EPI == EPI_ITEM_QKV && by == 1 ? 1.4426950408889634f / sqrtf((float)g.d) : 1.0f;
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
       const f32x4 b = par4(0, j);
 #pragma unroll
-      for (int i = 0; i < MI; ++i) put4(i, j, acc[i][j] + b);
+      for (int i = 0; i < MI; ++i) put4(i, j, (acc[i][j] + b) * ksc);
     }
     lds_barrier();
     if (EPI == EPI_ITEM_QKV) {
