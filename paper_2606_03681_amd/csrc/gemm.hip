@@ -106,11 +106,15 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   constexpr int NBB = BN / 64;         // 1 KB blocks of B per wave and stage
   constexpr int RING_BYTES = S * STAGE_EL * 2;
   constexpr int TILE_BYTES = BM * TS * 2;
-  __shared__ __attribute__((aligned(16))) char smem[RING_BYTES > TILE_BYTES ? RING_BYTES : TILE_BYTES];
+  // The epilogue's tile and its row / column reduction arrays reuse the ring once it drains.
+  constexpr int RED_BYTES = 2 * BM * 4, CRED_BYTES = 4 * BN * 4;
+  constexpr int EPI_BYTES = TILE_BYTES + RED_BYTES + CRED_BYTES;
+  __shared__ __attribute__((aligned(16))) char smem[RING_BYTES > EPI_BYTES ? RING_BYTES : EPI_BYTES];
   bf16* ring = reinterpret_cast<bf16*>(smem);  // stage slot s: A at s*STAGE_EL, B after A
   bf16* tile = reinterpret_cast<bf16*>(smem);  // epilogue: [BM][TS], after the main loop
-  __shared__ float red[2][BM];
-  __shared__ float cred[2][2][BN];
+  float (*red)[BM] = reinterpret_cast<float (*)[BM]>(smem + TILE_BYTES);          // [2][BM]
+  float (*cred)[2][BN] =
+      reinterpret_cast<float (*)[2][BN]>(smem + TILE_BYTES + RED_BYTES);        // [2][2][BN]
   __shared__ __attribute__((aligned(16))) float cpar[3][BN];  // bias, gamma, beta of the tile
   __shared__ int64_t rbase[BM];  // epilogue: per-row element offset for the current mode
 
