@@ -41,6 +41,20 @@
  *
  * Supported envelope: B >= 1, R >= 1, 0 <= C <= 255, heads >= 1, d = E/heads in {16, 32},
  * 32 <= E <= 256 with E % 32 == 0, 32 <= H <= 1024 with H % 32 == 0.
+ *
+ * Pre-norm block (dims->block == TFM_BLOCK_PRENORM): the block of the paper's current best
+ * record (Sec. 5 "Residual Decay" and "RMSNorm, Thinking Rows", the Fig. 4 caption, App. B.6,
+ * Tab. 7), with c = dims->decay (0.95^i for block i of a stack):
+ *
+ *     X' = c X
+ *     H1 = X' + FeatureAttention(RMS1(X'))
+ *     H2 = H1 + ItemAttention(RMS2(H1))
+ *     Y  = H2 + W2 GELU(W1 RMS3(H2) + b1) + b2,      RMS(u) = g * u / sqrt(mean(u^2) + 1e-6)
+ *
+ * Its packed parameters are those of the post-norm block without the shifts, ending
+ * g1[E] g2[E] g3[E] (RMSNorm weights).  Thinking rows are train rows that the caller prepends
+ * (n_train counts them); inside the block they are ordinary rows.  The pre-norm block runs in
+ * bfloat16 only, with E in {64, 128, 192, 256} and H a multiple of E.
  */
 #ifndef TFM_LAYER_H
 #define TFM_LAYER_H
@@ -53,11 +67,16 @@ extern "C" {
 #endif
 
 typedef enum { TFM_F32 = 0, TFM_BF16 = 1 } tfm_dtype;
+typedef enum { TFM_BLOCK_POSTNORM = 0, TFM_BLOCK_PRENORM = 1 } tfm_block;
 
-/* Problem dimensions.  C counts feature cells; each row has S = C + 1 cells. */
+/* Problem dimensions.  C counts feature cells; each row has S = C + 1 cells.  block selects
+ * the layer variant (a zero-initialised struct selects the post-norm block); decay is the
+ * factor the pre-norm block multiplies its input by (ignored by the post-norm block). */
 typedef struct {
   int32_t B, R, C, E, heads, H;
   int32_t dtype; /* tfm_dtype */
+  int32_t block; /* tfm_block */
+  float decay;
 } tfm_dims;
 
 /* Return codes. */

@@ -33,7 +33,11 @@ enum {
                      // stored times log2(e)/sqrt(d)
   EPI_LN = 4,        // out = LN(C + bias + resid); xhat, rstd saved
   EPI_LN_BWD = 5,    // dh = C + resid; out = LN'(dh) with xhat = aux, rstd_in; column partials
-  EPI_DX = 6         // out (native) = C + resid
+  EPI_DX = 6,        // out (native) = C (+ bias) + resid
+  // pre-norm block
+  EPI_RMS = 7,       // h = C + bias + rscale * resid -> out; out2 = gamma h rstd; rstd saved
+  EPI_RMS_BWD = 8    // out (omode) = oscale (resid + RMS'(C)) with h = aux, rstd_in; column
+                     // partials of C * h * rstd_in (the norm-weight gradient)
 };
 
 struct GemmArgs {
@@ -59,7 +63,11 @@ struct GemmArgs {
   float* rstd;
   const float* rstd_in;
   const bf16* aux;
-  float* part;  // EPI_LN_BWD: [gridDim.x][2][BN] partial sums (dgamma, dbeta)
+  float* part;  // EPI_LN_BWD: [row tiles][2][BN] partial sums (dgamma, dbeta);
+                //   EPI_RMS_BWD: [row tiles][BN] (dgamma)
+  float rscale;  // EPI_RMS: factor on resid
+  float oscale;  // EPI_RMS_BWD: factor on the output
+  float eps;     // EPI_RMS, EPI_RMS_BWD: RMSNorm epsilon
   Geo g;
 };
 
@@ -112,6 +120,11 @@ hipError_t launch_wgrad_mfma(const WgradArgs& a, hipStream_t s);
 // overwrites part (it is scratch).
 hipError_t launch_reduce_z(int Z, int64_t count, int64_t stride, float* part, float* out,
                            int accumulate, hipStream_t s);
+
+// Pre-norm block input: xs = decay * X (compact), r = gamma xs / sqrt(mean(xs^2) + eps)
+// (compact), rstd [N].
+hipError_t launch_rms_in(const Geo& g, const bf16* X, float decay, const float* gamma, float eps,
+                         bf16* xs, bf16* r, float* rstd, hipStream_t s);
 
 // Backward of the last LayerNorm from the native upstream gradient: dz = LN3'(dY) at active
 // cells (compact), plus per-block partial column sums of dY * xhat and dY into

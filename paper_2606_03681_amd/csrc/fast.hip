@@ -190,6 +190,78 @@ hipError_t launch_ln_out_bwd(const Geo& g, const bf16* dY, const bf16* xhat, con
   return hipGetLastError();
 }
 
+// Pre-norm block input: x' = decay * X (native rows) and r = gamma x' / sqrt(mean(x'^2) + eps),
+// both written compact, with rstd.  Same thread layout as the LN3 backward above: a half-wave
+// per cell, lane l holding features 8l .. 8l+7, four cells per half-wave in flight.
+__global__ __launch_bounds__(512) void k_rms_in(Geo g, const bf16* __restrict__ X, float decay,
+                                                const float* __restrict__ gamma, float eps,
+                                                bf16* __restrict__ xs, bf16* __restrict__ r,
+                                                float* __restrict__ rstd) {
+  const int tid = threadIdx.x, hw = tid >> 5, l = tid & 31;
+  const int E = g.E;
+  const bool act = 8 * l < E;
+  float gm[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) gm[j] = act ? gamma[8 * l + j] : 0.f;
+  const int64_t c0 = (int64_t)blockIdx.x * LN_CELLS;
+  const int col0 = (int)(c0 / g.R), r0 = (int)(c0 - (int64_t)col0 * g.R);
+  for (int base = hw; base < LN_CELLS; base += 16 * LN_BATCH) {
+    uint4 xv[LN_BATCH];
+    int64_t pc[LN_BATCH];
+    bool ok[LN_BATCH];
+#pragma unroll
+    for (int u = 0; u < LN_BATCH; ++u) {
+      const int cc = base + 16 * u;
+      const int64_t p = c0 + cc;
+      pc[u] = p;
+      ok[u] = cc < LN_CELLS && p < g.N;
+      xv[u] = make_uint4(0, 0, 0, 0);
+      if (ok[u] && act) {
+        int col = col0, rr = r0 + cc;
+        while (rr >= g.R) {
+          rr -= g.R;
+          ++col;
+        }
+        const int64_t nat = ((int64_t)g.col_ds[col] * g.R + rr) * g.S + g.col_c[col];
+        xv[u] = ldu4(X + nat * E + 8 * l);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < LN_BATCH; ++u) {
+      float x[8];
+      float ss = 0.f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        x[j] = decay * bf2f(u4_elem(xv[u], j));
+        ss += x[j] * x[j];
+      }
+#pragma unroll
+      for (int o = 1; o < 32; o <<= 1) ss += __shfl_xor(ss, o, 64);
+      const float rs = 1.0f / sqrtf(ss / E + eps);
+      if (ok[u] && l == 0) rstd[pc[u]] = rs;
+      if (ok[u] && act) {
+        uint4 a, b;
+        a.x = pack2(x[0], x[1]); a.y = pack2(x[2], x[3]);
+        a.z = pack2(x[4], x[5]); a.w = pack2(x[6], x[7]);
+        b.x = pack2(gm[0] * x[0] * rs, gm[1] * x[1] * rs);
+        b.y = pack2(gm[2] * x[2] * rs, gm[3] * x[3] * rs);
+        b.z = pack2(gm[4] * x[4] * rs, gm[5] * x[5] * rs);
+        b.w = pack2(gm[6] * x[6] * rs, gm[7] * x[7] * rs);
+        stu4(xs + pc[u] * E + 8 * l, a);
+        stu4(r + pc[u] * E + 8 * l, b);
+      }
+    }
+  }
+}
+
+hipError_t launch_rms_in(const Geo& g, const bf16* X, float decay, const float* gamma, float eps,
+                         bf16* xs, bf16* r, float* rstd, hipStream_t s) {
+  const int64_t nb = (g.N + LN_CELLS - 1) / LN_CELLS;
+  if (nb == 0) return hipSuccess;
+  k_rms_in<<<(unsigned)nb, 512, 0, s>>>(g, X, decay, gamma, eps, xs, r, rstd);
+  return hipGetLastError();
+}
+
 size_t fast_workspace_bytes(int B, int R, int S, int E, int heads, int H, bool bf16) {
   (void)heads;
   if (!bf16) return 0;

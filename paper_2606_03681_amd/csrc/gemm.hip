@@ -197,7 +197,8 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   // per-column epilogue parameters of this column tile, staged once
   if (tid < BN) {
     cpar[0][tid] = a.bias ? a.bias[n0 + tid] : 0.f;
-    if (EPI == EPI_LN || EPI == EPI_LN_BWD) cpar[1][tid] = a.gamma[tid];
+    if (EPI == EPI_LN || EPI == EPI_LN_BWD || EPI == EPI_RMS || EPI == EPI_RMS_BWD)
+      cpar[1][tid] = a.gamma[tid];
     if (EPI == EPI_LN) cpar[2][tid] = a.beta[tid];
   }
 
@@ -206,8 +207,9 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   // costing a memory round trip after the main loop.
   constexpr int CPRW = BN / 8;              // 16-byte chunks per tile row
   constexpr int NCH = BM * CPRW / 256;      // chunks per thread of one tile
-  constexpr bool IN0 = EPI == EPI_GELU_BWD || EPI == EPI_DX || EPI == EPI_LN || EPI == EPI_LN_BWD;
-  constexpr bool IN1 = EPI == EPI_LN_BWD;
+  constexpr bool IN0 = EPI == EPI_GELU_BWD || EPI == EPI_DX || EPI == EPI_LN ||
+                      EPI == EPI_LN_BWD || EPI == EPI_RMS || EPI == EPI_RMS_BWD;
+  constexpr bool IN1 = EPI == EPI_LN_BWD || EPI == EPI_RMS_BWD;
   uint4 pin0[IN0 ? NCH : 1], pin1[IN1 ? NCH : 1];
   if (IN0) {
     if (tid < BM) {
@@ -215,7 +217,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
       int64_t off = -1;
       if (m < a.M) {
         if (EPI == EPI_GELU_BWD) off = m * a.ldo;
-        else if (EPI == EPI_LN) off = row_addr(g, a.rmode, m, BN);
+        else if (EPI == EPI_LN || EPI == EPI_RMS) off = row_addr(g, a.rmode, m, BN);
         else off = m * BN;
       }
       rbase[tid] = off;
@@ -406,7 +408,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
 #pragma unroll
     for (int i = 0; i < MI; ++i)
 #pragma unroll
-      for (int j = 0; j < NB; ++j) acc[i][j] += tile4(i, j);
+      for (int j = 0; j < NB; ++j) acc[i][j] += tile4(i, j) + par4(0, j);
     lds_barrier();
 #pragma unroll
     for (int i = 0; i < MI; ++i)
@@ -538,6 +540,84 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
     store_tile(a.out, 0, false);
     return;
   }
+
+  // ---- pre-norm RMSNorm epilogues (BN == E, n0 == 0)
+  if (EPI == EPI_RMS) {
+    // h = C + bias + rscale * resid -> out; r = gamma h / sqrt(mean(h^2) + eps) -> out2
+    fill_tile(pin0);
+    lds_barrier();
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const f32x4 b = par4(0, j);
+#pragma unroll
+      for (int i = 0; i < MI; ++i) val[i][j] = acc[i][j] + b + a.rscale * tile4(i, j);
+    }
+    float ms[MI];
+    row_sum([&](int i, int j) { return val[i][j] * val[i][j]; }, ms);
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j) put4(i, j, val[i][j]);
+    set_rows(ROWS_COMPACT, BN, -1);
+    lds_barrier();
+    store_tile(a.out, 0, false);
+    lds_barrier();
+#pragma unroll
+    for (int i = 0; i < MI; ++i) {
+      const float rs = 1.0f / sqrtf(ms[i] + a.eps);
+      if (wn == 0 && lg == 0 && m0 + rloc(i) < a.M) a.rstd[m0 + rloc(i)] = rs;
+#pragma unroll
+      for (int j = 0; j < NB; ++j) put4(i, j, par4(1, j) * val[i][j] * rs);
+    }
+    lds_barrier();
+    store_tile(a.out2, 0, false);
+    return;
+  }
+
+  if (EPI == EPI_RMS_BWD) {
+    // dr = C, uhat = h rstd_in:  out = oscale (resid + rstd_in (gamma dr - uhat mean(gamma dr
+    // uhat))); column partials of dr uhat per workgroup
+    fill_tile(pin1);  // h
+    lds_barrier();
+    float rsi[MI];
+#pragma unroll
+    for (int i = 0; i < MI; ++i) rsi[i] = m0 + rloc(i) < a.M ? a.rstd_in[m0 + rloc(i)] : 0.f;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      f32x4 s1 = zero4();
+#pragma unroll
+      for (int i = 0; i < MI; ++i) s1 += acc[i][j] * tile4(i, j) * rsi[i];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float t1 = sum16(s1[q]);
+        if (lr == 0) cred[0][wm][cb0 + j * 16 + q] = t1;
+      }
+    }
+    float m1[MI];
+    row_sum([&](int i, int j) { return par4(1, j) * acc[i][j] * tile4(i, j) * rsi[i]; }, m1);
+    if (tid < BN) a.part[bx * BN + tid] = cred[0][0][tid] + cred[0][1][tid];
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+        val[i][j] = rsi[i] * (par4(1, j) * acc[i][j] - tile4(i, j) * (rsi[i] * m1[i]));
+    lds_barrier();
+    fill_tile(pin0);  // resid
+    lds_barrier();
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j) val[i][j] = a.oscale * (val[i][j] + tile4(i, j));
+    lds_barrier();
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j) put4(i, j, val[i][j]);
+    set_rows(a.omode, BN, -1);
+    lds_barrier();
+    store_tile(a.out, 0, false);
+    return;
+  }
 }
 
 template <int BN>
@@ -552,6 +632,8 @@ static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
     case EPI_LN: k_gemm<BN, EPI_LN><<<grid, 256, 0, s>>>(a); break;
     case EPI_LN_BWD: k_gemm<BN, EPI_LN_BWD><<<grid, 256, 0, s>>>(a); break;
     case EPI_DX: k_gemm<BN, EPI_DX><<<grid, 256, 0, s>>>(a); break;
+    case EPI_RMS: k_gemm<BN, EPI_RMS><<<grid, 256, 0, s>>>(a); break;
+    case EPI_RMS_BWD: k_gemm<BN, EPI_RMS_BWD><<<grid, 256, 0, s>>>(a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

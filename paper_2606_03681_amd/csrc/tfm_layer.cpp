@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -37,6 +38,8 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Dims {
   int B, R, C, S, E, heads, d, H, dtype;
+  int block;       // TFM_BLOCK_POSTNORM or TFM_BLOCK_PRENORM
+  float decay;     // pre-norm block: factor on the block input
   size_t tsz;      // bytes per stored element
   int64_t Nmax;    // B * R * S
   int words;       // 32-bit mask words per dataset
@@ -66,6 +69,18 @@ int check_dims(const tfm_dims* p, Dims& d) {
                 (long long)kMaxCells);
   d.tsz = d.dtype == TFM_F32 ? 4 : 2;
   d.words = (d.S + 31) / 32;
+  d.block = p->block;
+  d.decay = p->decay;
+  if (d.block != TFM_BLOCK_POSTNORM && d.block != TFM_BLOCK_PRENORM)
+    return fail(TFM_ERR_DIMS, "block %d is neither TFM_BLOCK_POSTNORM nor TFM_BLOCK_PRENORM",
+                d.block);
+  if (d.block == TFM_BLOCK_PRENORM) {
+    if (d.dtype != TFM_BF16 || !(d.E == 64 || d.E == 128 || d.E == 192 || d.E == 256) ||
+        d.H % d.E)
+      return fail(TFM_ERR_DIMS, "the pre-norm block needs TFM_BF16, E in {64, 128, 192, 256} "
+                                "and H a multiple of E");
+    if (!std::isfinite(d.decay)) return fail(TFM_ERR_DIMS, "decay must be finite");
+  }
   return TFM_OK;
 }
 
@@ -75,7 +90,9 @@ struct POff {
   size_t g1, be1, g2, be2, g3, be3, total;
 };
 
-POff param_offsets(int E, int H) {
+// Packed order of include/tfm_layer.h; the pre-norm block has RMSNorm weights g1, g2, g3 only
+// (its be* offsets are unused).
+POff param_offsets(int E, int H, int block = TFM_BLOCK_POSTNORM) {
   POff o;
   size_t x = 0;
   auto take = [&](size_t n) { size_t r = x; x += n; return r; };
@@ -85,8 +102,13 @@ POff param_offsets(int E, int H) {
   o.Wo_i = take((size_t)E * E); o.bo_i = take(E);
   o.W1 = take((size_t)H * E); o.b1 = take(H);
   o.W2 = take((size_t)E * H); o.b2 = take(E);
-  o.g1 = take(E); o.be1 = take(E); o.g2 = take(E); o.be2 = take(E);
-  o.g3 = take(E); o.be3 = take(E);
+  if (block == TFM_BLOCK_PRENORM) {
+    o.g1 = take(E); o.g2 = take(E); o.g3 = take(E);
+    o.be1 = o.be2 = o.be3 = 0;
+  } else {
+    o.g1 = take(E); o.be1 = take(E); o.g2 = take(E); o.be2 = take(E);
+    o.g3 = take(E); o.be3 = take(E);
+  }
   o.total = x;
   return o;
 }
@@ -126,6 +148,45 @@ SavedLayout saved_layout(const Dims& d) {
   L.rs3 = a.take(N * 4);
   L.total = a.off;
   return L;
+}
+
+// Saved state of the pre-norm block: x' = decay X, r1 = RMS1(x'), the residual stream h1, h2
+// and the norm outputs r2, r3 (the GEMM inputs), rstd of each norm, the attention state and
+// the MLP pre-activation and activation.
+struct PreSaved {
+  size_t xs, r1, rs1, qkvf, of, lsef, h1, r2, rs2, qi, ki, vi, oi, lsei, h2, r3, rs3, g, u;
+  size_t total;
+};
+
+PreSaved pre_saved_layout(const Dims& d) {
+  PreSaved L;
+  Arena a;
+  const size_t N = (size_t)d.Nmax, t = d.tsz, E = d.E;
+  L.xs = a.take(N * E * t);
+  L.r1 = a.take(N * E * t);
+  L.rs1 = a.take(N * 4);
+  L.qkvf = a.take(N * 3 * E * t);
+  L.of = a.take(N * E * t);
+  L.lsef = a.take(N * d.heads * 4);
+  L.h1 = a.take(N * E * t);
+  L.r2 = a.take(N * E * t);
+  L.rs2 = a.take(N * 4);
+  L.qi = a.take(N * E * t);
+  L.ki = a.take(N * E * t);
+  L.vi = a.take(N * E * t);
+  L.oi = a.take(N * E * t);
+  L.lsei = a.take(N * d.heads * 4);
+  L.h2 = a.take(N * E * t);
+  L.r3 = a.take(N * E * t);
+  L.rs3 = a.take(N * 4);
+  L.g = a.take(N * d.H * t);
+  L.u = a.take(N * d.H * t);
+  L.total = a.off;
+  return L;
+}
+
+size_t saved_total(const Dims& d) {
+  return d.block == TFM_BLOCK_PRENORM ? pre_saved_layout(d).total : saved_layout(d).total;
 }
 
 struct WsLayout {
@@ -607,6 +668,158 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   return TFM_OK;
 }
 
+// ---- pre-norm RMSNorm block (bfloat16, MFMA path) --------------------------------------------
+constexpr float kRmsEps = 1e-6f;
+
+int fwd_pre(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* prm,
+            tfm::bf16* Y, char* sv, const PreSaved& S, char* ws, const WsLayout& W,
+            hipStream_t s) {
+  using namespace tfm;
+  typedef tfm::bf16 T;
+  const POff o = param_offsets(d.E, d.H, d.block);
+  const FastWs f = fast_ws(d, ws, W);
+  const int E = d.E, H = d.H;
+  const int64_t N = g.N;
+  STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, s));
+  T* xs = (T*)(sv + S.xs);
+  T* r1 = (T*)(sv + S.r1);
+  T* qkvf = (T*)(sv + S.qkvf);
+  T* of = (T*)(sv + S.of);
+  T* h1 = (T*)(sv + S.h1);
+  T* r2 = (T*)(sv + S.r2);
+  T* oi = (T*)(sv + S.oi);
+  T* h2 = (T*)(sv + S.h2);
+  T* r3 = (T*)(sv + S.r3);
+  // x' = decay X, r1 = RMS1(x')
+  STEP("rms_in/hbm", launch_rms_in(g, X, d.decay, prm + o.g1, kRmsEps, xs, r1,
+                                   (float*)(sv + S.rs1), s));
+  GemmArgs a = gemm_base(g, N, 3 * E, E, EPI_BIAS);
+  a.A = r1; a.lda = E; a.Bt = f.w + f.wo.qkv_f; a.bias = prm + o.bqkv_f; a.out = qkvf;
+  a.ldo = 3 * E;
+  STEP("feat_qkv/mfma", launch_gemm(a, s));
+  if (feat_attn_mfma_ok(g))
+    STEP("feat_attn_fwd/mfma", launch_feat_attn_fwd(g, qkvf, of, (float*)(sv + S.lsef), s));
+  else
+    STEP("feat_attn_fwd/valu",
+         launch_feat_attn_fwd_simple<T>(g, qkvf, of, (float*)(sv + S.lsef), s));
+  // h1 = x' + O_f Wo_f^T + bo_f, r2 = RMS2(h1)
+  a = gemm_base(g, N, E, E, EPI_RMS);
+  a.A = of; a.lda = E; a.Bt = f.w + f.wo.o_f; a.bias = prm + o.bo_f;
+  a.resid = xs; a.rmode = ROWS_COMPACT; a.rscale = 1.0f; a.gamma = prm + o.g2; a.eps = kRmsEps;
+  a.out = h1; a.out2 = r2; a.rstd = (float*)(sv + S.rs2);
+  STEP("feat_out_rms2/mfma", launch_gemm(a, s));
+  // item Q (all rows), K and V (train rows), head-major
+  a = gemm_base(g, N, 3 * E, E, EPI_ITEM_QKV);
+  a.A = r2; a.lda = E; a.Bt = f.w + f.wo.qkv_i; a.bias = prm + o.bqkv_i;
+  a.out = (T*)(sv + S.qi); a.out2 = (T*)(sv + S.ki); a.out3 = (T*)(sv + S.vi);
+  STEP("item_qkv/mfma", launch_gemm(a, s));
+  STEP("item_attn_fwd/mfma", launch_item_attn_fwd(g, (T*)(sv + S.qi), (T*)(sv + S.ki),
+                                                  (T*)(sv + S.vi), oi, (float*)(sv + S.lsei),
+                                                  s));
+  // h2 = h1 + O_i Wo_i^T + bo_i, r3 = RMS3(h2)
+  a = gemm_base(g, N, E, E, EPI_RMS);
+  a.A = oi; a.lda = E; a.Bt = f.w + f.wo.o_i; a.bias = prm + o.bo_i;
+  a.resid = h1; a.rmode = ROWS_COMPACT; a.rscale = 1.0f; a.gamma = prm + o.g3; a.eps = kRmsEps;
+  a.out = h2; a.out2 = r3; a.rstd = (float*)(sv + S.rs3);
+  STEP("item_out_rms3/mfma", launch_gemm(a, s));
+  // G = r3 W1^T + b1, U = GELU(G)
+  a = gemm_base(g, N, H, E, EPI_GELU_FWD);
+  a.A = r3; a.lda = E; a.Bt = f.w + f.wo.w1; a.bias = prm + o.b1;
+  a.out = (T*)(sv + S.g); a.out2 = (T*)(sv + S.u); a.ldo = H;
+  STEP("mlp_up/mfma", launch_gemm(a, s));
+  // Y = h2 + U W2^T + b2, native
+  a = gemm_base(g, N, E, H, EPI_DX);
+  a.A = (T*)(sv + S.u); a.lda = H; a.Bt = f.w + f.wo.w2; a.bias = prm + o.b2; a.resid = h2;
+  a.out = Y;
+  STEP("mlp_down_res/mfma", launch_gemm(a, s));
+  STEP("zero_inactive/hbm", launch_zero_inactive(g, Y, s));
+  return TFM_OK;
+}
+
+int bwd_pre(const Dims& d, const tfm::Geo& g, const float* prm, const char* sv,
+            const PreSaved& S, const tfm::bf16* dY, tfm::bf16* dX, float* grads, int accumulate,
+            char* ws, const WsLayout& W, hipStream_t s) {
+  using namespace tfm;
+  typedef tfm::bf16 T;
+  const POff o = param_offsets(d.E, d.H, d.block);
+  const FastWs f = fast_ws(d, ws, W);
+  const int E = d.E, H = d.H;
+  const int64_t N = g.N;
+  const int tiles = (int)tfm::gemm_row_tiles(N);
+  FastGrads G{f, g, grads, accumulate, s};
+  STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, s));
+  T* dyc = (T*)(ws + W.tb);    // dY, compact
+  T* dh2 = (T*)(ws + W.te);
+  T* dh1 = (T*)(ws + W.tf);
+  T* dgb = (T*)(ws + W.th1);
+  T* dqkv = (T*)(ws + W.tqkv);
+  STEP("gather/hbm", launch_gather<T>(g, dY, dyc, s));
+  // dG = (dY W2) * GELU'(G)
+  GemmArgs a = gemm_base(g, N, H, E, EPI_GELU_BWD);
+  a.A = dyc; a.lda = E; a.Bt = f.wt + f.wo.w2; a.out = dgb; a.ldo = H;
+  a.aux = (const T*)(sv + S.g);
+  STEP("mlp_down_dx/mfma", launch_gemm(a, s));
+  CHK(G.run(dyc, E, (const T*)(sv + S.u), H, ROWS_COMPACT, o.W2, o.b2));
+  CHK(G.run(dgb, H, (const T*)(sv + S.r3), E, ROWS_COMPACT, o.W1, o.b1));
+  // dh2 = dY + RMS3'(dG W1)
+  a = gemm_base(g, N, E, H, EPI_RMS_BWD);
+  a.A = dgb; a.lda = H; a.Bt = f.wt + f.wo.w1; a.resid = dyc; a.aux = (const T*)(sv + S.h2);
+  a.rstd_in = (const float*)(sv + S.rs3); a.gamma = prm + o.g3; a.eps = kRmsEps;
+  a.oscale = 1.0f; a.omode = ROWS_COMPACT; a.out = dh2; a.part = f.lnpart;
+  STEP("mlp_up_dx_rms3/mfma", launch_gemm(a, s));
+  STEP("reduce/hbm", launch_reduce_z(tiles, E, E, f.lnpart, grads + o.g3, accumulate, s));
+  // item attention
+  T* doi = (T*)(ws + W.tc);
+  a = gemm_base(g, N, E, E, EPI_BIAS);
+  a.A = dh2; a.lda = E; a.Bt = f.wt + f.wo.o_i; a.out = doi; a.ldo = E;
+  STEP("item_out_dx/mfma", launch_gemm(a, s));
+  CHK(G.run(dh2, E, (const T*)(sv + S.oi), E, ROWS_COMPACT, o.Wo_i, o.bo_i));
+  T* dq = (T*)(ws + W.tq);
+  T* dk = (T*)(ws + W.tk);
+  T* dv = (T*)(ws + W.tv);
+  const T* qi = (const T*)(sv + S.qi);
+  const T* ki = (const T*)(sv + S.ki);
+  const T* vi = (const T*)(sv + S.vi);
+  const T* oi = (const T*)(sv + S.oi);
+  const float* lsei = (const float*)(sv + S.lsei);
+  float* Dq = (float*)(ws + W.D);
+  STEP("item_attn_dq/mfma", launch_item_attn_dq(g, qi, ki, vi, oi, doi, lsei, Dq, dq, s));
+  STEP("item_attn_dkdv/mfma", launch_item_attn_dkdv(g, qi, ki, vi, oi, doi, lsei, Dq, dk, dv, s));
+  CHK(G.run(dq, 3 * E, (const T*)(sv + S.r2), E, ROWS_COMPACT, o.Wqkv_i, o.bqkv_i, dk, dv));
+  // dh1 = dh2 + RMS2'(dQKV_i Wqkv_i), the gradients read head-major in place
+  a = gemm_base(g, N, E, 3 * E, EPI_RMS_BWD);
+  a.A = dq; a.A2 = dk; a.A3 = dv; a.amode = ROWS_ITEM_HM; a.lda = 3 * E;
+  a.Bt = f.wt + f.wo.qkv_i; a.resid = dh2; a.aux = (const T*)(sv + S.h1);
+  a.rstd_in = (const float*)(sv + S.rs2); a.gamma = prm + o.g2; a.eps = kRmsEps;
+  a.oscale = 1.0f; a.omode = ROWS_COMPACT; a.out = dh1; a.part = f.lnpart;
+  STEP("item_qkv_dx_rms2/mfma", launch_gemm(a, s));
+  STEP("reduce/hbm", launch_reduce_z(tiles, E, E, f.lnpart, grads + o.g2, accumulate, s));
+  // feature attention
+  T* dof = (T*)(ws + W.tc);
+  a = gemm_base(g, N, E, E, EPI_BIAS);
+  a.A = dh1; a.lda = E; a.Bt = f.wt + f.wo.o_f; a.out = dof; a.ldo = E;
+  STEP("feat_out_dx/mfma", launch_gemm(a, s));
+  CHK(G.run(dh1, E, (const T*)(sv + S.of), E, ROWS_COMPACT, o.Wo_f, o.bo_f));
+  if (feat_attn_mfma_ok(g))
+    STEP("feat_attn_bwd/mfma",
+         launch_feat_attn_bwd(g, (const T*)(sv + S.qkvf), (const T*)(sv + S.of), dof,
+                              (const float*)(sv + S.lsef), dqkv, s));
+  else
+    STEP("feat_attn_bwd/valu",
+         launch_feat_attn_bwd_simple<T>(g, (const T*)(sv + S.qkvf), (const T*)(sv + S.of), dof,
+                                        (const float*)(sv + S.lsef), dqkv, s));
+  CHK(G.run(dqkv, 3 * E, (const T*)(sv + S.r1), E, ROWS_COMPACT, o.Wqkv_f, o.bqkv_f));
+  // dX = decay (dh1 + RMS1'(dQKV_f Wqkv_f)), native
+  a = gemm_base(g, N, E, 3 * E, EPI_RMS_BWD);
+  a.A = dqkv; a.lda = 3 * E; a.Bt = f.wt + f.wo.qkv_f; a.resid = dh1;
+  a.aux = (const T*)(sv + S.xs); a.rstd_in = (const float*)(sv + S.rs1); a.gamma = prm + o.g1;
+  a.eps = kRmsEps; a.oscale = d.decay; a.omode = ROWS_NATIVE; a.out = dX; a.part = f.lnpart;
+  STEP("feat_qkv_dx_rms1/mfma", launch_gemm(a, s));
+  STEP("reduce/hbm", launch_reduce_z(tiles, E, E, f.lnpart, grads + o.g1, accumulate, s));
+  STEP("zero_inactive/hbm", launch_zero_inactive(g, dX, s));
+  return TFM_OK;
+}
+
 }  // namespace
 
 // ============================================================================ C ABI
@@ -615,13 +828,13 @@ extern "C" {
 size_t tfm_layer_param_count(const tfm_dims* dims) {
   Dims d;
   if (check_dims(dims, d) != TFM_OK) return 0;
-  return param_offsets(d.E, d.H).total;
+  return param_offsets(d.E, d.H, d.block).total;
 }
 
 size_t tfm_layer_saved_bytes(const tfm_dims* dims) {
   Dims d;
   if (check_dims(dims, d) != TFM_OK) return 0;
-  return saved_layout(d).total;
+  return saved_total(d);
 }
 
 size_t tfm_layer_workspace_bytes(const tfm_dims* dims) {
@@ -643,8 +856,9 @@ int tfm_layer_fwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* c
                                  "16-byte aligned");
   const SavedLayout S = saved_layout(d);
   const WsLayout W = ws_layout(d);
-  if (saved_bytes < S.total)
-    return fail(TFM_ERR_BUFFER, "saved buffer has %zu bytes, %zu required", saved_bytes, S.total);
+  if (saved_bytes < saved_total(d))
+    return fail(TFM_ERR_BUFFER, "saved buffer has %zu bytes, %zu required", saved_bytes,
+                saved_total(d));
   if (workspace_bytes < W.total)
     return fail(TFM_ERR_BUFFER, "workspace has %zu bytes, %zu required", workspace_bytes,
                 W.total);
@@ -657,6 +871,9 @@ int tfm_layer_fwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* c
   tfm::Geo g;
   rc = setup_geo(d, P, ws, W, g, s);
   if (rc) return rc;
+  if (d.block == TFM_BLOCK_PRENORM)
+    return fwd_pre(d, g, (const tfm::bf16*)X, params, (tfm::bf16*)Y, sv, pre_saved_layout(d), ws,
+                   W, s);
   if (d.dtype == TFM_F32)
     return fwd_simple<float>(d, g, (const float*)X, params, (float*)Y, sv, S, ws, W, s);
   if (fast_eligible(d))
@@ -678,8 +895,9 @@ int tfm_layer_bwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* c
                                  "non-null and 16-byte aligned");
   const SavedLayout S = saved_layout(d);
   const WsLayout W = ws_layout(d);
-  if (saved_bytes < S.total)
-    return fail(TFM_ERR_BUFFER, "saved buffer has %zu bytes, %zu required", saved_bytes, S.total);
+  if (saved_bytes < saved_total(d))
+    return fail(TFM_ERR_BUFFER, "saved buffer has %zu bytes, %zu required", saved_bytes,
+                saved_total(d));
   if (workspace_bytes < W.total)
     return fail(TFM_ERR_BUFFER, "workspace has %zu bytes, %zu required", workspace_bytes,
                 W.total);
@@ -691,6 +909,9 @@ int tfm_layer_bwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* c
   tfm::Geo g;
   rc = setup_geo(d, P, ws, W, g, s);
   if (rc) return rc;
+  if (d.block == TFM_BLOCK_PRENORM)
+    return bwd_pre(d, g, params, (const char*)saved, pre_saved_layout(d), (const tfm::bf16*)dY,
+                   (tfm::bf16*)dX, grads, accumulate, ws, W, s);
   if (d.dtype == TFM_F32)
     return bwd_simple<float>(d, g, (const float*)X, params, (const char*)saved, S,
                              (const float*)dY, (float*)dX, grads, accumulate, ws, W, s);

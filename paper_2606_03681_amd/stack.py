@@ -26,9 +26,10 @@ def to_host(t, dtype):
 
 
 class Stack:
-    """L layers with independent parameters over the same n_train / cell_mask."""
+    """L layers with independent parameters over the same n_train / cell_mask.  For the pre-norm
+    block, layer l multiplies its input by decay_base ** l."""
 
-    def __init__(self, dims, n_train, cell_mask, params, device="cuda"):
+    def __init__(self, dims, n_train, cell_mask, params, device="cuda", decay_base=0.95):
         self.dims = dims
         self.n_train = np.ascontiguousarray(n_train, dtype=np.int32)
         self.cell_mask = np.ascontiguousarray(cell_mask, dtype=np.uint8)
@@ -37,6 +38,13 @@ class Stack:
                        torch.from_numpy(np.ascontiguousarray(p, dtype=np.float32)).to(device)
                        for p in params]
         self.L = len(self.params)
+        self.layer_dims = [dims] * self.L
+        if dims.block == tfm.TFM_BLOCK_PRENORM:
+            self.layer_dims = []
+            for l in range(self.L):
+                dl = tfm.tfm_dims.from_buffer_copy(dims)
+                dl.decay = decay_base ** l
+                self.layer_dims.append(dl)
         self.elt = torch.float32 if dims.dtype == tfm.TFM_F32 else torch.bfloat16
         self.shape = (dims.B, dims.R, dims.C + 1, dims.E)
         sb, wb = tfm.saved_bytes(dims), tfm.workspace_bytes(dims)
@@ -54,7 +62,7 @@ class Stack:
         """Runs every layer; returns the last layer's output (a buffer owned by the stack)."""
         self.inputs = [X] + self.acts[:-1]
         for l in range(self.L):
-            tfm.layer_fwd(self.dims, self.n_train, self.cell_mask, self.inputs[l],
+            tfm.layer_fwd(self.layer_dims[l], self.n_train, self.cell_mask, self.inputs[l],
                           self.params[l], self.acts[l], self.saved[l], self.workspace)
         return self.acts[-1]
 
@@ -64,7 +72,7 @@ class Stack:
         g = dY
         for l in range(self.L - 1, -1, -1):
             out = self.dxs[l % 2]
-            tfm.layer_bwd(self.dims, self.n_train, self.cell_mask, self.inputs[l],
+            tfm.layer_bwd(self.layer_dims[l], self.n_train, self.cell_mask, self.inputs[l],
                           self.params[l], self.saved[l], g, out, self.grads[l], accumulate,
                           self.workspace)
             g = out

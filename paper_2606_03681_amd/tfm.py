@@ -14,6 +14,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtfmlaye
 _lib = None
 
 TFM_F32, TFM_BF16 = 0, 1
+TFM_BLOCK_POSTNORM, TFM_BLOCK_PRENORM = 0, 1
 ERRORS = {
     -1: "TFM_ERR_DIMS", -2: "TFM_ERR_HEAD_DIM", -3: "TFM_ERR_NTRAIN", -4: "TFM_ERR_MASK",
     -5: "TFM_ERR_POINTER", -6: "TFM_ERR_HIP", -7: "TFM_ERR_BUFFER",
@@ -30,12 +31,15 @@ class TfmError(RuntimeError):
 
 
 class tfm_dims(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_int32) for n in ("B", "R", "C", "E", "heads", "H", "dtype")]
+    _fields_ = [(n, ctypes.c_int32) for n in ("B", "R", "C", "E", "heads", "H", "dtype",
+                                               "block")] + [("decay", ctypes.c_float)]
 
 
-def make_dims(B, R, C, E, heads, H, dtype):
+def make_dims(B, R, C, E, heads, H, dtype, block="post", decay=1.0):
     dt = {"f32": TFM_F32, "bf16": TFM_BF16}.get(dtype, dtype)
-    return tfm_dims(int(B), int(R), int(C), int(E), int(heads), int(H), int(dt))
+    bk = {"post": TFM_BLOCK_POSTNORM, "pre": TFM_BLOCK_PRENORM}.get(block, block)
+    return tfm_dims(int(B), int(R), int(C), int(E), int(heads), int(H), int(dt), int(bk),
+                    float(decay))
 
 
 def lib():

@@ -87,6 +87,11 @@ TEST_CONFIGS = {
                               heads=6, H=384, layers=2, cells="normal", weights="xavier_bias"),
     "d16-bf16": dict(name="d16-bf16", dtype="bf16", B=3, R=130, n_train=97, C=7, E=64,
                      heads=4, H=128, layers=1, cells="normal", weights="xavier_bias"),
+    # pre-norm RMSNorm block with residual decay (the current best record's block), at d = 32
+    "prenorm-small-bf16": dict(name="prenorm-small-bf16", dtype="bf16", B=4, R=200,
+                               n_train=(1, 200), C=20, active=(0, 20), mask="random", E=64,
+                               heads=2, H=192, layers=2, cells="normal", weights="xavier_bias",
+                               block="pre"),
 }
 
 
@@ -112,9 +117,19 @@ def default_seed(cfg):
 # Parameter layout (packed order of the C-ABI; see include/tfm_layer.h)
 # ---------------------------------------------------------------------------------------------
 
-def param_layout(E, H):
+def param_layout(E, H, block="post"):
     """(name, shape, kind) in packed order; kind is 'w' (weight [out, in]), 'b' (bias),
-    'g' (norm scale) or 'n' (norm shift)."""
+    'g' (norm scale) or 'n' (norm shift).  The pre-norm block has RMSNorm weights only."""
+    if block == "pre":
+        return [
+            ("Wqkv_f", (3 * E, E), "w"), ("bqkv_f", (3 * E,), "b"),
+            ("Wo_f", (E, E), "w"), ("bo_f", (E,), "b"),
+            ("Wqkv_i", (3 * E, E), "w"), ("bqkv_i", (3 * E,), "b"),
+            ("Wo_i", (E, E), "w"), ("bo_i", (E,), "b"),
+            ("W1", (H, E), "w"), ("b1", (H,), "b"),
+            ("W2", (E, H), "w"), ("b2", (E,), "b"),
+            ("g1", (E,), "g"), ("g2", (E,), "g"), ("g3", (E,), "g"),
+        ]
     return [
         ("Wqkv_f", (3 * E, E), "w"), ("bqkv_f", (3 * E,), "b"),
         ("Wo_f", (E, E), "w"), ("bo_f", (E,), "b"),
@@ -128,13 +143,13 @@ def param_layout(E, H):
     ]
 
 
-def param_count(E, H):
-    return sum(int(np.prod(s)) for _, s, _ in param_layout(E, H))
+def param_count(E, H, block="post"):
+    return sum(int(np.prod(s)) for _, s, _ in param_layout(E, H, block))
 
 
-def _draw_params(rng, E, H, style):
+def _draw_params(rng, E, H, style, block="post"):
     parts = []
-    for _, shape, kind in param_layout(E, H):
+    for _, shape, kind in param_layout(E, H, block):
         n = int(np.prod(shape))
         if style == "small_normal":
             v = rng.normal(0.0, 0.02, n)
@@ -172,6 +187,10 @@ class Workload:
     @property
     def dtype(self):
         return self.cfg["dtype"]
+
+    @property
+    def block(self):
+        return self.cfg.get("block", "post")
 
     @property
     def dims(self):
@@ -257,7 +276,7 @@ def make_workload(which, seed=None, datasets=None, with_dY=True):
     meta_rng = np.random.default_rng(kids[0])
     n_train_all, mask_all = _metadata(cfg, meta_rng)
     params = [_draw_params(np.random.default_rng(kids[1 + l]), cfg["E"], cfg["H"],
-                           cfg["weights"]) for l in range(L)]
+                           cfg["weights"], cfg.get("block", "post")) for l in range(L)]
     ds = np.arange(B) if datasets is None else np.asarray(datasets, dtype=np.int64)
     X = []
     dY = []

@@ -17,15 +17,28 @@ def nerr(a, b):
     return float(np.abs(a - b).max() / (den if den > 0 else 1.0))
 
 
+def _unpack(w):
+    return oracle.unpack_prenorm_params if w.block == "pre" else oracle.unpack_params
+
+
+def _param_names(w):
+    return oracle.PRENORM_PARAM_ORDER if w.block == "pre" else oracle.PARAM_ORDER
+
+
 def oracle_params(w):
-    return [oracle.unpack_params(p, w.cfg["E"], w.cfg["H"]) for p in w.params64()]
+    return [_unpack(w)(p, w.cfg["E"], w.cfg["H"]) for p in w.params64()]
 
 
 def oracle_stack(w, X=None, dY=None):
-    """Oracle forward + backward of the whole stack on the workload."""
+    """Oracle forward + backward of the whole stack on the workload (post-norm blocks, or
+    pre-norm blocks whose layer l scales its input by 0.95 ** l)."""
     X = w.X64() if X is None else X
     dY = w.dY64() if dY is None else dY
     Ps = oracle_params(w)
+    if w.block == "pre":
+        Y, caches = oracle.prenorm_stack_forward(X, Ps, w.n_train, w.cell_mask, w.cfg["heads"])
+        dX, grads = oracle.prenorm_stack_backward(dY, caches)
+        return Y, dX, [oracle.pack_prenorm_params(g) for g in grads]
     Y, caches = oracle.stack_forward(X, Ps, w.n_train, w.cell_mask, w.cfg["heads"])
     dX, grads = oracle.stack_backward(dY, caches)
     return Y, dX, [oracle.pack_params(g) for g in grads]
@@ -50,7 +63,8 @@ def gpu_stack(w, X=None, dY=None, keep_acts=False, params=None, storage=False):
     dt = w.dtype
     conv = (lambda t: storage_of(t, dt)) if storage else \
         (lambda t: wl.storage_to_f64(storage_of(t, dt), dt))
-    dims = tfm.make_dims(dtype=dt, **{k: v for k, v in w.dims.items() if k != "dtype"})
+    dims = tfm.make_dims(dtype=dt, block=w.block,
+                         **{k: v for k, v in w.dims.items() if k != "dtype"})
     st = Stack(dims, w.n_train, w.cell_mask, w.params if params is None else params)
     Xd = to_device(w.X if X is None else X, dt)
     dYd = to_device(w.dY if dY is None else dY, dt)
@@ -74,9 +88,9 @@ def compare_all(w, gpu, ref, tol=None):
     errs = {"Y": nerr(gpu["Y"], Y), "dX": nerr(gpu["dX"], dX)}
     E, H = w.cfg["E"], w.cfg["H"]
     for l, (gg, gr) in enumerate(zip(gpu["grads"], grads)):
-        pg = oracle.unpack_params(gg, E, H)
-        pr = oracle.unpack_params(gr, E, H)
-        for k in oracle.PARAM_ORDER:
+        pg = _unpack(w)(gg, E, H)
+        pr = _unpack(w)(gr, E, H)
+        for k in _param_names(w):
             errs[f"L{l}.{k}"] = nerr(pg[k], pr[k])
     bad = {k: v for k, v in errs.items() if not v <= tol}
     assert not bad, f"parity above {tol}: {bad}"

@@ -48,6 +48,18 @@ def test_param_count_matches_formula():
     assert tfm.param_count(_dims(E=192, H=384, heads=6)) == 445632
 
 
+def test_prenorm_param_count_and_sizes():
+    """The pre-norm block drops the three LayerNorm shifts; its packed count matches the
+    workload generator's layout, and its saved state has room for x' and the norm outputs."""
+    for E, H, heads in ((64, 192, 2), (192, 384, 6), (256, 768, 8)):
+        d = _dims(E=E, H=H, heads=heads, dtype="bf16", block="pre", decay=0.95)
+        assert tfm.param_count(d) == 8 * E * E + 8 * E + 2 * E * H + H + 4 * E
+        assert tfm.param_count(d) == wl.param_count(E, H, "pre")
+        post = _dims(E=E, H=H, heads=heads, dtype="bf16")
+        assert tfm.param_count(post) - tfm.param_count(d) == 3 * E
+        assert tfm.saved_bytes(d) > 0 and tfm.workspace_bytes(d) > 0
+
+
 def test_sizes_positive_and_grow_with_batch():
     d1, d2 = _dims(), _dims(B=4)
     assert 0 < tfm.saved_bytes(d1) < tfm.saved_bytes(d2)
@@ -58,6 +70,10 @@ def test_sizes_positive_and_grow_with_batch():
     (dict(B=0), -1), (dict(R=0), -1), (dict(C=-1), -1), (dict(C=300), -1),
     (dict(E=48), -1), (dict(E=512), -1), (dict(H=100), -1), (dict(dtype=7), -1),
     (dict(heads=3), -2), (dict(E=64, heads=1), -2), (dict(E=256, heads=2), -2),
+    (dict(block=2), -1), (dict(block="pre"), -1),                  # pre-norm needs bf16
+    (dict(block="pre", dtype="bf16", E=96, heads=3), -1),          # ... and E in {64,...,256}
+    (dict(block="pre", dtype="bf16", H=96), -1),                   # ... and H % E == 0
+    (dict(block="pre", dtype="bf16", decay=float("nan")), -1),
 ])
 def test_invalid_dims_rejected(kw, code):
     d = _dims(**kw)

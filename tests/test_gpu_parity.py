@@ -36,7 +36,8 @@ def _gpu():
     tfm.lib()
 
 
-@pytest.mark.parametrize("name", [0, "ragged-small-f32", "ragged-small-bf16", "d16-bf16"])
+@pytest.mark.parametrize("name", [0, "ragged-small-f32", "ragged-small-bf16", "d16-bf16",
+                                  "prenorm-small-bf16"])
 def test_parity_full(name):
     w = wl.make_workload(name)
     _say(f"[parity] {w.cfg['name']} seed={w.seed}")
