@@ -96,11 +96,16 @@ def cpu_baseline(cfg_index, seed):
         threads = os.cpu_count()
     w = wl.make_workload(cfg_index, seed=seed, datasets=[0])
     E, H, heads = w.cfg["E"], w.cfg["H"], w.cfg["heads"]
-    P = oracle.unpack_params(w.params64()[0], E, H)
     X, dY = w.X64(), w.dY64()
     t0 = time.perf_counter()
-    _, cache = oracle.layer_forward(X, P, w.n_train, w.cell_mask, heads)
-    oracle.layer_backward(dY, cache)
+    if w.block == "pre":
+        P = oracle.unpack_prenorm_params(w.params64()[0], E, H)
+        _, cache = oracle.prenorm_layer_forward(X, P, w.n_train, w.cell_mask, heads, 1.0)
+        oracle.prenorm_layer_backward(dY, cache)
+    else:
+        P = oracle.unpack_params(w.params64()[0], E, H)
+        _, cache = oracle.layer_forward(X, P, w.n_train, w.cell_mask, heads)
+        oracle.layer_backward(dY, cache)
     dt = time.perf_counter() - t0
     cells = int(w.cfg["R"] * np.count_nonzero(w.cell_mask[0]))
     return {"value": cells / dt, "unit": "cells/s", "cores": int(threads), "kind": "oracle",
@@ -114,7 +119,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--config", default="2",
+                    help="workload: an index of the baseline configurations, or a name")
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true",
@@ -145,12 +151,15 @@ def main():
     from paper_2606_03681_amd import tfm
     from paper_2606_03681_amd.stack import Stack, to_device
 
+    if str(args.config).isdigit():
+        args.config = int(args.config)
     cfg = wl.get_config(args.config)
     seed = wl.default_seed(cfg) if args.seed is None else args.seed
     print(f"[bench] generating {cfg['name']} seed={seed}", file=sys.stderr, flush=True)
     w = wl.make_workload(args.config, seed=seed)
     counts = wl.work_counts(w.n_train, w.cell_mask, cfg["R"], cfg["E"], cfg["H"], cfg["layers"])
-    dims = tfm.make_dims(dtype=w.dtype, **{k: v for k, v in w.dims.items() if k != "dtype"})
+    dims = tfm.make_dims(dtype=w.dtype, block=w.block,
+                         **{k: v for k, v in w.dims.items() if k != "dtype"})
     torch.cuda.set_device(0)
     st = Stack(dims, w.n_train, w.cell_mask, w.params)
     X = to_device(w.X, w.dtype)
@@ -219,6 +228,7 @@ def main():
         "config": {"workload": cfg["name"], "B": cfg["B"], "R": cfg["R"],
                    "n_train": str(cfg["n_train"]), "C": cfg["C"], "E": cfg["E"],
                    "heads": cfg["heads"], "H": cfg["H"], "layers": cfg["layers"],
+                   "block": cfg.get("block", "post"), "thinking_rows": cfg.get("thinking", 0),
                    "seed": seed, "active_cell_layers": counts["cell_layers"]},
         "tflops": round(tflops, 3), "mfma_peak_frac": round(tflops / peak, 5),
         "wall_ms_per_step": round(wall * 1e3 / args.steps, 4),

@@ -39,7 +39,7 @@
  * launches anything: on error nothing is launched, the return code is negative and
  * tfm_last_error() describes it.
  *
- * Supported envelope: B >= 1, R >= 1, 0 <= C <= 255, heads >= 1, d = E/heads in {16, 32},
+ * Supported envelope: B >= 1, R >= 1, 0 <= C <= 255, heads >= 1, d = E/heads in {16, 32, 64},
  * 32 <= E <= 256 with E % 32 == 0, 32 <= H <= 1024 with H % 32 == 0.
  *
  * Pre-norm block (dims->block == TFM_BLOCK_PRENORM): the block of the paper's current best
@@ -83,7 +83,7 @@ typedef struct {
 enum {
   TFM_OK = 0,
   TFM_ERR_DIMS = -1,      /* dimension outside the supported envelope */
-  TFM_ERR_HEAD_DIM = -2,  /* E % heads != 0 or d = E/heads not supported */
+  TFM_ERR_HEAD_DIM = -2,  /* E % heads != 0 or d = E/heads not in {16, 32, 64} */
   TFM_ERR_NTRAIN = -3,    /* some n_train[b] outside [1, R] */
   TFM_ERR_MASK = -4,      /* target cell of some dataset inactive */
   TFM_ERR_POINTER = -5,   /* null or misaligned pointer */

@@ -18,6 +18,7 @@
 #include <math.h>
 
 #include "attn.h"
+#include "attn_frag.h"
 #include "mfma.h"
 
 namespace tfm {
@@ -25,56 +26,6 @@ namespace tfm {
 namespace {
 
 constexpr float LOG2E = 1.4426950408889634f;
-constexpr int SMAX = 128;       // cells per row handled here
-constexpr int NKB = SMAX / 16;  // 16-cell blocks
-constexpr int TSF = SMAX + 8;   // LDS row stride of the transposed tiles (elements)
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-
-template <int D>
-struct FDot;
-
-template <>
-struct FDot<32> {
-  typedef bf16x8 frag;
-  static constexpr int FB = 16;
-  static __device__ __forceinline__ frag buf(rsrc_t r, uint32_t off) {
-    uint4 u = bload16(r, off);
-    return *reinterpret_cast<bf16x8*>(&u);
-  }
-  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, zero4(), 0, 0, 0);
-  }
-  static __device__ __forceinline__ float dot(const frag& a, const frag& b) {
-    const uint4 ua = *reinterpret_cast<const uint4*>(&a);
-    const uint4 ub = *reinterpret_cast<const uint4*>(&b);
-    float s = 0.f;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) s = fmaf(bf2f(u4_elem(ua, j)), bf2f(u4_elem(ub, j)), s);
-    return s;
-  }
-};
-
-template <>
-struct FDot<16> {
-  typedef s16x4 frag;
-  static constexpr int FB = 8;
-  static __device__ __forceinline__ frag buf(rsrc_t r, uint32_t off) {
-    uint2 u = bload8(r, off);
-    return *reinterpret_cast<s16x4*>(&u);
-  }
-  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b) {
-    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, zero4(), 0, 0, 0);
-  }
-  static __device__ __forceinline__ float dot(const frag& a, const frag& b) {
-    const uint2 ua = *reinterpret_cast<const uint2*>(&a);
-    const uint2 ub = *reinterpret_cast<const uint2*>(&b);
-    const uint4 wa = make_uint4(ua.x, ua.y, 0, 0), wb = make_uint4(ub.x, ub.y, 0, 0);
-    float s = 0.f;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) s = fmaf(bf2f(u4_elem(wa, j)), bf2f(u4_elem(wb, j)), s);
-    return s;
-  }
-};
 
 // Makes this wave's LDS writes visible to its own later LDS reads (no workgroup barrier: each
 // wave owns its LDS region).
@@ -113,32 +64,30 @@ __device__ __forceinline__ bool pair_of(const Geo& g, int64_t t, Pair& p) {
   return true;
 }
 
-// Write the row-role fragments fr[kb] (lane: cell kb*16 + c, dims lg*EPL .. lg*EPL + EPL-1)
-// transposed into dst[d][TSF] for the first nks 16-cell blocks.
-template <int D>
-__device__ __forceinline__ void stage_frag(const typename FDot<D>::frag* fr, int nks, int c,
+// Write the row-role fragments fr[kb] (lane: cell kb*16 + c) transposed into dst[d][TSF] for
+// the first nks of the NKB 16-cell blocks.
+template <int D, int NKB, int TSF>
+__device__ __forceinline__ void stage_frag(const typename HF<D>::frag* fr, int nks, int c,
                                            int lg, bf16* dst) {
-  constexpr int EPL = FDot<D>::FB / 2;
 #pragma unroll
   for (int kb = 0; kb < NKB; ++kb)
     if (kb < nks) {
-      const uint2* u = reinterpret_cast<const uint2*>(&fr[kb]);
 #pragma unroll
-      for (int j = 0; j < EPL; ++j) {
-        const uint32_t wd = j < 4 ? (j < 2 ? u[0].x : u[0].y) : (j < 6 ? u[1].x : u[1].y);
-        dst[(lg * EPL + j) * TSF + kb * 16 + c] = (bf16)(j & 1 ? wd >> 16 : wd & 0xffff);
-      }
+      for (int j = 0; j < HF<D>::EPL; ++j)
+        dst[HF<D>::dim(lg, j) * TSF + kb * 16 + c] = HF<D>::elem(fr[kb], j);
     }
 }
 
 }  // namespace
 
 // ================================================================================ forward
-template <int D>
+template <int D, int SM>
 __global__ __launch_bounds__(256) void k_feat_attn_fwd(Geo g, const bf16* __restrict__ qkv,
                                                        bf16* __restrict__ o,
                                                        float* __restrict__ lse) {
   constexpr int DB = D / 16;
+  constexpr int NKB = SM / 16;   // 16-cell blocks of the longest row handled
+  constexpr int TSF = SM + 8;    // LDS row stride of the transposed tiles (elements)
   __shared__ __attribute__((aligned(16))) bf16 Vt[4][D * TSF];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int c = lane & 15, lg = lane >> 4;
@@ -153,19 +102,19 @@ __global__ __launch_bounds__(256) void k_feat_attn_fwd(Geo g, const bf16* __rest
 
   bf16* vt = Vt[w];
   const int nks = (nkb + 1) & ~1;  // staged blocks: whole pairs of 16-cell blocks
-  typedef typename FDot<D>::frag frag;
+  typedef typename HF<D>::frag frag;
   frag kf[NKB], qf[NKB];
   {
     frag vf[NKB];
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb)
       if (kb < nks) {
-        const uint32_t row = (uint32_t)(kb * 16 + c) * cs + lg * FDot<D>::FB;
-        kf[kb] = FDot<D>::buf(rq, row + ok);
-        vf[kb] = FDot<D>::buf(rq, row + ov);
-        qf[kb] = FDot<D>::buf(rq, row + oq);
+        const uint32_t row = (uint32_t)(kb * 16 + c) * cs;
+        kf[kb] = HF<D>::buf(rq, row + ok, lg);
+        vf[kb] = HF<D>::buf(rq, row + ov, lg);
+        qf[kb] = HF<D>::buf(rq, row + oq, lg);
       }
-    stage_frag<D>(vf, nks, c, lg, vt);
+    stage_frag<D, NKB, TSF>(vf, nks, c, lg, vt);
   }
   wave_lds_sync();
 
@@ -180,7 +129,7 @@ __global__ __launch_bounds__(256) void k_feat_attn_fwd(Geo g, const bf16* __rest
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb) {
       if (kb < nkb) {
-        s[kb] = FDot<D>::mma(kf[kb], qf[qb]);
+        s[kb] = HF<D>::mma(kf[kb], qf[qb]);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           if (kb * 16 + lg * 4 + i >= S) s[kb][i] = -INFINITY;
@@ -232,17 +181,19 @@ __global__ __launch_bounds__(256) void k_feat_attn_fwd(Geo g, const bf16* __rest
 }
 
 // ================================================================================ backward
-template <int D>
+template <int D, int SM>
 __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __restrict__ qkv,
                                                        const bf16* __restrict__ o,
                                                        const bf16* __restrict__ dout,
                                                        const float* __restrict__ lse,
                                                        bf16* __restrict__ dqkv) {
   constexpr int DB = D / 16;
+  constexpr int NKB = SM / 16;   // 16-cell blocks of the longest row handled
+  constexpr int TSF = SM + 8;    // LDS row stride of the transposed tiles (elements)
   // per wave: sweep 1 uses [0, D*TSF) for K^T; sweep 2 uses Q^T then dO^T
   __shared__ __attribute__((aligned(16))) bf16 T[4][2 * D * TSF];
-  __shared__ __attribute__((aligned(16))) float Lr[4][SMAX];
-  __shared__ __attribute__((aligned(16))) float Dr[4][SMAX];
+  __shared__ __attribute__((aligned(16))) float Lr[4][SM];
+  __shared__ __attribute__((aligned(16))) float Dr[4][SM];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int c = lane & 15, lg = lane >> 4;
   Pair pr;
@@ -263,7 +214,7 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
   const uint64_t dcs = (uint64_t)g.R * 3 * E;  // elements between cells in dQKV
 
   // every fragment of the pair in the row role (lane: cell kb*16 + c), loaded up front
-  typedef typename FDot<D>::frag frag;
+  typedef typename HF<D>::frag frag;
   const int nks = (nkb + 1) & ~1;  // staged blocks: whole pairs of 16-cell blocks
   frag kf[NKB], vf[NKB], qf[NKB], df[NKB];
   float nbq[NKB], dq[NKB];  // per query kb*16 + c: -lse * log2(e) and D = rowsum(dO * O)
@@ -271,12 +222,11 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
   for (int kb = 0; kb < NKB; ++kb)
     if (kb < nks) {
       const uint32_t rr = (uint32_t)(kb * 16 + c);
-      const uint32_t fo = lg * FDot<D>::FB;
-      kf[kb] = FDot<D>::buf(rq, rr * cs + hk + fo);
-      vf[kb] = FDot<D>::buf(rq, rr * cs + hv + fo);
-      qf[kb] = FDot<D>::buf(rq, rr * cs + hq + fo);
-      df[kb] = FDot<D>::buf(rdo, rr * ecs + hq + fo);
-      dq[kb] = FDot<D>::dot(df[kb], FDot<D>::buf(ro, rr * ecs + hq + fo));
+      kf[kb] = HF<D>::buf(rq, rr * cs + hk, lg);
+      vf[kb] = HF<D>::buf(rq, rr * cs + hv, lg);
+      qf[kb] = HF<D>::buf(rq, rr * cs + hq, lg);
+      df[kb] = HF<D>::buf(rdo, rr * ecs + hq, lg);
+      dq[kb] = hf_dot<D>(df[kb], HF<D>::buf(ro, rr * ecs + hq, lg));
       nbq[kb] = (int)rr < S ? -lse[(pr.cell0 + (int64_t)rr * g.R) * g.heads + pr.head] * LOG2E
                             : 0.f;
     }
@@ -290,7 +240,7 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
         Dr[w][kb * 16 + c] = dq[kb];
       }
     }
-  stage_frag<D>(kf, nks, c, lg, t0);  // K^T
+  stage_frag<D, NKB, TSF>(kf, nks, c, lg, t0);  // K^T
   wave_lds_sync();
 
   // ---- sweep 1 (query-major): dQ^T = K^T dS^T, one pair of key blocks (32 keys) at a time
@@ -309,8 +259,8 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
       for (int h = 0; h < 2; ++h) {
         const int kb = 2 * ks + h;
         if (kb < nkb) {
-          const f32x4 s = FDot<D>::mma(kf[kb], qf[qb]);
-          const f32x4 dp = FDot<D>::mma(vf[kb], df[qb]);
+          const f32x4 s = HF<D>::mma(kf[kb], qf[qb]);
+          const f32x4 dp = HF<D>::mma(vf[kb], df[qb]);
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             float p = exp2_hw(fmaf(s[i], c2, nbq[qb]));
@@ -337,8 +287,8 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
   }
   wave_lds_sync();
   // ---- sweep 2 (key-major): dV^T += dO^T P, dK^T += Q^T dS over all query blocks
-  stage_frag<D>(qf, nks, c, lg, t0);  // Q^T
-  stage_frag<D>(df, nks, c, lg, t1);  // dO^T
+  stage_frag<D, NKB, TSF>(qf, nks, c, lg, t0);  // Q^T
+  stage_frag<D, NKB, TSF>(df, nks, c, lg, t1);  // dO^T
   wave_lds_sync();
 #pragma unroll
   for (int kb = 0; kb < NKB; ++kb) {
@@ -353,8 +303,8 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const int qb = 2 * ks + h;
-          const f32x4 s = FDot<D>::mma(qf[qb], kf[kb]);
-          const f32x4 dp = FDot<D>::mma(df[qb], vf[kb]);
+          const f32x4 s = HF<D>::mma(qf[qb], kf[kb]);
+          const f32x4 dp = HF<D>::mma(df[qb], vf[kb]);
           const float4 l4 = *reinterpret_cast<const float4*>(&Lr[w][qb * 16 + lg * 4]);
           const float4 d4 = *reinterpret_cast<const float4*>(&Dr[w][qb * 16 + lg * 4]);
           const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dv4[4] = {d4.x, d4.y, d4.z, d4.w};
@@ -389,30 +339,61 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
   }
 }
 
+// Longest row (cells) handled by the MFMA kernels for head dim d: all of a pair's fragments
+// stay in registers, four arrays of them in the backward pass.
+static int feat_attn_smax(int d) { return d == 64 ? 64 : 128; }
+
 bool feat_attn_mfma_ok(const Geo& g) {
-  return g.S <= SMAX && (int64_t)g.R * g.S * 3 * g.E * 2 < (int64_t(1) << 31);
+  return (g.d == 16 || g.d == 32 || g.d == 64) && g.S <= feat_attn_smax(g.d) &&
+         (int64_t)g.R * g.S * 3 * g.E * 2 < (int64_t(1) << 31);
+}
+
+template <int D>
+static hipError_t feat_fwd_d(const Geo& g, unsigned grid, const bf16* qkv, bf16* o, float* lse,
+                             hipStream_t s) {
+  if (g.S <= 32)
+    k_feat_attn_fwd<D, 32><<<grid, 256, 0, s>>>(g, qkv, o, lse);
+  else if (g.S <= 64)
+    k_feat_attn_fwd<D, 64><<<grid, 256, 0, s>>>(g, qkv, o, lse);
+  else if (D < 64)
+    k_feat_attn_fwd<D, (D < 64 ? 128 : 64)><<<grid, 256, 0, s>>>(g, qkv, o, lse);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t feat_bwd_d(const Geo& g, unsigned grid, const bf16* qkv, const bf16* o,
+                             const bf16* dout, const float* lse, bf16* dqkv, hipStream_t s) {
+  if (g.S <= 32)
+    k_feat_attn_bwd<D, 32><<<grid, 256, 0, s>>>(g, qkv, o, dout, lse, dqkv);
+  else if (g.S <= 64)
+    k_feat_attn_bwd<D, 64><<<grid, 256, 0, s>>>(g, qkv, o, dout, lse, dqkv);
+  else if (D < 64)
+    k_feat_attn_bwd<D, (D < 64 ? 128 : 64)><<<grid, 256, 0, s>>>(g, qkv, o, dout, lse, dqkv);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
 }
 
 hipError_t launch_feat_attn_fwd(const Geo& g, const bf16* qkv, bf16* o, float* lse,
                                 hipStream_t s) {
+  if (!feat_attn_mfma_ok(g)) return hipErrorInvalidValue;
   const int64_t pairs = (int64_t)g.B * g.R * g.heads;
   const unsigned grid = (unsigned)((pairs + 3) / 4);
-  if (g.d == 16)
-    k_feat_attn_fwd<16><<<grid, 256, 0, s>>>(g, qkv, o, lse);
-  else
-    k_feat_attn_fwd<32><<<grid, 256, 0, s>>>(g, qkv, o, lse);
-  return hipGetLastError();
+  if (g.d == 16) return feat_fwd_d<16>(g, grid, qkv, o, lse, s);
+  if (g.d == 32) return feat_fwd_d<32>(g, grid, qkv, o, lse, s);
+  return feat_fwd_d<64>(g, grid, qkv, o, lse, s);
 }
 
 hipError_t launch_feat_attn_bwd(const Geo& g, const bf16* qkv, const bf16* o, const bf16* dout,
                                 const float* lse, bf16* dqkv, hipStream_t s) {
+  if (!feat_attn_mfma_ok(g)) return hipErrorInvalidValue;
   const int64_t pairs = (int64_t)g.B * g.R * g.heads;
   const unsigned grid = (unsigned)((pairs + 3) / 4);
-  if (g.d == 16)
-    k_feat_attn_bwd<16><<<grid, 256, 0, s>>>(g, qkv, o, dout, lse, dqkv);
-  else
-    k_feat_attn_bwd<32><<<grid, 256, 0, s>>>(g, qkv, o, dout, lse, dqkv);
-  return hipGetLastError();
+  if (g.d == 16) return feat_bwd_d<16>(g, grid, qkv, o, dout, lse, dqkv, s);
+  if (g.d == 32) return feat_bwd_d<32>(g, grid, qkv, o, dout, lse, dqkv, s);
+  return feat_bwd_d<64>(g, grid, qkv, o, dout, lse, dqkv, s);
 }
 
 }  // namespace tfm

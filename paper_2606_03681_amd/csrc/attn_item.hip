@@ -17,6 +17,7 @@
 #include <math.h>
 
 #include "attn.h"
+#include "attn_frag.h"
 #include "mfma.h"
 
 namespace tfm {
@@ -26,33 +27,6 @@ namespace {
 constexpr int KT = 64;   // keys per tile
 constexpr int QWV = 32;  // queries per wave
 constexpr int QWG = 128; // queries per workgroup
-
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-
-template <int D>
-struct QK;
-
-// S^T block = K (16 keys x 32 dims) * Q^T (32 dims x 16 queries)
-template <>
-struct QK<32> {
-  typedef bf16x8 frag;
-  static __device__ __forceinline__ frag load(const bf16* row, int lg) { return ld8(row + lg * 8); }
-  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b, const f32x4& c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-  }
-};
-
-// d = 16: v_mfma_f32_16x16x16_bf16, lane holds A[c][4g .. 4g+3]
-template <>
-struct QK<16> {
-  typedef s16x4 frag;
-  static __device__ __forceinline__ frag load(const bf16* row, int lg) {
-    return *reinterpret_cast<const s16x4*>(row + lg * 4);
-  }
-  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b, const f32x4& c) {
-    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
-  }
-};
 
 __device__ __forceinline__ uint32_t pk_bf16(float a, float b) { return pack2(a, b); }
 
@@ -65,7 +39,7 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
                                                        bf16* __restrict__ o,
                                                        float* __restrict__ lse, int QT) {
   constexpr int KS = D + 8;   // LDS row stride of K (elements; conflict-free 16-byte reads)
-  constexpr int VS = 48;      // LDS row stride of V (96 bytes: conflict-free transpose reads)
+  constexpr int VS = tr_stride<D>();  // LDS row stride of V (conflict-free transpose reads)
   constexpr int DB = D / 16;  // 16-wide dim blocks
   constexpr int CPR = D / 8;  // 16-byte chunks per key row
   __shared__ __attribute__((aligned(16))) bf16 Ks[2][KT * KS];
@@ -88,35 +62,35 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
   const int qw0 = qt * QWG + wave * QWV;
 
   // Q^T fragments (B operand): lane holds query qw0 + qb*16 + c
-  typename QK<D>::frag qf[2];
+  typename HF<D>::frag qf[2];
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
     int qq = qw0 + qb * 16 + c;
-    if (qq < R) {
-      qf[qb] = QK<D>::load(Qp + (int64_t)qq * D, lg);
-    } else {
-      qf[qb] = typename QK<D>::frag{};
-    }
+    qf[qb] = qq < R ? HF<D>::glob(Qp + (int64_t)qq * D, lg) : HF<D>::zero();
   }
 
-  // staging: thread -> (key, 16-byte chunk of its dims)
-  const int skey = tid / CPR, sch = (tid % CPR) * 8;
-  const bool stager = tid < KT * CPR;
-  uint4 rk = make_uint4(0, 0, 0, 0), rv = make_uint4(0, 0, 0, 0);
+  // staging: item it = tid + 256 i -> (key it / CPR, 16-byte chunk of its dims)
+  constexpr int NSI = (KT * CPR + 255) / 256;  // staging items per thread
+  uint4 rk[NSI], rv[NSI];
   auto gload = [&](int t0) {
-    int t = t0 + skey;
-    if (stager && t < n) {
-      rk = ldu4(Kp + (int64_t)t * D + sch);
-      rv = ldu4(Vp + (int64_t)t * D + sch);
-    } else {
-      rk = make_uint4(0, 0, 0, 0);
-      rv = make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < NSI; ++i) {
+      const int it = tid + 256 * i;
+      const int t = t0 + it / CPR, ch = (it % CPR) * 8;
+      const bool ok = it < KT * CPR && t < n;
+      rk[i] = ok ? ldu4(Kp + (int64_t)t * D + ch) : make_uint4(0, 0, 0, 0);
+      rv[i] = ok ? ldu4(Vp + (int64_t)t * D + ch) : make_uint4(0, 0, 0, 0);
     }
   };
   auto sstore = [&](int buf) {
-    if (!stager) return;
-    stu4(&Ks[buf][skey * KS + sch], rk);
-    stu4(&Vs[buf][skey * VS + sch], rv);
+#pragma unroll
+    for (int i = 0; i < NSI; ++i) {
+      const int it = tid + 256 * i;
+      if (it >= KT * CPR) break;
+      const int key = it / CPR, ch = (it % CPR) * 8;
+      stu4(&Ks[buf][key * KS + ch], rk[i]);
+      stu4(&Vs[buf][key * VS + ch], rv[i]);
+    }
   };
 
   // K arrives pre-multiplied by log2(e)/sqrt(d), so S^T = K Q^T is in the exp2 domain.  The MFMA
@@ -151,9 +125,9 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
     }
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      typename QK<D>::frag kf = QK<D>::load(&Ks[cur][(kb * 16 + c) * KS], lg);
+      const typename HF<D>::frag kf = HF<D>::lds(&Ks[cur][(kb * 16 + c) * KS], lg);
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) sc[kb][qb] = QK<D>::mma(kf, qf[qb], init[qb]);
+      for (int qb = 0; qb < 2; ++qb) sc[kb][qb] = HF<D>::mma(kf, qf[qb], init[qb]);
     }
     if (tail) {
 #pragma unroll
@@ -251,8 +225,12 @@ hipError_t launch_item_attn_fwd(const Geo& g, const bf16* q, const bf16* k, cons
   const int64_t grid = (P + 7) / 8 * 8 * QT;
   if (g.d == 16)
     k_item_attn_fwd<16><<<(unsigned)grid, 256, 0, s>>>(g, q, k, v, o, lse, QT);
-  else
+  else if (g.d == 32)
     k_item_attn_fwd<32><<<(unsigned)grid, 256, 0, s>>>(g, q, k, v, o, lse, QT);
+  else if (g.d == 64)
+    k_item_attn_fwd<64><<<(unsigned)grid, 256, 0, s>>>(g, q, k, v, o, lse, QT);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

@@ -24,6 +24,7 @@
 #include <math.h>
 
 #include "attn.h"
+#include "attn_frag.h"
 #include "mfma.h"
 
 namespace tfm {
@@ -31,60 +32,6 @@ namespace tfm {
 namespace {
 
 constexpr float LOG2E = 1.4426950408889634f;
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-
-// Products over the head dimension: A (16 rows x D) times B (D x 16 cols).
-template <int D>
-struct Dot;
-
-template <>
-struct Dot<32> {
-  typedef bf16x8 frag;
-  static constexpr int FB = 16;  // bytes of a fragment per lane
-  static __device__ __forceinline__ frag lds(const bf16* row, int lg) { return ld8(row + lg * 8); }
-  static __device__ __forceinline__ frag buf(rsrc_t r, uint32_t off) {
-    uint4 u = bload16(r, off);
-    return *reinterpret_cast<bf16x8*>(&u);
-  }
-  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b, const f32x4& c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-  }
-  // sum over the lane's 8 elements of a * b
-  static __device__ __forceinline__ float dot(const frag& a, const frag& b) {
-    const uint4 ua = *reinterpret_cast<const uint4*>(&a);
-    const uint4 ub = *reinterpret_cast<const uint4*>(&b);
-    float s = 0.f;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) s = fmaf(bf2f(u4_elem(ua, j)), bf2f(u4_elem(ub, j)), s);
-    return s;
-  }
-};
-
-template <>
-struct Dot<16> {
-  typedef s16x4 frag;
-  static constexpr int FB = 8;
-  static __device__ __forceinline__ frag lds(const bf16* row, int lg) {
-    return *reinterpret_cast<const s16x4*>(row + lg * 4);
-  }
-  static __device__ __forceinline__ frag buf(rsrc_t r, uint32_t off) {
-    uint2 u = bload8(r, off);
-    return *reinterpret_cast<s16x4*>(&u);
-  }
-  static __device__ __forceinline__ f32x4 mma(const frag& a, const frag& b, const f32x4& c) {
-    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
-  }
-  static __device__ __forceinline__ float dot(const frag& a, const frag& b) {
-    const uint2 ua = *reinterpret_cast<const uint2*>(&a);
-    const uint2 ub = *reinterpret_cast<const uint2*>(&b);
-    const uint4 wa = make_uint4(ua.x, ua.y, 0, 0), wb = make_uint4(ub.x, ub.y, 0, 0);
-    float s = 0.f;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) s = fmaf(bf2f(u4_elem(wa, j)), bf2f(u4_elem(wb, j)), s);
-    return s;
-  }
-};
-
 __device__ __forceinline__ bf16x8 cat8(uint2 lo, uint2 hi) {
   uint4 u = make_uint4(lo.x, lo.y, hi.x, hi.y);
   return *reinterpret_cast<bf16x8*>(&u);
@@ -114,7 +61,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
   constexpr int DB = D / 16;
   constexpr int CPR = D / 8;      // 16-byte chunks per row of d values
   constexpr int NIT = QC * CPR / 128;  // staging items per thread (128 threads per tensor)
-  constexpr int RS = 48;          // LDS row stride of Q / dO (96 bytes: see ld_tr8)
+  constexpr int RS = tr_stride<D>();  // LDS row stride of Q / dO (see ld_tr8)
   __shared__ __attribute__((aligned(16))) bf16 Qs[2][QC * RS];
   __shared__ __attribute__((aligned(16))) bf16 dOs[2][QC * RS];
   __shared__ __attribute__((aligned(16))) float Dq[2][QC];
@@ -148,12 +95,12 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
   // this lane's key column of key block kb in the S layout: t0 + w*32 + kb*16 + c; keys past
   // n read K = V = 0 here and their dK, dV are never written, so no key masking is needed
   const int kw0 = t0 + w * KW;
-  typename Dot<D>::frag kf[2], vf[2];
+  typename HF<D>::frag kf[2], vf[2];
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
     const uint32_t key = (uint32_t)(kw0 + kb * 16 + c);
-    kf[kb] = Dot<D>::buf(rK, key * rowQ + lg * Dot<D>::FB);
-    vf[kb] = Dot<D>::buf(rV, key * rowQ + lg * Dot<D>::FB);
+    kf[kb] = HF<D>::buf(rK, key * rowQ, lg);
+    vf[kb] = HF<D>::buf(rV, key * rowQ, lg);
   }
 
   // staging: threads 0-127 move Q, threads 128-255 move dO (and D and the LSE); each handles
@@ -208,15 +155,15 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
     uint32_t pw[2][4][2], sw[2][4][2];
 #pragma unroll
     for (int qb = 0; qb < 4; ++qb) {
-      const typename Dot<D>::frag qa = Dot<D>::lds(&Qs[b][(qb * 16 + c) * RS], lg);
-      const typename Dot<D>::frag da = Dot<D>::lds(&dOs[b][(qb * 16 + c) * RS], lg);
+      const typename HF<D>::frag qa = HF<D>::lds(&Qs[b][(qb * 16 + c) * RS], lg);
+      const typename HF<D>::frag da = HF<D>::lds(&dOs[b][(qb * 16 + c) * RS], lg);
       // seeds: -lse log2(e) and -D of the lane's 4 query rows
       const f32x4 nl = *reinterpret_cast<const f32x4*>(&Lq[b][qb * 16 + lg * 4]);
       const f32x4 nd = *reinterpret_cast<const f32x4*>(&Dq[b][qb * 16 + lg * 4]);
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        const f32x4 s = Dot<D>::mma(qa, kf[kb], nl);     // S log2(e) - lse log2(e)
-        const f32x4 dp = Dot<D>::mma(da, vf[kb], nd);    // dP - D
+        const f32x4 s = HF<D>::mma(qa, kf[kb], nl);     // S log2(e) - lse log2(e)
+        const f32x4 dp = HF<D>::mma(da, vf[kb], nd);    // dP - D
         const float p0 = exp2_hw(s[0]), p1 = exp2_hw(s[1]);
         const float p2 = exp2_hw(s[2]), p3 = exp2_hw(s[3]);
         pw[kb][qb][0] = pack2(p0, p1);
@@ -276,7 +223,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
   constexpr int KTL = 64;         // keys per tile
   constexpr int DB = D / 16;
   constexpr int CPR = D / 8;
-  constexpr int KS = 48;          // LDS row stride of K ([key][d]; 96 bytes: see ld_tr8)
+  constexpr int KS = tr_stride<D>();  // LDS row stride of K ([key][d]; see ld_tr8)
   constexpr int VS = D + 8;       // LDS row stride of V (conflict-free 16-byte row reads)
   __shared__ __attribute__((aligned(16))) bf16 Ks[2][KTL * KS];
   __shared__ __attribute__((aligned(16))) bf16 Vs[2][KTL * VS];
@@ -304,15 +251,15 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
   const int qw0 = qt * 128 + w * 32;
   // per query block: Q^T and dO^T fragments (B operands), D = rowsum(dO o O), -lse log2(e);
   // queries past R read as zero (their results are not written)
-  typename Dot<D>::frag qf[2], df[2];
+  typename HF<D>::frag qf[2], df[2];
   float Dv[2], nb[2];
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
     const uint32_t qq = (uint32_t)(qw0 + qb * 16 + c);
-    qf[qb] = Dot<D>::buf(rQ, qq * rowQ + lg * Dot<D>::FB);
-    df[qb] = Dot<D>::buf(rdO, qq * rowO + lg * Dot<D>::FB);
-    const typename Dot<D>::frag of = Dot<D>::buf(rO, qq * rowO + lg * Dot<D>::FB);
-    float dot = Dot<D>::dot(df[qb], of);
+    qf[qb] = HF<D>::buf(rQ, qq * rowQ, lg);
+    df[qb] = HF<D>::buf(rdO, qq * rowO, lg);
+    const typename HF<D>::frag of = HF<D>::buf(rO, qq * rowO, lg);
+    float dot = hf_dot<D>(df[qb], of);
     dot += __shfl_xor(dot, 16, 64);
     dot += __shfl_xor(dot, 32, 64);
     Dv[qb] = dot;
@@ -320,20 +267,29 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
     if (lg == 0 && (int)qq < R) Dbuf[prob * R + qq] = dot;
   }
 
-  // key tile staging: thread -> (key, 16-byte chunk of its d values); keys past n read 0
-  const int skey = tid / CPR, sch = (tid % CPR) * 8;
-  const bool stager = tid < KTL * CPR;
-  uint4 rk = make_uint4(0, 0, 0, 0), rv = make_uint4(0, 0, 0, 0);
+  // key tile staging: item it = tid + 256 i -> (key it / CPR, 16-byte chunk of its d values);
+  // keys past n read 0
+  constexpr int NSI = (KTL * CPR + 255) / 256;  // staging items per thread
+  uint4 rk[NSI], rv[NSI];
   auto gload = [&](int t0) {
-    if (stager) {
-      rk = bload16(rK, (uint32_t)(t0 + skey) * rowQ + sch * 2);
-      rv = bload16(rV, (uint32_t)(t0 + skey) * rowQ + sch * 2);
+#pragma unroll
+    for (int i = 0; i < NSI; ++i) {
+      const int it = tid + 256 * i;
+      const uint32_t key = (uint32_t)(t0 + it / CPR), ch = (it % CPR) * 8;
+      const bool ok = it < KTL * CPR;
+      rk[i] = ok ? bload16(rK, key * rowQ + ch * 2) : make_uint4(0, 0, 0, 0);
+      rv[i] = ok ? bload16(rV, key * rowQ + ch * 2) : make_uint4(0, 0, 0, 0);
     }
   };
   auto sstore = [&](int b) {
-    if (!stager) return;
-    stu4(&Ks[b][skey * KS + sch], rk);
-    stu4(&Vs[b][skey * VS + sch], rv);
+#pragma unroll
+    for (int i = 0; i < NSI; ++i) {
+      const int it = tid + 256 * i;
+      if (it >= KTL * CPR) break;
+      const int key = it / CPR, ch = (it % CPR) * 8;
+      stu4(&Ks[b][key * KS + ch], rk[i]);
+      stu4(&Vs[b][key * VS + ch], rv[i]);
+    }
   };
 
   f32x4 acc[DB][2];
@@ -351,12 +307,12 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
     f32x4 dsv[4][2];
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      const typename Dot<D>::frag kfr = Dot<D>::lds(&Ks[b][(kb * 16 + c) * KS], lg);
-      const typename Dot<D>::frag vfr = Dot<D>::lds(&Vs[b][(kb * 16 + c) * VS], lg);
+      const typename HF<D>::frag kfr = HF<D>::lds(&Ks[b][(kb * 16 + c) * KS], lg);
+      const typename HF<D>::frag vfr = HF<D>::lds(&Vs[b][(kb * 16 + c) * VS], lg);
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) {
-        const f32x4 s = Dot<D>::mma(kfr, qf[qb], snl[qb]);    // exponent of P^T
-        const f32x4 dp = Dot<D>::mma(vfr, df[qb], snd[qb]);   // dP^T - D
+        const f32x4 s = HF<D>::mma(kfr, qf[qb], snl[qb]);    // exponent of P^T
+        const f32x4 dp = HF<D>::mma(vfr, df[qb], snd[qb]);   // dP^T - D
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           float p = exp2_hw(s[i]);
@@ -415,8 +371,12 @@ hipError_t launch_item_attn_dq(const Geo& g, const bf16* q, const bf16* k, const
   const unsigned grid = (unsigned)((P + 7) / 8 * 8 * QT);
   if (g.d == 16)
     k_item_attn_dq<16><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dq, QT);
-  else
+  else if (g.d == 32)
     k_item_attn_dq<32><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dq, QT);
+  else if (g.d == 64)
+    k_item_attn_dq<64><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dq, QT);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
@@ -428,8 +388,12 @@ hipError_t launch_item_attn_dkdv(const Geo& g, const bf16* q, const bf16* k, con
   const unsigned grid = (unsigned)((P + 7) / 8 * 8 * KT);
   if (g.d == 16)
     k_item_attn_dkdv<16><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dk, dv, KT);
-  else
+  else if (g.d == 32)
     k_item_attn_dkdv<32><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dk, dv, KT);
+  else if (g.d == 64)
+    k_item_attn_dkdv<64><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dk, dv, KT);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

@@ -502,8 +502,10 @@ hipError_t launch_feat_attn_fwd_simple(const Geo& g, const T* qkv, T* o, float* 
   int64_t total = (int64_t)g.B * g.R * g.heads * g.S;
   if (g.d == 16)
     k_feat_attn_fwd<T, 16><<<grid_for(total), TFM_BLOCK, 0, s>>>(g, qkv, o, lse);
-  else
+  else if (g.d == 32)
     k_feat_attn_fwd<T, 32><<<grid_for(total), TFM_BLOCK, 0, s>>>(g, qkv, o, lse);
+  else
+    k_feat_attn_fwd<T, 64><<<grid_for(total), TFM_BLOCK, 0, s>>>(g, qkv, o, lse);
   return hipGetLastError();
 }
 
@@ -589,8 +591,10 @@ hipError_t launch_feat_attn_bwd_simple(const Geo& g, const T* qkv, const T* o, c
   int64_t total = (int64_t)g.B * g.R * g.heads * g.S;
   if (g.d == 16)
     k_feat_attn_bwd<T, 16><<<grid_for(total), TFM_BLOCK, 0, s>>>(g, qkv, o, dout, lse, dqkv);
-  else
+  else if (g.d == 32)
     k_feat_attn_bwd<T, 32><<<grid_for(total), TFM_BLOCK, 0, s>>>(g, qkv, o, dout, lse, dqkv);
+  else
+    k_feat_attn_bwd<T, 64><<<grid_for(total), TFM_BLOCK, 0, s>>>(g, qkv, o, dout, lse, dqkv);
   return hipGetLastError();
 }
 
@@ -647,8 +651,10 @@ hipError_t launch_item_attn_fwd_simple(const Geo& g, const T* q, const T* k, con
   int64_t total = (int64_t)g.NC * g.heads * g.R;
   if (g.d == 16)
     k_item_attn_fwd<T, 16><<<grid_for(total), TFM_BLOCK, 0, s>>>(g, q, k, v, o, lse);
-  else
+  else if (g.d == 32)
     k_item_attn_fwd<T, 32><<<grid_for(total), TFM_BLOCK, 0, s>>>(g, q, k, v, o, lse);
+  else
+    k_item_attn_fwd<T, 64><<<grid_for(total), TFM_BLOCK, 0, s>>>(g, q, k, v, o, lse);
   return hipGetLastError();
 }
 
@@ -769,10 +775,14 @@ hipError_t launch_item_attn_bwd_simple(const Geo& g, const T* q, const T* k, con
     k_item_rowdot<T, 16><<<grid, TFM_BLOCK, 0, s>>>(g, o, dout, D);
     k_item_attn_dq<T, 16><<<grid, TFM_BLOCK, 0, s>>>(g, q, k, v, dout, lse, D, dq);
     k_item_attn_dkv<T, 16><<<grid, TFM_BLOCK, 0, s>>>(g, q, k, v, dout, lse, D, dk, dv);
-  } else {
+  } else if (g.d == 32) {
     k_item_rowdot<T, 32><<<grid, TFM_BLOCK, 0, s>>>(g, o, dout, D);
     k_item_attn_dq<T, 32><<<grid, TFM_BLOCK, 0, s>>>(g, q, k, v, dout, lse, D, dq);
     k_item_attn_dkv<T, 32><<<grid, TFM_BLOCK, 0, s>>>(g, q, k, v, dout, lse, D, dk, dv);
+  } else {
+    k_item_rowdot<T, 64><<<grid, TFM_BLOCK, 0, s>>>(g, o, dout, D);
+    k_item_attn_dq<T, 64><<<grid, TFM_BLOCK, 0, s>>>(g, q, k, v, dout, lse, D, dq);
+    k_item_attn_dkv<T, 64><<<grid, TFM_BLOCK, 0, s>>>(g, q, k, v, dout, lse, D, dk, dv);
   }
   return hipGetLastError();
 }

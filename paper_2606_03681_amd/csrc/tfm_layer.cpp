@@ -60,8 +60,8 @@ int check_dims(const tfm_dims* p, Dims& d) {
   if (d.heads < 1 || d.E % d.heads)
     return fail(TFM_ERR_HEAD_DIM, "E=%d is not a multiple of heads=%d", d.E, d.heads);
   d.d = d.E / d.heads;
-  if (d.d != 16 && d.d != 32)
-    return fail(TFM_ERR_HEAD_DIM, "head dim E/heads=%d not supported (16 or 32)", d.d);
+  if (d.d != 16 && d.d != 32 && d.d != 64)
+    return fail(TFM_ERR_HEAD_DIM, "head dim E/heads=%d not supported (16, 32 or 64)", d.d);
   d.S = d.C + 1;
   d.Nmax = (int64_t)d.B * d.R * d.S;
   if (d.Nmax > kMaxCells)

@@ -87,6 +87,16 @@ TEST_CONFIGS = {
                               heads=6, H=384, layers=2, cells="normal", weights="xavier_bias"),
     "d16-bf16": dict(name="d16-bf16", dtype="bf16", B=3, R=130, n_train=97, C=7, E=64,
                      heads=4, H=128, layers=1, cells="normal", weights="xavier_bias"),
+    # head dim 64 (the current best record's width per head), post-norm, bf16 and fp32
+    "d64-bf16": dict(name="d64-bf16", dtype="bf16", B=3, R=130, n_train=97, C=7, E=128,
+                     heads=2, H=256, layers=1, cells="normal", weights="xavier_bias"),
+    "d64-f32": dict(name="d64-f32", dtype="f32", B=2, R=40, n_train=30, C=5, E=64, heads=1,
+                    H=64, layers=1, cells="normal", weights="xavier_bias"),
+    # pre-norm block at d = 64 with rows of up to 41 active cells
+    "prenorm-d64-bf16": dict(name="prenorm-d64-bf16", dtype="bf16", B=4, R=160,
+                             n_train=(1, 160), C=40, active=(0, 40), mask="random", E=128,
+                             heads=2, H=384, layers=2, cells="normal", weights="xavier_bias",
+                             block="pre"),
     # pre-norm RMSNorm block with residual decay (the current best record's block), at d = 32
     "prenorm-small-bf16": dict(name="prenorm-small-bf16", dtype="bf16", B=4, R=200,
                                n_train=(1, 200), C=20, active=(0, 20), mask="random", E=64,
@@ -95,11 +105,25 @@ TEST_CONFIGS = {
 }
 
 
+# Workloads of the widened scope (not parity configurations of the baseline block).
+#   record9-bf16: the current best record's block (Tab. 7): pre-norm RMSNorm, residual decay,
+#   E = 256 with 4 heads of 64, MLP 768, 5 blocks; 1000 data rows plus 24 thinking rows
+#   prepended as train rows (750 labelled data rows); 100 features in groups of 5 give 20 cells
+#   plus the target cell per row.
+EXTRA_CONFIGS = {
+    "record9-bf16": dict(name="record9-bf16", dtype="bf16", B=16, R=1024, n_train=774, C=20,
+                         E=256, heads=4, H=768, layers=5, cells="normal", weights="xavier",
+                         block="pre", thinking=24),
+}
+
+
 def get_config(which):
     if isinstance(which, int):
         return dict(CONFIGS[which], index=which)
     if which in TEST_CONFIGS:
         return dict(TEST_CONFIGS[which], index=None)
+    if which in EXTRA_CONFIGS:
+        return dict(EXTRA_CONFIGS[which], index=None)
     for i, c in enumerate(CONFIGS):
         if c["name"] == which:
             return dict(c, index=i)
@@ -278,11 +302,17 @@ def make_workload(which, seed=None, datasets=None, with_dY=True):
     params = [_draw_params(np.random.default_rng(kids[1 + l]), cfg["E"], cfg["H"],
                            cfg["weights"], cfg.get("block", "post")) for l in range(L)]
     ds = np.arange(B) if datasets is None else np.asarray(datasets, dtype=np.int64)
+    T = cfg.get("thinking", 0)
+    # thinking rows: one table [T, E] broadcast into rows [0, T) of every active cell column
+    table = meta_rng.normal(0.0, 1.0, (T, cfg["E"])) if T else None
     X = []
     dY = []
     for b in ds:
-        X.append(to_storage(_draw_cells(cfg, np.random.default_rng(kids[1 + L + b]),
-                                        int(n_train_all[b])), cfg["dtype"]))
+        x = _draw_cells(cfg, np.random.default_rng(kids[1 + L + b]), int(n_train_all[b]))
+        if T:
+            act = np.flatnonzero(mask_all[b])
+            x[:T][:, act, :] = table[:, None, :]
+        X.append(to_storage(x, cfg["dtype"]))
         if with_dY:
             g = np.random.default_rng(kids[1 + L + B + b]).normal(
                 0.0, 1.0, (cfg["R"], cfg["C"] + 1, cfg["E"]))

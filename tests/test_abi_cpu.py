@@ -69,7 +69,7 @@ def test_sizes_positive_and_grow_with_batch():
 @pytest.mark.parametrize("kw,code", [
     (dict(B=0), -1), (dict(R=0), -1), (dict(C=-1), -1), (dict(C=300), -1),
     (dict(E=48), -1), (dict(E=512), -1), (dict(H=100), -1), (dict(dtype=7), -1),
-    (dict(heads=3), -2), (dict(E=64, heads=1), -2), (dict(E=256, heads=2), -2),
+    (dict(heads=3), -2), (dict(E=128, heads=1), -2), (dict(E=256, heads=2), -2),
     (dict(block=2), -1), (dict(block="pre"), -1),                  # pre-norm needs bf16
     (dict(block="pre", dtype="bf16", E=96, heads=3), -1),          # ... and E in {64,...,256}
     (dict(block="pre", dtype="bf16", H=96), -1),                   # ... and H % E == 0
