@@ -27,9 +27,10 @@ def to_host(t, dtype):
 
 class Stack:
     """L layers with independent parameters over the same n_train / cell_mask.  For the pre-norm
-    block, layer l multiplies its input by decay_base ** l."""
+    block, layer l multiplies its input by decay_base ** (first_layer + l)."""
 
-    def __init__(self, dims, n_train, cell_mask, params, device="cuda", decay_base=0.95):
+    def __init__(self, dims, n_train, cell_mask, params, device="cuda", decay_base=0.95,
+                 first_layer=0):
         self.dims = dims
         self.n_train = np.ascontiguousarray(n_train, dtype=np.int32)
         self.cell_mask = np.ascontiguousarray(cell_mask, dtype=np.uint8)
@@ -43,7 +44,7 @@ class Stack:
             self.layer_dims = []
             for l in range(self.L):
                 dl = tfm.tfm_dims.from_buffer_copy(dims)
-                dl.decay = decay_base ** l
+                dl.decay = decay_base ** (first_layer + l)
                 self.layer_dims.append(dl)
         self.elt = torch.float32 if dims.dtype == tfm.TFM_F32 else torch.bfloat16
         self.shape = (dims.B, dims.R, dims.C + 1, dims.E)

@@ -52,7 +52,7 @@ def storage_of(t, dtype):
     return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
 
 
-def gpu_stack(w, X=None, dY=None, keep_acts=False, params=None, storage=False):
+def gpu_stack(w, X=None, dY=None, keep_acts=False, params=None, storage=False, first_layer=0):
     """GPU forward + backward of the whole stack (or of the given per-layer params).
 
     Returns float64 host arrays, or storage arrays (see storage_of) with storage=True."""
@@ -65,7 +65,8 @@ def gpu_stack(w, X=None, dY=None, keep_acts=False, params=None, storage=False):
         (lambda t: wl.storage_to_f64(storage_of(t, dt), dt))
     dims = tfm.make_dims(dtype=dt, block=w.block,
                          **{k: v for k, v in w.dims.items() if k != "dtype"})
-    st = Stack(dims, w.n_train, w.cell_mask, w.params if params is None else params)
+    st = Stack(dims, w.n_train, w.cell_mask, w.params if params is None else params,
+               first_layer=first_layer)
     Xd = to_device(w.X if X is None else X, dt)
     dYd = to_device(w.dY if dY is None else dY, dt)
     Y = st.forward(Xd)
@@ -105,7 +106,8 @@ def sample_rows(n, R, k_train=8, k_test=8, seed=0):
     return tr, te
 
 
-def oracle_rows(Xb, mask_b, P, heads, n, rows_train, rows_test, dYq=None):
+def oracle_rows(Xb, mask_b, P, heads, n, rows_train, rows_test, dYq=None, block="post",
+                decay=1.0):
     """Oracle on one dataset, outputs only at the sampled rows (train rows first).
 
     Xb: (R, S, E) float64 cell tensor of the dataset; returns Y at the sampled rows
@@ -115,8 +117,14 @@ def oracle_rows(Xb, mask_b, P, heads, n, rows_train, rows_test, dYq=None):
     keep = np.concatenate([np.arange(n), rows_test]).astype(np.int64)
     z = Xb[keep][:, act, :]
     q = np.concatenate([rows_train, np.arange(n, n + len(rows_test))]).astype(np.int64)
-    Y, c = oracle.dataset_forward(z, P, heads, n, query_rows=q)
+    if block == "pre":
+        Y, c = oracle.prenorm_dataset_forward(z, P, heads, n, decay, query_rows=q)
+    else:
+        Y, c = oracle.dataset_forward(z, P, heads, n, query_rows=q)
     if dYq is None:
         return Y, None, None, act, keep
-    dz, g = oracle.dataset_backward(dYq, c, P, heads)
+    if block == "pre":
+        dz, g = oracle.prenorm_dataset_backward(dYq, c, P, heads)
+    else:
+        dz, g = oracle.dataset_backward(dYq, c, P, heads)
     return Y, dz, g, act, keep

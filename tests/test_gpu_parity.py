@@ -104,10 +104,11 @@ def test_test_rows_do_not_change_train_outputs():
         assert np.array_equal(a["Y"][b, :n], c["Y"][b, :n])
 
 
-@pytest.mark.parametrize("cfg", [2, 3, 4])
+@pytest.mark.parametrize("cfg", [2, 3, 4, "record9-bf16"])
 def test_full_size_sampled_rows(cfg):
     """Full-size workload in the benchmark's launch configuration, sampled rows per layer."""
     w = wl.make_workload(cfg)
+    pre = w.block == "pre"
     dt, heads, R = w.dtype, w.cfg["heads"], w.cfg["R"]
     tol = TOL[dt]
     _say(f"[full] cfg{cfg} {w.cfg['name']}: GPU stack")
@@ -122,7 +123,8 @@ def test_full_size_sampled_rows(cfg):
             tr, te = sample_rows(n, R, seed=100 * l + b)
             rows = np.concatenate([tr, te])
             Xb = wl.storage_to_f64(inputs[l][b], dt)
-            Yq, _, _, act, keep = oracle_rows(Xb, w.cell_mask[b], Ps[l], heads, n, tr, te)
+            Yq, _, _, act, keep = oracle_rows(Xb, w.cell_mask[b], Ps[l], heads, n, tr, te,
+                                              block=w.block, decay=0.95 ** l)
             Yg = wl.storage_to_f64(run["acts"][l][b][rows][:, act], dt)
             e = nerr(Yg, Yq)
             _say(f"[full] cfg{cfg} layer {l} dataset {b} fwd err {e:.3g}")
@@ -130,9 +132,11 @@ def test_full_size_sampled_rows(cfg):
             # backward of this layer alone, upstream gradient only at the sampled rows
             dY = np.zeros_like(w.dY)
             dY[b][rows[:, None], act[None, :]] = w.dY[b][rows[:, None], act[None, :]]
-            g = gpu_stack(w, X=inputs[l], dY=dY, params=[w.params[l]], storage=True)
+            g = gpu_stack(w, X=inputs[l], dY=dY, params=[w.params[l]], storage=True,
+                          first_layer=l)
             dYq = wl.storage_to_f64(dY[b][rows][:, act], dt)
-            _, dz, gr, _, _ = oracle_rows(Xb, w.cell_mask[b], Ps[l], heads, n, tr, te, dYq)
+            _, dz, gr, _, _ = oracle_rows(Xb, w.cell_mask[b], Ps[l], heads, n, tr, te, dYq,
+                                          block=w.block, decay=0.95 ** l)
             dXg = wl.storage_to_f64(g["dX"], dt)
             e = nerr(dXg[b][keep][:, act], dz)
             _say(f"[full] cfg{cfg} layer {l} dataset {b} dX err {e:.3g}")
@@ -142,8 +146,10 @@ def test_full_size_sampled_rows(cfg):
             assert np.all(dXg[others] == 0)
             rest = np.setdiff1d(np.arange(R), keep)
             assert np.all(dXg[b][rest] == 0)
-            pg = oracle.unpack_params(g["grads"][0], w.cfg["E"], w.cfg["H"])
-            worst = max(nerr(pg[k], gr[k]) for k in oracle.PARAM_ORDER)
+            unpack = oracle.unpack_prenorm_params if pre else oracle.unpack_params
+            names = oracle.PRENORM_PARAM_ORDER if pre else oracle.PARAM_ORDER
+            pg = unpack(g["grads"][0], w.cfg["E"], w.cfg["H"])
+            worst = max(nerr(pg[k], gr[k]) for k in names)
             _say(f"[full] cfg{cfg} layer {l} dataset {b} grads worst err {worst:.3g}")
-            for k in oracle.PARAM_ORDER:
+            for k in names:
                 assert nerr(pg[k], gr[k]) <= tol, k
