@@ -116,6 +116,24 @@ int tfm_layer_bwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* c
                   void* workspace, size_t workspace_bytes, void* stream);
 
 /* Message describing the last non-zero return of this thread ("" if none). */
+/* Thinking rows (Sec. 5 "RMSNorm, Thinking Rows", App. B.6, Tab. 7): learned E-vectors
+ * prepended along the row axis, broadcast over the cell columns and counted as train rows.
+ * dims, n_train and cell_mask describe the stack input X[B][R][C+1][E] whose rows [0, T) are the
+ * thinking rows (n_train includes them, 1 <= T <= min(n_train)).
+ *
+ * tfm_thinking_rows_fwd writes table[T][E] (device, float32, rounded to dims->dtype) into rows
+ * [0, T) of every active cell column of X and 0 into rows [0, T) of inactive columns; other rows
+ * are left untouched. */
+int tfm_thinking_rows_fwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* cell_mask,
+                          int T, const float* table, void* X, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
+/* Gradient of the broadcast: dtable[T][E] (device, float32) = sum over datasets and active cell
+ * columns of dX rows [0, T), added to dtable when accumulate != 0, summed in a fixed order. */
+int tfm_thinking_rows_bwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* cell_mask,
+                          int T, const void* dX, float* dtable, int accumulate, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
 const char* tfm_last_error(void);
 
 #ifdef __cplusplus

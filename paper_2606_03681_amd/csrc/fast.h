@@ -126,6 +126,14 @@ hipError_t launch_reduce_z(int Z, int64_t count, int64_t stride, float* part, fl
 hipError_t launch_rms_in(const Geo& g, const bf16* X, float decay, const float* gamma, float eps,
                          bf16* xs, bf16* r, float* rstd, hipStream_t s);
 
+// Thinking rows: broadcast of table[T][E] into rows [0, T) of the native X (0 at inactive
+// columns), and its gradient summed over datasets and active columns in a fixed order.
+template <class TT>
+hipError_t launch_thinking_fwd(const Geo& g, int T, const float* table, TT* X, hipStream_t s);
+template <class TT>
+hipError_t launch_thinking_bwd(const Geo& g, int T, const TT* dX, float* dtable, int accumulate,
+                               hipStream_t s);
+
 // Backward of the last LayerNorm from the native upstream gradient: dz = LN3'(dY) at active
 // cells (compact), plus per-block partial column sums of dY * xhat and dY into
 // part [blocks][2][E].  Returns the number of blocks through *nblocks.

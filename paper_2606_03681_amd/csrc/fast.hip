@@ -262,6 +262,60 @@ hipError_t launch_rms_in(const Geo& g, const bf16* X, float decay, const float* 
   return hipGetLastError();
 }
 
+// Thinking rows: rows [0, T) of X get the table (float32 [T][E]) at active cell columns and 0 at
+// inactive ones; one thread per element of those rows.
+template <class TT>
+__global__ void k_thinking_fwd(Geo g, int T, const float* __restrict__ table, TT* __restrict__ X) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t per = (int64_t)T * g.S * g.E;
+  if (i >= per * g.B) return;
+  const int b = (int)(i / per);
+  const int64_t rest = i - b * per;
+  const int t = (int)(rest / ((int64_t)g.S * g.E));
+  const int c = (int)(rest / g.E % g.S);
+  const int e = (int)(rest % g.E);
+  const bool act = g.colmap[b * g.S + c] >= 0;
+  st(X + (((int64_t)b * g.R + t) * g.S + c) * g.E + e, act ? table[t * g.E + e] : 0.f);
+}
+
+// dtable[t][e] (+)= sum over datasets b and active columns c of dX[b][t][c][e], in (b, c) order.
+template <class TT>
+__global__ void k_thinking_bwd(Geo g, int T, const TT* __restrict__ dX, float* __restrict__ dtable,
+                               int accumulate) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)T * g.E) return;
+  const int t = (int)(i / g.E), e = (int)(i % g.E);
+  float s = 0.f;
+  for (int b = 0; b < g.B; ++b)
+    for (int c = 0; c < g.S; ++c)
+      if (g.colmap[b * g.S + c] >= 0) s += ld(dX + (((int64_t)b * g.R + t) * g.S + c) * g.E + e);
+  dtable[i] = (accumulate ? dtable[i] : 0.f) + s;
+}
+
+template <class TT>
+hipError_t launch_thinking_fwd(const Geo& g, int T, const float* table, TT* X, hipStream_t s) {
+  const int64_t n = (int64_t)g.B * T * g.S * g.E;
+  if (n == 0) return hipSuccess;
+  k_thinking_fwd<TT><<<(unsigned)((n + 255) / 256), 256, 0, s>>>(g, T, table, X);
+  return hipGetLastError();
+}
+
+template <class TT>
+hipError_t launch_thinking_bwd(const Geo& g, int T, const TT* dX, float* dtable, int accumulate,
+                               hipStream_t s) {
+  const int64_t n = (int64_t)T * g.E;
+  if (n == 0) return hipSuccess;
+  k_thinking_bwd<TT><<<(unsigned)((n + 255) / 256), 256, 0, s>>>(g, T, dX, dtable, accumulate);
+  return hipGetLastError();
+}
+
+template hipError_t launch_thinking_fwd<float>(const Geo&, int, const float*, float*, hipStream_t);
+template hipError_t launch_thinking_fwd<bf16>(const Geo&, int, const float*, bf16*, hipStream_t);
+template hipError_t launch_thinking_bwd<float>(const Geo&, int, const float*, float*, int,
+                                               hipStream_t);
+template hipError_t launch_thinking_bwd<bf16>(const Geo&, int, const bf16*, float*, int,
+                                              hipStream_t);
+
 size_t fast_workspace_bytes(int B, int R, int S, int E, int heads, int H, bool bf16) {
   (void)heads;
   if (!bf16) return 0;

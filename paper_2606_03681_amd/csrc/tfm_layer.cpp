@@ -923,4 +923,59 @@ int tfm_layer_bwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* c
                                s);
 }
 
+// Shared checks of the thinking-row calls (the dims, the workspace that holds the column map,
+// the plan from n_train and the mask, 1 <= T <= every n_train), then the column map upload.
+static int thinking_setup(const tfm_dims* dims, const int32_t* n_train, const uint8_t* cell_mask,
+                          int T, void* workspace, size_t workspace_bytes, Dims& d, tfm::Geo& g,
+                          hipStream_t s) {
+  int rc = check_dims(dims, d);
+  if (rc) return rc;
+  if (!aligned(workspace)) return fail(TFM_ERR_POINTER, "workspace must be 16-byte aligned");
+  const WsLayout W = ws_layout(d);
+  if (workspace_bytes < W.total)
+    return fail(TFM_ERR_BUFFER, "workspace has %zu bytes, %zu required", workspace_bytes,
+                W.total);
+  Plan P;
+  rc = make_plan(d, n_train, cell_mask, P);
+  if (rc) return rc;
+  for (int b = 0; b < d.B; ++b)
+    if (T < 1 || T > n_train[b])
+      return fail(TFM_ERR_DIMS, "T=%d thinking rows outside [1, n_train[%d]=%d]", T, b,
+                  n_train[b]);
+  return setup_geo(d, P, (char*)workspace, W, g, s);
+}
+
+int tfm_thinking_rows_fwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* cell_mask,
+                          int T, const float* table, void* X, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  Dims d;
+  tfm::Geo g;
+  hipStream_t s = (hipStream_t)stream;
+  if (!aligned(table) || !aligned(X))
+    return fail(TFM_ERR_POINTER, "table and X must be non-null and 16-byte aligned");
+  int rc = thinking_setup(dims, n_train, cell_mask, T, workspace, workspace_bytes, d, g, s);
+  if (rc) return rc;
+  if (d.dtype == TFM_F32) HIPCHK(tfm::launch_thinking_fwd<float>(g, T, table, (float*)X, s));
+  else HIPCHK(tfm::launch_thinking_fwd<tfm::bf16>(g, T, table, (tfm::bf16*)X, s));
+  return TFM_OK;
+}
+
+int tfm_thinking_rows_bwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* cell_mask,
+                          int T, const void* dX, float* dtable, int accumulate, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  Dims d;
+  tfm::Geo g;
+  hipStream_t s = (hipStream_t)stream;
+  if (!aligned(dX) || !aligned(dtable))
+    return fail(TFM_ERR_POINTER, "dX and dtable must be non-null and 16-byte aligned");
+  int rc = thinking_setup(dims, n_train, cell_mask, T, workspace, workspace_bytes, d, g, s);
+  if (rc) return rc;
+  if (d.dtype == TFM_F32)
+    HIPCHK(tfm::launch_thinking_bwd<float>(g, T, (const float*)dX, dtable, accumulate, s));
+  else
+    HIPCHK(tfm::launch_thinking_bwd<tfm::bf16>(g, T, (const tfm::bf16*)dX, dtable, accumulate,
+                                               s));
+  return TFM_OK;
+}
+
 }  // extern "C"

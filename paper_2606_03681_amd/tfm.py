@@ -20,8 +20,8 @@ ERRORS = {
     -5: "TFM_ERR_POINTER", -6: "TFM_ERR_HIP", -7: "TFM_ERR_BUFFER",
 }
 EXPORTS = ("tfm_layer_param_count", "tfm_layer_saved_bytes", "tfm_layer_workspace_bytes",
-           "tfm_layer_fwd", "tfm_layer_bwd", "tfm_last_error", "tfm_prof_enable",
-           "tfm_prof_collect", "tfm_prof_step")
+           "tfm_layer_fwd", "tfm_layer_bwd", "tfm_thinking_rows_fwd", "tfm_thinking_rows_bwd",
+           "tfm_last_error", "tfm_prof_enable", "tfm_prof_collect", "tfm_prof_step")
 
 
 class TfmError(RuntimeError):
@@ -63,6 +63,10 @@ def lib():
         L.tfm_layer_bwd.restype = i32
         L.tfm_layer_bwd.argtypes = [P(tfm_dims), vp, vp, vp, vp, vp, sz, vp, vp, vp, i32, vp,
                                     sz, vp]
+        L.tfm_thinking_rows_fwd.restype = i32
+        L.tfm_thinking_rows_fwd.argtypes = [P(tfm_dims), vp, vp, i32, vp, vp, vp, sz, vp]
+        L.tfm_thinking_rows_bwd.restype = i32
+        L.tfm_thinking_rows_bwd.argtypes = [P(tfm_dims), vp, vp, i32, vp, vp, i32, vp, sz, vp]
         L.tfm_prof_enable.restype = i32
         L.tfm_prof_enable.argtypes = [i32]
         L.tfm_prof_collect.restype = i32
@@ -137,6 +141,31 @@ def layer_bwd(dims, n_train, cell_mask, X, params, saved, dY, dX, grads, accumul
                              saved.numel() * saved.element_size(), _ptr(dY), _ptr(dX),
                              _ptr(grads), int(bool(accumulate)), _ptr(workspace),
                              workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(rc)
+
+
+def thinking_rows_fwd(dims, n_train, cell_mask, T, table, X, workspace, stream=None):
+    """tfm_thinking_rows_fwd: writes table (device float32 [T, E]) into rows [0, T) of X
+    (device [B, R, C+1, E]) at active columns, 0 at inactive ones."""
+    nt, ntp = _host(n_train, np.int32)
+    cm, cmp_ = _host(cell_mask, np.uint8)
+    rc = lib().tfm_thinking_rows_fwd(ctypes.byref(dims), ntp, cmp_, int(T), _ptr(table), _ptr(X),
+                                     _ptr(workspace),
+                                     workspace.numel() * workspace.element_size(),
+                                     _stream(stream))
+    _check(rc)
+
+
+def thinking_rows_bwd(dims, n_train, cell_mask, T, dX, dtable, accumulate, workspace,
+                      stream=None):
+    """tfm_thinking_rows_bwd: dtable (device float32 [T, E]) gets (or adds) the sum of dX rows
+    [0, T) over datasets and active columns."""
+    nt, ntp = _host(n_train, np.int32)
+    cm, cmp_ = _host(cell_mask, np.uint8)
+    rc = lib().tfm_thinking_rows_bwd(ctypes.byref(dims), ntp, cmp_, int(T), _ptr(dX),
+                                     _ptr(dtable), int(bool(accumulate)), _ptr(workspace),
+                                     workspace.numel() * workspace.element_size(),
+                                     _stream(stream))
     _check(rc)
 
 

@@ -117,3 +117,29 @@ def test_bad_metadata_and_pointers_rejected_before_launch(call):
     rc = tfm.lib().tfm_layer_fwd(ctypes.byref(d), None, None, 1 << 20, 1 << 20, 1 << 20,
                                  1 << 20, 1 << 40, 1 << 20, 1 << 40, None)
     assert rc == -5
+
+
+def _call_think(d, n_train, mask, T, ptr=1 << 20, wb=1 << 40, bwd=False):
+    nt = np.ascontiguousarray(n_train, dtype=np.int32)
+    cm = np.ascontiguousarray(mask, dtype=np.uint8)
+    if bwd:
+        return tfm.lib().tfm_thinking_rows_bwd(ctypes.byref(d), nt.ctypes.data, cm.ctypes.data,
+                                               T, ptr, ptr, 0, ptr, wb, None)
+    return tfm.lib().tfm_thinking_rows_fwd(ctypes.byref(d), nt.ctypes.data, cm.ctypes.data, T,
+                                           ptr, ptr, ptr, wb, None)
+
+
+@pytest.mark.parametrize("bwd", [False, True])
+def test_thinking_rows_arguments_rejected_before_launch(bwd):
+    d = _dims()
+    mask = np.ones((2, 9), np.uint8)
+    assert _call_think(d, [5, 5], mask, 0, bwd=bwd) == -1
+    assert _call_think(d, [5, 3], mask, 4, bwd=bwd) == -1
+    assert "thinking rows" in tfm.last_error()
+    assert _call_think(d, [0, 5], mask, 1, bwd=bwd) == -3
+    bad = mask.copy()
+    bad[0, 8] = 0
+    assert _call_think(d, [5, 5], bad, 1, bwd=bwd) == -4
+    assert _call_think(d, [5, 5], mask, 1, ptr=0, bwd=bwd) == -5
+    assert _call_think(d, [5, 5], mask, 1, ptr=(1 << 20) + 8, bwd=bwd) == -5
+    assert _call_think(d, [5, 5], mask, 1, wb=16, bwd=bwd) == -7

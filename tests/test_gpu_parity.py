@@ -153,3 +153,39 @@ def test_full_size_sampled_rows(cfg):
             _say(f"[full] cfg{cfg} layer {l} dataset {b} grads worst err {worst:.3g}")
             for k in names:
                 assert nerr(pg[k], gr[k]) <= tol, k
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_thinking_rows_against_oracle(dtype):
+    """Broadcast of the thinking-row table and its gradient, bit-exact for the broadcast (a copy
+    with one rounding to the storage type) and within the float32 summation bound for dtable."""
+    import torch
+    from paper_2606_03681_amd import tfm
+    from paper_2606_03681_amd.stack import to_device, to_host
+    rng = np.random.default_rng(41)
+    B, R, C, E, T = 3, 40, 13, 64, 5
+    n_train = np.array([7, 5, 30], np.int32)
+    mask = (rng.random((B, C + 1)) < 0.7).astype(np.uint8)
+    mask[:, C] = 1
+    dims = tfm.make_dims(B, R, C, E, 2, 128, dtype)
+    ws = torch.empty(tfm.workspace_bytes(dims), dtype=torch.uint8, device="cuda")
+    X = wl.to_storage(rng.normal(size=(B, R, C + 1, E)), dtype)
+    table = rng.normal(size=(T, E)).astype(np.float32)
+    Xd = to_device(X, dtype)
+    tfm.thinking_rows_fwd(dims, n_train, mask, T, torch.from_numpy(table).cuda(), Xd, ws)
+    got = to_host(Xd, dtype)
+    ref = oracle.thinking_rows_forward(wl.storage_to_f64(X[:, T:], dtype),
+                                       wl.storage_to_f64(wl.to_storage(table, dtype), dtype),
+                                       mask)
+    assert np.array_equal(got, ref)
+    dX = wl.to_storage(rng.normal(size=(B, R, C + 1, E)), dtype)
+    dt = torch.full((T, E), 7.0, device="cuda")
+    tfm.thinking_rows_bwd(dims, n_train, mask, T, to_device(dX, dtype), dt, False, ws)
+    _, dref = oracle.thinking_rows_backward(wl.storage_to_f64(dX, dtype), mask, T)
+    n_terms = int(mask.sum())
+    bound = n_terms * 2.0 ** -24 * np.abs(wl.storage_to_f64(dX, dtype)[:, :T]).sum(axis=(0, 2))
+    assert np.all(np.abs(dt.cpu().numpy() - dref) <= bound + 1e-30)
+    dt2 = dt.clone()
+    tfm.thinking_rows_bwd(dims, n_train, mask, T, to_device(dX, dtype), dt2, True, ws)
+    torch.cuda.synchronize()
+    assert np.allclose(dt2.cpu().numpy(), 2 * dt.cpu().numpy(), rtol=1e-6, atol=0)
