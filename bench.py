@@ -23,6 +23,7 @@ sys.path.insert(0, ROOT)
 from paper_2606_03681_amd import workloads as wl  # noqa: E402
 
 METRIC = "two-axis layer fwd+bwd cells/sec (bf16) + % MFMA peak, 1x MI355X"
+METRIC_INFER = "two-axis layer forward-only (context + query chunks) cells/sec (bf16), 1x MI355X"
 PEAK_TFLOPS = {"mfma_bf16": 2516.6, "mfma_f32": 157.3, "alu_f32": 157.3}
 HBM_PEAK_GBS = 8000.0
 
@@ -85,9 +86,10 @@ def git_rev():
         return None
 
 
-def cpu_baseline(cfg_index, seed):
+def cpu_baseline(cfg_index, seed, forward_only=False):
     """The float64 oracle, untuned, on a bounded sample of the same workload: one dataset
-    through one layer, forward and backward, at the workload's full per-dataset shape."""
+    through one layer, forward and backward (or forward only), at the workload's full
+    per-dataset shape."""
     import oracle
     try:
         from threadpoolctl import threadpool_info
@@ -101,15 +103,18 @@ def cpu_baseline(cfg_index, seed):
     if w.block == "pre":
         P = oracle.unpack_prenorm_params(w.params64()[0], E, H)
         _, cache = oracle.prenorm_layer_forward(X, P, w.n_train, w.cell_mask, heads, 1.0)
-        oracle.prenorm_layer_backward(dY, cache)
+        if not forward_only:
+            oracle.prenorm_layer_backward(dY, cache)
     else:
         P = oracle.unpack_params(w.params64()[0], E, H)
         _, cache = oracle.layer_forward(X, P, w.n_train, w.cell_mask, heads)
-        oracle.layer_backward(dY, cache)
+        if not forward_only:
+            oracle.layer_backward(dY, cache)
     dt = time.perf_counter() - t0
     cells = int(w.cfg["R"] * np.count_nonzero(w.cell_mask[0]))
+    kind = "fwd" if forward_only else "fwd+bwd"
     return {"value": cells / dt, "unit": "cells/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"dataset 0 of the workload, 1 layer fwd+bwd, {cells} active cells, "
+            "sample": f"dataset 0 of the workload, 1 layer {kind}, {cells} active cells, "
                       f"{dt:.1f} s, host {platform.processor() or platform.machine()} "
                       f"({os.cpu_count()} logical CPUs)"}
 
@@ -125,6 +130,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true",
                     help="skip the per-step event timing (roofline of the dominant kernel)")
+    ap.add_argument("--infer", action="store_true",
+                    help="time the forward-only path instead: the context rows (the longest "
+                         "train prefix) through every layer with key/value caches, then the "
+                         "remaining rows as query chunks through every layer")
+    ap.add_argument("--query-chunk", type=int, default=0,
+                    help="rows per query chunk of --infer (0: all remaining rows at once)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run 5 device-to-device copies of MIB MiB (the known-size copy "
                          "that scales the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -161,14 +172,34 @@ def main():
     dims = tfm.make_dims(dtype=w.dtype, block=w.block,
                          **{k: v for k, v in w.dims.items() if k != "dtype"})
     torch.cuda.set_device(0)
-    st = Stack(dims, w.n_train, w.cell_mask, w.params)
-    X = to_device(w.X, w.dtype)
-    dY = to_device(w.dY, w.dtype)
-    del w.X, w.dY
+    if args.infer:
+        from paper_2606_03681_amd.stack import InferStack
+        R = cfg["R"]
+        Rc = int(np.max(w.n_train))
+        chunk = args.query_chunk if args.query_chunk > 0 else max(R - Rc, 1)
+        spans = [(a, min(a + chunk, R)) for a in range(Rc, R, chunk)]
+        dctx = tfm.make_dims(dtype=w.dtype, block=w.block,
+                             **{k: (Rc if k == "R" else v) for k, v in w.dims.items()
+                                if k != "dtype"})
+        st = InferStack(dctx, w.n_train, w.cell_mask, w.params, max_query_rows=chunk)
+        Xc = to_device(np.ascontiguousarray(w.X[:, :Rc]), w.dtype)
+        Xq = [to_device(np.ascontiguousarray(w.X[:, a:b]), w.dtype) for a, b in spans]
+        X = dY = None
+        del w.X, w.dY
 
-    def step():
-        st.forward(X)
-        st.backward(dY)
+        def step():
+            st.context(Xc)
+            for x in Xq:
+                st.query(x)
+    else:
+        st = Stack(dims, w.n_train, w.cell_mask, w.params)
+        X = to_device(w.X, w.dtype)
+        dY = to_device(w.dY, w.dtype)
+        del w.X, w.dY
+
+        def step():
+            st.forward(X)
+            st.backward(dY)
 
     print(f"[bench] warmup {args.warmup}", file=sys.stderr, flush=True)
     for _ in range(args.warmup):
@@ -194,7 +225,8 @@ def main():
         tfm.prof_enable(False)
     ms_per_step = ev_ms / args.steps
     value = counts["cell_layers"] * args.steps / (ev_ms / 1e3)
-    tflops = counts["flops_fwd_bwd"] / (ms_per_step / 1e3) / 1e12
+    step_total = counts["flops_fwd_bwd"] / 3 if args.infer else counts["flops_fwd_bwd"]
+    tflops = step_total / (ms_per_step / 1e3) / 1e12
     peak = PEAK_TFLOPS["mfma_bf16"] if w.dtype == "bf16" else PEAK_TFLOPS["mfma_f32"]
 
     roof = None
@@ -211,6 +243,10 @@ def main():
             n, ms = prof[dom]
             avg_s = ms / n / 1e3
             f = fl[dom.split("/")[0]]
+            if args.infer:
+                # the context and query launches of a step differ in size: their flops sum to
+                # the whole-table figure of each layer, so use flops over time per step
+                f = f * cfg["layers"] * args.steps / n
             achieved = f / avg_s / 1e12
             mfma = dom.endswith("/mfma")
             pk = peak if mfma else PEAK_TFLOPS["alu_f32"]
@@ -221,7 +257,8 @@ def main():
                     "flops_per_launch": f, "avg_launch_ms": round(ms / n, 5)}
 
     out = {
-        "metric": METRIC, "value": round(value, 1), "unit": "cells/s", "n_gpus": 1,
+        "metric": METRIC_INFER if args.infer else METRIC, "value": round(value, 1),
+        "unit": "cells/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
         "data": "synthetic",
@@ -230,16 +267,19 @@ def main():
                    "heads": cfg["heads"], "H": cfg["H"], "layers": cfg["layers"],
                    "block": cfg.get("block", "post"), "thinking_rows": cfg.get("thinking", 0),
                    "seed": seed, "active_cell_layers": counts["cell_layers"]},
+        "mode": "forward-only" if args.infer else "forward+backward",
         "tflops": round(tflops, 3), "mfma_peak_frac": round(tflops / peak, 5),
         "wall_ms_per_step": round(wall * 1e3 / args.steps, 4),
         "roofline": roof, "steps_profile": steps_out, "git": git_rev(),
         "gpu": torch.cuda.get_device_name(0),
     }
+    if args.infer:
+        out["config"].update(context_rows=Rc, query_chunks=[b - a for a, b in spans])
     del st, X, dY
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(args.config, seed)
+        out["cpu_baseline"] = cpu_baseline(args.config, seed, forward_only=args.infer)
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)

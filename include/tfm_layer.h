@@ -84,11 +84,11 @@ enum {
   TFM_OK = 0,
   TFM_ERR_DIMS = -1,      /* dimension outside the supported envelope */
   TFM_ERR_HEAD_DIM = -2,  /* E % heads != 0 or d = E/heads not in {16, 32, 64} */
-  TFM_ERR_NTRAIN = -3,    /* some n_train[b] outside [1, R] */
+  TFM_ERR_NTRAIN = -3,    /* some n_train[b] outside [1, R] (query calls: [1, context_rows]) */
   TFM_ERR_MASK = -4,      /* target cell of some dataset inactive */
   TFM_ERR_POINTER = -5,   /* null or misaligned pointer */
   TFM_ERR_HIP = -6,       /* a HIP launch failed */
-  TFM_ERR_BUFFER = -7     /* saved or workspace buffer smaller than required */
+  TFM_ERR_BUFFER = -7     /* saved, workspace or cache buffer smaller than required */
 };
 
 /* Number of float32 parameters of one layer: 8E^2 + 8E + 2EH + H + 7E. 0 on invalid dims. */
@@ -115,11 +115,11 @@ int tfm_layer_bwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* c
                   const void* dY, void* dX, float* grads, int accumulate,
                   void* workspace, size_t workspace_bytes, void* stream);
 
-/* Message describing the last non-zero return of this thread ("" if none). */
 /* Thinking rows (Sec. 5 "RMSNorm, Thinking Rows", App. B.6, Tab. 7): learned E-vectors
  * prepended along the row axis, broadcast over the cell columns and counted as train rows.
  * dims, n_train and cell_mask describe the stack input X[B][R][C+1][E] whose rows [0, T) are the
- * thinking rows (n_train includes them, 1 <= T <= min(n_train)).
+ * thinking rows (n_train includes them, 1 <= T <= min(n_train)); workspace is a
+ * tfm_layer_workspace_bytes() scratch (it holds the column map).
  *
  * tfm_thinking_rows_fwd writes table[T][E] (device, float32, rounded to dims->dtype) into rows
  * [0, T) of every active cell column of X and 0 into rows [0, T) of inactive columns; other rows
@@ -134,6 +134,46 @@ int tfm_thinking_rows_bwd(const tfm_dims* dims, const int32_t* n_train, const ui
                           int T, const void* dX, float* dtable, int accumulate, void* workspace,
                           size_t workspace_bytes, void* stream);
 
+/* Forward-only (inference) calls: the evaluation of Sec. 3 "Evaluation" and App. "Evaluation
+ * Pipeline" runs the model forward on the train folds of a table as labelled rows and on the
+ * held-out fold as unlabelled ones, in bf16 autocast (the inference row of the ablation table of
+ * App. "SDPA, bf16, LR, Width").  No row attends to an unlabelled row, so the keys and values
+ * of the item-axis attention depend on the train rows only.  The calls exploit that:
+ *
+ *   tfm_layer_fwd_context  runs the layer forward on X[B][R][C+1][E] exactly as tfm_layer_fwd
+ *       does (same Y, bit for bit), keeps nothing for a backward pass, and writes the item-axis
+ *       keys and values of the train rows [0, n_train[b]) into kv_cache.
+ *   tfm_layer_fwd_query    runs the layer forward on further rows Xq[B][Rq][C+1][E] (dims->R =
+ *       Rq) that are all unlabelled: each attends, on the item axis, to the n_train[b] keys and
+ *       values a context call left in kv_cache.  Its Y equals the rows a tfm_layer_fwd call on
+ *       [context rows; query rows] would give them.
+ *
+ * So a stack of layers encodes the train rows once (a context call per layer, one cache per
+ * layer) and then answers any number of query chunks, each through all layers, with memory
+ * proportional to the chunk.  Both calls need TFM_BF16 and E in {64, 128, 192, 256} with H a
+ * multiple of E (either block).  The query call needs the n_train, cell_mask, params and dims
+ * (other than R) of the context call that wrote kv_cache, and context_rows = that call's R;
+ * n_train[b] must lie in [1, context_rows]. */
+
+/* Bytes of scratch of one forward-only call with dims->R rows (0 on invalid or unsupported
+ * dims). */
+size_t tfm_infer_workspace_bytes(const tfm_dims* dims);
+
+/* Bytes of the key/value cache of one layer whose context call has dims->R rows (opaque
+ * layout: keys and values of every possible active column, head-major, bfloat16). */
+size_t tfm_infer_cache_bytes(const tfm_dims* dims);
+
+int tfm_layer_fwd_context(const tfm_dims* dims, const int32_t* n_train, const uint8_t* cell_mask,
+                          const void* X, const float* params, void* Y, void* kv_cache,
+                          size_t cache_bytes, void* workspace, size_t workspace_bytes,
+                          void* stream);
+
+int tfm_layer_fwd_query(const tfm_dims* dims, int32_t context_rows, const int32_t* n_train,
+                        const uint8_t* cell_mask, const void* X, const float* params,
+                        const void* kv_cache, size_t cache_bytes, void* Y, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+/* Message describing the last non-zero return of this thread ("" if none). */
 const char* tfm_last_error(void);
 
 #ifdef __cplusplus

@@ -5,11 +5,13 @@
 
 namespace tfm {
 
-// Item-axis attention forward.  q/k/v head-major [col][head][R][d] (k, v valid for train
-// rows), o cell-major [cell][E], lse [col][head][R] (natural log of the softmax denominator
-// including the 1/sqrt(d) scale).
+// Item-axis attention forward.  q head-major [col][head][R][d], k/v head-major
+// [col][head][kR][d] valid for the first n_train rows (kR = R when kR <= 0; a larger kR lets the
+// queries of one call read keys and values kept from another call with more rows), o
+// cell-major [cell][E], lse [col][head][R] (natural log of the softmax denominator including
+// the 1/sqrt(d) scale).
 hipError_t launch_item_attn_fwd(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
-                                bf16* o, float* lse, hipStream_t s);
+                                bf16* o, float* lse, hipStream_t s, int kR = 0);
 
 // Item-axis attention backward: dq, dk, dv head-major (dk, dv for train rows only).
 // Backward in two launches, dQ first: it also writes Dbuf ([problem][R] float32) with

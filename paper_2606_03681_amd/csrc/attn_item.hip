@@ -37,7 +37,8 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
                                                        const bf16* __restrict__ k,
                                                        const bf16* __restrict__ v,
                                                        bf16* __restrict__ o,
-                                                       float* __restrict__ lse, int QT) {
+                                                       float* __restrict__ lse, int QT,
+                                                       int kR) {
   constexpr int KS = D + 8;   // LDS row stride of K (elements; conflict-free 16-byte reads)
   constexpr int VS = tr_stride<D>();  // LDS row stride of V (conflict-free transpose reads)
   constexpr int DB = D / 16;  // 16-wide dim blocks
@@ -54,8 +55,8 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
   const int n = g.ds[g.col_ds[col]].n_train;
   const int R = g.R;
   const bf16* Qp = q + prob * R * D;
-  const bf16* Kp = k + prob * R * D;
-  const bf16* Vp = v + prob * R * D;
+  const bf16* Kp = k + prob * kR * D;  // keys and values: kR rows per problem
+  const bf16* Vp = v + prob * kR * D;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int c = lane & 15, lg = lane >> 4;
@@ -219,16 +220,17 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
 }
 
 hipError_t launch_item_attn_fwd(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
-                                bf16* o, float* lse, hipStream_t s) {
+                                bf16* o, float* lse, hipStream_t s, int kR) {
+  if (kR <= 0) kR = g.R;
   const int QT = (g.R + QWG - 1) / QWG;
   const int64_t P = (int64_t)g.NC * g.heads;
   const int64_t grid = (P + 7) / 8 * 8 * QT;
   if (g.d == 16)
-    k_item_attn_fwd<16><<<(unsigned)grid, 256, 0, s>>>(g, q, k, v, o, lse, QT);
+    k_item_attn_fwd<16><<<(unsigned)grid, 256, 0, s>>>(g, q, k, v, o, lse, QT, kR);
   else if (g.d == 32)
-    k_item_attn_fwd<32><<<(unsigned)grid, 256, 0, s>>>(g, q, k, v, o, lse, QT);
+    k_item_attn_fwd<32><<<(unsigned)grid, 256, 0, s>>>(g, q, k, v, o, lse, QT, kR);
   else if (g.d == 64)
-    k_item_attn_fwd<64><<<(unsigned)grid, 256, 0, s>>>(g, q, k, v, o, lse, QT);
+    k_item_attn_fwd<64><<<(unsigned)grid, 256, 0, s>>>(g, q, k, v, o, lse, QT, kR);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -359,7 +359,8 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
       store_tile(dst, 0, true);
       return;
     }
-    store_tile(a.out, n0, false);
+    // the GELU epilogue may skip the pre-activation store (out == nullptr: forward-only calls)
+    if (EPI != EPI_GELU_FWD || a.out) store_tile(a.out, n0, false);
     if (EPI == EPI_GELU_FWD) {
       // U = GELU of the stored (bf16) pre-activation, computed in place of the accumulators
 #pragma unroll
@@ -463,9 +464,9 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
       const float rs = 1.0f / sqrtf(var[i] + 1e-5f);
 #pragma unroll
       for (int j = 0; j < NB; ++j) val[i][j] = (val[i][j] - mean[i]) * rs;
-      if (wn == 0 && lg == 0 && m0 + rloc(i) < a.M) a.rstd[m0 + rloc(i)] = rs;
+      if (a.rstd && wn == 0 && lg == 0 && m0 + rloc(i) < a.M) a.rstd[m0 + rloc(i)] = rs;
     }
-    // h = gamma * x-hat + beta -> out (omode); x-hat -> xhat (compact)
+    // h = gamma * x-hat + beta -> out (omode); x-hat -> xhat (compact) unless xhat is null
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
       const f32x4 gm = par4(1, j), bt = par4(2, j);
@@ -475,6 +476,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
     set_rows(a.omode, BN, -1);
     lds_barrier();
     store_tile(a.out, 0, false);
+    if (!a.xhat) return;
     lds_barrier();
 #pragma unroll
     for (int i = 0; i < MI; ++i)
@@ -565,7 +567,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
 #pragma unroll
     for (int i = 0; i < MI; ++i) {
       const float rs = 1.0f / sqrtf(ms[i] + a.eps);
-      if (wn == 0 && lg == 0 && m0 + rloc(i) < a.M) a.rstd[m0 + rloc(i)] = rs;
+      if (a.rstd && wn == 0 && lg == 0 && m0 + rloc(i) < a.M) a.rstd[m0 + rloc(i)] = rs;
 #pragma unroll
       for (int j = 0; j < NB; ++j) put4(i, j, par4(1, j) * val[i][j] * rs);
     }

@@ -119,6 +119,21 @@ struct Arena {
   size_t take(size_t bytes) { size_t r = off; off = align_up(off + bytes); return r; }
 };
 
+// Offsets of the device copy of the plan inside a workspace.
+struct MetaOff {
+  size_t blob, ds, col_ds, col_c, colmap;
+};
+
+MetaOff take_meta(const Dims& d, Arena& a) {
+  MetaOff L;
+  L.blob = a.take((size_t)d.B * (3 + d.words) * 4);
+  L.ds = a.take((size_t)d.B * sizeof(tfm::DsInfo));
+  L.col_ds = a.take((size_t)d.B * d.S * 4);
+  L.col_c = a.take((size_t)d.B * d.S * 4);
+  L.colmap = a.take((size_t)d.B * d.S * 4);
+  return L;
+}
+
 struct SavedLayout {
   size_t qkvf, of, lsef, h1, xh1, rs1, qi, ki, vi, oi, lsei, h2, xh2, rs2, g, u, xh3, rs3;
   size_t total;
@@ -190,7 +205,7 @@ size_t saved_total(const Dims& d) {
 }
 
 struct WsLayout {
-  size_t blob, ds, col_ds, col_c, colmap;
+  MetaOff meta;
   size_t xc, ta, tb, tc, td, te, tf, th1, th2, tq, tk, tv, tqkv, D, part, cpart, cpart2;
   size_t fast;  // region owned by the MFMA path
   size_t total;
@@ -201,11 +216,7 @@ WsLayout ws_layout(const Dims& d) {
   WsLayout L;
   Arena a;
   const size_t N = (size_t)d.Nmax, t = d.tsz, E = d.E;
-  L.blob = a.take((size_t)d.B * (3 + d.words) * 4);
-  L.ds = a.take((size_t)d.B * sizeof(tfm::DsInfo));
-  L.col_ds = a.take((size_t)d.B * d.S * 4);
-  L.col_c = a.take((size_t)d.B * d.S * 4);
-  L.colmap = a.take((size_t)d.B * d.S * 4);
+  L.meta = take_meta(d, a);
   L.xc = a.take(N * E * t);
   L.ta = a.take(N * E * t);
   L.tb = a.take(N * E * t);
@@ -241,13 +252,16 @@ struct Plan {
   std::vector<int32_t> blob;
 };
 
-int make_plan(const Dims& d, const int32_t* n_train, const uint8_t* mask, Plan& P) {
+// nt_max: the largest allowed n_train (R, or the context rows of a query call).
+int make_plan(const Dims& d, const int32_t* n_train, const uint8_t* mask, Plan& P,
+              int nt_max = -1) {
+  if (nt_max < 0) nt_max = d.R;
   if (!n_train || !mask) return fail(TFM_ERR_POINTER, "n_train or cell_mask is null");
   P.blob.assign((size_t)d.B * (3 + d.words), 0);
   int col = 0;
   for (int b = 0; b < d.B; ++b) {
-    if (n_train[b] < 1 || n_train[b] > d.R)
-      return fail(TFM_ERR_NTRAIN, "n_train[%d]=%d outside [1, R=%d]", b, n_train[b], d.R);
+    if (n_train[b] < 1 || n_train[b] > nt_max)
+      return fail(TFM_ERR_NTRAIN, "n_train[%d]=%d outside [1, %d]", b, n_train[b], nt_max);
     const uint8_t* m = mask + (size_t)b * d.S;
     if (!m[d.C]) return fail(TFM_ERR_MASK, "target cell (index C=%d) of dataset %d inactive",
                              d.C, b);
@@ -281,7 +295,7 @@ int make_plan(const Dims& d, const int32_t* n_train, const uint8_t* mask, Plan& 
     tfm::prof_end(s);                \
   } while (0)
 
-int setup_geo(const Dims& d, const Plan& P, char* ws, const WsLayout& W, tfm::Geo& g,
+int setup_geo(const Dims& d, const Plan& P, char* ws, const MetaOff& W, tfm::Geo& g,
               hipStream_t s) {
   int32_t* blob = (int32_t*)(ws + W.blob);
   g.B = d.B; g.R = d.R; g.S = d.S; g.E = d.E; g.heads = d.heads; g.d = d.d; g.H = d.H;
@@ -499,61 +513,77 @@ tfm::GemmArgs gemm_base(const tfm::Geo& g, int64_t M, int N, int K, int epi) {
   return a;
 }
 
-int fwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* prm,
-             tfm::bf16* Y, char* sv, const SavedLayout& S, char* ws, const WsLayout& W,
-             hipStream_t s) {
-  using namespace tfm;
+// Buffers of one forward pass on the MFMA path.  The training forward points them into the
+// saved state; the forward-only calls point them into the workspace (reused where lifetimes
+// allow; the optional ones null) and into the caller's key/value cache.
+struct FwdBufs {
+  tfm::bf16 *qkvf = nullptr, *of = nullptr, *h1 = nullptr, *qi = nullptr, *ki = nullptr,
+            *vi = nullptr, *oi = nullptr, *h2 = nullptr, *u = nullptr;
+  tfm::bf16 *xh1 = nullptr, *xh2 = nullptr, *xh3 = nullptr, *g = nullptr;  // optional
+  tfm::bf16 *xs = nullptr, *r1 = nullptr, *r2 = nullptr, *r3 = nullptr;    // pre-norm block
+  float *lsef = nullptr, *lsei = nullptr, *rs1 = nullptr, *rs2 = nullptr, *rs3 = nullptr;
+  bool query = false;  // ki / vi hold the keys and values of a context call: project Q only
+  int kR = 0;          // rows per (column, head) of ki / vi; 0: R
+};
+
+FwdBufs bufs_from_saved(char* sv, const SavedLayout& S) {
   typedef tfm::bf16 T;
+  FwdBufs b;
+  b.qkvf = (T*)(sv + S.qkvf); b.of = (T*)(sv + S.of); b.lsef = (float*)(sv + S.lsef);
+  b.h1 = (T*)(sv + S.h1); b.xh1 = (T*)(sv + S.xh1); b.rs1 = (float*)(sv + S.rs1);
+  b.qi = (T*)(sv + S.qi); b.ki = (T*)(sv + S.ki); b.vi = (T*)(sv + S.vi);
+  b.oi = (T*)(sv + S.oi); b.lsei = (float*)(sv + S.lsei);
+  b.h2 = (T*)(sv + S.h2); b.xh2 = (T*)(sv + S.xh2); b.rs2 = (float*)(sv + S.rs2);
+  b.g = (T*)(sv + S.g); b.u = (T*)(sv + S.u); b.xh3 = (T*)(sv + S.xh3);
+  b.rs3 = (float*)(sv + S.rs3);
+  return b;
+}
+
+int fwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* prm,
+             tfm::bf16* Y, const FwdBufs& b, const FastWs& f, hipStream_t s) {
+  using namespace tfm;
   const POff o = param_offsets(d.E, d.H);
-  const FastWs f = fast_ws(d, ws, W);
   const int E = d.E, H = d.H;
   const int64_t N = g.N;
   STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, s));
-  T* qkvf = (T*)(sv + S.qkvf);
-  T* of = (T*)(sv + S.of);
-  T* h1 = (T*)(sv + S.h1);
-  T* h2 = (T*)(sv + S.h2);
-  T* oi = (T*)(sv + S.oi);
   // feature Q|K|V from the native cells
   GemmArgs a = gemm_base(g, N, 3 * E, E, EPI_BIAS);
   a.A = X; a.amode = ROWS_NATIVE; a.lda = E;
-  a.Bt = f.w + f.wo.qkv_f; a.bias = prm + o.bqkv_f; a.out = qkvf; a.ldo = 3 * E;
+  a.Bt = f.w + f.wo.qkv_f; a.bias = prm + o.bqkv_f; a.out = b.qkvf; a.ldo = 3 * E;
   STEP("feat_qkv/mfma", launch_gemm(a, s));
   if (feat_attn_mfma_ok(g))
-    STEP("feat_attn_fwd/mfma", launch_feat_attn_fwd(g, qkvf, of, (float*)(sv + S.lsef), s));
+    STEP("feat_attn_fwd/mfma", launch_feat_attn_fwd(g, b.qkvf, b.of, b.lsef, s));
   else
-    STEP("feat_attn_fwd/valu",
-         launch_feat_attn_fwd_simple<T>(g, qkvf, of, (float*)(sv + S.lsef), s));
+    STEP("feat_attn_fwd/valu", launch_feat_attn_fwd_simple<bf16>(g, b.qkvf, b.of, b.lsef, s));
   // H1 = LN1(X + O_f Wo_f^T + bo_f)
   a = gemm_base(g, N, E, E, EPI_LN);
-  a.A = of; a.lda = E; a.Bt = f.w + f.wo.o_f; a.bias = prm + o.bo_f;
+  a.A = b.of; a.lda = E; a.Bt = f.w + f.wo.o_f; a.bias = prm + o.bo_f;
   a.resid = X; a.rmode = ROWS_NATIVE; a.gamma = prm + o.g1; a.beta = prm + o.be1;
-  a.out = h1; a.omode = ROWS_COMPACT; a.xhat = (T*)(sv + S.xh1); a.rstd = (float*)(sv + S.rs1);
+  a.out = b.h1; a.omode = ROWS_COMPACT; a.xhat = b.xh1; a.rstd = b.rs1;
   STEP("feat_out_ln1/mfma", launch_gemm(a, s));
-  // item Q (all rows), K, V (train rows), head-major
-  a = gemm_base(g, N, 3 * E, E, EPI_ITEM_QKV);
-  a.A = h1; a.lda = E; a.Bt = f.w + f.wo.qkv_i; a.bias = prm + o.bqkv_i;
-  a.out = (T*)(sv + S.qi); a.out2 = (T*)(sv + S.ki); a.out3 = (T*)(sv + S.vi);
+  // item Q (all rows), K, V (train rows), head-major; Q only when K/V come from a context call
+  a = gemm_base(g, N, b.query ? E : 3 * E, E, EPI_ITEM_QKV);
+  a.A = b.h1; a.lda = E; a.Bt = f.w + f.wo.qkv_i; a.bias = prm + o.bqkv_i;
+  a.out = b.qi; a.out2 = b.ki; a.out3 = b.vi;
   STEP("item_qkv/mfma", launch_gemm(a, s));
-  STEP("item_attn_fwd/mfma", launch_item_attn_fwd(g, (T*)(sv + S.qi), (T*)(sv + S.ki),
-                                                   (T*)(sv + S.vi), oi, (float*)(sv + S.lsei),
-                                                   s));
+  STEP("item_attn_fwd/mfma",
+       launch_item_attn_fwd(g, b.qi, b.ki, b.vi, b.oi, b.lsei, s, b.kR));
   // H2 = LN2(H1 + O_i Wo_i^T + bo_i)
   a = gemm_base(g, N, E, E, EPI_LN);
-  a.A = oi; a.lda = E; a.Bt = f.w + f.wo.o_i; a.bias = prm + o.bo_i;
-  a.resid = h1; a.rmode = ROWS_COMPACT; a.gamma = prm + o.g2; a.beta = prm + o.be2;
-  a.out = h2; a.omode = ROWS_COMPACT; a.xhat = (T*)(sv + S.xh2); a.rstd = (float*)(sv + S.rs2);
+  a.A = b.oi; a.lda = E; a.Bt = f.w + f.wo.o_i; a.bias = prm + o.bo_i;
+  a.resid = b.h1; a.rmode = ROWS_COMPACT; a.gamma = prm + o.g2; a.beta = prm + o.be2;
+  a.out = b.h2; a.omode = ROWS_COMPACT; a.xhat = b.xh2; a.rstd = b.rs2;
   STEP("item_out_ln2/mfma", launch_gemm(a, s));
   // G = H2 W1^T + b1, U = GELU(G)
   a = gemm_base(g, N, H, E, EPI_GELU_FWD);
-  a.A = h2; a.lda = E; a.Bt = f.w + f.wo.w1; a.bias = prm + o.b1;
-  a.out = (T*)(sv + S.g); a.out2 = (T*)(sv + S.u); a.ldo = H;
+  a.A = b.h2; a.lda = E; a.Bt = f.w + f.wo.w1; a.bias = prm + o.b1;
+  a.out = b.g; a.out2 = b.u; a.ldo = H;
   STEP("mlp_up/mfma", launch_gemm(a, s));
   // Y = LN3(H2 + U W2^T + b2), written to the native layout
   a = gemm_base(g, N, E, H, EPI_LN);
-  a.A = (T*)(sv + S.u); a.lda = H; a.Bt = f.w + f.wo.w2; a.bias = prm + o.b2;
-  a.resid = h2; a.rmode = ROWS_COMPACT; a.gamma = prm + o.g3; a.beta = prm + o.be3;
-  a.out = Y; a.omode = ROWS_NATIVE; a.xhat = (T*)(sv + S.xh3); a.rstd = (float*)(sv + S.rs3);
+  a.A = b.u; a.lda = H; a.Bt = f.w + f.wo.w2; a.bias = prm + o.b2;
+  a.resid = b.h2; a.rmode = ROWS_COMPACT; a.gamma = prm + o.g3; a.beta = prm + o.be3;
+  a.out = Y; a.omode = ROWS_NATIVE; a.xhat = b.xh3; a.rstd = b.rs3;
   STEP("mlp_down_ln3/mfma", launch_gemm(a, s));
   STEP("zero_inactive/hbm", launch_zero_inactive(g, Y, s));
   return TFM_OK;
@@ -671,65 +701,64 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
 // ---- pre-norm RMSNorm block (bfloat16, MFMA path) --------------------------------------------
 constexpr float kRmsEps = 1e-6f;
 
-int fwd_pre(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* prm,
-            tfm::bf16* Y, char* sv, const PreSaved& S, char* ws, const WsLayout& W,
-            hipStream_t s) {
-  using namespace tfm;
+FwdBufs bufs_from_pre_saved(char* sv, const PreSaved& S) {
   typedef tfm::bf16 T;
+  FwdBufs b;
+  b.xs = (T*)(sv + S.xs); b.r1 = (T*)(sv + S.r1); b.rs1 = (float*)(sv + S.rs1);
+  b.qkvf = (T*)(sv + S.qkvf); b.of = (T*)(sv + S.of); b.lsef = (float*)(sv + S.lsef);
+  b.h1 = (T*)(sv + S.h1); b.r2 = (T*)(sv + S.r2); b.rs2 = (float*)(sv + S.rs2);
+  b.qi = (T*)(sv + S.qi); b.ki = (T*)(sv + S.ki); b.vi = (T*)(sv + S.vi);
+  b.oi = (T*)(sv + S.oi); b.lsei = (float*)(sv + S.lsei);
+  b.h2 = (T*)(sv + S.h2); b.r3 = (T*)(sv + S.r3); b.rs3 = (float*)(sv + S.rs3);
+  b.g = (T*)(sv + S.g); b.u = (T*)(sv + S.u);
+  return b;
+}
+
+int fwd_pre(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* prm,
+            tfm::bf16* Y, const FwdBufs& b, const FastWs& f, hipStream_t s) {
+  using namespace tfm;
   const POff o = param_offsets(d.E, d.H, d.block);
-  const FastWs f = fast_ws(d, ws, W);
   const int E = d.E, H = d.H;
   const int64_t N = g.N;
   STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, s));
-  T* xs = (T*)(sv + S.xs);
-  T* r1 = (T*)(sv + S.r1);
-  T* qkvf = (T*)(sv + S.qkvf);
-  T* of = (T*)(sv + S.of);
-  T* h1 = (T*)(sv + S.h1);
-  T* r2 = (T*)(sv + S.r2);
-  T* oi = (T*)(sv + S.oi);
-  T* h2 = (T*)(sv + S.h2);
-  T* r3 = (T*)(sv + S.r3);
   // x' = decay X, r1 = RMS1(x')
-  STEP("rms_in/hbm", launch_rms_in(g, X, d.decay, prm + o.g1, kRmsEps, xs, r1,
-                                   (float*)(sv + S.rs1), s));
+  STEP("rms_in/hbm", launch_rms_in(g, X, d.decay, prm + o.g1, kRmsEps, b.xs, b.r1, b.rs1, s));
   GemmArgs a = gemm_base(g, N, 3 * E, E, EPI_BIAS);
-  a.A = r1; a.lda = E; a.Bt = f.w + f.wo.qkv_f; a.bias = prm + o.bqkv_f; a.out = qkvf;
+  a.A = b.r1; a.lda = E; a.Bt = f.w + f.wo.qkv_f; a.bias = prm + o.bqkv_f; a.out = b.qkvf;
   a.ldo = 3 * E;
   STEP("feat_qkv/mfma", launch_gemm(a, s));
   if (feat_attn_mfma_ok(g))
-    STEP("feat_attn_fwd/mfma", launch_feat_attn_fwd(g, qkvf, of, (float*)(sv + S.lsef), s));
+    STEP("feat_attn_fwd/mfma", launch_feat_attn_fwd(g, b.qkvf, b.of, b.lsef, s));
   else
-    STEP("feat_attn_fwd/valu",
-         launch_feat_attn_fwd_simple<T>(g, qkvf, of, (float*)(sv + S.lsef), s));
+    STEP("feat_attn_fwd/valu", launch_feat_attn_fwd_simple<bf16>(g, b.qkvf, b.of, b.lsef, s));
   // h1 = x' + O_f Wo_f^T + bo_f, r2 = RMS2(h1)
   a = gemm_base(g, N, E, E, EPI_RMS);
-  a.A = of; a.lda = E; a.Bt = f.w + f.wo.o_f; a.bias = prm + o.bo_f;
-  a.resid = xs; a.rmode = ROWS_COMPACT; a.rscale = 1.0f; a.gamma = prm + o.g2; a.eps = kRmsEps;
-  a.out = h1; a.out2 = r2; a.rstd = (float*)(sv + S.rs2);
+  a.A = b.of; a.lda = E; a.Bt = f.w + f.wo.o_f; a.bias = prm + o.bo_f;
+  a.resid = b.xs; a.rmode = ROWS_COMPACT; a.rscale = 1.0f; a.gamma = prm + o.g2;
+  a.eps = kRmsEps; a.out = b.h1; a.out2 = b.r2; a.rstd = b.rs2;
   STEP("feat_out_rms2/mfma", launch_gemm(a, s));
-  // item Q (all rows), K and V (train rows), head-major
-  a = gemm_base(g, N, 3 * E, E, EPI_ITEM_QKV);
-  a.A = r2; a.lda = E; a.Bt = f.w + f.wo.qkv_i; a.bias = prm + o.bqkv_i;
-  a.out = (T*)(sv + S.qi); a.out2 = (T*)(sv + S.ki); a.out3 = (T*)(sv + S.vi);
+  // item Q (all rows), K and V (train rows), head-major; Q only when K/V come from a context
+  // call
+  a = gemm_base(g, N, b.query ? E : 3 * E, E, EPI_ITEM_QKV);
+  a.A = b.r2; a.lda = E; a.Bt = f.w + f.wo.qkv_i; a.bias = prm + o.bqkv_i;
+  a.out = b.qi; a.out2 = b.ki; a.out3 = b.vi;
   STEP("item_qkv/mfma", launch_gemm(a, s));
-  STEP("item_attn_fwd/mfma", launch_item_attn_fwd(g, (T*)(sv + S.qi), (T*)(sv + S.ki),
-                                                  (T*)(sv + S.vi), oi, (float*)(sv + S.lsei),
-                                                  s));
+  STEP("item_attn_fwd/mfma",
+       launch_item_attn_fwd(g, b.qi, b.ki, b.vi, b.oi, b.lsei, s, b.kR));
   // h2 = h1 + O_i Wo_i^T + bo_i, r3 = RMS3(h2)
   a = gemm_base(g, N, E, E, EPI_RMS);
-  a.A = oi; a.lda = E; a.Bt = f.w + f.wo.o_i; a.bias = prm + o.bo_i;
-  a.resid = h1; a.rmode = ROWS_COMPACT; a.rscale = 1.0f; a.gamma = prm + o.g3; a.eps = kRmsEps;
-  a.out = h2; a.out2 = r3; a.rstd = (float*)(sv + S.rs3);
+  a.A = b.oi; a.lda = E; a.Bt = f.w + f.wo.o_i; a.bias = prm + o.bo_i;
+  a.resid = b.h1; a.rmode = ROWS_COMPACT; a.rscale = 1.0f; a.gamma = prm + o.g3;
+  a.eps = kRmsEps; a.out = b.h2; a.out2 = b.r3; a.rstd = b.rs3;
   STEP("item_out_rms3/mfma", launch_gemm(a, s));
   // G = r3 W1^T + b1, U = GELU(G)
   a = gemm_base(g, N, H, E, EPI_GELU_FWD);
-  a.A = r3; a.lda = E; a.Bt = f.w + f.wo.w1; a.bias = prm + o.b1;
-  a.out = (T*)(sv + S.g); a.out2 = (T*)(sv + S.u); a.ldo = H;
+  a.A = b.r3; a.lda = E; a.Bt = f.w + f.wo.w1; a.bias = prm + o.b1;
+  a.out = b.g; a.out2 = b.u; a.ldo = H;
   STEP("mlp_up/mfma", launch_gemm(a, s));
   // Y = h2 + U W2^T + b2, native
   a = gemm_base(g, N, E, H, EPI_DX);
-  a.A = (T*)(sv + S.u); a.lda = H; a.Bt = f.w + f.wo.w2; a.bias = prm + o.b2; a.resid = h2;
+  a.A = b.u; a.lda = H; a.Bt = f.w + f.wo.w2; a.bias = prm + o.b2; a.resid = b.h2;
   a.out = Y;
   STEP("mlp_down_res/mfma", launch_gemm(a, s));
   STEP("zero_inactive/hbm", launch_zero_inactive(g, Y, s));
@@ -820,6 +849,132 @@ int bwd_pre(const Dims& d, const tfm::Geo& g, const float* prm, const char* sv,
   return TFM_OK;
 }
 
+// ---- forward-only calls ----------------------------------------------------------------------
+// Workspace of a forward-only call: the plan, the bf16 weights, and the activations of one
+// pass with lifetimes overlapped (p1: feature Q|K|V, then GELU output; p2: feature attention
+// output, then item attention output; p3: h1; p4: item Q, then h2 (post-norm); pre-norm adds
+// p5: x', then h2, and p6: r1, then r2, then r3), one rstd and one log-sum-exp scratch.
+struct InferLayout {
+  MetaOff meta;
+  size_t w, wt, p1, p2, p3, p4, p5, p6, rs, lse, total;
+};
+
+bool infer_eligible(const Dims& d) {
+  return d.dtype == TFM_BF16 && (d.E == 64 || d.E == 128 || d.E == 192 || d.E == 256) &&
+         d.H % d.E == 0;
+}
+
+InferLayout infer_layout(const Dims& d) {
+  InferLayout L;
+  Arena a;
+  const size_t N = (size_t)d.Nmax, E = d.E;
+  const tfm::WOff wo = tfm::weight_offsets(d.E, d.H);
+  L.meta = take_meta(d, a);
+  L.w = a.take((size_t)wo.total * 2);
+  L.wt = a.take((size_t)wo.total * 2);
+  L.p1 = a.take(N * (3 * E > (size_t)d.H ? 3 * E : (size_t)d.H) * 2);
+  L.p2 = a.take(N * E * 2);
+  L.p3 = a.take(N * E * 2);
+  L.p4 = a.take(N * E * 2);
+  const bool pre = d.block == TFM_BLOCK_PRENORM;
+  L.p5 = pre ? a.take(N * E * 2) : 0;
+  L.p6 = pre ? a.take(N * E * 2) : 0;
+  L.rs = a.take(N * 4);
+  L.lse = a.take(N * d.heads * 4);
+  L.total = a.off;
+  return L;
+}
+
+// Key/value cache of one layer: K then V, head-major [column][head][R][d] over every possible
+// active column (B * (C + 1)), R = the context rows.
+size_t cache_half(const Dims& d) { return align_up((size_t)d.B * d.S * d.R * d.E * 2); }
+
+FwdBufs infer_bufs(const Dims& d, char* ws, const InferLayout& L, tfm::bf16* kc, tfm::bf16* vc,
+                   bool query, int kR) {
+  typedef tfm::bf16 T;
+  FwdBufs b;
+  T* p1 = (T*)(ws + L.p1);
+  T* p2 = (T*)(ws + L.p2);
+  T* p3 = (T*)(ws + L.p3);
+  T* p4 = (T*)(ws + L.p4);
+  float* rs = (float*)(ws + L.rs);
+  float* lse = (float*)(ws + L.lse);
+  b.qkvf = p1; b.u = p1;
+  b.of = p2; b.oi = p2;
+  b.h1 = p3;
+  b.qi = p4;
+  b.ki = kc; b.vi = vc;
+  b.lsef = lse; b.lsei = lse;
+  b.rs1 = b.rs2 = b.rs3 = rs;
+  if (d.block == TFM_BLOCK_PRENORM) {
+    T* p5 = (T*)(ws + L.p5);
+    T* p6 = (T*)(ws + L.p6);
+    b.xs = p5; b.h2 = p5;
+    b.r1 = b.r2 = b.r3 = p6;
+  } else {
+    b.h2 = p4;
+  }
+  b.query = query;
+  b.kR = kR;
+  return b;
+}
+
+FastWs infer_fast_ws(const Dims& d, char* ws, const InferLayout& L) {
+  FastWs f{};
+  f.wo = tfm::weight_offsets(d.E, d.H);
+  f.w = (tfm::bf16*)(ws + L.w);
+  f.wt = (tfm::bf16*)(ws + L.wt);
+  return f;
+}
+
+// Shared part of the two forward-only calls.  ctx_rows < 0: a context call (dims->R rows, the
+// cache written); otherwise a query call whose cache came from a context call with ctx_rows
+// rows.
+int infer_call(const tfm_dims* dims, int ctx_rows, const int32_t* n_train,
+               const uint8_t* cell_mask, const void* X, const float* params, void* Y,
+               void* cache, size_t cache_bytes, void* workspace, size_t workspace_bytes,
+               hipStream_t s) {
+  Dims d;
+  int rc = check_dims(dims, d);
+  if (rc) return rc;
+  if (!infer_eligible(d))
+    return fail(TFM_ERR_DIMS, "forward-only calls need TFM_BF16, E in {64, 128, 192, 256} and H "
+                              "a multiple of E");
+  const bool query = ctx_rows >= 0;
+  Dims dc = d;  // the dims the cache was laid out for
+  if (query) {
+    if (ctx_rows < 1) return fail(TFM_ERR_DIMS, "context_rows=%d must be >= 1", ctx_rows);
+    tfm_dims pc = *dims;
+    pc.R = ctx_rows;
+    rc = check_dims(&pc, dc);
+    if (rc) return rc;
+  }
+  if (!aligned(X) || !aligned(params) || !aligned(Y) || !aligned(cache) || !aligned(workspace))
+    return fail(TFM_ERR_POINTER, "X, params, Y, kv_cache and workspace must be non-null and "
+                                 "16-byte aligned");
+  const InferLayout L = infer_layout(d);
+  if (workspace_bytes < L.total)
+    return fail(TFM_ERR_BUFFER, "workspace has %zu bytes, %zu required", workspace_bytes,
+                L.total);
+  if (cache_bytes < 2 * cache_half(dc))
+    return fail(TFM_ERR_BUFFER, "kv_cache has %zu bytes, %zu required", cache_bytes,
+                2 * cache_half(dc));
+  Plan P;
+  rc = make_plan(d, n_train, cell_mask, P, query ? ctx_rows : d.R);
+  if (rc) return rc;
+  char* ws = (char*)workspace;
+  tfm::Geo g;
+  rc = setup_geo(d, P, ws, L.meta, g, s);
+  if (rc) return rc;
+  tfm::bf16* kc = (tfm::bf16*)cache;
+  tfm::bf16* vc = (tfm::bf16*)((char*)cache + cache_half(dc));
+  const FwdBufs b = infer_bufs(d, ws, L, kc, vc, query, query ? ctx_rows : d.R);
+  const FastWs f = infer_fast_ws(d, ws, L);
+  if (d.block == TFM_BLOCK_PRENORM)
+    return fwd_pre(d, g, (const tfm::bf16*)X, params, (tfm::bf16*)Y, b, f, s);
+  return fwd_fast(d, g, (const tfm::bf16*)X, params, (tfm::bf16*)Y, b, f, s);
+}
+
 }  // namespace
 
 // ============================================================================ C ABI
@@ -869,15 +1024,16 @@ int tfm_layer_fwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* c
   char* ws = (char*)workspace;
   char* sv = (char*)saved;
   tfm::Geo g;
-  rc = setup_geo(d, P, ws, W, g, s);
+  rc = setup_geo(d, P, ws, W.meta, g, s);
   if (rc) return rc;
   if (d.block == TFM_BLOCK_PRENORM)
-    return fwd_pre(d, g, (const tfm::bf16*)X, params, (tfm::bf16*)Y, sv, pre_saved_layout(d), ws,
-                   W, s);
+    return fwd_pre(d, g, (const tfm::bf16*)X, params, (tfm::bf16*)Y,
+                   bufs_from_pre_saved(sv, pre_saved_layout(d)), fast_ws(d, ws, W), s);
   if (d.dtype == TFM_F32)
     return fwd_simple<float>(d, g, (const float*)X, params, (float*)Y, sv, S, ws, W, s);
   if (fast_eligible(d))
-    return fwd_fast(d, g, (const tfm::bf16*)X, params, (tfm::bf16*)Y, sv, S, ws, W, s);
+    return fwd_fast(d, g, (const tfm::bf16*)X, params, (tfm::bf16*)Y, bufs_from_saved(sv, S),
+                    fast_ws(d, ws, W), s);
   return fwd_simple<tfm::bf16>(d, g, (const tfm::bf16*)X, params, (tfm::bf16*)Y, sv, S, ws, W,
                                s);
 }
@@ -907,7 +1063,7 @@ int tfm_layer_bwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* c
   hipStream_t s = (hipStream_t)stream;
   char* ws = (char*)workspace;
   tfm::Geo g;
-  rc = setup_geo(d, P, ws, W, g, s);
+  rc = setup_geo(d, P, ws, W.meta, g, s);
   if (rc) return rc;
   if (d.block == TFM_BLOCK_PRENORM)
     return bwd_pre(d, g, params, (const char*)saved, pre_saved_layout(d), (const tfm::bf16*)dY,
@@ -942,7 +1098,7 @@ static int thinking_setup(const tfm_dims* dims, const int32_t* n_train, const ui
     if (T < 1 || T > n_train[b])
       return fail(TFM_ERR_DIMS, "T=%d thinking rows outside [1, n_train[%d]=%d]", T, b,
                   n_train[b]);
-  return setup_geo(d, P, (char*)workspace, W, g, s);
+  return setup_geo(d, P, (char*)workspace, W.meta, g, s);
 }
 
 int tfm_thinking_rows_fwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* cell_mask,
@@ -976,6 +1132,41 @@ int tfm_thinking_rows_bwd(const tfm_dims* dims, const int32_t* n_train, const ui
     HIPCHK(tfm::launch_thinking_bwd<tfm::bf16>(g, T, (const tfm::bf16*)dX, dtable, accumulate,
                                                s));
   return TFM_OK;
+}
+
+size_t tfm_infer_workspace_bytes(const tfm_dims* dims) {
+  Dims d;
+  if (check_dims(dims, d) != TFM_OK) return 0;
+  if (!infer_eligible(d)) {
+    fail(TFM_ERR_DIMS, "forward-only calls need TFM_BF16, E in {64, 128, 192, 256} and H a "
+                       "multiple of E");
+    return 0;
+  }
+  return infer_layout(d).total;
+}
+
+size_t tfm_infer_cache_bytes(const tfm_dims* dims) {
+  Dims d;
+  if (check_dims(dims, d) != TFM_OK) return 0;
+  return 2 * cache_half(d);
+}
+
+int tfm_layer_fwd_context(const tfm_dims* dims, const int32_t* n_train, const uint8_t* cell_mask,
+                          const void* X, const float* params, void* Y, void* kv_cache,
+                          size_t cache_bytes, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  return infer_call(dims, -1, n_train, cell_mask, X, params, Y, kv_cache, cache_bytes,
+                    workspace, workspace_bytes, (hipStream_t)stream);
+}
+
+int tfm_layer_fwd_query(const tfm_dims* dims, int32_t context_rows, const int32_t* n_train,
+                        const uint8_t* cell_mask, const void* X, const float* params,
+                        const void* kv_cache, size_t cache_bytes, void* Y, void* workspace,
+                        size_t workspace_bytes, void* stream) {
+  if (context_rows < 0) return fail(TFM_ERR_DIMS, "context_rows=%d must be >= 1", context_rows);
+  return infer_call(dims, context_rows, n_train, cell_mask, X, params, Y,
+                    const_cast<void*>(kv_cache), cache_bytes, workspace, workspace_bytes,
+                    (hipStream_t)stream);
 }
 
 }  // extern "C"

@@ -78,3 +78,79 @@ class Stack:
                           self.workspace)
             g = out
         return g
+
+
+class InferStack:
+    """Forward-only evaluation of L layers (no saved state): `context` runs the context rows
+    (train rows first) through every layer once and keeps one key/value cache per layer;
+    `query` then runs any number of chunks of unlabelled rows through every layer against
+    those caches.  For the pre-norm block, layer l multiplies its input by
+    decay_base ** (first_layer + l)."""
+
+    def __init__(self, dims, n_train, cell_mask, params, max_query_rows, device="cuda",
+                 decay_base=0.95, first_layer=0):
+        self.n_train = np.ascontiguousarray(n_train, dtype=np.int32)
+        self.cell_mask = np.ascontiguousarray(cell_mask, dtype=np.uint8)
+        self.device = device
+        self.params = [p if isinstance(p, torch.Tensor) else
+                       torch.from_numpy(np.ascontiguousarray(p, dtype=np.float32)).to(device)
+                       for p in params]
+        self.L = len(self.params)
+        self.Rc, self.Rq = dims.R, int(max_query_rows)
+        self.ctx_dims = self._layer_dims(dims, dims.R, decay_base, first_layer)
+        self.q_dims = None
+        self.decay_base, self.first_layer, self.base = decay_base, first_layer, dims
+        self.elt = torch.bfloat16
+        wb = max(tfm.infer_workspace_bytes(self.ctx_dims[0]),
+                 tfm.infer_workspace_bytes(self._copy(dims, self.Rq)))
+        cb = tfm.infer_cache_bytes(self.ctx_dims[0])
+        if wb == 0 or cb == 0:
+            raise tfm.TfmError(-1, tfm.last_error())
+        self.workspace = torch.empty(wb, dtype=torch.uint8, device=device)
+        self.caches = [torch.empty(cb, dtype=torch.uint8, device=device) for _ in range(self.L)]
+        S, E = dims.C + 1, dims.E
+        self.ctx_out = [torch.empty((dims.B, self.Rc, S, E), dtype=self.elt, device=device)
+                        for _ in range(min(self.L, 2))]
+        self.q_flat = [torch.empty(dims.B * self.Rq * S * E, dtype=self.elt, device=device)
+                       for _ in range(min(self.L, 2))]
+
+    @staticmethod
+    def _copy(dims, R):
+        d = tfm.tfm_dims.from_buffer_copy(dims)
+        d.R = int(R)
+        return d
+
+    def _layer_dims(self, dims, R, decay_base, first_layer):
+        out = []
+        for l in range(len(self.params)):
+            d = self._copy(dims, R)
+            if dims.block == tfm.TFM_BLOCK_PRENORM:
+                d.decay = decay_base ** (first_layer + l)
+            out.append(d)
+        return out
+
+    def context(self, X):
+        """X: [B, Rc, C+1, E] bfloat16.  Returns the last layer's output (owned buffer)."""
+        h = X
+        for l in range(self.L):
+            out = self.ctx_out[l % 2]
+            tfm.layer_fwd_context(self.ctx_dims[l], self.n_train, self.cell_mask, h,
+                                  self.params[l], out, self.caches[l], self.workspace)
+            h = out
+        return h
+
+    def query(self, Xq):
+        """Xq: [B, Rq', C+1, E] bfloat16 unlabelled rows (contiguous), Rq' <= max_query_rows.
+        Returns the last layer's output for them (a view of an owned buffer)."""
+        Rq = Xq.shape[1]
+        if Rq > self.Rq:
+            raise ValueError(f"{Rq} query rows exceed max_query_rows={self.Rq}")
+        dims = self._layer_dims(self.base, Rq, self.decay_base, self.first_layer)
+        h = Xq
+        for l in range(self.L):
+            B, _, S, E = Xq.shape
+            out = self.q_flat[l % 2][:B * Rq * S * E].view(B, Rq, S, E)
+            tfm.layer_fwd_query(dims[l], self.Rc, self.n_train, self.cell_mask, h,
+                                self.params[l], self.caches[l], out, self.workspace)
+            h = out
+        return h

@@ -21,7 +21,9 @@ ERRORS = {
 }
 EXPORTS = ("tfm_layer_param_count", "tfm_layer_saved_bytes", "tfm_layer_workspace_bytes",
            "tfm_layer_fwd", "tfm_layer_bwd", "tfm_thinking_rows_fwd", "tfm_thinking_rows_bwd",
-           "tfm_last_error", "tfm_prof_enable", "tfm_prof_collect", "tfm_prof_step")
+           "tfm_infer_workspace_bytes", "tfm_infer_cache_bytes", "tfm_layer_fwd_context",
+           "tfm_layer_fwd_query", "tfm_last_error", "tfm_prof_enable", "tfm_prof_collect",
+           "tfm_prof_step")
 
 
 class TfmError(RuntimeError):
@@ -53,7 +55,8 @@ def lib():
         P = ctypes.POINTER
         vp, sz, i32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
         for name in ("tfm_layer_param_count", "tfm_layer_saved_bytes",
-                     "tfm_layer_workspace_bytes"):
+                     "tfm_layer_workspace_bytes", "tfm_infer_workspace_bytes",
+                     "tfm_infer_cache_bytes"):
             getattr(L, name).restype = sz
             getattr(L, name).argtypes = [P(tfm_dims)]
         L.tfm_last_error.restype = ctypes.c_char_p
@@ -67,6 +70,11 @@ def lib():
         L.tfm_thinking_rows_fwd.argtypes = [P(tfm_dims), vp, vp, i32, vp, vp, vp, sz, vp]
         L.tfm_thinking_rows_bwd.restype = i32
         L.tfm_thinking_rows_bwd.argtypes = [P(tfm_dims), vp, vp, i32, vp, vp, i32, vp, sz, vp]
+        L.tfm_layer_fwd_context.restype = i32
+        L.tfm_layer_fwd_context.argtypes = [P(tfm_dims), vp, vp, vp, vp, vp, vp, sz, vp, sz, vp]
+        L.tfm_layer_fwd_query.restype = i32
+        L.tfm_layer_fwd_query.argtypes = [P(tfm_dims), i32, vp, vp, vp, vp, vp, sz, vp, vp, sz,
+                                          vp]
         L.tfm_prof_enable.restype = i32
         L.tfm_prof_enable.argtypes = [i32]
         L.tfm_prof_collect.restype = i32
@@ -92,6 +100,14 @@ def saved_bytes(dims):
 
 def workspace_bytes(dims):
     return lib().tfm_layer_workspace_bytes(ctypes.byref(dims))
+
+
+def infer_workspace_bytes(dims):
+    return lib().tfm_infer_workspace_bytes(ctypes.byref(dims))
+
+
+def infer_cache_bytes(dims):
+    return lib().tfm_infer_cache_bytes(ctypes.byref(dims))
 
 
 def _ptr(t):
@@ -166,6 +182,33 @@ def thinking_rows_bwd(dims, n_train, cell_mask, T, dX, dtable, accumulate, works
                                      _ptr(dtable), int(bool(accumulate)), _ptr(workspace),
                                      workspace.numel() * workspace.element_size(),
                                      _stream(stream))
+    _check(rc)
+
+
+def _nbytes(t):
+    return t.numel() * t.element_size()
+
+
+def layer_fwd_context(dims, n_train, cell_mask, X, params, Y, kv_cache, workspace, stream=None):
+    """tfm_layer_fwd_context: forward without saved state; the train rows' item-axis keys and
+    values go to kv_cache (a device byte tensor of infer_cache_bytes(dims))."""
+    nt, ntp = _host(n_train, np.int32)
+    cm, cmp_ = _host(cell_mask, np.uint8)
+    rc = lib().tfm_layer_fwd_context(ctypes.byref(dims), ntp, cmp_, _ptr(X), _ptr(params),
+                                     _ptr(Y), _ptr(kv_cache), _nbytes(kv_cache), _ptr(workspace),
+                                     _nbytes(workspace), _stream(stream))
+    _check(rc)
+
+
+def layer_fwd_query(dims, context_rows, n_train, cell_mask, X, params, kv_cache, Y, workspace,
+                    stream=None):
+    """tfm_layer_fwd_query: forward of unlabelled rows X [B, Rq, C+1, E] against the keys and
+    values a context call with context_rows rows left in kv_cache."""
+    nt, ntp = _host(n_train, np.int32)
+    cm, cmp_ = _host(cell_mask, np.uint8)
+    rc = lib().tfm_layer_fwd_query(ctypes.byref(dims), int(context_rows), ntp, cmp_, _ptr(X),
+                                   _ptr(params), _ptr(kv_cache), _nbytes(kv_cache), _ptr(Y),
+                                   _ptr(workspace), _nbytes(workspace), _stream(stream))
     _check(rc)
 
 

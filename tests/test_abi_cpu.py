@@ -143,3 +143,52 @@ def test_thinking_rows_arguments_rejected_before_launch(bwd):
     assert _call_think(d, [5, 5], mask, 1, ptr=0, bwd=bwd) == -5
     assert _call_think(d, [5, 5], mask, 1, ptr=(1 << 20) + 8, bwd=bwd) == -5
     assert _call_think(d, [5, 5], mask, 1, wb=16, bwd=bwd) == -7
+
+
+def test_forward_only_sizes():
+    d = _dims(dtype="bf16", E=192, heads=6, H=384, R=1024, C=100, B=16)
+    wb = tfm.infer_workspace_bytes(d)
+    assert 0 < wb < tfm.saved_bytes(d)
+    cb = tfm.infer_cache_bytes(d)
+    half = 16 * 101 * 1024 * 192 * 2
+    assert cb == 2 * ((half + 255) // 256 * 256)
+    assert tfm.infer_workspace_bytes(_dims(dtype="f32")) == 0
+    assert "TFM_BF16" in tfm.last_error()
+    pre = _dims(dtype="bf16", E=256, heads=4, H=768, block="pre")
+    assert tfm.infer_workspace_bytes(pre) > tfm.infer_workspace_bytes(
+        _dims(dtype="bf16", E=256, heads=4, H=768))
+
+
+def _ctx(d, n_train, mask, ptr=1 << 20, cb=1 << 40, wb=1 << 40):
+    nt = np.ascontiguousarray(n_train, dtype=np.int32)
+    cm = np.ascontiguousarray(mask, dtype=np.uint8)
+    return tfm.lib().tfm_layer_fwd_context(ctypes.byref(d), nt.ctypes.data, cm.ctypes.data, ptr,
+                                           ptr, ptr, ptr, cb, ptr, wb, None)
+
+
+def _qry(d, rc, n_train, mask, ptr=1 << 20, cb=1 << 40, wb=1 << 40):
+    nt = np.ascontiguousarray(n_train, dtype=np.int32)
+    cm = np.ascontiguousarray(mask, dtype=np.uint8)
+    return tfm.lib().tfm_layer_fwd_query(ctypes.byref(d), rc, nt.ctypes.data, cm.ctypes.data,
+                                         ptr, ptr, ptr, cb, ptr, ptr, wb, None)
+
+
+def test_forward_only_arguments_rejected_before_launch():
+    d = _dims(dtype="bf16")
+    mask = np.ones((2, 9), np.uint8)
+    assert _ctx(_dims(), [5, 5], mask) == -1              # fp32
+    assert _ctx(d, [5, 65], mask) == -3
+    assert _ctx(d, [5, 5], mask, ptr=0) == -5
+    assert _ctx(d, [5, 5], mask, cb=16) == -7
+    assert _ctx(d, [5, 5], mask, wb=16) == -7
+    q = _dims(dtype="bf16", R=8)                          # 8 query rows
+    assert _qry(q, 0, [5, 5], mask) == -1
+    assert _qry(q, -3, [5, 5], mask) == -1
+    assert _qry(q, 32, [5, 33], mask) == -3               # n_train beyond the context rows
+    assert _qry(q, 32, [20, 32], mask, ptr=(1 << 20) + 2) == -5
+    need = tfm.infer_cache_bytes(_dims(dtype="bf16", R=32))
+    assert _qry(q, 32, [20, 32], mask, cb=need - 1) == -7
+    assert "kv_cache" in tfm.last_error()
+    bad = mask.copy()
+    bad[1, 8] = 0
+    assert _qry(q, 32, [20, 32], bad) == -4
