@@ -52,7 +52,7 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
   if (prob >= (int64_t)g.NC * g.heads) return;
   const int64_t col = prob / g.heads;
   const int head = (int)(prob - col * g.heads);
-  const int n = g.ds[g.col_ds[col]].n_train;
+  const int n = g.col_ntr[col];
   const int R = g.R;
   const bf16* Qp = q + prob * R * D;
   const bf16* Kp = k + prob * kR * D;  // keys and values: kR rows per problem

@@ -73,7 +73,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
   if (prob >= (int64_t)g.NC * g.heads) return;
   const int64_t col = prob / g.heads;
   const int head = (int)(prob - col * g.heads);
-  const int n = g.ds[g.col_ds[col]].n_train;
+  const int n = g.col_ntr[col];
   const int t0 = kt * 4 * KW;
   if (t0 >= n) return;
   const int R = g.R, E = g.E;
@@ -234,7 +234,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
   if (prob >= (int64_t)g.NC * g.heads) return;
   const int64_t col = prob / g.heads;
   const int head = (int)(prob - col * g.heads);
-  const int n = g.ds[g.col_ds[col]].n_train;
+  const int n = g.col_ntr[col];
   const int R = g.R, E = g.E;
 
   const uint32_t rowQ = D * 2, rowO = (uint32_t)E * 2;

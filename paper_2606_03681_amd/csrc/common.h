@@ -31,13 +31,17 @@ struct Geo {
   const int32_t* col_ds;   // [NC] dataset of each active column
   const int32_t* col_c;    // [NC] native cell column of each active column
   const int32_t* colmap;   // [B*S] native (b, c) -> global active column, or -1
+  // Per-column copies of the above that a kernel reads with one load instead of a dependent
+  // pair: the native cell index of the column's row 0, (col_ds * R) * S + col_c, and the
+  // train-prefix length of the column's dataset.
+  const int64_t* col_cell0;  // [NC]
+  const int32_t* col_ntr;    // [NC]
 };
 
 __host__ __device__ inline int64_t native_cell(const Geo& g, int64_t p) {
   int64_t col = p / g.R;
   int64_t r = p - col * g.R;
-  int64_t b = g.col_ds[col];
-  return ((b * g.R + r) * g.S + g.col_c[col]);
+  return g.col_cell0[col] + r * g.S;
 }
 
 // bfloat16 storage as raw 16-bit patterns; round to nearest even on store.

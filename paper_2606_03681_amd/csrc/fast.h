@@ -20,7 +20,7 @@ __device__ __forceinline__ int64_t item_hm_offset(const Geo& g, int64_t col, int
   const int p = k / g.E, within = k - p * g.E;
   const int head = within / g.d, j = within - head * g.d;
   *part = p;
-  if (p > 0 && r >= g.ds[g.col_ds[col]].n_train) return -1;
+  if (p > 0 && r >= g.col_ntr[col]) return -1;
   return ((col * g.heads + head) * g.R + r) * g.d + j;
 }
 

@@ -129,7 +129,7 @@ __global__ __launch_bounds__(512) void k_ln_out_bwd(Geo g, const bf16* __restric
           r -= g.R;
           ++col;
         }
-        const int64_t nat = ((int64_t)g.col_ds[col] * g.R + r) * g.S + g.col_c[col];
+        const int64_t nat = g.col_cell0[col] + (int64_t)r * g.S;
         rs[u] = rstd[p];
         if (act) {
           dyv[u] = ldu4(dY + nat * E + 8 * l);
@@ -222,7 +222,7 @@ __global__ __launch_bounds__(512) void k_rms_in(Geo g, const bf16* __restrict__ 
           rr -= g.R;
           ++col;
         }
-        const int64_t nat = ((int64_t)g.col_ds[col] * g.R + rr) * g.S + g.col_c[col];
+        const int64_t nat = g.col_cell0[col] + (int64_t)rr * g.S;
         xv[u] = ldu4(X + nat * E + 8 * l);
       }
     }

@@ -134,15 +134,19 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   if (m0 >= a.M) return;
   const int n0 = by * BN;
   const Geo& g = a.g;
+  // item Q|K|V: which of the three this column tile is (BN divides E), and its first column
+  // within that part
+  const int part = EPI == EPI_ITEM_QKV ? n0 / g.E : 0;
+  const int pc0 = n0 - part * g.E;
 
-  if (EPI == EPI_ITEM_QKV && by > 0) {
+  if (EPI == EPI_ITEM_QKV && part > 0) {
     // K and V exist for train rows only: skip tiles made of test rows alone
     int64_t last = m0 + BM - 1 < a.M ? m0 + BM - 1 : a.M - 1;
     int64_t c0 = m0 / g.R, c1 = last / g.R;
     bool any = false;
     for (int64_t c = c0; c <= c1 && !any; ++c) {
       int64_t rlo = c == c0 ? m0 - c0 * g.R : 0;
-      any = rlo < g.ds[g.col_ds[c]].n_train;
+      any = rlo < g.col_ntr[c];
     }
     if (!any) return;
   }
@@ -163,7 +167,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
     if (arow_ok) {
       hcol = am / g.R;
       hr = (int)(am - hcol * g.R);
-      hntr = g.ds[g.col_ds[hcol]].n_train;
+      hntr = g.col_ntr[hcol];
     }
   } else if (arow_ok) {
     aptr = a.A + row_addr(g, a.amode, am, a.lda) + akc * 8;
@@ -292,7 +296,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
         if (hm_part >= 0) {
           const int64_t col = m / g.R;
           const int r = (int)(m - col * g.R);
-          if (hm_part == 0 || r < g.ds[g.col_ds[col]].n_train)
+          if (hm_part == 0 || r < g.col_ntr[col])
             off = (col * g.heads * g.R + r) * (int64_t)g.d;
         } else {
           off = mode == ROWS_NATIVE ? native_cell(g, m) * g.E : m * ld;
@@ -317,7 +321,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
       if (off < 0) continue;
       int64_t o = off + c0 + cc;
       if (hm) {
-        const int head = cc / g.d, jj = cc - head * g.d;
+        const int head = (pc0 + cc) / g.d, jj = pc0 + cc - head * g.d;
         o = off + (int64_t)head * g.R * g.d + jj;
       }
       stu4(dst + o, ldu4(&tile[row * TS + cc]));
@@ -340,13 +344,13 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
 
   if (EPI == EPI_BIAS || EPI == EPI_GELU_FWD || EPI == EPI_ITEM_QKV) {
     if (EPI == EPI_ITEM_QKV)
-      set_rows(ROWS_COMPACT, 0, by);
+      set_rows(ROWS_COMPACT, 0, part);
     else
       set_rows(ROWS_COMPACT, a.ldo, -1);
     // item K is stored pre-multiplied by log2(e)/sqrt(d) (in fp32, before the bf16 rounding):
     // the attention kernels then get scores in the exp2 domain straight from the MFMA
     const float ksc =
-        EPI == EPI_ITEM_QKV && by == 1 ? 1.4426950408889634f / sqrtf((float)g.d) : 1.0f;
+        EPI == EPI_ITEM_QKV && part == 1 ? 1.4426950408889634f / sqrtf((float)g.d) : 1.0f;
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
       const f32x4 b = par4(0, j);
@@ -355,7 +359,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
     }
     lds_barrier();
     if (EPI == EPI_ITEM_QKV) {
-      bf16* dst = by == 0 ? a.out : (by == 1 ? a.out2 : a.out3);
+      bf16* dst = part == 0 ? a.out : (part == 1 ? a.out2 : a.out3);
       store_tile(dst, 0, true);
       return;
     }

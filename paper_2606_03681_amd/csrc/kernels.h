@@ -11,8 +11,9 @@ namespace tfm {
 hipError_t launch_upload(const int32_t* host, int64_t count, int32_t* dst, hipStream_t s);
 // Expands the per-dataset blob {n_train, col0, S_b, mask words...} into DsInfo and the
 // column maps of Geo.
-hipError_t launch_expand_meta(const int32_t* blob, int B, int S, int words, DsInfo* ds,
-                              int32_t* col_ds, int32_t* col_c, int32_t* colmap, hipStream_t s);
+hipError_t launch_expand_meta(const int32_t* blob, int B, int R, int S, int words, DsInfo* ds,
+                              int32_t* col_ds, int32_t* col_c, int32_t* colmap,
+                              int64_t* col_cell0, int32_t* col_ntr, hipStream_t s);
 
 // ---- data movement between the native [B][R][S][E] layout and active cells ------------------
 template <class T>

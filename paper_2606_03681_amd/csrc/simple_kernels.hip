@@ -51,8 +51,9 @@ hipError_t launch_upload(const int32_t* host, int64_t count, int32_t* dst, hipSt
   return hipSuccess;
 }
 
-__global__ void k_expand_meta(const int32_t* blob, int B, int S, int W, DsInfo* ds,
-                              int32_t* col_ds, int32_t* col_c, int32_t* colmap) {
+__global__ void k_expand_meta(const int32_t* blob, int B, int R, int S, int W, DsInfo* ds,
+                              int32_t* col_ds, int32_t* col_c, int32_t* colmap,
+                              int64_t* col_cell0, int32_t* col_ntr) {
   int64_t t = gtid();
   if (t >= (int64_t)B * S) return;
   int b = (int)(t / S), c = (int)(t % S);
@@ -71,12 +72,16 @@ __global__ void k_expand_meta(const int32_t* blob, int B, int S, int W, DsInfo* 
   col_ds[gcol] = b;
   col_c[gcol] = c;
   colmap[t] = gcol;
+  col_cell0[gcol] = (int64_t)b * R * S + c;
+  col_ntr[gcol] = e[0];
 }
 
-hipError_t launch_expand_meta(const int32_t* blob, int B, int S, int words, DsInfo* ds,
-                              int32_t* col_ds, int32_t* col_c, int32_t* colmap, hipStream_t s) {
-  k_expand_meta<<<grid_for((int64_t)B * S), TFM_BLOCK, 0, s>>>(blob, B, S, words, ds, col_ds,
-                                                                 col_c, colmap);
+hipError_t launch_expand_meta(const int32_t* blob, int B, int R, int S, int words, DsInfo* ds,
+                              int32_t* col_ds, int32_t* col_c, int32_t* colmap,
+                              int64_t* col_cell0, int32_t* col_ntr, hipStream_t s) {
+  k_expand_meta<<<grid_for((int64_t)B * S), TFM_BLOCK, 0, s>>>(blob, B, R, S, words, ds, col_ds,
+                                                                 col_c, colmap, col_cell0,
+                                                                 col_ntr);
   return hipGetLastError();
 }
 
@@ -184,7 +189,7 @@ __global__ __launch_bounds__(256) void k_linear(int64_t M, int Nout, int K,
         int head = within / g.d, jj = within - head * g.d;
         int64_t col = m / g.R;
         int r = (int)(m - col * g.R);
-        if (part > 0 && r >= g.ds[g.col_ds[col]].n_train) continue;
+        if (part > 0 && r >= g.col_ntr[col]) continue;
         TO* base = part == 0 ? out : (part == 1 ? kout : vout);
         st(base + (((int64_t)col * g.heads + head) * g.R + r) * g.d + jj, v);
       }
@@ -612,7 +617,7 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const T* __restric
   const int64_t ch = t / g.R;  // col * heads + head
   const int head = (int)(ch % g.heads);
   const int64_t col = ch / g.heads;
-  const int n = g.ds[g.col_ds[col]].n_train;
+  const int n = g.col_ntr[col];
   const float tau = 1.0f / sqrtf((float)D);
   const int64_t base = ch * g.R;
   float qv[D];
@@ -688,7 +693,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const T* __restrict
   const int64_t ch = t / g.R;
   const int head = (int)(ch % g.heads);
   const int64_t col = ch / g.heads;
-  const int n = g.ds[g.col_ds[col]].n_train;
+  const int n = g.col_ntr[col];
   const float tau = 1.0f / sqrtf((float)D);
   const int64_t base = ch * g.R;
   float qv[D], dov[D], acc[D];
@@ -730,7 +735,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dkv(Geo g, const T* __restric
   const int64_t ch = t / g.R;
   const int head = (int)(ch % g.heads);
   const int64_t col = ch / g.heads;
-  const int n = g.ds[g.col_ds[col]].n_train;
+  const int n = g.col_ntr[col];
   if (tk >= n) return;
   const float tau = 1.0f / sqrtf((float)D);
   const int64_t base = ch * g.R;
@@ -800,7 +805,7 @@ __global__ void k_item_dqkv_to_cells(Geo g, const T* __restrict__ dq, const T* _
     int64_t col = p / g.R;
     int r = (int)(p - col * g.R);
     const T* src = part == 0 ? dq : (part == 1 ? dk : dv);
-    if (part > 0 && r >= g.ds[g.col_ds[col]].n_train) {
+    if (part > 0 && r >= g.col_ntr[col]) {
       st(dqkv + i, 0.f);
     } else {
       dqkv[i] = src[((col * g.heads + head) * g.R + r) * g.d + j];

@@ -121,7 +121,7 @@ struct Arena {
 
 // Offsets of the device copy of the plan inside a workspace.
 struct MetaOff {
-  size_t blob, ds, col_ds, col_c, colmap;
+  size_t blob, ds, col_ds, col_c, colmap, col_cell0, col_ntr;
 };
 
 MetaOff take_meta(const Dims& d, Arena& a) {
@@ -131,6 +131,8 @@ MetaOff take_meta(const Dims& d, Arena& a) {
   L.col_ds = a.take((size_t)d.B * d.S * 4);
   L.col_c = a.take((size_t)d.B * d.S * 4);
   L.colmap = a.take((size_t)d.B * d.S * 4);
+  L.col_cell0 = a.take((size_t)d.B * d.S * 8);
+  L.col_ntr = a.take((size_t)d.B * d.S * 4);
   return L;
 }
 
@@ -305,10 +307,13 @@ int setup_geo(const Dims& d, const Plan& P, char* ws, const MetaOff& W, tfm::Geo
   g.col_ds = (const int32_t*)(ws + W.col_ds);
   g.col_c = (const int32_t*)(ws + W.col_c);
   g.colmap = (const int32_t*)(ws + W.colmap);
+  g.col_cell0 = (const int64_t*)(ws + W.col_cell0);
+  g.col_ntr = (const int32_t*)(ws + W.col_ntr);
   HIPCHK(tfm::launch_upload(P.blob.data(), (int64_t)P.blob.size(), blob, s));
-  HIPCHK(tfm::launch_expand_meta(blob, d.B, d.S, d.words, (tfm::DsInfo*)(ws + W.ds),
+  HIPCHK(tfm::launch_expand_meta(blob, d.B, d.R, d.S, d.words, (tfm::DsInfo*)(ws + W.ds),
                                  (int32_t*)(ws + W.col_ds), (int32_t*)(ws + W.col_c),
-                                 (int32_t*)(ws + W.colmap), s));
+                                 (int32_t*)(ws + W.colmap), (int64_t*)(ws + W.col_cell0),
+                                 (int32_t*)(ws + W.col_ntr), s));
   return TFM_OK;
 }
 

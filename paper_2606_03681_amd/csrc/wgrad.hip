@@ -50,29 +50,35 @@ __device__ __forceinline__ void cur_init(Cursor& c, const Geo& g, int64_t m, int
     c.hmo = head * g.R * g.d + (within - head * g.d);
     c.addr = 0;
     if (c.rem > 0) {
-      c.ntr = g.ds[g.col_ds[c.col]].n_train;
+      c.ntr = g.col_ntr[c.col];
       c.addr = ((int64_t)c.col * g.heads * g.R + c.r) * g.d + c.hmo;
     }
   }
 }
 
+// The load is always issued (a row that does not exist reads the operand's first chunk, and
+// *ok tells the consumer to use zeros instead): with no branch around it and no use of the
+// value until the slice is stored to LDS, the number of loads in flight is fixed and each wait
+// counts exactly the older loads instead of draining all of them.
 template <int MODE>
 __device__ __forceinline__ uint4 cur_load(const Cursor& c, const bf16* p0, const bf16* p1,
-                                          const bf16* p2) {
-  uint4 v = make_uint4(0, 0, 0, 0);
-  if (c.rem > 0) {
-    if (MODE == ROWS_ITEM_HM) {
-      const bf16* base = c.part == 0 ? p0 : (c.part == 1 ? p1 : p2);
-      if (c.part == 0 || c.r < c.ntr) v = ldu4(base + c.addr);
-    } else {
-      v = ldu4(p0 + c.addr);
-    }
+                                          const bf16* p2, bool* ok) {
+  bool v = c.rem > 0;
+  const bf16* base = p0;
+  if (MODE == ROWS_ITEM_HM) {
+    base = c.part == 0 ? p0 : (c.part == 1 ? p1 : p2);
+    v = v && (c.part == 0 || c.r < c.ntr);
   }
-  return v;
+  *ok = v;
+  return ldu4(base + (v ? c.addr : 0));
 }
 
+// cell0 / ntr: the column metadata (entry col - lo for column col); the workgroup's own copy
+// in LDS where it has one, so that crossing into the next column costs no global load (whose
+// wait would also wait for every data load in flight).
 template <int MODE>
-__device__ __forceinline__ void cur_advance(Cursor& c, const Geo& g, int64_t ld, int f) {
+__device__ __forceinline__ void cur_advance(Cursor& c, const Geo& g, int64_t ld, int f,
+                                            const int64_t* cell0, const int32_t* ntr, int lo) {
   c.rem -= MS;
   if (MODE == ROWS_COMPACT) {
     c.addr += MS * ld;
@@ -89,17 +95,19 @@ __device__ __forceinline__ void cur_advance(Cursor& c, const Geo& g, int64_t ld,
   }
   if (c.rem <= 0) return;
   if (MODE == ROWS_NATIVE) {
-    c.addr = (((int64_t)g.col_ds[c.col] * g.R + c.r) * g.S + g.col_c[c.col]) * g.E + f;
+    c.addr = (cell0[c.col - lo] + (int64_t)c.r * g.S) * g.E + f;
   } else {
-    c.ntr = g.ds[g.col_ds[c.col]].n_train;
+    c.ntr = ntr[c.col - lo];
     c.addr = ((int64_t)c.col * g.heads * g.R + c.r) * g.d + c.hmo;
   }
 }
 }  // namespace
 
 // 512 threads = 8 waves in a 2 (n) x 4 (k) arrangement; tile BN x BK.  dY is in layout YM
-// (compact or head-major item gradients), X in layout XM (compact or native).
-template <int BN, int BK, int YM, int XM>
+// (compact or head-major item gradients), X in layout XM (compact or native).  TBL: the
+// workgroup copies the metadata of the columns its chunk spans into LDS (requires R >= MS, so
+// that a chunk spans at most WGRAD_CHUNK / MS + 1 columns).
+template <int BN, int BK, int YM, int XM, bool TBL>
 __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
   constexpr int NBW = BN / 32;      // 16-row blocks per wave along n (BN/2 rows)
   constexpr int KBW = BK / 64;      // 16-col blocks per wave along k (BK/4 cols)
@@ -127,9 +135,26 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
   const int64_t me = mb + a.chunk < a.M ? mb + a.chunk : a.M;
   const Geo& g = a.g;
 
+  constexpr int CT = WGRAD_CHUNK / MS + 2;
+  __shared__ int64_t tcell[TBL ? CT : 1];
+  __shared__ int32_t tntr[TBL ? CT : 1];
+  const int lo = TBL ? (int)(mb / g.R) : 0;
+  if (TBL) {
+    const int ncol = (int)((me - 1) / g.R) - lo + 1;
+    for (int i = tid; i < ncol && i < CT; i += 512) {
+      tcell[i] = g.col_cell0[lo + i];
+      tntr[i] = g.col_ntr[lo + i];
+    }
+    __syncthreads();
+  }
+  const int64_t* cell0 = TBL ? tcell : g.col_cell0;
+  const int32_t* ntrp = TBL ? tntr : g.col_ntr;
+
   // staging: threads 0-255 stage dY features [n0, n0+BN), threads 256-511 X features
   // [k0, k0+BK); chunk ch -> cell ch / (width/8) of the slice, features (ch % (width/8)) * 8
-  const bool opa = tid < 256;
+  // role of the wave (uniform across it: scalar branches, so the two roles' loads are never
+  // taken for one instruction stream)
+  const bool opa = __builtin_amdgcn_readfirstlane(w) < 4;
   const int st = tid & 255;
   constexpr int CPM = CPA > CPB ? CPA : CPB;
   Cursor cu[CPM];  // one array for both roles (a select between two arrays would not stay in
@@ -143,35 +168,38 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
       if (i < CPB) cur_init<XM>(cu[i], g, mb + ch / (BK / 8), me, k0 + (ch % (BK / 8)) * 8, a.ldx);
     }
   }
-  auto gload = [&](uint4* r) {
-#pragma unroll
-    for (int i = 0; i < CPM; ++i) {
-      const int ch = st + 256 * i;
-      if (opa) {
-        if (i < CPA) {
-          r[i] = cur_load<YM>(cu[i], a.dY, a.dY2, a.dY3);
-          cur_advance<YM>(cu[i], g, a.ldy, n0 + (ch % (BN / 8)) * 8);
-        }
-      } else {
-        if (i < CPB) {
-          r[i] = cur_load<XM>(cu[i], a.X, nullptr, nullptr);
-          cur_advance<XM>(cu[i], g, a.ldx, k0 + (ch % (BK / 8)) * 8);
-        }
-      }
-    }
-  };
-  auto sstore = [&](const uint4* r, int b) {
+  // one role branch around all of a thread's loads (not one per load), so that the other
+  // role's loads never precede them on any path
+  auto gload = [&](uint4* r, bool* okr) {
     if (opa) {
 #pragma unroll
       for (int i = 0; i < CPA; ++i) {
         const int ch = st + 256 * i;
-        stu4(&As[b][(ch / (BN / 8)) * LSA + (ch % (BN / 8)) * 8], r[i]);
+        r[i] = cur_load<YM>(cu[i], a.dY, a.dY2, a.dY3, &okr[i]);
+        cur_advance<YM>(cu[i], g, a.ldy, n0 + (ch % (BN / 8)) * 8, cell0, ntrp, lo);
       }
     } else {
 #pragma unroll
       for (int i = 0; i < CPB; ++i) {
         const int ch = st + 256 * i;
-        stu4(&Bs[b][(ch / (BK / 8)) * LSB + (ch % (BK / 8)) * 8], r[i]);
+        r[i] = cur_load<XM>(cu[i], a.X, nullptr, nullptr, &okr[i]);
+        cur_advance<XM>(cu[i], g, a.ldx, k0 + (ch % (BK / 8)) * 8, cell0, ntrp, lo);
+      }
+    }
+  };
+  const uint4 z4 = make_uint4(0u, 0u, 0u, 0u);
+  auto sstore = [&](const uint4* r, const bool* okr, int b) {
+    if (opa) {
+#pragma unroll
+      for (int i = 0; i < CPA; ++i) {
+        const int ch = st + 256 * i;
+        stu4(&As[b][(ch / (BN / 8)) * LSA + (ch % (BN / 8)) * 8], okr[i] ? r[i] : z4);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < CPB; ++i) {
+        const int ch = st + 256 * i;
+        stu4(&Bs[b][(ch / (BK / 8)) * LSB + (ch % (BK / 8)) * 8], okr[i] ? r[i] : z4);
       }
     }
   };
@@ -211,24 +239,27 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
   };
 
   // Two register sets: slice s + 2 is loaded while slice s is multiplied, and slice s + 1
-  // (loaded one step earlier) goes to LDS at the end of step s.
+  // (loaded one step earlier) goes to LDS at the end of step s.  Loads and stores run
+  // unconditionally (slices past the end are zero and never multiplied), so the loads in
+  // flight are always the same ones.
   const int64_t steps = (me - mb + MS - 1) / MS;
   uint4 r0[CPM], r1[CPM];
-  if (steps > 0) gload(r0);
-  if (steps > 1) gload(r1);
-  if (steps > 0) sstore(r0, 0);
+  bool ok0[CPM], ok1[CPM];
+  gload(r0, ok0);
+  gload(r1, ok1);
+  sstore(r0, ok0, 0);
   lds_barrier();
   for (int64_t s = 0; s < steps; s += 2) {
     // even step s: compute buffer 0; r0 refills with slice s + 2; r1 (slice s + 1) -> buffer 1
-    if (s + 2 < steps) gload(r0);
+    gload(r0, ok0);
     compute(0);
-    if (s + 1 < steps) sstore(r1, 1);
+    sstore(r1, ok1, 1);
     lds_barrier();
     if (s + 1 >= steps) break;
     // odd step s + 1: compute buffer 1; r1 refills with slice s + 3; r0 (slice s + 2) -> 0
-    if (s + 3 < steps) gload(r1);
+    gload(r1, ok1);
     compute(1);
-    if (s + 2 < steps) sstore(r0, 0);
+    sstore(r0, ok0, 0);
     lds_barrier();
   }
 
@@ -326,14 +357,19 @@ static hipError_t wgrad_modes(const WgradArgs& b, dim3 grid, hipStream_t s) {
   const bool yhm = b.ymode == ROWS_ITEM_HM, xnat = b.xmode == ROWS_NATIVE;
   if (b.ymode != ROWS_COMPACT && !yhm) return hipErrorInvalidValue;
   if (b.xmode != ROWS_COMPACT && !xnat) return hipErrorInvalidValue;
-  if (yhm && xnat)
-    k_wgrad<BN, BK, ROWS_ITEM_HM, ROWS_NATIVE><<<grid, 512, 0, s>>>(b);
-  else if (yhm)
-    k_wgrad<BN, BK, ROWS_ITEM_HM, ROWS_COMPACT><<<grid, 512, 0, s>>>(b);
-  else if (xnat)
-    k_wgrad<BN, BK, ROWS_COMPACT, ROWS_NATIVE><<<grid, 512, 0, s>>>(b);
-  else
-    k_wgrad<BN, BK, ROWS_COMPACT, ROWS_COMPACT><<<grid, 512, 0, s>>>(b);
+  const bool tbl = b.g.R >= MS;
+  if (yhm && xnat) {
+    if (tbl) k_wgrad<BN, BK, ROWS_ITEM_HM, ROWS_NATIVE, true><<<grid, 512, 0, s>>>(b);
+    else k_wgrad<BN, BK, ROWS_ITEM_HM, ROWS_NATIVE, false><<<grid, 512, 0, s>>>(b);
+  } else if (yhm) {
+    if (tbl) k_wgrad<BN, BK, ROWS_ITEM_HM, ROWS_COMPACT, true><<<grid, 512, 0, s>>>(b);
+    else k_wgrad<BN, BK, ROWS_ITEM_HM, ROWS_COMPACT, false><<<grid, 512, 0, s>>>(b);
+  } else if (xnat) {
+    if (tbl) k_wgrad<BN, BK, ROWS_COMPACT, ROWS_NATIVE, true><<<grid, 512, 0, s>>>(b);
+    else k_wgrad<BN, BK, ROWS_COMPACT, ROWS_NATIVE, false><<<grid, 512, 0, s>>>(b);
+  } else {
+    k_wgrad<BN, BK, ROWS_COMPACT, ROWS_COMPACT, false><<<grid, 512, 0, s>>>(b);
+  }
   return hipGetLastError();
 }
 
