@@ -184,9 +184,11 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
     const int k0 = st * BK;
     const bf16* src = arow_ok ? aptr + k0 : zero;
     if (a.amode == ROWS_ITEM_HM) {
-      // k -> part (Q, K, V), head, offset in head; K and V rows exist for train rows only
-      const int k = k0 + akc * 8;
-      const int part = k / BN, within = k - part * BN;
+      // k -> part (Q, K, V), head, offset in head; K and V rows exist for train rows only.
+      // A stage never straddles two parts (BK divides BN), so the part follows from k0 alone
+      // and the base pointer is chosen by a scalar branch.
+      const int part = k0 / BN;
+      const int within = k0 - part * BN + akc * 8;
       const int head = within / g.d, jj = within - head * g.d;
       const bf16* base = part == 0 ? a.A : (part == 1 ? a.A2 : a.A3);
       src = arow_ok && (part == 0 || hr < hntr)
