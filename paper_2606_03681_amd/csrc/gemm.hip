@@ -17,8 +17,6 @@ namespace tfm {
 
 namespace {
 
-constexpr int BM = GEMM_BM;
-constexpr int MI = BM / 32;  // 16-row blocks per wave (2 x 2 waves, each BM/2 rows)
 constexpr int BK = 32;       // k per pipeline stage: one 64-byte LDS row per operand row
 
 // Source of the 16-byte loads of rows that do not exist (past M, or K/V rows of test cells).
@@ -96,8 +94,10 @@ __device__ __forceinline__ f32x4 unpack4(uint2 u) {
 
 }  // namespace
 
-template <int BN, int EPI>
+template <int BN, int EPI, int BM>
 __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
+  constexpr int MI = BM / 32;          // 16-row blocks per wave (2 x 2 waves, each BM/2 rows)
+  constexpr int NBA = BM / 64;         // 1 KB blocks of A per wave and stage
   constexpr int NB = BN / 32;          // 16-wide column blocks per wave
   constexpr int TS = BN + 8;           // epilogue tile row stride (elements)
   constexpr int S = 3;  // pipeline stages in the LDS ring (48 KB at E = 192: 3 workgroups per CU)
@@ -155,22 +155,32 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   // [k0, k0+32), straight from memory into the stage's LDS slot (global_load_lds: lane L of a
   // wave fills bytes 16L..16L+15 of the wave's 1 KB block).  LDS position p (16-byte units)
   // holds row p / 4, k chunk kslot^-1(p % 4); this lane's A position is wave*64 + lane.
-  const int ar = (wave * 64 + lane) >> 2;
-  const int akc = kslot(ar, lane & 3);
-  const int64_t am = m0 + ar;
-  const bool arow_ok = am < a.M;
+  // This lane's A positions: block t covers rows 16 (wave + 4 t) .. + 15.
   const bf16* zero = reinterpret_cast<const bf16*>(&kZeroChunk);
-  const bf16* aptr = zero;  // row address + chunk, for compact / native rows
-  int64_t hcol = 0;
-  int hr = 0, hntr = 0;
-  if (a.amode == ROWS_ITEM_HM) {
-    if (arow_ok) {
-      hcol = am / g.R;
-      hr = (int)(am - hcol * g.R);
-      hntr = g.col_ntr[hcol];
+  int akc[NBA];
+  bool arow_ok[NBA];
+  const bf16* aptr[NBA];  // row address + chunk, for compact / native rows
+  int64_t hcol[NBA];
+  int hr[NBA], hntr[NBA];
+#pragma unroll
+  for (int t = 0; t < NBA; ++t) {
+    const int ar = ((wave + 4 * t) * 64 + lane) >> 2;
+    akc[t] = kslot(ar, lane & 3);
+    const int64_t am = m0 + ar;
+    arow_ok[t] = am < a.M;
+    aptr[t] = zero;
+    hcol[t] = 0;
+    hr[t] = 0;
+    hntr[t] = 0;
+    if (a.amode == ROWS_ITEM_HM) {
+      if (arow_ok[t]) {
+        hcol[t] = am / g.R;
+        hr[t] = (int)(am - hcol[t] * g.R);
+        hntr[t] = g.col_ntr[hcol[t]];
+      }
+    } else if (arow_ok[t]) {
+      aptr[t] = a.A + row_addr(g, a.amode, am, a.lda) + akc[t] * 8;
     }
-  } else if (arow_ok) {
-    aptr = a.A + row_addr(g, a.amode, am, a.lda) + akc * 8;
   }
   const bf16* bptr[NBB];
 #pragma unroll
@@ -182,20 +192,23 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   auto issue = [&](int st) {
     bf16* sa = ring + (st % S) * STAGE_EL;
     const int k0 = st * BK;
-    const bf16* src = arow_ok ? aptr + k0 : zero;
-    if (a.amode == ROWS_ITEM_HM) {
-      // k -> part (Q, K, V), head, offset in head; K and V rows exist for train rows only.
-      // A stage never straddles two parts (BK divides BN), so the part follows from k0 alone
-      // and the base pointer is chosen by a scalar branch.
-      const int part = k0 / BN;
-      const int within = k0 - part * BN + akc * 8;
-      const int head = within / g.d, jj = within - head * g.d;
-      const bf16* base = part == 0 ? a.A : (part == 1 ? a.A2 : a.A3);
-      src = arow_ok && (part == 0 || hr < hntr)
-                ? base + ((hcol * g.heads + head) * g.R + hr) * (int64_t)g.d + jj
-                : zero;
+#pragma unroll
+    for (int t = 0; t < NBA; ++t) {
+      const bf16* src = arow_ok[t] ? aptr[t] + k0 : zero;
+      if (a.amode == ROWS_ITEM_HM) {
+        // k -> part (Q, K, V), head, offset in head; K and V rows exist for train rows only.
+        // A stage never straddles two parts (BK divides BN), so the part follows from k0
+        // alone and the base pointer is chosen by a scalar branch.
+        const int part = k0 / BN;
+        const int within = k0 - part * BN + akc[t] * 8;
+        const int head = within / g.d, jj = within - head * g.d;
+        const bf16* base = part == 0 ? a.A : (part == 1 ? a.A2 : a.A3);
+        src = arow_ok[t] && (part == 0 || hr[t] < hntr[t])
+                  ? base + ((hcol[t] * g.heads + head) * g.R + hr[t]) * (int64_t)g.d + jj
+                  : zero;
+      }
+      lds_dma16(src, sa + (wave + 4 * t) * 512);
     }
-    lds_dma16(src, sa + wave * 512);
 #pragma unroll
     for (int t = 0; t < NBB; ++t) lds_dma16(bptr[t] + k0, sa + A_EL + (wave + 4 * t) * 512);
   };
@@ -256,7 +269,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
     if (st < KT) issue(st);
   for (int kt = 0; kt < KT; ++kt) {
     if (kt + S - 2 < KT) {
-      asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"((S - 2) * (1 + NBB)) : "memory");
+      asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"((S - 2) * (NBA + NBB)) : "memory");
     } else {
       asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
     }
@@ -630,18 +643,39 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
 
 template <int BN>
 static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
-  const int64_t mt = (a.M + BM - 1) / BM;
+  // 128-row tiles (each weight tile staged through LDS serves twice the rows), except for the
+  // epilogues that write per-tile column partial sums (their buffers are sized by GEMM_BM) and
+  // prefetch two input tiles, and, at BN = 256, those that prefetch one: at 128 rows their
+  // registers would spill.
+  const bool in0 = a.epi == EPI_GELU_BWD || a.epi == EPI_LN || a.epi == EPI_DX ||
+                   a.epi == EPI_RMS;
+  const bool wide = !(a.epi == EPI_LN_BWD || a.epi == EPI_RMS_BWD) && (BN <= 192 || !in0);
+  const int bm = wide ? 128 : GEMM_BM;
+  const int64_t mt = (a.M + bm - 1) / bm;
   const dim3 grid((unsigned)((mt + 7) / 8 * 8 * (a.N / BN)));
+  if (wide) {
+    switch (a.epi) {
+      case EPI_BIAS: k_gemm<BN, EPI_BIAS, 128><<<grid, 256, 0, s>>>(a); break;
+      case EPI_GELU_FWD: k_gemm<BN, EPI_GELU_FWD, 128><<<grid, 256, 0, s>>>(a); break;
+      case EPI_GELU_BWD: k_gemm<BN, EPI_GELU_BWD, 128><<<grid, 256, 0, s>>>(a); break;
+      case EPI_ITEM_QKV: k_gemm<BN, EPI_ITEM_QKV, 128><<<grid, 256, 0, s>>>(a); break;
+      case EPI_LN: k_gemm<BN, EPI_LN, 128><<<grid, 256, 0, s>>>(a); break;
+      case EPI_DX: k_gemm<BN, EPI_DX, 128><<<grid, 256, 0, s>>>(a); break;
+      case EPI_RMS: k_gemm<BN, EPI_RMS, 128><<<grid, 256, 0, s>>>(a); break;
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
   switch (a.epi) {
-    case EPI_BIAS: k_gemm<BN, EPI_BIAS><<<grid, 256, 0, s>>>(a); break;
-    case EPI_GELU_FWD: k_gemm<BN, EPI_GELU_FWD><<<grid, 256, 0, s>>>(a); break;
-    case EPI_GELU_BWD: k_gemm<BN, EPI_GELU_BWD><<<grid, 256, 0, s>>>(a); break;
-    case EPI_ITEM_QKV: k_gemm<BN, EPI_ITEM_QKV><<<grid, 256, 0, s>>>(a); break;
-    case EPI_LN: k_gemm<BN, EPI_LN><<<grid, 256, 0, s>>>(a); break;
-    case EPI_LN_BWD: k_gemm<BN, EPI_LN_BWD><<<grid, 256, 0, s>>>(a); break;
-    case EPI_DX: k_gemm<BN, EPI_DX><<<grid, 256, 0, s>>>(a); break;
-    case EPI_RMS: k_gemm<BN, EPI_RMS><<<grid, 256, 0, s>>>(a); break;
-    case EPI_RMS_BWD: k_gemm<BN, EPI_RMS_BWD><<<grid, 256, 0, s>>>(a); break;
+    case EPI_BIAS: k_gemm<BN, EPI_BIAS, GEMM_BM><<<grid, 256, 0, s>>>(a); break;
+    case EPI_GELU_FWD: k_gemm<BN, EPI_GELU_FWD, GEMM_BM><<<grid, 256, 0, s>>>(a); break;
+    case EPI_GELU_BWD: k_gemm<BN, EPI_GELU_BWD, GEMM_BM><<<grid, 256, 0, s>>>(a); break;
+    case EPI_ITEM_QKV: k_gemm<BN, EPI_ITEM_QKV, GEMM_BM><<<grid, 256, 0, s>>>(a); break;
+    case EPI_LN: k_gemm<BN, EPI_LN, GEMM_BM><<<grid, 256, 0, s>>>(a); break;
+    case EPI_LN_BWD: k_gemm<BN, EPI_LN_BWD, GEMM_BM><<<grid, 256, 0, s>>>(a); break;
+    case EPI_DX: k_gemm<BN, EPI_DX, GEMM_BM><<<grid, 256, 0, s>>>(a); break;
+    case EPI_RMS: k_gemm<BN, EPI_RMS, GEMM_BM><<<grid, 256, 0, s>>>(a); break;
+    case EPI_RMS_BWD: k_gemm<BN, EPI_RMS_BWD, GEMM_BM><<<grid, 256, 0, s>>>(a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -168,38 +168,46 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
       if (i < CPB) cur_init<XM>(cu[i], g, mb + ch / (BK / 8), me, k0 + (ch % (BK / 8)) * 8, a.ldx);
     }
   }
-  // one role branch around all of a thread's loads (not one per load), so that the other
-  // role's loads never precede them on any path
-  auto gload = [&](uint4* r, bool* okr) {
+  // One role branch around all of a thread's loads (not one per load), so that the other
+  // role's loads never precede them on any path; the zeroing of missing rows is deferred to
+  // the LDS store (okm: bit i set when chunk i of the slice exists).
+  static_assert(CPA == CPB, "square tiles: with unequal chunk counts the compiler merges the "
+                            "two role branches with non-constant indices (scratch arrays)");
+  auto gload = [&](uint4* r, uint32_t& okm) __attribute__((always_inline)) {
+    okm = 0u;
     if (opa) {
 #pragma unroll
       for (int i = 0; i < CPA; ++i) {
         const int ch = st + 256 * i;
-        r[i] = cur_load<YM>(cu[i], a.dY, a.dY2, a.dY3, &okr[i]);
+        bool ok;
+        r[i] = cur_load<YM>(cu[i], a.dY, a.dY2, a.dY3, &ok);
+        okm |= ok ? 1u << i : 0u;
         cur_advance<YM>(cu[i], g, a.ldy, n0 + (ch % (BN / 8)) * 8, cell0, ntrp, lo);
       }
     } else {
 #pragma unroll
       for (int i = 0; i < CPB; ++i) {
         const int ch = st + 256 * i;
-        r[i] = cur_load<XM>(cu[i], a.X, nullptr, nullptr, &okr[i]);
+        bool ok;
+        r[i] = cur_load<XM>(cu[i], a.X, nullptr, nullptr, &ok);
+        okm |= ok ? 1u << i : 0u;
         cur_advance<XM>(cu[i], g, a.ldx, k0 + (ch % (BK / 8)) * 8, cell0, ntrp, lo);
       }
     }
   };
   const uint4 z4 = make_uint4(0u, 0u, 0u, 0u);
-  auto sstore = [&](const uint4* r, const bool* okr, int b) {
+  auto sstore = [&](const uint4* r, uint32_t okm, int b) __attribute__((always_inline)) {
     if (opa) {
 #pragma unroll
       for (int i = 0; i < CPA; ++i) {
         const int ch = st + 256 * i;
-        stu4(&As[b][(ch / (BN / 8)) * LSA + (ch % (BN / 8)) * 8], okr[i] ? r[i] : z4);
+        stu4(&As[b][(ch / (BN / 8)) * LSA + (ch % (BN / 8)) * 8], (okm >> i) & 1u ? r[i] : z4);
       }
     } else {
 #pragma unroll
       for (int i = 0; i < CPB; ++i) {
         const int ch = st + 256 * i;
-        stu4(&Bs[b][(ch / (BK / 8)) * LSB + (ch % (BK / 8)) * 8], okr[i] ? r[i] : z4);
+        stu4(&Bs[b][(ch / (BK / 8)) * LSB + (ch % (BK / 8)) * 8], (okm >> i) & 1u ? r[i] : z4);
       }
     }
   };
@@ -217,7 +225,7 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
 #pragma unroll
   for (int i = 0; i < NBW; ++i) bacc[i] = 0.f;
 
-  auto compute = [&](int b) {
+  auto compute = [&](int b) __attribute__((always_inline)) {
     bf16x8 af[NBW], bfr[KBW];
 #pragma unroll
     for (int i = 0; i < NBW; ++i) af[i] = frag(As[b], LSA, wn * (BN / 2) + i * 16);
@@ -244,7 +252,7 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
   // flight are always the same ones.
   const int64_t steps = (me - mb + MS - 1) / MS;
   uint4 r0[CPM], r1[CPM];
-  bool ok0[CPM], ok1[CPM];
+  uint32_t ok0, ok1;
   gload(r0, ok0);
   gload(r1, ok1);
   sstore(r0, ok0, 0);
@@ -375,7 +383,9 @@ static hipError_t wgrad_modes(const WgradArgs& b, dim3 grid, hipStream_t s) {
 
 hipError_t launch_wgrad_mfma(const WgradArgs& a, hipStream_t s) {
   const int Z = wgrad_chunks(a.M);
-  const int BN = a.g.E, BK = a.g.E > 192 ? 128 : a.g.E;
+  // Square tiles (the two staging roles then move equal chunk counts); E = 256 takes 128 x 128
+  // tiles, whose accumulators fit the registers of a 512-thread workgroup.
+  const int BN = a.g.E > 192 ? 128 : a.g.E, BK = BN;
   if (a.N % BN || a.K % BK) return hipErrorInvalidValue;
   const dim3 grid((unsigned)(((int64_t)Z + 7) / 8 * 8 * (a.N / BN) * (a.K / BK)));
   WgradArgs b = a;
@@ -384,7 +394,6 @@ hipError_t launch_wgrad_mfma(const WgradArgs& a, hipStream_t s) {
     case 64: return wgrad_modes<64, 64>(b, grid, s);
     case 128: return wgrad_modes<128, 128>(b, grid, s);
     case 192: return wgrad_modes<192, 192>(b, grid, s);
-    case 256: return wgrad_modes<256, 128>(b, grid, s);
     default: return hipErrorInvalidValue;
   }
 }
