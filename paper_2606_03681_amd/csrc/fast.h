@@ -76,6 +76,9 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
 // Cells per block tile of the MFMA GEMM; EPI_LN_BWD writes one partial row per tile.
 constexpr int GEMM_BM = 64;
 inline int64_t gemm_row_tiles(int64_t M) { return (M + GEMM_BM - 1) / GEMM_BM; }
+// Row tiles of one launch of epilogue epi at column tile BN (the launch picks 64 or 128 rows);
+// never more than gemm_row_tiles(M).
+int64_t gemm_tiles(int epi, int BN, int64_t M);
 
 // bf16 copies of the six weight matrices of one layer, as stored ([out][in]) and transposed.
 // Offsets (elements) inside w / wt follow the packed parameter order of the weights:

@@ -229,6 +229,11 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   constexpr bool IN0 = EPI == EPI_GELU_BWD || EPI == EPI_DX || EPI == EPI_LN ||
                       EPI == EPI_LN_BWD || EPI == EPI_RMS || EPI == EPI_RMS_BWD;
   constexpr bool IN1 = EPI == EPI_LN_BWD || EPI == EPI_RMS_BWD;
+  // Input tiles are prefetched at 64 rows; at 128 rows the second one (and at BN = 256 the
+  // first too) is loaded when the main loop ends: prefetched, they would not fit in registers
+  // next to the accumulators.
+  constexpr bool IN0_PRE = IN0 && (BM == 64 || BN <= 192);
+  constexpr bool IN1_PRE = IN1 && BM == 64;
   uint4 pin0[IN0 ? NCH : 1], pin1[IN1 ? NCH : 1];
   if (IN0) {
     if (tid < BM) {
@@ -248,8 +253,8 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
       const int ch = tid + 256 * c;
       const int64_t off = rbase[ch / CPRW];
       const int cc = (ch % CPRW) * 8;
-      pin0[c] = off >= 0 ? ldu4(src0 + off + cc) : make_uint4(0, 0, 0, 0);
-      if (IN1) pin1[c] = off >= 0 ? ldu4(a.aux + off + cc) : make_uint4(0, 0, 0, 0);
+      if (IN0_PRE) pin0[c] = off >= 0 ? ldu4(src0 + off + cc) : make_uint4(0, 0, 0, 0);
+      if (IN1_PRE) pin1[c] = off >= 0 ? ldu4(a.aux + off + cc) : make_uint4(0, 0, 0, 0);
     }
   }
 
@@ -293,6 +298,17 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
       for (int j = 0; j < NB; ++j) acc[i][j] = mfma16(bfr[j], af[i], acc[i][j]);
   }
   lds_barrier();  // every wave is done with the ring before the epilogue tile reuses it
+  if ((IN0 && !IN0_PRE) || (IN1 && !IN1_PRE)) {
+    const bf16* src0 = EPI == EPI_GELU_BWD ? a.aux + n0 : a.resid;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int ch = tid + 256 * c;
+      const int64_t off = rbase[ch / CPRW];
+      const int cc = (ch % CPRW) * 8;
+      if (IN0 && !IN0_PRE) pin0[c] = off >= 0 ? ldu4(src0 + off + cc) : make_uint4(0, 0, 0, 0);
+      if (IN1 && !IN1_PRE) pin1[c] = off >= 0 ? ldu4(a.aux + off + cc) : make_uint4(0, 0, 0, 0);
+    }
+  }
 
   // ---- epilogues.  acc[i][j][q] is C[row, col] with
   //   row = m0 + wm*BM/2 + i*16 + lr,  col = n0 + wn*BN/2 + j*16 + lg*4 + q
@@ -644,12 +660,11 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
 template <int BN>
 static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
   // 128-row tiles (each weight tile staged through LDS serves twice the rows), except for the
-  // epilogues that write per-tile column partial sums (their buffers are sized by GEMM_BM) and
-  // prefetch two input tiles, and, at BN = 256, those that prefetch one: at 128 rows their
-  // registers would spill.
+  // two-input epilogues at BN = 256, which would spill.  gemm_tiles() gives the row-tile count
+  // (the partial-sum rows of LN_BWD / RMS_BWD).
   const bool in0 = a.epi == EPI_GELU_BWD || a.epi == EPI_LN || a.epi == EPI_DX ||
                    a.epi == EPI_RMS;
-  const bool wide = !(a.epi == EPI_LN_BWD || a.epi == EPI_RMS_BWD) && (BN <= 192 || !in0);
+  const bool wide = !(BN > 192 && (a.epi == EPI_LN_BWD || a.epi == EPI_RMS_BWD));
   const int bm = wide ? 128 : GEMM_BM;
   const int64_t mt = (a.M + bm - 1) / bm;
   const dim3 grid((unsigned)((mt + 7) / 8 * 8 * (a.N / BN)));
@@ -657,12 +672,19 @@ static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
     switch (a.epi) {
       case EPI_BIAS: k_gemm<BN, EPI_BIAS, 128><<<grid, 256, 0, s>>>(a); break;
       case EPI_GELU_FWD: k_gemm<BN, EPI_GELU_FWD, 128><<<grid, 256, 0, s>>>(a); break;
-      case EPI_GELU_BWD: k_gemm<BN, EPI_GELU_BWD, 128><<<grid, 256, 0, s>>>(a); break;
       case EPI_ITEM_QKV: k_gemm<BN, EPI_ITEM_QKV, 128><<<grid, 256, 0, s>>>(a); break;
+      case EPI_GELU_BWD: k_gemm<BN, EPI_GELU_BWD, 128><<<grid, 256, 0, s>>>(a); break;
       case EPI_LN: k_gemm<BN, EPI_LN, 128><<<grid, 256, 0, s>>>(a); break;
       case EPI_DX: k_gemm<BN, EPI_DX, 128><<<grid, 256, 0, s>>>(a); break;
       case EPI_RMS: k_gemm<BN, EPI_RMS, 128><<<grid, 256, 0, s>>>(a); break;
-      default: return hipErrorInvalidValue;
+      default:
+        if constexpr (BN <= 192) {
+          if (a.epi == EPI_LN_BWD) k_gemm<BN, EPI_LN_BWD, 128><<<grid, 256, 0, s>>>(a);
+          else if (a.epi == EPI_RMS_BWD) k_gemm<BN, EPI_RMS_BWD, 128><<<grid, 256, 0, s>>>(a);
+          else return hipErrorInvalidValue;
+        } else {
+          return hipErrorInvalidValue;
+        }
     }
     return hipGetLastError();
   }
@@ -679,6 +701,11 @@ static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+int64_t gemm_tiles(int epi, int BN, int64_t M) {
+  const int bm = BN > 192 && (epi == EPI_LN_BWD || epi == EPI_RMS_BWD) ? GEMM_BM : 128;
+  return (M + bm - 1) / bm;
 }
 
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {

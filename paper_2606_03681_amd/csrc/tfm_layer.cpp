@@ -625,7 +625,7 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   const FastWs f = fast_ws(d, ws, W);
   const int E = d.E, H = d.H;
   const int64_t N = g.N;
-  const int tiles = (int)tfm::gemm_row_tiles(N);
+  const int tiles = (int)tfm::gemm_tiles(tfm::EPI_LN_BWD, E, N);
   FastGrads G{f, g, grads, accumulate, s};
   STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, s));
   T* dz3 = (T*)(ws + W.tb);
@@ -779,7 +779,7 @@ int bwd_pre(const Dims& d, const tfm::Geo& g, const float* prm, const char* sv,
   const FastWs f = fast_ws(d, ws, W);
   const int E = d.E, H = d.H;
   const int64_t N = g.N;
-  const int tiles = (int)tfm::gemm_row_tiles(N);
+  const int tiles = (int)tfm::gemm_tiles(tfm::EPI_RMS_BWD, E, N);
   FastGrads G{f, g, grads, accumulate, s};
   STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, s));
   T* dyc = (T*)(ws + W.tb);    // dY, compact
