@@ -241,7 +241,8 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
       int64_t off = -1;
       if (m < a.M) {
         if (EPI == EPI_GELU_BWD) off = m * a.ldo;
-        else if (EPI == EPI_LN || EPI == EPI_RMS) off = row_addr(g, a.rmode, m, BN);
+        else if (EPI == EPI_LN || EPI == EPI_RMS || EPI == EPI_RMS_BWD)
+          off = row_addr(g, a.rmode, m, BN);
         else off = m * BN;
       }
       rbase[tid] = off;
@@ -254,7 +255,11 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
       const int64_t off = rbase[ch / CPRW];
       const int cc = (ch % CPRW) * 8;
       if (IN0_PRE) pin0[c] = off >= 0 ? ldu4(src0 + off + cc) : make_uint4(0, 0, 0, 0);
-      if (IN1_PRE) pin1[c] = off >= 0 ? ldu4(a.aux + off + cc) : make_uint4(0, 0, 0, 0);
+      // The second input is always compact rows (x-hat, or h).  Rows past M read row M - 1
+      // instead of zeros (no select on the loaded value): their accumulators and first input
+      // are zero, so they add nothing to the column sums and are never stored.
+      const int64_t m1 = m0 + ch / CPRW < a.M ? m0 + ch / CPRW : a.M - 1;
+      if (IN1_PRE) pin1[c] = ldu4(a.aux + m1 * BN + cc);
     }
   }
 
@@ -306,7 +311,8 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
       const int64_t off = rbase[ch / CPRW];
       const int cc = (ch % CPRW) * 8;
       if (IN0 && !IN0_PRE) pin0[c] = off >= 0 ? ldu4(src0 + off + cc) : make_uint4(0, 0, 0, 0);
-      if (IN1 && !IN1_PRE) pin1[c] = off >= 0 ? ldu4(a.aux + off + cc) : make_uint4(0, 0, 0, 0);
+      const int64_t m1 = m0 + ch / CPRW < a.M ? m0 + ch / CPRW : a.M - 1;  // (as above)
+      if (IN1 && !IN1_PRE) pin1[c] = ldu4(a.aux + m1 * BN + cc);
     }
   }
 

@@ -601,11 +601,13 @@ struct FastGrads {
   float* grads;
   int accumulate;
   hipStream_t s;
+  // ymode: layout of dY (compact, native; head-major item gradients when dY2 is given)
   int run(const tfm::bf16* dY, int N, const tfm::bf16* X, int K, int xmode, size_t offW,
-          size_t offb, const tfm::bf16* dY2 = nullptr, const tfm::bf16* dY3 = nullptr) {
+          size_t offb, const tfm::bf16* dY2 = nullptr, const tfm::bf16* dY3 = nullptr,
+          int ymode = tfm::ROWS_COMPACT) {
     tfm::WgradArgs a{};
     a.M = g.N; a.N = N; a.K = K; a.dY = dY; a.ldy = N; a.X = X; a.ldx = K; a.xmode = xmode;
-    a.dY2 = dY2; a.dY3 = dY3; a.ymode = dY2 ? tfm::ROWS_ITEM_HM : tfm::ROWS_COMPACT;
+    a.dY2 = dY2; a.dY3 = dY3; a.ymode = dY2 ? tfm::ROWS_ITEM_HM : ymode;
     a.part = f.wpart; a.bpart = f.bpart; a.g = g;
     const int Z = tfm::wgrad_chunks(g.N);
     STEP("wgrad/mfma", tfm::launch_wgrad_mfma(a, s));
@@ -782,22 +784,23 @@ int bwd_pre(const Dims& d, const tfm::Geo& g, const float* prm, const char* sv,
   const int tiles = (int)tfm::gemm_tiles(tfm::EPI_RMS_BWD, E, N);
   FastGrads G{f, g, grads, accumulate, s};
   STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, s));
-  T* dyc = (T*)(ws + W.tb);    // dY, compact
   T* dh2 = (T*)(ws + W.te);
   T* dh1 = (T*)(ws + W.tf);
   T* dgb = (T*)(ws + W.th1);
   T* dqkv = (T*)(ws + W.tqkv);
-  STEP("gather/hbm", launch_gather<T>(g, dY, dyc, s));
+  // dY is read in its native layout by the three steps that need it (no compact copy)
   // dG = (dY W2) * GELU'(G)
   GemmArgs a = gemm_base(g, N, H, E, EPI_GELU_BWD);
-  a.A = dyc; a.lda = E; a.Bt = f.wt + f.wo.w2; a.out = dgb; a.ldo = H;
+  a.A = dY; a.amode = ROWS_NATIVE; a.lda = E; a.Bt = f.wt + f.wo.w2; a.out = dgb; a.ldo = H;
   a.aux = (const T*)(sv + S.g);
   STEP("mlp_down_dx/mfma", launch_gemm(a, s));
-  CHK(G.run(dyc, E, (const T*)(sv + S.u), H, ROWS_COMPACT, o.W2, o.b2));
+  CHK(G.run(dY, E, (const T*)(sv + S.u), H, ROWS_COMPACT, o.W2, o.b2, nullptr, nullptr,
+            ROWS_NATIVE));
   CHK(G.run(dgb, H, (const T*)(sv + S.r3), E, ROWS_COMPACT, o.W1, o.b1));
   // dh2 = dY + RMS3'(dG W1)
   a = gemm_base(g, N, E, H, EPI_RMS_BWD);
-  a.A = dgb; a.lda = H; a.Bt = f.wt + f.wo.w1; a.resid = dyc; a.aux = (const T*)(sv + S.h2);
+  a.A = dgb; a.lda = H; a.Bt = f.wt + f.wo.w1; a.resid = dY; a.rmode = ROWS_NATIVE;
+  a.aux = (const T*)(sv + S.h2);
   a.rstd_in = (const float*)(sv + S.rs3); a.gamma = prm + o.g3; a.eps = kRmsEps;
   a.oscale = 1.0f; a.omode = ROWS_COMPACT; a.out = dh2; a.part = f.lnpart;
   STEP("mlp_up_dx_rms3/mfma", launch_gemm(a, s));

@@ -104,7 +104,7 @@ __device__ __forceinline__ void cur_advance(Cursor& c, const Geo& g, int64_t ld,
 }  // namespace
 
 // 512 threads = 8 waves in a 2 (n) x 4 (k) arrangement; tile BN x BK.  dY is in layout YM
-// (compact or head-major item gradients), X in layout XM (compact or native).  TBL: the
+// (compact, native or head-major item gradients), X in layout XM (compact or native).  TBL: the
 // workgroup copies the metadata of the columns its chunk spans into LDS (requires R >= MS, so
 // that a chunk spans at most WGRAD_CHUNK / MS + 1 columns).
 template <int BN, int BK, int YM, int XM, bool TBL>
@@ -363,10 +363,15 @@ int wgrad_chunks(int64_t M) {
 template <int BN, int BK>
 static hipError_t wgrad_modes(const WgradArgs& b, dim3 grid, hipStream_t s) {
   const bool yhm = b.ymode == ROWS_ITEM_HM, xnat = b.xmode == ROWS_NATIVE;
-  if (b.ymode != ROWS_COMPACT && !yhm) return hipErrorInvalidValue;
+  const bool ynat = b.ymode == ROWS_NATIVE;
+  if (b.ymode != ROWS_COMPACT && !yhm && !ynat) return hipErrorInvalidValue;
   if (b.xmode != ROWS_COMPACT && !xnat) return hipErrorInvalidValue;
+  if (ynat && xnat) return hipErrorInvalidValue;
   const bool tbl = b.g.R >= MS;
-  if (yhm && xnat) {
+  if (ynat) {
+    if (tbl) k_wgrad<BN, BK, ROWS_NATIVE, ROWS_COMPACT, true><<<grid, 512, 0, s>>>(b);
+    else k_wgrad<BN, BK, ROWS_NATIVE, ROWS_COMPACT, false><<<grid, 512, 0, s>>>(b);
+  } else if (yhm && xnat) {
     if (tbl) k_wgrad<BN, BK, ROWS_ITEM_HM, ROWS_NATIVE, true><<<grid, 512, 0, s>>>(b);
     else k_wgrad<BN, BK, ROWS_ITEM_HM, ROWS_NATIVE, false><<<grid, 512, 0, s>>>(b);
   } else if (yhm) {
