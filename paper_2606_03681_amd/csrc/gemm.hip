@@ -100,7 +100,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
   constexpr int NBA = BM / 64;         // 1 KB blocks of A per wave and stage
   constexpr int NB = BN / 32;          // 16-wide column blocks per wave
   constexpr int TS = BN + 8;           // epilogue tile row stride (elements)
-  constexpr int S = 3;  // pipeline stages in the LDS ring (48 KB at E = 192: 3 workgroups per CU)
+  constexpr int S = 3;  // pipeline stages in the LDS ring (60 KB at E = 192 and 128 rows: 2 workgroups per CU)
   constexpr int A_EL = BM * BK;        // elements of one stage's A rows
   constexpr int STAGE_EL = (BM + BN) * BK;
   constexpr int NBB = BN / 64;         // 1 KB blocks of B per wave and stage

@@ -115,3 +115,28 @@ def test_query_rows_independent_of_each_other():
                                          "bf16")), "bf16")
     torch.cuda.synchronize()
     assert np.array_equal(a[:, 10:11], one)
+
+
+@pytest.mark.parametrize("cfg", [2, "record9-bf16"])
+def test_full_size_forward_only_matches_training_forward(cfg):
+    """The benchmark's forward-only configuration at full size (context = the longest train
+    prefix, the remaining rows as query chunks of 128 and a ragged tail): bit-identical to the
+    training forward, whose outputs the full-size sampled-row parity test checks against the
+    oracle."""
+    import torch
+    from paper_2606_03681_amd.stack import InferStack, to_device
+    w = wl.make_workload(cfg)
+    R = w.cfg["R"]
+    Rc = int(np.max(w.n_train))
+    _say(f"[infer-full] {w.cfg['name']} Rc={Rc}")
+    full = _train_forward(w, w.X, w.n_train)
+    inf = InferStack(_dims(w, Rc), w.n_train, w.cell_mask, w.params, max_query_rows=128)
+    got = [storage_of(inf.context(to_device(np.ascontiguousarray(w.X[:, :Rc]), "bf16")), "bf16")]
+    for a in range(Rc, R, 128):
+        b = min(a + 128, R) if a + 128 < R else R
+        got.append(storage_of(inf.query(to_device(np.ascontiguousarray(w.X[:, a:b]), "bf16")),
+                              "bf16"))
+    torch.cuda.synchronize()
+    got = np.concatenate(got, axis=1)
+    for b in range(got.shape[0]):
+        assert np.array_equal(got[b], full[b]), f"dataset {b}"
