@@ -108,8 +108,9 @@ TEST_CONFIGS = {
 # Workloads of the widened scope (not parity configurations of the baseline block).
 #   record9-bf16: the current best record's block (Tab. 7): pre-norm RMSNorm, residual decay,
 #   E = 256 with 4 heads of 64, MLP 768, 5 blocks; 1000 data rows plus 24 thinking rows
-#   prepended as train rows (750 labelled data rows); 100 features in groups of 5 give 20 cells
-#   plus the target cell per row.
+#   prepended as train rows (750 labelled data rows); 20 features, the most the pretraining
+#   prior draws (Sec. 4.1), and repeated grouping makes one group of 5 per feature column, so
+#   20 feature cells plus the target cell per row.
 EXTRA_CONFIGS = {
     "record9-bf16": dict(name="record9-bf16", dtype="bf16", B=16, R=1024, n_train=774, C=20,
                          E=256, heads=4, H=768, layers=5, cells="normal", weights="xavier",
