@@ -24,6 +24,8 @@ from paper_2606_03681_amd import workloads as wl  # noqa: E402
 
 METRIC = "two-axis layer fwd+bwd cells/sec (bf16) + % MFMA peak, 1x MI355X"
 METRIC_INFER = "two-axis layer forward-only (context + query chunks) cells/sec (bf16), 1x MI355X"
+METRIC_STEP = ("full training step (encoders, stack fwd+bwd, decoder and loss) cells/sec (bf16), "
+               "1x MI355X")
 PEAK_TFLOPS = {"mfma_bf16": 2516.6, "mfma_f32": 157.3, "alu_f32": 157.3}
 HBM_PEAK_GBS = 8000.0
 
@@ -136,6 +138,10 @@ def main():
                          "remaining rows as query chunks through every layer")
     ap.add_argument("--query-chunk", type=int, default=0,
                     help="rows per query chunk of --infer (0: all remaining rows at once)")
+    ap.add_argument("--full-step", action="store_true",
+                    help="time a whole training step instead: encoders (and thinking rows), the "
+                         "stack forward and backward, the decoder with the loss, and the "
+                         "encoders' gradients, from feature values and labels in HBM")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run 5 device-to-device copies of MIB MiB (the known-size copy "
                          "that scales the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -167,7 +173,11 @@ def main():
     cfg = wl.get_config(args.config)
     seed = wl.default_seed(cfg) if args.seed is None else args.seed
     print(f"[bench] generating {cfg['name']} seed={seed}", file=sys.stderr, flush=True)
-    w = wl.make_workload(args.config, seed=seed)
+    w = wl.make_workload(args.config, seed=seed, with_dY=not args.full_step)
+    ends_in = None
+    if args.full_step:
+        ends_in = wl.make_ends_inputs(w)
+        w.cell_mask = ends_in.cell_mask
     counts = wl.work_counts(w.n_train, w.cell_mask, cfg["R"], cfg["E"], cfg["H"], cfg["layers"])
     dims = tfm.make_dims(dtype=w.dtype, block=w.block,
                          **{k: v for k, v in w.dims.items() if k != "dtype"})
@@ -191,6 +201,17 @@ def main():
             st.context(Xc)
             for x in Xq:
                 st.query(x)
+    elif args.full_step:
+        from paper_2606_03681_amd.stack import TrainStep
+        e = ends_in
+        ends = tfm.make_ends(e.G, e.offsets, e.F, e.T, e.Hd, e.K, e.mean)
+        st = TrainStep(dims, ends, w.n_train, e.n_feat, e.n_class, w.params, e.params, e.table)
+        X = torch.from_numpy(e.x).cuda()
+        dY = torch.from_numpy(e.labels).cuda()
+        del w.X
+
+        def step():
+            st.run(X, dY)
     else:
         st = Stack(dims, w.n_train, w.cell_mask, w.params)
         X = to_device(w.X, w.dtype)
@@ -257,7 +278,8 @@ def main():
                     "flops_per_launch": f, "avg_launch_ms": round(ms / n, 5)}
 
     out = {
-        "metric": METRIC_INFER if args.infer else METRIC, "value": round(value, 1),
+        "metric": METRIC_INFER if args.infer else (METRIC_STEP if args.full_step else METRIC),
+        "value": round(value, 1),
         "unit": "cells/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
@@ -267,7 +289,8 @@ def main():
                    "heads": cfg["heads"], "H": cfg["H"], "layers": cfg["layers"],
                    "block": cfg.get("block", "post"), "thinking_rows": cfg.get("thinking", 0),
                    "seed": seed, "active_cell_layers": counts["cell_layers"]},
-        "mode": "forward-only" if args.infer else "forward+backward",
+        "mode": "forward-only" if args.infer else (
+            "training step" if args.full_step else "forward+backward"),
         "tflops": round(tflops, 3), "mfma_peak_frac": round(tflops / peak, 5),
         "wall_ms_per_step": round(wall * 1e3 / args.steps, 4),
         "roofline": roof, "steps_profile": steps_out, "git": git_rev(),
@@ -275,6 +298,14 @@ def main():
     }
     if args.infer:
         out["config"].update(context_rows=Rc, query_chunks=[b - a for a, b in spans])
+    if args.full_step:
+        e = ends_in
+        out["config"].update(group_size=e.G, group_shifts=list(e.offsets), decoder_hidden=e.Hd,
+                             classes=e.K, decoder_input="feature mean" if e.mean else "target")
+        out["loss"] = float(st.loss[0].item())
+        out["ends_ms_per_step"] = round(sum(
+            v["avg_ms"] * v["launches"] for k, v in steps_out.items()
+            if k.startswith(("encode_", "dec_"))) / args.steps, 4) if steps_out else None
     del st, X, dY
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:

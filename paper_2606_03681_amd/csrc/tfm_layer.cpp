@@ -986,6 +986,14 @@ int infer_call(const tfm_dims* dims, int ctx_rows, const int32_t* n_train,
 }  // namespace
 
 // ============================================================================ C ABI
+namespace tfm {
+int abi_fail(int code, const char* msg) { return fail(code, "%s", msg); }
+int abi_check_dims(const void* dims) {
+  Dims d;
+  return check_dims((const tfm_dims*)dims, d);
+}
+}  // namespace tfm
+
 extern "C" {
 
 size_t tfm_layer_param_count(const tfm_dims* dims) {

@@ -154,3 +154,62 @@ class InferStack:
                                 self.params[l], self.caches[l], out, self.workspace)
             h = out
         return h
+
+
+class TrainStep:
+    """One training step through the whole model: the encoders build the stack input (and the
+    thinking-row table fills its first T rows), the stack runs forward, the decoder computes the
+    loss and the gradient of the stack output, the stack runs backward and the encoders (and the
+    table) receive their gradients.  Allocation and call order only."""
+
+    def __init__(self, dims, ends, n_train, n_feat, n_class, params, ends_params, table=None,
+                 device="cuda", decay_base=0.95):
+        self.dims, self.ends = dims, ends
+        self.n_train = np.ascontiguousarray(n_train, dtype=np.int32)
+        self.n_feat = np.ascontiguousarray(n_feat, dtype=np.int32)
+        self.n_class = np.ascontiguousarray(n_class, dtype=np.int32)
+        C = dims.C
+        self.cell_mask = np.zeros((dims.B, C + 1), np.uint8)
+        for b, m in enumerate(self.n_feat):
+            self.cell_mask[b, :m] = 1
+        self.cell_mask[:, C] = 1
+        self.stack = Stack(dims, self.n_train, self.cell_mask, params, device=device,
+                           decay_base=decay_base)
+        self.ends_params = ends_params if isinstance(ends_params, torch.Tensor) else \
+            torch.from_numpy(np.ascontiguousarray(ends_params, dtype=np.float32)).to(device)
+        self.T = ends.T
+        self.table = None
+        if self.T:
+            self.table = table if isinstance(table, torch.Tensor) else \
+                torch.from_numpy(np.ascontiguousarray(table, dtype=np.float32)).to(device)
+            self.table_grad = torch.empty_like(self.table)
+        wb = tfm.ends_workspace_bytes(dims, ends)
+        if wb == 0:
+            raise tfm.TfmError(-1, tfm.last_error())
+        self.ends_ws = torch.empty(wb, dtype=torch.uint8, device=device)
+        self.X = torch.empty(self.stack.shape, dtype=self.stack.elt, device=device)
+        self.dY = torch.empty(self.stack.shape, dtype=self.stack.elt, device=device)
+        self.loss = torch.empty(4, dtype=torch.float32, device=device)
+        self.ends_grads = torch.empty_like(self.ends_params)
+        self.Y = self.dX = None
+
+    def run(self, x, labels):
+        """x: device float32 [B, R-T, F]; labels: device int32 [B, R-T].  Returns the loss as a
+        device tensor of one element; gradients land in stack.grads, ends_grads, table_grad."""
+        d, e = self.dims, self.ends
+        if self.T:
+            tfm.thinking_rows_fwd(d, self.n_train, self.cell_mask, self.T, self.table, self.X,
+                                  self.stack.workspace)
+        tfm.encode_fwd(d, e, self.n_train, self.n_feat, x, labels, self.ends_params, self.X,
+                       self.ends_ws)
+        self.Y = self.stack.forward(self.X)
+        tfm.decode_loss(d, e, self.n_train, self.n_feat, self.n_class, labels, self.Y,
+                        self.ends_params, self.loss, None, self.dY, self.ends_grads, False,
+                        self.ends_ws)
+        self.dX = self.stack.backward(self.dY)
+        if self.T:
+            tfm.thinking_rows_bwd(d, self.n_train, self.cell_mask, self.T, self.dX,
+                                  self.table_grad, False, self.stack.workspace)
+        tfm.encode_bwd(d, e, self.n_train, self.n_feat, x, labels, self.dX, self.ends_grads,
+                       False, self.ends_ws)
+        return self.loss[:1]

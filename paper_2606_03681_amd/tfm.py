@@ -1,4 +1,4 @@
-"""Thin ctypes binding of libtfmlayer.so (C ABI in include/tfm_layer.h).
+"""Thin ctypes binding of libtfmlayer.so (C ABI in include/tfm_layer.h and include/tfm_ends.h).
 
 Argument marshalling only: every step of the layer runs in the library's HIP kernels.  torch
 supplies device memory and the stream.  There is no fallback: if the library is missing, every
@@ -23,7 +23,8 @@ EXPORTS = ("tfm_layer_param_count", "tfm_layer_saved_bytes", "tfm_layer_workspac
            "tfm_layer_fwd", "tfm_layer_bwd", "tfm_thinking_rows_fwd", "tfm_thinking_rows_bwd",
            "tfm_infer_workspace_bytes", "tfm_infer_cache_bytes", "tfm_layer_fwd_context",
            "tfm_layer_fwd_query", "tfm_last_error", "tfm_prof_enable", "tfm_prof_collect",
-           "tfm_prof_step")
+           "tfm_prof_step", "tfm_ends_param_count", "tfm_ends_workspace_bytes", "tfm_encode_fwd",
+           "tfm_encode_bwd", "tfm_decode_fwd", "tfm_decode_loss")
 
 
 class TfmError(RuntimeError):
@@ -42,6 +43,19 @@ def make_dims(B, R, C, E, heads, H, dtype, block="post", decay=1.0):
     bk = {"post": TFM_BLOCK_POSTNORM, "pre": TFM_BLOCK_PRENORM}.get(block, block)
     return tfm_dims(int(B), int(R), int(C), int(E), int(heads), int(H), int(dt), int(bk),
                     float(decay))
+
+
+class tfm_ends(ctypes.Structure):
+    _fields_ = [("G", ctypes.c_int32), ("offsets", ctypes.c_int32 * 8)] + \
+        [(n, ctypes.c_int32) for n in ("F", "T", "Hd", "K", "decode_mean")]
+
+
+def make_ends(G, offsets, F, T, Hd, K, decode_mean):
+    offs = list(offsets)
+    if len(offs) != G or G > 8:
+        raise ValueError(f"need G = {G} <= 8 offsets, got {offs}")
+    arr = (ctypes.c_int32 * 8)(*(offs + [0] * (8 - len(offs))))
+    return tfm_ends(int(G), arr, int(F), int(T), int(Hd), int(K), int(bool(decode_mean)))
 
 
 def lib():
@@ -75,6 +89,19 @@ def lib():
         L.tfm_layer_fwd_query.restype = i32
         L.tfm_layer_fwd_query.argtypes = [P(tfm_dims), i32, vp, vp, vp, vp, vp, sz, vp, vp, sz,
                                           vp]
+        E_ = P(tfm_ends)
+        for name in ("tfm_ends_param_count", "tfm_ends_workspace_bytes"):
+            getattr(L, name).restype = sz
+            getattr(L, name).argtypes = [P(tfm_dims), E_]
+        L.tfm_encode_fwd.restype = i32
+        L.tfm_encode_fwd.argtypes = [P(tfm_dims), E_, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.tfm_encode_bwd.restype = i32
+        L.tfm_encode_bwd.argtypes = [P(tfm_dims), E_, vp, vp, vp, vp, vp, vp, i32, vp, sz, vp]
+        L.tfm_decode_fwd.restype = i32
+        L.tfm_decode_fwd.argtypes = [P(tfm_dims), E_, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.tfm_decode_loss.restype = i32
+        L.tfm_decode_loss.argtypes = [P(tfm_dims), E_, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                      i32, vp, sz, vp]
         L.tfm_prof_enable.restype = i32
         L.tfm_prof_enable.argtypes = [i32]
         L.tfm_prof_collect.restype = i32
@@ -209,6 +236,61 @@ def layer_fwd_query(dims, context_rows, n_train, cell_mask, X, params, kv_cache,
     rc = lib().tfm_layer_fwd_query(ctypes.byref(dims), int(context_rows), ntp, cmp_, _ptr(X),
                                    _ptr(params), _ptr(kv_cache), _nbytes(kv_cache), _ptr(Y),
                                    _ptr(workspace), _nbytes(workspace), _stream(stream))
+    _check(rc)
+
+
+def ends_param_count(dims, ends):
+    return lib().tfm_ends_param_count(ctypes.byref(dims), ctypes.byref(ends))
+
+
+def ends_workspace_bytes(dims, ends):
+    return lib().tfm_ends_workspace_bytes(ctypes.byref(dims), ctypes.byref(ends))
+
+
+def encode_fwd(dims, ends, n_train, n_feat, x, labels, params, X, workspace, stream=None):
+    """tfm_encode_fwd.  n_train, n_feat: host int32 [B]; x: device float32 [B, R-T, F];
+    labels: device int32 [B, R-T]; params: device float32 packed ends vector; X: device
+    [B, R, C+1, E] (rows [T, R) written)."""
+    nt, ntp = _host(n_train, np.int32)
+    nf, nfp = _host(n_feat, np.int32)
+    rc = lib().tfm_encode_fwd(ctypes.byref(dims), ctypes.byref(ends), ntp, nfp, _ptr(x),
+                              _ptr(labels), _ptr(params), _ptr(X), _ptr(workspace),
+                              _nbytes(workspace), _stream(stream))
+    _check(rc)
+
+
+def encode_bwd(dims, ends, n_train, n_feat, x, labels, dX, grads, accumulate, workspace,
+               stream=None):
+    """tfm_encode_bwd: the encoder entries of grads from dX (device [B, R, C+1, E])."""
+    nt, ntp = _host(n_train, np.int32)
+    nf, nfp = _host(n_feat, np.int32)
+    rc = lib().tfm_encode_bwd(ctypes.byref(dims), ctypes.byref(ends), ntp, nfp, _ptr(x),
+                              _ptr(labels), _ptr(dX), _ptr(grads), int(bool(accumulate)),
+                              _ptr(workspace), _nbytes(workspace), _stream(stream))
+    _check(rc)
+
+
+def decode_fwd(dims, ends, n_train, n_feat, Y, params, logits, workspace, stream=None):
+    """tfm_decode_fwd: logits (device float32 [T_test, K]) of the unlabelled rows of Y."""
+    nt, ntp = _host(n_train, np.int32)
+    nf, nfp = _host(n_feat, np.int32)
+    rc = lib().tfm_decode_fwd(ctypes.byref(dims), ctypes.byref(ends), ntp, nfp, _ptr(Y),
+                              _ptr(params), _ptr(logits), _ptr(workspace), _nbytes(workspace),
+                              _stream(stream))
+    _check(rc)
+
+
+def decode_loss(dims, ends, n_train, n_feat, n_class, labels, Y, params, loss, logits, dY, grads,
+                accumulate, workspace, stream=None):
+    """tfm_decode_loss: loss (device float32 [1]), logits (device float32 [T_test, K] or None),
+    dY (device like Y) and the decoder entries of grads."""
+    nt, ntp = _host(n_train, np.int32)
+    nf, nfp = _host(n_feat, np.int32)
+    nc, ncp = _host(n_class, np.int32)
+    rc = lib().tfm_decode_loss(ctypes.byref(dims), ctypes.byref(ends), ntp, nfp, ncp,
+                               _ptr(labels), _ptr(Y), _ptr(params), _ptr(loss), _ptr(logits),
+                               _ptr(dY), _ptr(grads), int(bool(accumulate)), _ptr(workspace),
+                               _nbytes(workspace), _stream(stream))
     _check(rc)
 
 

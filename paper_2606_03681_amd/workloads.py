@@ -346,3 +346,95 @@ def work_counts(n_train, cell_mask, R, E, H, layers):
         flops += forward_flops(R, E, H, int(n_train[b]), S)
     return dict(cell_layers=cells * layers, flops_fwd_bwd=3 * flops * layers,
                 active_cells=cells)
+
+
+# ---------------------------------------------------------------------------------------------
+# Inputs of the stack's two ends (encoders, decoder, loss) for a full training step
+# ---------------------------------------------------------------------------------------------
+
+@dataclass
+class EndsInputs:
+    G: int                        # feature group size
+    offsets: tuple                # group shifts
+    F: int                        # columns per row of x
+    T: int                        # thinking rows at the head of the stack input
+    Hd: int                       # decoder hidden width
+    K: int                        # decoder outputs
+    mean: bool                    # decoder input: mean of the feature cells (else target cell)
+    n_feat: np.ndarray            # int32 [B']
+    n_class: np.ndarray           # int32 [B']
+    cell_mask: np.ndarray         # uint8 [B', C+1]: feature cells [0, n_feat) and the target
+    x: np.ndarray                 # float32 [B', R-T, F]
+    labels: np.ndarray            # int32 [B', R-T]
+    params: np.ndarray            # float32 packed ends vector
+    table: np.ndarray = None      # float32 [T, E] thinking rows, or None
+
+
+# Group shifts: (0, 1, 3) as the paper gives for groups of 3; for groups of 5 the paper gives
+# none, and (0, 1, 3, 7, 12) keeps all pairwise differences distinct.
+GROUP_SHIFTS = {1: (0,), 3: (0, 1, 3), 5: (0, 1, 3, 7, 12)}
+
+
+def ends_param_layout(E, G, Hd, K):
+    """(name, shape, fan_in, fan_out) in the packed order of the C-ABI (include/tfm_ends.h)."""
+    return [("W_fe", (E, G), G, E), ("b_fe", (E,), 0, 0), ("W_te", (E,), 1, E),
+            ("b_te", (E,), 0, 0), ("W_d1", (Hd, E), E, Hd), ("b_d1", (Hd,), 0, 0),
+            ("W_d2", (K, Hd), Hd, K), ("b_d2", (K,), 0, 0)]
+
+
+def _is_prefix_mask(mask_row):
+    C = len(mask_row) - 1
+    m = int(np.count_nonzero(mask_row[:C]))
+    return m >= 1 and bool(np.all(mask_row[:m])) and mask_row[C] == 1
+
+
+def make_ends_inputs(w, seed=None, G=None, mean=None, K=10, Hd=None, bias_scale=0.2,
+                     n_class=None):
+    """Draw the ends' inputs for workload w: feature values x ~ N(0, 1), labels uniform over each
+    dataset's classes (2..K unless n_class is given), Xavier-uniform weights, N(0, bias_scale^2)
+    biases, a N(0, 1) thinking-row table.  Defaults follow the block: the post-norm baseline
+    encodes single features and decodes the target cell; the pre-norm record groups 5 features
+    and decodes the feature mean (Tab. 7).  The feature count of a dataset is its workload's
+    when the workload's mask is a prefix mask, else drawn from [1, C]."""
+    cfg = w.cfg
+    pre = cfg.get("block", "post") == "pre"
+    G = (5 if pre else 1) if G is None else G
+    mean = pre if mean is None else mean
+    Hd = cfg["H"] if Hd is None else Hd
+    T = cfg.get("thinking", 0)
+    B_all, R, C, E = cfg["B"], cfg["R"], cfg["C"], cfg["E"]
+    seed = (w.seed + 7919) if seed is None else seed
+    kids = np.random.SeedSequence(seed).spawn(2 + B_all)
+    meta = np.random.default_rng(kids[0])
+    nc_all = (meta.integers(2, K + 1, size=B_all) if n_class is None
+              else np.broadcast_to(np.asarray(n_class), (B_all,)).copy())
+    nf_draw = meta.integers(1, C + 1, size=B_all)
+    table = meta.normal(0.0, 1.0, (T, E)).astype(np.float32) if T else None
+    prng = np.random.default_rng(kids[1])
+    parts = []
+    for _, shape, fi, fo in ends_param_layout(E, G, Hd, K):
+        n = int(np.prod(shape))
+        if fi:
+            a = np.sqrt(6.0 / (fi + fo))
+            parts.append(prng.uniform(-a, a, n))
+        else:
+            parts.append(prng.normal(0.0, bias_scale, n))
+    params = np.concatenate(parts).astype(np.float32)
+    ds = w.datasets
+    B = len(ds)
+    n_feat = np.empty(B, np.int32)
+    mask = np.zeros((B, C + 1), np.uint8)
+    xs, labs = [], []
+    for i, b in enumerate(ds):
+        m = (int(np.count_nonzero(w.cell_mask[i][:C])) if _is_prefix_mask(w.cell_mask[i])
+             else int(nf_draw[b]))
+        n_feat[i] = m
+        mask[i, :m] = 1
+        mask[i, C] = 1
+        r = np.random.default_rng(kids[2 + b])
+        xs.append(r.normal(0.0, 1.0, (R - T, C)).astype(np.float32))
+        labs.append(r.integers(0, nc_all[b], R - T).astype(np.int32))
+    return EndsInputs(G=G, offsets=GROUP_SHIFTS.get(G, tuple(range(G))), F=C, T=T, Hd=Hd, K=K,
+                      mean=bool(mean), n_feat=n_feat, n_class=nc_all[ds].astype(np.int32),
+                      cell_mask=mask, x=np.stack(xs), labels=np.stack(labs), params=params,
+                      table=table)

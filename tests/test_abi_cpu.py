@@ -192,3 +192,98 @@ def test_forward_only_arguments_rejected_before_launch():
     bad = mask.copy()
     bad[1, 8] = 0
     assert _qry(q, 32, [20, 32], bad) == -4
+
+
+# ---- the stack's two ends (include/tfm_ends.h) -------------------------------------------------
+
+def _ends(**kw):
+    base = dict(G=5, offsets=(0, 1, 3, 7, 12), F=8, T=0, Hd=96, K=10, decode_mean=1)
+    base.update(kw)
+    return tfm.make_ends(**base)
+
+
+def test_ends_param_count_and_workspace():
+    d = _dims(E=64)
+    e = _ends()
+    assert tfm.ends_param_count(d, e) == 64 * 5 + 3 * 64 + 96 * 64 + 96 + 10 * 96 + 10
+    wb = tfm.ends_workspace_bytes(d, e)
+    assert wb > 0
+    # more rows, more decoder rows to hold
+    assert tfm.ends_workspace_bytes(_dims(E=64, R=128), e) > wb
+    # thinking rows are never decoder rows
+    assert tfm.ends_workspace_bytes(d, _ends(T=8)) < wb
+
+
+@pytest.mark.parametrize("kw", [dict(G=0, offsets=()), dict(K=65), dict(K=0), dict(T=64),
+                                dict(T=-1), dict(Hd=0), dict(F=0), dict(decode_mean=2),
+                                dict(G=1, offsets=(-1,)), dict(G=1, offsets=((1 << 20) + 1,))])
+def test_ends_invalid_shape_rejected(kw):
+    if kw.get("decode_mean") == 2:
+        e = _ends()
+        e.decode_mean = 2
+    elif kw.get("G") == 0:
+        e = _ends()
+        e.G = 0
+    else:
+        e = _ends(**kw)
+    assert tfm.ends_param_count(_dims(), e) == 0
+    assert tfm.ends_workspace_bytes(_dims(), e) == 0
+    assert tfm.last_error()
+
+
+def _enc(d, e, n_train, n_feat, ptr=1 << 20, wb=1 << 40, bwd=False):
+    nt = np.ascontiguousarray(n_train, dtype=np.int32)
+    nf = np.ascontiguousarray(n_feat, dtype=np.int32)
+    L = tfm.lib()
+    if bwd:
+        return L.tfm_encode_bwd(ctypes.byref(d), ctypes.byref(e), nt.ctypes.data, nf.ctypes.data,
+                                ptr, ptr, ptr, ptr, 0, ptr, wb, None)
+    return L.tfm_encode_fwd(ctypes.byref(d), ctypes.byref(e), nt.ctypes.data, nf.ctypes.data,
+                            ptr, ptr, ptr, ptr, ptr, wb, None)
+
+
+def _dec(d, e, n_train, n_feat, n_class, ptr=1 << 20, wb=1 << 40, logits=None):
+    nt = np.ascontiguousarray(n_train, dtype=np.int32)
+    nf = np.ascontiguousarray(n_feat, dtype=np.int32)
+    nc = np.ascontiguousarray(n_class, dtype=np.int32)
+    return tfm.lib().tfm_decode_loss(ctypes.byref(d), ctypes.byref(e), nt.ctypes.data,
+                                     nf.ctypes.data, nc.ctypes.data, ptr, ptr, ptr, ptr, logits,
+                                     ptr, ptr, 0, ptr, wb, None)
+
+
+@pytest.mark.parametrize("bwd", [False, True])
+def test_encoder_arguments_rejected_before_launch(bwd):
+    d = _dims()                                   # B=2, R=64, C=8
+    e = _ends(T=4)
+    assert _enc(d, e, [4, 9], [8, 8], bwd=bwd) == -3      # no labelled data row
+    assert "n_train" in tfm.last_error()
+    assert _enc(d, e, [9, 65], [8, 8], bwd=bwd) == -3
+    assert _enc(d, e, [9, 9], [0, 8], bwd=bwd) == -1
+    assert _enc(d, e, [9, 9], [8, 9], bwd=bwd) == -1      # beyond C
+    assert _enc(d, _ends(F=5), [9, 9], [6, 5], bwd=bwd) == -1   # beyond F
+    assert "n_feat" in tfm.last_error()
+    assert _enc(d, e, [9, 9], [8, 8], ptr=0, bwd=bwd) == -5
+    assert _enc(d, e, [9, 9], [8, 8], ptr=(1 << 20) + 4, bwd=bwd) == -5
+    assert _enc(d, e, [9, 9], [8, 8], wb=16, bwd=bwd) == -7
+    assert _enc(_dims(C=0), e, [9, 9], [1, 1], bwd=bwd) == -1
+    rc = tfm.lib().tfm_encode_fwd(ctypes.byref(d), ctypes.byref(e), None, None, 1 << 20,
+                                  1 << 20, 1 << 20, 1 << 20, 1 << 20, 1 << 40, None)
+    assert rc == -5
+
+
+def test_decoder_arguments_rejected_before_launch():
+    d = _dims()
+    e = _ends()
+    assert _dec(d, e, [9, 9], [8, 8], [2, 11]) == -1      # more classes than outputs
+    assert "n_class" in tfm.last_error()
+    assert _dec(d, e, [9, 9], [8, 8], [0, 2]) == -1
+    assert _dec(d, e, [0, 9], [8, 8], [2, 2]) == -3
+    assert _dec(d, e, [9, 9], [8, 8], [2, 2], ptr=0) == -5
+    assert _dec(d, e, [9, 9], [8, 8], [2, 2], logits=(1 << 20) + 4) == -5
+    assert _dec(d, e, [9, 9], [8, 8], [2, 2], wb=16) == -7
+    nt = np.array([9, 9], np.int32)
+    nf = np.array([8, 8], np.int32)
+    rc = tfm.lib().tfm_decode_loss(ctypes.byref(d), ctypes.byref(e), nt.ctypes.data,
+                                   nf.ctypes.data, None, 1 << 20, 1 << 20, 1 << 20, 1 << 20,
+                                   None, 1 << 20, 1 << 20, 0, 1 << 20, 1 << 40, None)
+    assert rc == -5

@@ -1,0 +1,374 @@
+"""GPU parity of the stack's two ends (include/tfm_ends.h) against the float64 oracle of
+oracle/ends.py: the encoders, the decoder with the loss, a whole training step through
+encoders, stack and decoder on small shapes, and the ends of the full-size workloads in the
+benchmark's launch configuration.  Tolerance: normwise-max relative error <= 1e-4 (float32
+storage) and <= 2e-2 (bfloat16 storage) per tensor, and the same relative bound on the loss."""
+
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import ends as oe
+from paper_2606_03681_amd import workloads as wl
+from paper_2606_03681_amd.stack import to_device
+
+from _harness import TOL, nerr, oracle_params
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    from paper_2606_03681_amd import tfm
+    tfm.lib()
+
+
+def _setup(name, T=None, G=None, mean=None, dtype=None, n_train=None):
+    w = wl.make_workload(name, with_dY=False)
+    cfg = dict(w.cfg)
+    if T is not None:
+        cfg["thinking"] = T
+    if dtype is not None:
+        cfg["dtype"] = dtype
+    w.cfg = cfg
+    T = cfg.get("thinking", 0)
+    if n_train is not None:
+        w.n_train = np.asarray(n_train, np.int32)
+    w.n_train = np.maximum(w.n_train, T + 1).astype(np.int32)
+    e = wl.make_ends_inputs(w, G=G, mean=mean)
+    return w, e
+
+
+def _dims(w):
+    from paper_2606_03681_amd import tfm
+    return tfm.make_dims(dtype=w.dtype, block=w.block,
+                         **{k: v for k, v in w.dims.items() if k != "dtype"})
+
+
+def _ends(e):
+    from paper_2606_03681_amd import tfm
+    return tfm.make_ends(e.G, e.offsets, e.F, e.T, e.Hd, e.K, e.mean)
+
+
+def _dev(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _storage(t, dtype):
+    import torch
+    if dtype == "f32":
+        return t.detach().cpu().numpy()
+    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def _oparams(w, e):
+    return oe.unpack_ends_params(e.params.astype(np.float64), w.cfg["E"], e.G, e.Hd, e.K)
+
+
+def _full_labels(w, e):
+    """Labels aligned with the rows of the stack input (thinking rows get 0, never read)."""
+    y = np.zeros((len(w.n_train), w.cfg["R"]))
+    y[:, e.T:] = e.labels
+    return y
+
+
+def _oracle_encode(w, e, b=None):
+    sl = slice(None) if b is None else slice(b, b + 1)
+    return oe.encode_forward(e.x[sl], e.labels[sl].astype(np.float64),
+                             (w.n_train - e.T)[sl], e.n_feat[sl], w.cfg["C"], e.offsets,
+                             _oparams(w, e))
+
+
+def _ws(dims, en):
+    import torch
+    from paper_2606_03681_amd import tfm
+    return torch.empty(tfm.ends_workspace_bytes(dims, en), dtype=torch.uint8, device="cuda")
+
+
+def _elt(w):
+    import torch
+    return torch.float32 if w.dtype == "f32" else torch.bfloat16
+
+
+ENC_CASES = [("ragged-small-f32", 0, 1), ("ragged-small-f32", 3, 5),
+             ("ragged-small-bf16", 0, 3), ("prenorm-small-bf16", 7, 5), ("d64-f32", 2, 8)]
+
+
+@pytest.mark.parametrize("name,T,G", ENC_CASES)
+def test_encode_fwd_against_oracle(name, T, G):
+    import torch
+    from paper_2606_03681_amd import tfm
+    w, e = _setup(name, T=T, G=G)
+    dt, R, C = w.dtype, w.cfg["R"], w.cfg["C"]
+    dims, en = _dims(w), _ends(e)
+    X = torch.full((len(w.n_train), R, C + 1, w.cfg["E"]), 3.0, dtype=_elt(w), device="cuda")
+    tfm.encode_fwd(dims, en, w.n_train, e.n_feat, _dev(e.x), _dev(e.labels), _dev(e.params), X,
+                   _ws(dims, en))
+    got = wl.storage_to_f64(_storage(X, dt), dt)
+    ref, mask, _ = _oracle_encode(w, e)
+    err = nerr(got[:, T:], ref)
+    _say(f"[ends] encode_fwd {name} T={T} G={G}: err {err:.3g}")
+    assert err <= TOL[dt]
+    assert np.all(got[:, :T] == 3.0)                     # thinking rows untouched
+    for b in range(len(w.n_train)):
+        assert np.all(got[b, T:, ~mask[b].astype(bool)] == 0)
+    assert np.array_equal(mask, e.cell_mask.astype(bool))
+
+
+@pytest.mark.parametrize("name,T,G", ENC_CASES)
+def test_encode_bwd_against_oracle(name, T, G):
+    import torch
+    from paper_2606_03681_amd import tfm
+    w, e = _setup(name, T=T, G=G)
+    dt, R, C, E = w.dtype, w.cfg["R"], w.cfg["C"], w.cfg["E"]
+    dims, en = _dims(w), _ends(e)
+    rng = np.random.default_rng(77)
+    dX = wl.to_storage(rng.normal(size=(len(w.n_train), R, C + 1, E)), dt)
+    grads = torch.full((len(e.params),), 7.0, device="cuda")
+    ws = _ws(dims, en)
+    args = (dims, en, w.n_train, e.n_feat, _dev(e.x), _dev(e.labels), _dev(dX))
+    tfm.encode_bwd(*args, grads, False, ws)
+    _, _, cache = _oracle_encode(w, e)
+    ref = oe.encode_backward(wl.storage_to_f64(dX, dt)[:, T:], cache)
+    g = grads.double().cpu().numpy()
+    got = oe.unpack_ends_params(g, E, e.G, e.Hd, e.K)
+    for k in ("W_fe", "b_fe", "W_te", "b_te"):
+        err = nerr(got[k], ref[k])
+        _say(f"[ends] encode_bwd {name} T={T} G={G} {k}: err {err:.3g}")
+        assert err <= TOL[dt], k
+    nenc = E * e.G + 3 * E
+    assert np.all(g[nenc:] == 7.0)                       # decoder entries untouched
+    tfm.encode_bwd(*args, grads, True, ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(grads.double().cpu().numpy()[:nenc], 2 * g[:nenc])
+
+
+DEC_CASES = [("ragged-small-f32", 0, False), ("ragged-small-f32", 3, True),
+             ("ragged-small-bf16", 0, False), ("ragged-small-bf16", 0, True),
+             ("prenorm-small-bf16", 5, True), ("d64-f32", 0, True)]
+
+
+def _decode_gpu(w, e, Y, accumulate=False, logits=True):
+    import torch
+    from paper_2606_03681_amd import tfm
+    dims, en = _dims(w), _ends(e)
+    ntest = int((w.cfg["R"] - w.n_train).sum())
+    loss = torch.full((4,), -1.0, device="cuda")
+    lg = torch.empty((max(ntest, 1), e.K), device="cuda") if logits else None
+    dY = torch.full(Y.shape, 5.0, dtype=Y.dtype, device="cuda")
+    grads = torch.full((len(e.params),), 7.0, device="cuda")
+    tfm.decode_loss(dims, en, w.n_train, e.n_feat, e.n_class, _dev(e.labels), Y, _dev(e.params),
+                    loss, lg, dY, grads, accumulate, _ws(dims, en))
+    torch.cuda.synchronize()
+    return (float(loss[0].item()), None if lg is None else lg[:ntest].double().cpu().numpy(),
+            dY, grads.double().cpu().numpy())
+
+
+@pytest.mark.parametrize("name,T,mean", DEC_CASES)
+def test_decode_loss_against_oracle(name, T, mean):
+    w, e = _setup(name, T=T, mean=mean)
+    if len(w.n_train) >= 3:
+        # one dataset without unlabelled rows, one with a single class
+        w.n_train[0] = w.cfg["R"]
+        e.n_class[1] = 1
+        e.labels[1] = 0
+    dt, R, C, E = w.dtype, w.cfg["R"], w.cfg["C"], w.cfg["E"]
+    Ys = wl.to_storage(np.random.default_rng(5).normal(size=(len(w.n_train), R, C + 1, E)), dt)
+    loss, lg, dY, g = _decode_gpu(w, e, to_device(Ys, dt))
+    P = _oparams(w, e)
+    mode = "mean" if e.mean else "target"
+    rl, rdY, rdP, rlg = oe.decode_loss(wl.storage_to_f64(Ys, dt), _full_labels(w, e), w.n_train,
+                                       e.n_feat, e.n_class, C, P, mode)
+    tol = TOL[dt]
+    _say(f"[ends] decode {name} T={T} mean={mean}: loss {loss:.6g} vs {rl:.6g}")
+    assert abs(loss - rl) <= tol * abs(rl)
+    assert nerr(lg, rlg) <= tol
+    assert nerr(wl.storage_to_f64(_storage(dY, dt), dt), rdY) <= tol
+    got = oe.unpack_ends_params(g, E, e.G, e.Hd, e.K)
+    for k in ("W_d1", "b_d1", "W_d2", "b_d2"):
+        err = nerr(got[k], rdP[k])
+        _say(f"[ends] decode {name} {k}: err {err:.3g}")
+        assert err <= tol, k
+    assert np.all(g[:E * e.G + 3 * E] == 7.0)            # encoder entries untouched
+
+
+def test_decode_without_unlabelled_rows_gives_zeros():
+    import torch
+    w, e = _setup("ragged-small-f32", n_train=[200, 200, 200, 200])
+    Y = torch.randn((4, 200, 21, 64), device="cuda")
+    loss, _, dY, g = _decode_gpu(w, e, Y, logits=False)
+    assert loss == 0.0
+    assert torch.count_nonzero(dY).item() == 0
+    E = 64
+    assert np.all(g[E * e.G + 3 * E:] == 0) and np.all(g[:E * e.G + 3 * E] == 7.0)
+
+
+def test_decode_fwd_matches_the_loss_call_logits():
+    import torch
+    from paper_2606_03681_amd import tfm
+    w, e = _setup("ragged-small-bf16", mean=True)
+    Ys = wl.to_storage(np.random.default_rng(9).normal(
+        size=(len(w.n_train), w.cfg["R"], w.cfg["C"] + 1, w.cfg["E"])), "bf16")
+    Y = to_device(Ys, "bf16")
+    _, lg, _, _ = _decode_gpu(w, e, Y)
+    dims, en = _dims(w), _ends(e)
+    out = torch.empty((lg.shape[0], e.K), device="cuda")
+    tfm.decode_fwd(dims, en, w.n_train, e.n_feat, Y, _dev(e.params), out, _ws(dims, en))
+    torch.cuda.synchronize()
+    assert np.array_equal(out.double().cpu().numpy(), lg)
+
+
+def test_ends_bitwise_deterministic():
+    w, e = _setup("ragged-small-bf16", mean=True)
+    import torch
+    Ys = wl.to_storage(np.random.default_rng(3).normal(
+        size=(len(w.n_train), w.cfg["R"], w.cfg["C"] + 1, w.cfg["E"])), "bf16")
+    a = _decode_gpu(w, e, to_device(Ys, "bf16"))
+    b = _decode_gpu(w, e, to_device(Ys, "bf16"))
+    assert a[0] == b[0] and np.array_equal(a[3], b[3])
+    assert torch.equal(a[2], b[2])
+
+
+# ---- a whole training step ---------------------------------------------------------------------
+
+def _oracle_step(w, e):
+    T, C = e.T, w.cfg["C"]
+    P = _oparams(w, e)
+    Xd, _, cache = _oracle_encode(w, e)
+    X = oracle.thinking_rows_forward(Xd, e.table.astype(np.float64), e.cell_mask) if T else Xd
+    Ps = oracle_params(w)
+    heads = w.cfg["heads"]
+    if w.block == "pre":
+        Y, caches = oracle.prenorm_stack_forward(X, Ps, w.n_train, e.cell_mask, heads)
+    else:
+        Y, caches = oracle.stack_forward(X, Ps, w.n_train, e.cell_mask, heads)
+    mode = "mean" if e.mean else "target"
+    loss, dY, dP, _ = oe.decode_loss(Y, _full_labels(w, e), w.n_train, e.n_feat, e.n_class, C,
+                                     P, mode)
+    if w.block == "pre":
+        dX, grads = oracle.prenorm_stack_backward(dY, caches)
+        grads = [oracle.pack_prenorm_params(g) for g in grads]
+    else:
+        dX, grads = oracle.stack_backward(dY, caches)
+        grads = [oracle.pack_params(g) for g in grads]
+    dtable = None
+    if T:
+        dX, dtable = oracle.thinking_rows_backward(dX, e.cell_mask, T)
+    dP.update(oe.encode_backward(dX, cache))
+    return loss, grads, dP, dtable
+
+
+def _gpu_step(w, e):
+    import torch
+    from paper_2606_03681_amd.stack import TrainStep
+    ts = TrainStep(_dims(w), _ends(e), w.n_train, e.n_feat, e.n_class, w.params, e.params,
+                   e.table)
+    loss = ts.run(_dev(e.x), _dev(e.labels))
+    torch.cuda.synchronize()
+    return ts, float(loss.item())
+
+
+STEP_CASES = [("d64-f32", 0, None), ("ragged-small-f32", 2, None), ("d16-bf16", 0, None),
+              ("prenorm-small-bf16", 4, None), ("prenorm-d64-bf16", 6, None)]
+
+
+@pytest.mark.parametrize("name,T,G", STEP_CASES)
+def test_training_step_against_oracle(name, T, G):
+    w, e = _setup(name, T=T, G=G)
+    dt = w.dtype
+    tol = TOL[dt]
+    ts, loss = _gpu_step(w, e)
+    rl, rgrads, rdP, rdt = _oracle_step(w, e)
+    _say(f"[step] {name} T={T}: loss {loss:.6g} vs {rl:.6g}")
+    assert abs(loss - rl) <= tol * abs(rl)
+    unpack = oracle.unpack_prenorm_params if w.block == "pre" else oracle.unpack_params
+    names = oracle.PRENORM_PARAM_ORDER if w.block == "pre" else oracle.PARAM_ORDER
+    E, H = w.cfg["E"], w.cfg["H"]
+    worst = 0.0
+    for l, (gg, gr) in enumerate(zip(ts.stack.grads, rgrads)):
+        pg = unpack(gg.double().cpu().numpy(), E, H)
+        pr = unpack(gr, E, H)
+        for k in names:
+            err = nerr(pg[k], pr[k])
+            worst = max(worst, err)
+            assert err <= tol, (l, k, err)
+    got = oe.unpack_ends_params(ts.ends_grads.double().cpu().numpy(), E, e.G, e.Hd, e.K)
+    for k in oe.ENDS_PARAM_ORDER:
+        err = nerr(got[k], rdP[k])
+        worst = max(worst, err)
+        assert err <= tol, (k, err)
+    if T:
+        err = nerr(ts.table_grad.double().cpu().numpy(), rdt)
+        worst = max(worst, err)
+        assert err <= tol
+    _say(f"[step] {name} T={T}: worst gradient error {worst:.3g}")
+
+
+# ---- full-size workloads in the benchmark's launch configuration ------------------------------
+
+@pytest.mark.parametrize("cfg", [2, "record9-bf16"])
+def test_full_size_ends(cfg):
+    """The whole step at full size; the encoders are checked against the oracle on the data the
+    GPU step used (x, labels and the stack's dX as stored), the decoder on the stack output the
+    GPU produced (as stored)."""
+    w, e = _setup(cfg)
+    dt, C, E, T = w.dtype, w.cfg["C"], w.cfg["E"], e.T
+    tol = TOL[dt]
+    _say(f"[ends-full] {w.cfg['name']}: GPU step")
+    ts, loss = _gpu_step(w, e)
+    P = _oparams(w, e)
+    # encoder output, two datasets
+    for b in (0, len(w.n_train) - 1):
+        ref, _, _ = _oracle_encode(w, e, b)
+        got = wl.storage_to_f64(_storage(ts.X[b, T:], dt), dt)
+        err = nerr(got, ref[0])
+        _say(f"[ends-full] encode_fwd dataset {b}: err {err:.3g}")
+        assert err <= tol
+    # decoder on the GPU's Y: per-dataset oracle calls combined with the global row weights
+    ntest = w.cfg["R"] - w.n_train
+    Ttot = float(ntest.sum())
+    mode = "mean" if e.mean else "target"
+    rl = 0.0
+    rdP = {k: 0.0 for k in ("W_d1", "b_d1", "W_d2", "b_d2")}
+    worst_dy = 0.0
+    y = _full_labels(w, e)
+    for b in range(len(w.n_train)):
+        Yb = wl.storage_to_f64(_storage(ts.Y[b:b + 1], dt), dt)
+        lb, dYb, dPb, _ = oe.decode_loss(Yb, y[b:b + 1], w.n_train[b:b + 1], e.n_feat[b:b + 1],
+                                         e.n_class[b:b + 1], C, P, mode)
+        s = ntest[b] / Ttot
+        rl += lb * s
+        for k in rdP:
+            rdP[k] = rdP[k] + dPb[k] * s
+        gdY = wl.storage_to_f64(_storage(ts.dY[b], dt), dt)
+        worst_dy = max(worst_dy, nerr(gdY, dYb[0] * s))
+    _say(f"[ends-full] loss {loss:.6g} vs {rl:.6g}; dY err {worst_dy:.3g}")
+    assert abs(loss - rl) <= tol * abs(rl)
+    assert worst_dy <= tol
+    got = oe.unpack_ends_params(ts.ends_grads.double().cpu().numpy(), E, e.G, e.Hd, e.K)
+    for k in rdP:
+        err = nerr(got[k], rdP[k])
+        _say(f"[ends-full] decoder {k}: err {err:.3g}")
+        assert err <= tol, k
+    # encoder gradients from the GPU's dX
+    ref = {k: 0.0 for k in ("W_fe", "b_fe", "W_te", "b_te")}
+    for b in range(len(w.n_train)):
+        _, _, cache = _oracle_encode(w, e, b)
+        dXb = wl.storage_to_f64(_storage(ts.dX[b:b + 1, T:], dt), dt)
+        d = oe.encode_backward(dXb, cache)
+        for k in ref:
+            ref[k] = ref[k] + d[k]
+    for k in ref:
+        err = nerr(got[k], ref[k])
+        _say(f"[ends-full] encoder {k}: err {err:.3g}")
+        assert err <= tol, k
