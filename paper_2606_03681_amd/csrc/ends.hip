@@ -1,11 +1,12 @@
 // Kernels of the two ends of the stack (declarations and layout in ends.h).
 //
 // Encoder forward: one workgroup per ENC_ROWS data rows of one dataset; it stages the rows'
-// feature values and the encoder weights in LDS and writes whole rows of the stack input with
-// 16-byte stores (feature cells, zero padding cells, the target cell).  HBM-write bound.
-// Encoder backward: the same row slabs; each thread owns one 8-wide slice of E and a lane of
-// cells, accumulates the weight and bias gradients in registers, and the workgroup folds its
-// lanes in a fixed order into one partial row (summed over slabs in a fixed order afterwards).
+// feature values in LDS, keeps each thread's 8-wide slice of the encoder weights in registers
+// and writes whole rows of the stack input with 16-byte stores (feature cells, zero padding
+// cells, the target cell).  HBM-write bound.
+// Encoder backward: the same row slabs and slices; each thread accumulates its slice of the
+// weight and bias gradients in registers over a lane of cells, and the workgroup folds its lanes
+// in a fixed order into one partial row (summed over slabs in a fixed order afterwards).
 // HBM-read bound.
 // Decoder: gather of the decoder input, float32 GEMMs on the MFMA with bias/GELU epilogues, a
 // masked softmax cross entropy per row, and a scatter that writes the whole dY.
@@ -73,198 +74,270 @@ __device__ float train_label_mean(const int32_t* lab, int ntr, int64_t* red) {
 }
 
 // Shifts of the groups reduced mod m, so that column (c + o) mod m = c + om, minus m on wrap.
+template <int G>
 __device__ __forceinline__ void shifts_mod(const EndsGeo& g, int m, int* om) {
 #pragma unroll
-  for (int k = 0; k < ENDS_GMAX; ++k) om[k] = k < g.G ? g.off[k] % m : 0;
+  for (int k = 0; k < G; ++k) om[k] = g.off[k] % m;
 }
 
-// Stages the feature values of rows [i0, i0 + nrow) of dataset b (columns [0, m)).
+// Stages the feature values (columns [0, m)) of the workgroup's rows i0 + rr * rs, rr < nrow,
+// of dataset b.
 __device__ __forceinline__ void stage_rows(const EndsGeo& g, const float* x, int b, int i0,
-                                           int nrow, int m, float (*sx)[256]) {
+                                           int rs, int nrow, int m, float (*sx)[256]) {
   const int Rd = g.R - g.T;
   for (int i = threadIdx.x; i < nrow * m; i += blockDim.x) {
     const int rr = i / m, c = i - rr * m;
-    sx[rr][c] = x[((int64_t)b * Rd + i0 + rr) * g.F + c];
+    sx[rr][c] = x[((int64_t)b * Rd + i0 + rr * rs) * g.F + c];
   }
 }
 
+// Rows of an encoder workgroup: workgroup j of a dataset takes the data rows j, j + rs, ...
+// (rs = workgroups per dataset, at most ENC_ROWS rows), so that the workgroups running at one
+// time stream through neighbouring rows of HBM instead of a thousand separate regions.
+__device__ __forceinline__ int slab_rows(int Rd, int i0, int rs) {
+  const int n = (Rd - i0 + rs - 1) / rs;
+  return n < ENC_ROWS ? n : ENC_ROWS;
+}
+
 // ---- encoder ----------------------------------------------------------------------------------
-template <class T>
+// Thread layout of both encoder kernels: thread t owns the 8-wide slice ch = t % (E/8) of the
+// embedding and serves cell lane t / (E/8); the L = 256 / (E/8) lanes of a workgroup walk the
+// (row, cell) pairs of its slab, so that a wave touches consecutive 16-byte pieces of whole cells.
+struct Lanes {
+  int nch, L, ch, lane;
+  bool act;
+};
+__device__ __forceinline__ Lanes lanes_of(int E) {
+  Lanes l;
+  l.nch = E >> 3;
+  l.L = 256 / l.nch;
+  l.ch = threadIdx.x % l.nch;
+  l.lane = threadIdx.x / l.nch;
+  l.act = l.lane < l.L;
+  return l;
+}
+
+template <class T, int G>
 __global__ __launch_bounds__(256) void k_encode_fwd(EndsGeo g, const float* __restrict__ x,
                                                     const int32_t* __restrict__ lab,
                                                     const float* __restrict__ prm,
                                                     T* __restrict__ X) {
-  __shared__ float sW[256 * ENDS_GMAX];
-  __shared__ float sb[256], stw[256], stb[256];
   __shared__ float sx[ENC_ROWS][256];
+  __shared__ float stv[ENC_ROWS];
   __shared__ int64_t red[256];
   const int b = blockIdx.y;
   const EndsDs md = g.ds[b];
-  const int E = g.E, G = g.G, m = md.n_feat, C = g.S - 1;
+  const int E = g.E, m = md.n_feat, C = g.S - 1, S = g.S;
   const int Rd = g.R - g.T, ntr = md.n_train - g.T;
-  const int i0 = blockIdx.x * ENC_ROWS;
-  const int nrow = Rd - i0 < ENC_ROWS ? Rd - i0 : ENC_ROWS;
-  for (int i = threadIdx.x; i < E * G; i += 256) sW[i] = prm[i];
-  for (int i = threadIdx.x; i < E; i += 256) {
-    sb[i] = prm[E * G + i];
-    stw[i] = prm[E * G + E + i];
-    stb[i] = prm[E * G + 2 * E + i];
+  const int i0 = blockIdx.x, rs = gridDim.x;
+  const int nrow = slab_rows(Rd, i0, rs);
+  const Lanes ln = lanes_of(E);
+  // this thread's slice of the encoder weights, in registers
+  const int e0 = ln.ch * 8;
+  float w[8][G], bf[8], tw[8], tb[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+#pragma unroll
+    for (int k = 0; k < G; ++k) w[q][k] = prm[(e0 + q) * G + k];
+    bf[q] = prm[E * G + e0 + q];
+    tw[q] = prm[E * G + E + e0 + q];
+    tb[q] = prm[E * G + 2 * E + e0 + q];
   }
-  stage_rows(g, x, b, i0, nrow, m, sx);
+  stage_rows(g, x, b, i0, rs, nrow, m, sx);
   const float mean = train_label_mean(lab + (int64_t)b * Rd, ntr, red);  // barriers inside
-  int om[ENDS_GMAX];
-  shifts_mod(g, m, om);
-  const int nch = E >> 3, nvec = g.S * nch;
-  for (int rr = 0; rr < nrow; ++rr) {
-    const int i = i0 + rr;
-    const float tval = i < ntr ? (float)lab[(int64_t)b * Rd + i] : mean;
-    T* row = X + ((int64_t)b * g.R + g.T + i) * g.S * E;
-    for (int v = threadIdx.x; v < nvec; v += 256) {
-      const int c = v / nch, e0 = (v - c * nch) << 3;
-      float o[8];
-      if (c < m) {
-        float xg[ENDS_GMAX];
+  if (threadIdx.x < nrow) {
+    const int i = i0 + threadIdx.x * rs;
+    stv[threadIdx.x] = i < ntr ? (float)lab[(int64_t)b * Rd + i] : mean;
+  }
+  __syncthreads();
+  if (!ln.act) return;
+  int om[G];
+  shifts_mod<G>(g, m, om);
+  T* base = X + ((int64_t)b * g.R + g.T + i0) * S * E + e0;
+  const int64_t rstep = (int64_t)rs * S * E;
+  const int tot = nrow * S;
+  for (int p = ln.lane; p < tot; p += ln.L) {
+    const int rr = p / S, c = p - rr * S;
+    float o[8];
+    if (c < m) {
+      float xg[G];
 #pragma unroll
-        for (int k = 0; k < ENDS_GMAX; ++k) {
-          int j = c + om[k];
-          j = j >= m ? j - m : j;
-          xg[k] = k < G ? sx[rr][j] : 0.f;
-        }
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          float a = sb[e0 + q];
-#pragma unroll
-          for (int k = 0; k < ENDS_GMAX; ++k)
-            if (k < G) a = fmaf(sW[(e0 + q) * G + k], xg[k], a);
-          o[q] = a;
-        }
-      } else if (c == C) {
-#pragma unroll
-        for (int q = 0; q < 8; ++q) o[q] = fmaf(tval, stw[e0 + q], stb[e0 + q]);
-      } else {
-#pragma unroll
-        for (int q = 0; q < 8; ++q) o[q] = 0.f;
+      for (int k = 0; k < G; ++k) {
+        int j = c + om[k];
+        j = j >= m ? j - m : j;
+        xg[k] = sx[rr][j];
       }
-      st8(row + (int64_t)c * E + e0, o);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        float a = bf[q];
+#pragma unroll
+        for (int k = 0; k < G; ++k) a = fmaf(w[q][k], xg[k], a);
+        o[q] = a;
+      }
+    } else if (c == C) {
+      const float tv = stv[rr];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) o[q] = fmaf(tv, tw[q], tb[q]);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) o[q] = 0.f;
     }
+    st8(base + rr * rstep + (int64_t)c * E, o);
   }
 }
 
 // Folds one 8-wide register slice per (lane, slice) over the lanes in a fixed order and writes
 // out[e * os] for e in [0, E).  Contains barriers: every thread of the block calls it.
-__device__ __forceinline__ void fold_lanes(const float* v, bool act, int lane, int ch, int L,
-                                           int E, float* sred, float* out, int os) {
-  if (act) {
+__device__ __forceinline__ void fold_lanes(const float* v, const Lanes& ln, int E, float* sred,
+                                           float* out, int os) {
+  if (ln.act) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) sred[lane * E + ch * 8 + q] = v[q];
+    for (int q = 0; q < 8; ++q) sred[ln.lane * E + ln.ch * 8 + q] = v[q];
   }
   __syncthreads();
   for (int e = threadIdx.x; e < E; e += 256) {
     float s = 0.f;
-    for (int l = 0; l < L; ++l) s += sred[l * E + e];
+    for (int l = 0; l < ln.L; ++l) s += sred[l * E + e];
     out[(int64_t)e * os] = s;
   }
   __syncthreads();
 }
 
-template <class T>
+// Feature cells per unrolled step of the encoder backward: their loads are issued together.
+constexpr int ENC_BWD_UNROLL = 4;
+
+template <class T, int G>
 __global__ __launch_bounds__(256) void k_encode_bwd(EndsGeo g, const float* __restrict__ x,
                                                     const int32_t* __restrict__ lab,
                                                     const T* __restrict__ dX,
                                                     float* __restrict__ part) {
   __shared__ float sx[ENC_ROWS][256];
+  __shared__ float stv[ENC_ROWS];
   __shared__ float sred[2048];
   __shared__ int64_t red[256];
   const int b = blockIdx.y;
   const EndsDs md = g.ds[b];
-  const int E = g.E, G = g.G, m = md.n_feat, C = g.S - 1;
+  const int E = g.E, m = md.n_feat, C = g.S - 1, S = g.S;
   const int Rd = g.R - g.T, ntr = md.n_train - g.T;
-  const int i0 = blockIdx.x * ENC_ROWS;
-  const int nrow = Rd - i0 < ENC_ROWS ? Rd - i0 : ENC_ROWS;
-  stage_rows(g, x, b, i0, nrow, m, sx);
+  const int i0 = blockIdx.x, rs = gridDim.x;
+  const int nrow = slab_rows(Rd, i0, rs);
+  const Lanes ln = lanes_of(E);
+  stage_rows(g, x, b, i0, rs, nrow, m, sx);
   const float mean = train_label_mean(lab + (int64_t)b * Rd, ntr, red);  // barriers inside
-  int om[ENDS_GMAX];
-  shifts_mod(g, m, om);
-  const int nch = E >> 3, L = 256 / nch;
-  const int ch = threadIdx.x % nch, lane = threadIdx.x / nch;
-  const bool act = lane < L;
-  float aw[8][ENDS_GMAX], ab[8], atw[8], atb[8];
+  if (threadIdx.x < nrow) {
+    const int i = i0 + threadIdx.x * rs;
+    stv[threadIdx.x] = i < ntr ? (float)lab[(int64_t)b * Rd + i] : mean;
+  }
+  __syncthreads();
+  int om[G];
+  shifts_mod<G>(g, m, om);
+  float aw[8][G], ab[8], atw[8], atb[8];
 #pragma unroll
   for (int q = 0; q < 8; ++q) {
     ab[q] = atw[q] = atb[q] = 0.f;
 #pragma unroll
-    for (int k = 0; k < ENDS_GMAX; ++k) aw[q][k] = 0.f;
+    for (int k = 0; k < G; ++k) aw[q][k] = 0.f;
   }
-  if (act) {
-    for (int rr = 0; rr < nrow; ++rr) {
-      const int i = i0 + rr;
-      const T* row = dX + ((int64_t)b * g.R + g.T + i) * g.S * E + ch * 8;
-      for (int c = lane; c < m; c += L) {
-        float d[8], xg[ENDS_GMAX];
-        ld8(row + (int64_t)c * E, d);
+  const T* base = dX + ((int64_t)b * g.R + g.T + i0) * S * E + ln.ch * 8;
+  const int64_t rstep = (int64_t)rs * S * E;
+  if (ln.act) {
+    // feature cells: (row, cell) pairs of the slab, ENC_BWD_UNROLL loads in flight per lane;
+    // a pair past the end reloads the first pair of the step and is not accumulated
+    const int tot = nrow * m;
+    for (int p0 = ln.lane; p0 < tot; p0 += ENC_BWD_UNROLL * ln.L) {
+      float d[ENC_BWD_UNROLL][8];
+      int rrs[ENC_BWD_UNROLL], cs[ENC_BWD_UNROLL];
 #pragma unroll
-        for (int k = 0; k < ENDS_GMAX; ++k) {
-          int j = c + om[k];
-          j = j >= m ? j - m : j;
-          xg[k] = k < G ? sx[rr][j] : 0.f;
-        }
+      for (int u = 0; u < ENC_BWD_UNROLL; ++u) {
+        const int p = p0 + u * ln.L < tot ? p0 + u * ln.L : p0;
+        rrs[u] = p / m;
+        cs[u] = p - rrs[u] * m;
+        ld8(base + rrs[u] * rstep + (int64_t)cs[u] * E, d[u]);
+      }
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          ab[q] += d[q];
+      for (int u = 0; u < ENC_BWD_UNROLL; ++u) {
+        if (p0 + u * ln.L < tot) {
+          float xg[G];
 #pragma unroll
-          for (int k = 0; k < ENDS_GMAX; ++k) aw[q][k] = fmaf(d[q], xg[k], aw[q][k]);
+          for (int k = 0; k < G; ++k) {
+            int j = cs[u] + om[k];
+            j = j >= m ? j - m : j;
+            xg[k] = sx[rrs[u]][j];
+          }
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            ab[q] += d[u][q];
+#pragma unroll
+            for (int k = 0; k < G; ++k) aw[q][k] = fmaf(d[u][q], xg[k], aw[q][k]);
+          }
         }
       }
-      if (lane == 0) {
-        const float tval = i < ntr ? (float)lab[(int64_t)b * Rd + i] : mean;
-        float d[8];
-        ld8(row + (int64_t)C * E, d);
+    }
+    // target cells, one row per lane
+    for (int rr = ln.lane; rr < nrow; rr += ln.L) {
+      float d[8];
+      ld8(base + rr * rstep + (int64_t)C * E, d);
+      const float tv = stv[rr];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          atb[q] += d[q];
-          atw[q] = fmaf(d[q], tval, atw[q]);
-        }
+      for (int q = 0; q < 8; ++q) {
+        atb[q] += d[q];
+        atw[q] = fmaf(d[q], tv, atw[q]);
       }
     }
   }
   float* out = part + ((int64_t)blockIdx.y * gridDim.x + blockIdx.x) * ((int64_t)E * (G + 3));
 #pragma unroll
-  for (int k = 0; k < ENDS_GMAX; ++k) {
-    if (k < G) {  // uniform over the block
-      float v[8];
+  for (int k = 0; k < G; ++k) {
+    float v[8];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) v[q] = aw[q][k];
-      fold_lanes(v, act, lane, ch, L, E, sred, out + k, G);
-    }
+    for (int q = 0; q < 8; ++q) v[q] = aw[q][k];
+    fold_lanes(v, ln, E, sred, out + k, G);
   }
-  fold_lanes(ab, act, lane, ch, L, E, sred, out + (int64_t)E * G, 1);
-  fold_lanes(atw, act, lane, ch, L, E, sred, out + (int64_t)E * (G + 1), 1);
-  fold_lanes(atb, act, lane, ch, L, E, sred, out + (int64_t)E * (G + 2), 1);
+  fold_lanes(ab, ln, E, sred, out + (int64_t)E * G, 1);
+  fold_lanes(atw, ln, E, sred, out + (int64_t)E * (G + 1), 1);
+  fold_lanes(atb, ln, E, sred, out + (int64_t)E * (G + 2), 1);
 }
 
 // ---- decoder ----------------------------------------------------------------------------------
-// One wave per decoder row.
+// Decoder input: each thread reads one 8-wide slice of E of one decoder row (the lanes of a
+// workgroup take consecutive rows), summing the feature cells in ascending order for the mean.
 template <class T>
 __global__ __launch_bounds__(256) void k_decode_gather(EndsGeo g, const T* __restrict__ Y,
                                                        float* __restrict__ Z) {
-  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= g.Ttot) return;
-  const int lane = threadIdx.x & 63;
+  const Lanes ln = lanes_of(g.E);
+  const int64_t t = (int64_t)blockIdx.x * ln.L + ln.lane;
+  if (!ln.act || t >= g.Ttot) return;
   const int b = dataset_of(g, t);
   const EndsDs md = g.ds[b];
+  const int E = g.E, m = md.n_feat;
   const int r = md.n_train + (int)(t - md.test0);
-  const T* row = Y + ((int64_t)b * g.R + r) * g.S * g.E;
-  for (int e = lane; e < g.E; e += 64) {
-    float v;
-    if (g.mean) {
-      float s = 0.f;
-      for (int c = 0; c < md.n_feat; ++c) s += ld(row + (int64_t)c * g.E + e);
-      v = s / (float)md.n_feat;
-    } else {
-      v = ld(row + (int64_t)(g.S - 1) * g.E + e);
+  const T* row = Y + ((int64_t)b * g.R + r) * g.S * E + ln.ch * 8;
+  float v[8];
+  if (g.mean) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] = 0.f;
+    int c = 0;
+    for (; c + 4 <= m; c += 4) {
+      float d[4][8];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) ld8(row + (int64_t)(c + u) * E, d[u]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) v[q] += d[u][q];
     }
-    Z[t * g.E + e] = v;
+    for (; c < m; ++c) {
+      float d[8];
+      ld8(row + (int64_t)c * E, d);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[q] += d[q];
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] = v[q] / (float)m;
+  } else {
+    ld8(row + (int64_t)(g.S - 1) * E, v);
   }
+  st8(Z + t * E + ln.ch * 8, v);
 }
 
 // One workgroup per row (b, r) of dY.
@@ -347,29 +420,43 @@ __global__ __launch_bounds__(256) void k_sgemm(SgemmArgs a) {
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+  // staging coordinates of this thread's four A and four B elements of a K step
+  int a_mm[4], a_kk[4], b_nn[4], b_kk[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int idx = tid + 256 * q;
+    if (TA) { a_mm[q] = idx & 63; a_kk[q] = idx >> 6; }
+    else { a_kk[q] = idx & 15; a_mm[q] = idx >> 4; }
+    if (TB) { b_kk[q] = idx & 15; b_nn[q] = idx >> 4; }
+    else { b_nn[q] = idx & 63; b_kk[q] = idx >> 6; }
+  }
+  // the next K step's elements are loaded into registers while the current one is multiplied;
+  // every load reads a valid element (out-of-range ones read element 0 and are zeroed)
+  float ra[4], rb[4];
+  auto gload = [&](int k0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int gm = m0 + a_mm[q], gk = k0 + a_kk[q];
+      const bool oka = gm < a.M && gk < ke;
+      const int64_t oa = TA ? (int64_t)gk * a.lda + gm : (int64_t)gm * a.lda + gk;
+      const float va = a.A[oka ? oa : 0];
+      ra[q] = oka ? va : 0.f;
+      const int gn = n0 + b_nn[q], gkb = k0 + b_kk[q];
+      const bool okb = gn < a.N && gkb < ke;
+      const int64_t ob = TB ? (int64_t)gn * a.ldb + gkb : (int64_t)gkb * a.ldb + gn;
+      const float vb = a.B[okb ? ob : 0];
+      rb[q] = okb ? vb : 0.f;
+    }
+  };
+  if (kb < ke) gload(kb);
   for (int k0 = kb; k0 < ke; k0 += 16) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const int idx = tid + 256 * q;
-      int mm, kk;
-      if (TA) { mm = idx & 63; kk = idx >> 6; }
-      else { kk = idx & 15; mm = idx >> 4; }
-      int gm = m0 + mm, gk = k0 + kk;
-      float v = 0.f;
-      if (gm < a.M && gk < ke)
-        v = TA ? a.A[(int64_t)gk * a.lda + gm] : a.A[(int64_t)gm * a.lda + gk];
-      As[kk][mm] = v;
-      int nn;
-      if (TB) { kk = idx & 15; nn = idx >> 4; }
-      else { nn = idx & 63; kk = idx >> 6; }
-      const int gn = n0 + nn;
-      gk = k0 + kk;
-      float u = 0.f;
-      if (gn < a.N && gk < ke)
-        u = TB ? a.B[(int64_t)gn * a.ldb + gk] : a.B[(int64_t)gk * a.ldb + gn];
-      Bs[kk][nn] = u;
+      As[a_kk[q]][a_mm[q]] = ra[q];
+      Bs[b_kk[q]][b_nn[q]] = rb[q];
     }
     __syncthreads();
+    if (k0 + 16 < ke) gload(k0 + 16);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const int kr = ks * 4 + (l >> 4);
@@ -422,7 +509,14 @@ hipError_t launch_encode_fwd(const EndsGeo& g, const float* x, const int32_t* la
                              const float* prm, T* X, hipStream_t s) {
   const int Rd = g.R - g.T;
   dim3 grid((unsigned)((Rd + ENC_ROWS - 1) / ENC_ROWS), (unsigned)g.B);
-  k_encode_fwd<T><<<grid, 256, 0, s>>>(g, x, lab, prm, X);
+  switch (g.G) {
+#define TFM_ENC_G(G_) \
+  case G_: k_encode_fwd<T, G_><<<grid, 256, 0, s>>>(g, x, lab, prm, X); break;
+    TFM_ENC_G(1) TFM_ENC_G(2) TFM_ENC_G(3) TFM_ENC_G(4)
+    TFM_ENC_G(5) TFM_ENC_G(6) TFM_ENC_G(7) TFM_ENC_G(8)
+#undef TFM_ENC_G
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
@@ -436,14 +530,22 @@ hipError_t launch_encode_bwd(const EndsGeo& g, const float* x, const int32_t* la
                              float* part, hipStream_t s) {
   const int Rd = g.R - g.T;
   dim3 grid((unsigned)((Rd + ENC_ROWS - 1) / ENC_ROWS), (unsigned)g.B);
-  k_encode_bwd<T><<<grid, 256, 0, s>>>(g, x, lab, dX, part);
+  switch (g.G) {
+#define TFM_ENC_G(G_) \
+  case G_: k_encode_bwd<T, G_><<<grid, 256, 0, s>>>(g, x, lab, dX, part); break;
+    TFM_ENC_G(1) TFM_ENC_G(2) TFM_ENC_G(3) TFM_ENC_G(4)
+    TFM_ENC_G(5) TFM_ENC_G(6) TFM_ENC_G(7) TFM_ENC_G(8)
+#undef TFM_ENC_G
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
 template <class T>
 hipError_t launch_decode_gather(const EndsGeo& g, const T* Y, float* Z, hipStream_t s) {
   if (g.Ttot == 0) return hipSuccess;
-  k_decode_gather<T><<<(unsigned)((g.Ttot + 3) / 4), 256, 0, s>>>(g, Y, Z);
+  const int L = 256 / (g.E >> 3);
+  k_decode_gather<T><<<(unsigned)((g.Ttot + L - 1) / L), 256, 0, s>>>(g, Y, Z);
   return hipGetLastError();
 }
 

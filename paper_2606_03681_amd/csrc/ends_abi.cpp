@@ -28,7 +28,8 @@ int fail(int code, const char* fmt, ...) {
 }
 
 constexpr size_t kAlign = 256;
-constexpr int kRowChunk = 256;  // decoder rows per partial sum of the decoder's gradients
+constexpr int kRowChunk = 256;  // decoder rows per partial product of the weight gradients
+constexpr int kColChunk = 32;   // decoder rows per partial column sum of the bias gradients
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 bool aligned(const void* p) { return p && ((uintptr_t)p % 16) == 0; }
 
@@ -88,6 +89,7 @@ struct Ws {
 Ws ws_layout(const Shape& s) {
   const int64_t Tmax = (int64_t)s.B * (s.R - s.T - 1);
   const int64_t nz = (Tmax + kRowChunk - 1) / kRowChunk;
+  const int64_t nzc = (Tmax + kColChunk - 1) / kColChunk;
   const int64_t slabs = (int64_t)s.B * ((s.R - s.T + tfm::ENC_ROWS - 1) / tfm::ENC_ROWS);
   const size_t wmax = (size_t)s.Hd * (s.E > s.K ? s.E : s.K);
   Ws w;
@@ -108,7 +110,7 @@ Ws ws_layout(const Shape& s) {
   w.DH1 = take((size_t)Tmax * s.Hd * 4);
   w.DZ = take((size_t)Tmax * s.E * 4);
   w.wpart = take((size_t)nz * wmax * 4);
-  w.bpart = take((size_t)nz * (s.Hd > s.K ? s.Hd : s.K) * 4);
+  w.bpart = take((size_t)nzc * (s.Hd > s.K ? s.Hd : s.K) * 4);
   w.total = off;
   return w;
 }
@@ -215,8 +217,8 @@ int row_contraction(const float* A, int64_t lda, const float* B, int64_t ldb, in
 
 int column_sums(const float* A, int64_t lda, int N, int64_t rows, float* part, float* out,
                 int accumulate, hipStream_t st) {
-  const int nz = (int)((rows + kRowChunk - 1) / kRowChunk);
-  STEP("dec_bgrad/hbm", tfm::launch_colsum<float>(rows, N, A, lda, nullptr, 0, kRowChunk, part, st));
+  const int nz = (int)((rows + kColChunk - 1) / kColChunk);
+  STEP("dec_bgrad/hbm", tfm::launch_colsum<float>(rows, N, A, lda, nullptr, 0, kColChunk, part, st));
   STEP("dec_bgrad_reduce/hbm", tfm::launch_reduce_z(nz, N, N, part, out, accumulate, st));
   return TFM_OK;
 }
