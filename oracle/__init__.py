@@ -2,9 +2,9 @@
 
 TEST INFRASTRUCTURE ONLY: imported by the test-suite, the smoke check and the CPU-baseline leg
 of the benchmark, never by the GPU package.  See layer.py (the post-norm baseline block) and
-prenorm.py (the pre-norm RMSNorm block of the current best record) and ends.py (the encoders,
-decoder and loss around the stack) for what they compute and the readings they take where the
-paper is silent.
+prenorm.py (the pre-norm RMSNorm block of the current best record), ends.py (the encoders,
+decoder and loss around the stack) and optim.py (gradient clipping, Muon, schedule-free AdamW)
+for what they compute and the readings they take where the paper is silent.
 """
 
 from .layer import (LN_EPS, PARAM_ORDER, attention, attention_backward, attention_probs,
