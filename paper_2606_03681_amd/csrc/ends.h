@@ -55,18 +55,23 @@ hipError_t launch_cross_entropy(const EndsGeo& g, const float* logits, const int
 
 // float32 GEMM on the fp32 MFMA: C[M][N] = op(A)[M][K] op(B)[K][N] with an epilogue.
 // op(A)[m][k] = TA ? A[k*lda + m] : A[m*lda + k]; op(B)[k][n] = TB ? B[n*ldb + k] : B[k*ldb + n].
-enum { SG_BIAS = 0, SG_GELU = 1, SG_GELU_GRAD = 2 };
+enum { SG_BIAS = 0, SG_GELU = 1, SG_GELU_GRAD = 2, SG_AXPBY = 3 };
 struct SgemmArgs {
   const float* A;
   const float* B;
   float* C;
   float* C2;          // SG_GELU: GELU(C)
   const float* bias;  // [N] or null (SG_BIAS, SG_GELU)
-  const float* aux;   // SG_GELU_GRAD: pre-activation [M][ldc]; C = acc * GELU'(aux)
+  const float* aux;   // SG_GELU_GRAD: pre-activation, C = acc * GELU'(aux);
+                      // SG_AXPBY: C = alpha * acc + beta * aux  ([M][ldc] like C)
+  float alpha, beta;
   int64_t lda, ldb, ldc;
   int32_t M, N, K;
   int32_t kchunk;     // split-K: grid.z chunks of kchunk (multiple of 16); 0 = whole K
-  int64_t zstride;    // offset of chunk z's output (split-K partials)
+  int64_t zstride;    // offset of grid.z index z's output (split-K partials, or batch entries)
+  int32_t batch;      // kchunk == 0: grid.z runs over `batch` independent products whose A,
+  int64_t bsa, bsb;   // B and aux lie bsa, bsb and bsaux floats apart (C zstride apart)
+  int64_t bsaux;
 };
 hipError_t launch_sgemm(const SgemmArgs& a, bool ta, bool tb, int epi, hipStream_t s);
 

@@ -411,6 +411,10 @@ __global__ __launch_bounds__(256) void k_sgemm(SgemmArgs a) {
   __shared__ float As[16][68];
   __shared__ float Bs[16][68];
   const int m0 = blockIdx.x * 64, n0 = blockIdx.y * 64;
+  // batch entry (kchunk == 0; the strides are 0 for a single product) or K chunk
+  a.A += (int64_t)blockIdx.z * a.bsa;
+  a.B += (int64_t)blockIdx.z * a.bsb;
+  if (a.aux) a.aux += (int64_t)blockIdx.z * a.bsaux;
   const int kb = a.kchunk ? (int)blockIdx.z * a.kchunk : 0;
   const int ke = a.kchunk ? (kb + a.kchunk < a.K ? kb + a.kchunk : a.K) : a.K;
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
@@ -487,6 +491,8 @@ __global__ __launch_bounds__(256) void k_sgemm(SgemmArgs a) {
           float v = acc[i][j][q];
           if (EPI == SG_GELU_GRAD) {
             C[o] = v * gelu_exact_grad(a.aux[o]);
+          } else if (EPI == SG_AXPBY) {
+            C[o] = fmaf(a.alpha, v, a.beta * a.aux[o]);
           } else {
             if (a.bias) v += a.bias[col];
             C[o] = v;
@@ -564,7 +570,8 @@ hipError_t launch_cross_entropy(const EndsGeo& g, const float* logits, const int
 
 hipError_t launch_sgemm(const SgemmArgs& a, bool ta, bool tb, int epi, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
-  const unsigned nz = a.kchunk ? (unsigned)((a.K + a.kchunk - 1) / a.kchunk) : 1u;
+  const unsigned nz = a.kchunk ? (unsigned)((a.K + a.kchunk - 1) / a.kchunk)
+                               : (unsigned)(a.batch > 1 ? a.batch : 1);
   dim3 grid((unsigned)((a.M + 63) / 64), (unsigned)((a.N + 63) / 64), nz ? nz : 1u);
   if (!ta && tb && epi == SG_GELU) k_sgemm<false, true, SG_GELU><<<grid, 256, 0, s>>>(a);
   else if (!ta && tb && epi == SG_BIAS) k_sgemm<false, true, SG_BIAS><<<grid, 256, 0, s>>>(a);
@@ -572,6 +579,8 @@ hipError_t launch_sgemm(const SgemmArgs& a, bool ta, bool tb, int epi, hipStream
     k_sgemm<false, false, SG_GELU_GRAD><<<grid, 256, 0, s>>>(a);
   else if (!ta && !tb && epi == SG_BIAS) k_sgemm<false, false, SG_BIAS><<<grid, 256, 0, s>>>(a);
   else if (ta && !tb && epi == SG_BIAS) k_sgemm<true, false, SG_BIAS><<<grid, 256, 0, s>>>(a);
+  else if (!ta && tb && epi == SG_AXPBY) k_sgemm<false, true, SG_AXPBY><<<grid, 256, 0, s>>>(a);
+  else if (!ta && !tb && epi == SG_AXPBY) k_sgemm<false, false, SG_AXPBY><<<grid, 256, 0, s>>>(a);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -1,4 +1,5 @@
-"""Thin ctypes binding of libtfmlayer.so (C ABI in include/tfm_layer.h and include/tfm_ends.h).
+"""Thin ctypes binding of libtfmlayer.so (C ABI in include/tfm_layer.h, include/tfm_ends.h and
+include/tfm_optim.h).
 
 Argument marshalling only: every step of the layer runs in the library's HIP kernels.  torch
 supplies device memory and the stream.  There is no fallback: if the library is missing, every
@@ -24,7 +25,8 @@ EXPORTS = ("tfm_layer_param_count", "tfm_layer_saved_bytes", "tfm_layer_workspac
            "tfm_infer_workspace_bytes", "tfm_infer_cache_bytes", "tfm_layer_fwd_context",
            "tfm_layer_fwd_query", "tfm_last_error", "tfm_prof_enable", "tfm_prof_collect",
            "tfm_prof_step", "tfm_ends_param_count", "tfm_ends_workspace_bytes", "tfm_encode_fwd",
-           "tfm_encode_bwd", "tfm_decode_fwd", "tfm_decode_loss")
+           "tfm_encode_bwd", "tfm_decode_fwd", "tfm_decode_loss", "tfm_clip_workspace_bytes",
+           "tfm_clip_scale", "tfm_sfadamw_step", "tfm_muon_workspace_bytes", "tfm_muon_step")
 
 
 class TfmError(RuntimeError):
@@ -56,6 +58,16 @@ def make_ends(G, offsets, F, T, Hd, K, decode_mean):
         raise ValueError(f"need G = {G} <= 8 offsets, got {offs}")
     arr = (ctypes.c_int32 * 8)(*(offs + [0] * (8 - len(offs))))
     return tfm_ends(int(G), arr, int(F), int(T), int(Hd), int(K), int(bool(decode_mean)))
+
+
+class tfm_sfadamw(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_float) for n in ("lr", "beta1", "beta2", "eps", "weight_decay")] + \
+        [("warmup", ctypes.c_int32)]
+
+
+class tfm_muon(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_float) for n in ("lr", "momentum", "weight_decay")] + \
+        [("nesterov", ctypes.c_int32), ("ns_steps", ctypes.c_int32)]
 
 
 def lib():
@@ -102,6 +114,19 @@ def lib():
         L.tfm_decode_loss.restype = i32
         L.tfm_decode_loss.argtypes = [P(tfm_dims), E_, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                       i32, vp, sz, vp]
+        i64, f32 = ctypes.c_int64, ctypes.c_float
+        L.tfm_clip_workspace_bytes.restype = sz
+        L.tfm_clip_workspace_bytes.argtypes = [i32, P(i64)]
+        L.tfm_clip_scale.restype = i32
+        L.tfm_clip_scale.argtypes = [i32, P(vp), P(i64), f32, vp, vp, vp, sz, vp]
+        L.tfm_sfadamw_step.restype = i32
+        L.tfm_sfadamw_step.argtypes = [P(tfm_sfadamw), i64, i32, P(i64), P(i64), vp, vp, vp, vp,
+                                       vp, vp]
+        L.tfm_muon_workspace_bytes.restype = sz
+        L.tfm_muon_workspace_bytes.argtypes = [i32, i32, i32]
+        L.tfm_muon_step.restype = i32
+        L.tfm_muon_step.argtypes = [P(tfm_muon), i32, i32, i32, P(vp), P(vp), P(vp), vp, vp, sz,
+                                    vp]
         L.tfm_prof_enable.restype = i32
         L.tfm_prof_enable.argtypes = [i32]
         L.tfm_prof_collect.restype = i32
@@ -291,6 +316,54 @@ def decode_loss(dims, ends, n_train, n_feat, n_class, labels, Y, params, loss, l
                                _ptr(labels), _ptr(Y), _ptr(params), _ptr(loss), _ptr(logits),
                                _ptr(dY), _ptr(grads), int(bool(accumulate)), _ptr(workspace),
                                _nbytes(workspace), _stream(stream))
+    _check(rc)
+
+
+def _ptr_array(ptrs):
+    return (ctypes.c_void_p * len(ptrs))(*[int(p) for p in ptrs])
+
+
+def _i64_array(vals):
+    return (ctypes.c_int64 * len(vals))(*[int(v) for v in vals])
+
+
+def clip_workspace_bytes(counts):
+    return lib().tfm_clip_workspace_bytes(len(counts), _i64_array(counts))
+
+
+def clip_scale(grads, max_norm, scale, norm, workspace, stream=None):
+    """tfm_clip_scale over device float32 tensors (or (pointer, count) pairs): writes the clip
+    factor to scale[0] and the global norm to norm[0] (norm may be None)."""
+    ptrs = [g[0] if isinstance(g, tuple) else g.data_ptr() for g in grads]
+    counts = [g[1] if isinstance(g, tuple) else g.numel() for g in grads]
+    rc = lib().tfm_clip_scale(len(ptrs), _ptr_array(ptrs), _i64_array(counts), float(max_norm),
+                              _ptr(scale), _ptr(norm), _ptr(workspace), _nbytes(workspace),
+                              _stream(stream))
+    _check(rc)
+
+
+def sfadamw_step(hp, t, segments, y, z, v, grad, grad_scale=None, stream=None):
+    """tfm_sfadamw_step; segments: list of (offset, length) into the float32 vectors."""
+    offs = [o for o, _ in segments]
+    lens = [n for _, n in segments]
+    rc = lib().tfm_sfadamw_step(ctypes.byref(hp), int(t), len(segments), _i64_array(offs),
+                                _i64_array(lens), _ptr(y), _ptr(z), _ptr(v), _ptr(grad),
+                                _ptr(grad_scale), _stream(stream))
+    _check(rc)
+
+
+def muon_workspace_bytes(count, rows, cols):
+    return lib().tfm_muon_workspace_bytes(int(count), int(rows), int(cols))
+
+
+def muon_step(hp, rows, cols, W, G, buf, grad_scale, workspace, stream=None):
+    """tfm_muon_step on len(W) matrices of rows x cols; W, G, buf: lists of device pointers (or
+    tensors) of the same length."""
+    conv = [[p if isinstance(p, int) else p.data_ptr() for p in lst] for lst in (W, G, buf)]
+    rc = lib().tfm_muon_step(ctypes.byref(hp), len(conv[0]), int(rows), int(cols),
+                             _ptr_array(conv[0]), _ptr_array(conv[1]), _ptr_array(conv[2]),
+                             _ptr(grad_scale), _ptr(workspace), _nbytes(workspace),
+                             _stream(stream))
     _check(rc)
 
 

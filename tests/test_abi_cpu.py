@@ -287,3 +287,70 @@ def test_decoder_arguments_rejected_before_launch():
                                    nf.ctypes.data, None, 1 << 20, 1 << 20, 1 << 20, 1 << 20,
                                    None, 1 << 20, 1 << 20, 0, 1 << 20, 1 << 40, None)
     assert rc == -5
+
+
+# ---- the optimiser step (include/tfm_optim.h) --------------------------------------------------
+
+def _clip(nvec, counts, ptr=1 << 20, max_norm=1.0, wb=1 << 40, out=1 << 20):
+    ptrs = (ctypes.c_void_p * max(nvec, 1))(*([ptr] * max(nvec, 1)))
+    cnt = (ctypes.c_int64 * max(len(counts), 1))(*counts)
+    return tfm.lib().tfm_clip_scale(nvec, ptrs, cnt, max_norm, out, None, 1 << 20, wb, None)
+
+
+def test_clip_arguments_rejected_before_launch():
+    assert _clip(0, [4]) == -1
+    assert _clip(1, [-1]) == -1
+    assert _clip(1, [8], ptr=0) == -5
+    assert _clip(1, [8], ptr=(1 << 20) + 2) == -5
+    assert _clip(1, [8], max_norm=0.0) == -1
+    assert _clip(1, [8], max_norm=float("inf")) == -1
+    assert _clip(1, [8], out=(1 << 20) + 4) == -5
+    assert _clip(1, [8], wb=0) == -7
+    assert tfm.clip_workspace_bytes([10, 5000]) == 256
+    assert tfm.clip_workspace_bytes([4096 * 300]) == 300 * 4 + (256 - 300 * 4 % 256) % 256
+
+
+def _sf(hp=None, t=1, segs=((0, 4),), ptr=1 << 20):
+    hp = hp or tfm.tfm_sfadamw(1e-3, 0.9, 0.999, 1e-8, 0.0, 0)
+    off = (ctypes.c_int64 * max(len(segs), 1))(*[o for o, _ in segs])
+    ln = (ctypes.c_int64 * max(len(segs), 1))(*[n for _, n in segs])
+    return tfm.lib().tfm_sfadamw_step(ctypes.byref(hp), t, len(segs), off, ln, ptr, ptr, ptr, ptr,
+                                      None, None)
+
+
+def test_sfadamw_arguments_rejected_before_launch():
+    assert _sf(t=0) == -1
+    assert _sf(segs=()) == -1
+    assert _sf(segs=tuple((8 * k, 4) for k in range(65))) == -1
+    assert _sf(segs=((0, 10), (8, 4))) == -1                 # overlap
+    assert "overlap" in tfm.last_error()
+    assert _sf(segs=((-1, 4),)) == -1
+    assert _sf(hp=tfm.tfm_sfadamw(1e-3, 0.9, 1.0, 1e-8, 0.0, 0)) == -1
+    assert _sf(hp=tfm.tfm_sfadamw(-1.0, 0.9, 0.9, 1e-8, 0.0, 0)) == -1
+    assert _sf(hp=tfm.tfm_sfadamw(1e-3, 0.9, 0.9, 1e-8, 0.0, -2)) == -1
+    assert _sf(ptr=0) == -5
+    assert _sf(ptr=(1 << 20) + 2) == -5
+
+
+def _mu(count=2, rows=8, cols=8, hp=None, ptr=1 << 20, wb=1 << 40):
+    hp = hp or tfm.tfm_muon(0.02, 0.95, 0.0, 1, 5)
+    arr = (ctypes.c_void_p * max(count, 1))(*([ptr] * max(count, 1)))
+    return tfm.lib().tfm_muon_step(ctypes.byref(hp), count, rows, cols, arr, arr, arr, None,
+                                   1 << 20, wb, None)
+
+
+def test_muon_arguments_rejected_before_launch():
+    assert _mu(count=0) == -1
+    assert _mu(rows=0) == -1
+    assert _mu(cols=8193) == -1
+    assert _mu(hp=tfm.tfm_muon(0.02, 1.0, 0.0, 1, 5)) == -1
+    assert _mu(hp=tfm.tfm_muon(0.02, 0.9, 0.0, 1, 0)) == -1
+    assert _mu(hp=tfm.tfm_muon(0.02, 0.9, -0.1, 1, 5)) == -1
+    assert _mu(ptr=0) == -5
+    assert _mu(ptr=(1 << 20) + 2) == -5
+    assert _mu(wb=16) == -7
+    w1 = tfm.muon_workspace_bytes(8, 256, 256)
+    assert w1 >= 8 * 256 * 256 * 4 * 4
+    assert tfm.muon_workspace_bytes(16, 256, 256) > w1
+    assert tfm.muon_workspace_bytes(1, 768, 256) == tfm.muon_workspace_bytes(1, 256, 768)
+    assert tfm.muon_workspace_bytes(0, 8, 8) == 0
