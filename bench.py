@@ -140,8 +140,10 @@ def main():
                     help="rows per query chunk of --infer (0: all remaining rows at once)")
     ap.add_argument("--full-step", action="store_true",
                     help="time a whole training step instead: encoders (and thinking rows), the "
-                         "stack forward and backward, the decoder with the loss, and the "
-                         "encoders' gradients, from feature values and labels in HBM")
+                         "stack forward and backward, the decoder with the loss, the encoders' "
+                         "gradients and the optimiser step (clipping, Muon for the pre-norm "
+                         "record's hidden matrices, schedule-free AdamW), from feature values "
+                         "and labels in HBM")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run 5 device-to-device copies of MIB MiB (the known-size copy "
                          "that scales the FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -202,16 +204,19 @@ def main():
             for x in Xq:
                 st.query(x)
     elif args.full_step:
-        from paper_2606_03681_amd.stack import TrainStep
+        from paper_2606_03681_amd.stack import (OPTIM_BASELINE, OPTIM_RECORD, Optimizer,
+                                                TrainStep)
         e = ends_in
         ends = tfm.make_ends(e.G, e.offsets, e.F, e.T, e.Hd, e.K, e.mean)
         st = TrainStep(dims, ends, w.n_train, e.n_feat, e.n_class, w.params, e.params, e.table)
+        opt = Optimizer(st, OPTIM_RECORD if w.block == "pre" else OPTIM_BASELINE)
         X = torch.from_numpy(e.x).cuda()
         dY = torch.from_numpy(e.labels).cuda()
         del w.X
 
         def step():
             st.run(X, dY)
+            opt.step()
     else:
         st = Stack(dims, w.n_train, w.cell_mask, w.params)
         X = to_device(w.X, w.dtype)
@@ -306,6 +311,11 @@ def main():
         out["ends_ms_per_step"] = round(sum(
             v["avg_ms"] * v["launches"] for k, v in steps_out.items()
             if k.startswith(("encode_", "dec_"))) / args.steps, 4) if steps_out else None
+        out["optimizer_ms_per_step"] = round(sum(
+            v["avg_ms"] * v["launches"] for k, v in steps_out.items()
+            if k.startswith(("clip_", "sfadamw", "muon_"))) / args.steps, 4) if steps_out else None
+        out["optimizer"] = "schedule-free AdamW + Muon" if w.block == "pre" else \
+            "schedule-free AdamW"
     del st, X, dY
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:

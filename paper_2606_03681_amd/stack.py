@@ -6,6 +6,7 @@ import numpy as np
 import torch
 
 from . import tfm
+from . import workloads as wl
 from .workloads import bf16_bits_to_f32
 
 
@@ -213,3 +214,93 @@ class TrainStep:
         tfm.encode_bwd(d, e, self.n_train, self.n_feat, x, labels, self.dX, self.ends_grads,
                        False, self.ends_ws)
         return self.loss[:1]
+
+
+# Optimiser settings of Tab. 7 (baseline / current best record); b1, b2, eps and the absent
+# warm-up are the schedule-free defaults.
+OPTIM_BASELINE = dict(lr=1e-4, adamw_wd=0.0, clip=1.0, muon=False)
+OPTIM_RECORD = dict(lr=1e-3, adamw_wd=0.01, clip=2.0, muon=True, muon_lr_ratio=0.1,
+                    muon_momentum=0.96, muon_wd=0.1)
+
+
+def muon_matrices(E, H, block):
+    """(offset, rows, cols) of the hidden weight matrices in a packed layer vector that Muon
+    updates: Q, K and V of each attention as three E x E matrices, both output projections, W1
+    and W2."""
+    out = []
+    off = 0
+    for name, shape, kind in wl.param_layout(E, H, block):
+        n = int(np.prod(shape))
+        if name in ("Wqkv_f", "Wqkv_i"):
+            out += [(off + j * E * E, E, E) for j in range(3)]
+        elif kind == "w":
+            out.append((off, shape[0], shape[1]))
+        off += n
+    return out
+
+
+def adamw_segments(total, matrices):
+    """Segments of a packed vector of `total` floats not covered by the Muon matrices."""
+    covered = sorted((o, o + r * c) for o, r, c in matrices)
+    segs, pos = [], 0
+    for a, b in covered:
+        if a > pos:
+            segs.append((pos, a - pos))
+        pos = max(pos, b)
+    if pos < total:
+        segs.append((pos, total - pos))
+    return segs
+
+
+class Optimizer:
+    """The optimiser step of a TrainStep: gradients clipped by their global norm, Muon on the
+    blocks' hidden matrices (batched over all matrices of one shape), schedule-free AdamW on the
+    rest (every parameter, for the baseline settings).  The model's parameters are the
+    schedule-free y sequence; z starts as a copy of them."""
+
+    def __init__(self, ts, settings, beta1=0.9, beta2=0.999, eps=1e-8, warmup=0):
+        self.ts = ts
+        self.s = dict(settings)
+        dev = ts.ends_params.device
+        E, H = ts.dims.E, ts.dims.H
+        block = "pre" if ts.dims.block == tfm.TFM_BLOCK_PRENORM else "post"
+        self.hp = tfm.tfm_sfadamw(self.s["lr"], beta1, beta2, eps, self.s["adamw_wd"], warmup)
+        # (y, grad, z, v, segments) per parameter vector
+        self.vectors = []
+        mats = muon_matrices(E, H, block) if self.s["muon"] else []
+        for p, g in zip(ts.stack.params, ts.stack.grads):
+            self.vectors.append((p, g, p.clone(), torch.zeros_like(p),
+                                 adamw_segments(p.numel(), mats)))
+        extra = [(ts.ends_params, ts.ends_grads)]
+        if ts.T:
+            extra.append((ts.table.view(-1), ts.table_grad.view(-1)))
+        for p, g in extra:
+            self.vectors.append((p, g, p.clone(), torch.zeros_like(p), [(0, p.numel())]))
+        self.muon = {}
+        if mats:
+            self.muon_hp = tfm.tfm_muon(self.s["lr"] * self.s["muon_lr_ratio"],
+                                        self.s["muon_momentum"], self.s["muon_wd"], 1, 5)
+            self.bufs = [torch.zeros_like(p) for p in ts.stack.params]
+            for (o, r, c) in mats:
+                grp = self.muon.setdefault((r, c), ([], [], []))
+                for p, g, b in zip(ts.stack.params, ts.stack.grads, self.bufs):
+                    grp[0].append(p.data_ptr() + 4 * o)
+                    grp[1].append(g.data_ptr() + 4 * o)
+                    grp[2].append(b.data_ptr() + 4 * o)
+            wb = max(tfm.muon_workspace_bytes(len(v[0]), r, c) for (r, c), v in self.muon.items())
+            self.muon_ws = torch.empty(wb, dtype=torch.uint8, device=dev)
+        self.grads = [v[1] for v in self.vectors]
+        self.clip_ws = torch.empty(tfm.clip_workspace_bytes([g.numel() for g in self.grads]),
+                                   dtype=torch.uint8, device=dev)
+        self.scale = torch.empty(4, dtype=torch.float32, device=dev)
+        self.norm = torch.empty(4, dtype=torch.float32, device=dev)
+        self.t = 0
+
+    def step(self):
+        self.t += 1
+        tfm.clip_scale(self.grads, self.s["clip"], self.scale, self.norm, self.clip_ws)
+        for (r, c), (W, G, B) in self.muon.items():
+            tfm.muon_step(self.muon_hp, r, c, W, G, B, self.scale, self.muon_ws)
+        for y, g, z, v, segs in self.vectors:
+            if segs:
+                tfm.sfadamw_step(self.hp, self.t, segs, y, z, v, g, self.scale)

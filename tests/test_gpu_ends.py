@@ -372,3 +372,66 @@ def test_full_size_ends(cfg):
         err = nerr(got[k], ref[k])
         _say(f"[ends-full] encoder {k}: err {err:.3g}")
         assert err <= tol, k
+
+
+# ---- the optimiser step inside the training step -----------------------------------------------
+
+OPT_CASES = [("d64-f32", 0), ("ragged-small-f32", 2), ("prenorm-small-bf16", 4)]
+
+
+@pytest.mark.parametrize("name,T", OPT_CASES)
+def test_training_step_optimizer_against_oracle(name, T):
+    """Two training steps with the optimiser of Tab. 7 (baseline settings for the post-norm
+    block, the record's Muon + schedule-free AdamW for the pre-norm one).  The oracle's clip,
+    Muon and schedule-free AdamW, fed the gradients the GPU step produced, must give the same
+    parameter changes: this checks which parameters go to which optimiser, the clip over every
+    gradient, and the state carried from step to step."""
+    import torch
+    from oracle import optim
+    from paper_2606_03681_amd.stack import (OPTIM_BASELINE, OPTIM_RECORD, Optimizer, TrainStep,
+                                            muon_matrices)
+    w, e = _setup(name, T=T)
+    pre = w.block == "pre"
+    st = OPTIM_RECORD if pre else OPTIM_BASELINE
+    ts = TrainStep(_dims(w), _ends(e), w.n_train, e.n_feat, e.n_class, w.params, e.params,
+                   e.table)
+    opt = Optimizer(ts, st)
+    x, lab = _dev(e.x), _dev(e.labels)
+    E, H = w.cfg["E"], w.cfg["H"]
+    mats = muon_matrices(E, H, w.block) if st["muon"] else []
+    L = len(ts.stack.params)
+    host = lambda: [v[0].double().cpu().numpy().copy() for v in opt.vectors]  # noqa: E731
+    y0 = host()
+    sf = [optim.ScheduleFreeAdamW(y[np.concatenate([np.arange(o, o + n) for o, n in v[4]])],
+                                  st["lr"], weight_decay=st["adamw_wd"])
+          for y, v in zip(y0, opt.vectors)]
+    mbuf = {}
+    for step in range(2):
+        before = host()
+        ts.run(x, lab)
+        torch.cuda.synchronize()
+        grads = [v[1].double().cpu().numpy().copy() for v in opt.vectors]
+        opt.step()
+        torch.cuda.synchronize()
+        after = host()
+        _, scale = optim.clip_scale(grads, st["clip"])
+        for i, (v, b, a, g) in enumerate(zip(opt.vectors, before, after, grads)):
+            ref = b.copy()
+            idx = np.concatenate([np.arange(o, o + n) for o, n in v[4]])
+            ref[idx] = sf[i].step(scale * g[idx])
+            if i < L:
+                for (o, r, c) in mats:
+                    sl = slice(o, o + r * c)
+                    Wn, mbuf[(i, o)] = optim.muon_step(
+                        b[sl].reshape(1, r, c), scale * g[sl].reshape(1, r, c),
+                        mbuf.get((i, o), np.zeros((1, r, c))), st["lr"] * st["muon_lr_ratio"],
+                        st["muon_momentum"], st["muon_wd"])
+                    ref[sl] = Wn.ravel()
+            err = nerr(a - b, ref - b)
+            # the float32 bar, plus the rounding of the stored float32 parameters: half an ulp
+            # of the new value on the GPU, and the GPU's and the oracle's step-to-step drift
+            # by as much again per step (a 1e-4 step on a value of 1 resolves to 6e-4)
+            tol = 1e-4 + (step + 1) * 2 * 2.0 ** -24 * np.abs(b).max() / np.abs(ref - b).max()
+            _say(f"[train] {name} step {step} vector {i}: update err {err:.3g} (bound {tol:.3g})")
+            assert err <= tol, (step, i, err, tol)
+            assert np.abs(a - b).max() > 0
