@@ -94,18 +94,33 @@ __device__ __forceinline__ f32x4 unpack4(uint2 u) {
 
 }  // namespace
 
+// The single-output epilogues without row reductions (bias, head-major Q|K|V) pass their
+// output tile through LDS in two halves of BM/2 rows and keep one stage in flight ahead of the
+// MFMAs: 44 KB of LDS at E = 192, three workgroups per CU instead of two, so that one
+// workgroup's stores overlap more of the others' loads (their K loops are short: K = E); 8-9 %
+// faster per launch.  The GELU epilogue (two outputs, four barriers per half) was 17 % slower
+// that way, and wider tiles (E = 256) would need more registers than three workgroups per CU
+// leave: both keep the full tile.
+template <int EPI, int BN>
+constexpr bool gemm_half_tile() {
+  return (EPI == EPI_BIAS || EPI == EPI_ITEM_QKV) && BN <= 192;
+}
+
 template <int BN, int EPI, int BM>
-__global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
+__global__ __launch_bounds__(256, (gemm_half_tile<EPI, BN>() ? 3 : 2)) void k_gemm(GemmArgs a) {
   constexpr int MI = BM / 32;          // 16-row blocks per wave (2 x 2 waves, each BM/2 rows)
   constexpr int NBA = BM / 64;         // 1 KB blocks of A per wave and stage
   constexpr int NB = BN / 32;          // 16-wide column blocks per wave
   constexpr int TS = BN + 8;           // epilogue tile row stride (elements)
-  constexpr int S = 3;  // pipeline stages in the LDS ring (60 KB at E = 192 and 128 rows: 2 workgroups per CU)
+  constexpr bool HALF = gemm_half_tile<EPI, BN>();
+  // pipeline stages in the LDS ring (60 KB at E = 192 and 128 rows: 2 workgroups per CU; 40 KB
+  // with two stages)
+  constexpr int S = HALF ? 2 : 3;
   constexpr int A_EL = BM * BK;        // elements of one stage's A rows
   constexpr int STAGE_EL = (BM + BN) * BK;
   constexpr int NBB = BN / 64;         // 1 KB blocks of B per wave and stage
   constexpr int RING_BYTES = S * STAGE_EL * 2;
-  constexpr int TILE_BYTES = BM * TS * 2;
+  constexpr int TILE_BYTES = (HALF ? BM / 2 : BM) * TS * 2;
   // The epilogue's tile and its row / column reduction arrays reuse the ring once it drains.
   constexpr int RED_BYTES = 2 * BM * 4, CRED_BYTES = 4 * BN * 4;
   constexpr int EPI_BYTES = TILE_BYTES + RED_BYTES + CRED_BYTES;
@@ -379,6 +394,47 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs a) {
     return r;
   };
 
+  if (HALF) {
+    if (EPI == EPI_ITEM_QKV)
+      set_rows(ROWS_COMPACT, 0, part);
+    else
+      set_rows(ROWS_COMPACT, a.ldo, -1);
+    // item K is stored pre-multiplied by log2(e)/sqrt(d) (in fp32, before the bf16 rounding):
+    // the attention kernels then get scores in the exp2 domain straight from the MFMA
+    const float ksc =
+        EPI == EPI_ITEM_QKV && part == 1 ? 1.4426950408889634f / sqrtf((float)g.d) : 1.0f;
+    bf16* dst = EPI == EPI_ITEM_QKV ? (part == 0 ? a.out : (part == 1 ? a.out2 : a.out3))
+                                    : a.out;
+    // half h holds tile rows [h BM/2, (h + 1) BM/2): the rows of the waves with wm == h
+    for (int h = 0; h < 2; ++h) {
+      if (wm == h) {
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          const f32x4 b = par4(0, j);
+#pragma unroll
+          for (int i = 0; i < MI; ++i) {
+            const f32x4 v = (acc[i][j] + b) * ksc;
+            *reinterpret_cast<uint2*>(&tile[(i * 16 + lr) * TS + cb0 + j * 16]) =
+                make_uint2(pack2(v[0], v[1]), pack2(v[2], v[3]));
+          }
+        }
+      }
+      lds_barrier();
+      for (int ch = tid; ch < (BM / 2) * CPRW; ch += 256) {
+        const int rl = ch / CPRW, cc = (ch % CPRW) * 8;
+        const int64_t off = rbase[h * (BM / 2) + rl];
+        if (off < 0) continue;
+        int64_t o = off + (EPI == EPI_ITEM_QKV ? 0 : n0) + cc;
+        if (EPI == EPI_ITEM_QKV) {
+          const int head = (pc0 + cc) / g.d, jj = pc0 + cc - head * g.d;
+          o = off + (int64_t)head * g.R * g.d + jj;
+        }
+        stu4(dst + o, ldu4(&tile[rl * TS + cc]));
+      }
+      lds_barrier();  // the next half overwrites the tile
+    }
+    return;
+  }
   if (EPI == EPI_BIAS || EPI == EPI_GELU_FWD || EPI == EPI_ITEM_QKV) {
     if (EPI == EPI_ITEM_QKV)
       set_rows(ROWS_COMPACT, 0, part);
