@@ -90,7 +90,10 @@ int tfm_encode_bwd(const tfm_dims* dims, const tfm_ends* ends, const int32_t* n_
 
 /* Decoder forward only (evaluation): logits, device float32 [T_test][K] with T_test the number
  * of unlabelled rows of the batch, in (dataset, row) order; entries past a dataset's class
- * count are written as computed (the caller ignores them). */
+ * count are written as computed (the caller ignores them).  Here n_train[b] may be anything in
+ * [0, R] (T is not used): rows [n_train[b], R) are decoded, so the stack output of a chunk of
+ * unlabelled rows from the forward-only query calls of tfm_layer.h (n_train = 0) can be
+ * decoded directly. */
 int tfm_decode_fwd(const tfm_dims* dims, const tfm_ends* ends, const int32_t* n_train,
                    const int32_t* n_feat, const void* Y, const float* params, float* logits,
                    void* workspace, size_t workspace_bytes, void* stream);

@@ -81,13 +81,13 @@ Offsets param_offsets(const Shape& s) {
   return o;
 }
 
-// Workspace, sized for the most decoder rows the dims allow (every dataset with one train row
-// past the thinking rows).
+// Workspace, sized for the most decoder rows the dims allow (every row of every dataset: the
+// forward-only decoder call takes tables without labelled rows).
 struct Ws {
   size_t meta, epart, Z, H1, A1, LG, DL, LROW, DH1, DZ, wpart, bpart, total;
 };
 Ws ws_layout(const Shape& s) {
-  const int64_t Tmax = (int64_t)s.B * (s.R - s.T - 1);
+  const int64_t Tmax = (int64_t)s.B * s.R;
   const int64_t nz = (Tmax + kRowChunk - 1) / kRowChunk;
   const int64_t nzc = (Tmax + kColChunk - 1) / kColChunk;
   const int64_t slabs = (int64_t)s.B * ((s.R - s.T + tfm::ENC_ROWS - 1) / tfm::ENC_ROWS);
@@ -117,16 +117,19 @@ Ws ws_layout(const Shape& s) {
 
 // Per-dataset metadata: validates the host arrays, fills the device-side table through kernel
 // arguments and returns the geometry (n_class may be null for the calls that do not need it).
+// n_train[b] must lie in [nt_min, R]: T + 1 for the calls that need a labelled row, 0 for the
+// forward-only decoder.
 int setup(const Shape& s, const int32_t* n_train, const int32_t* n_feat, const int32_t* n_class,
-          char* ws, const Ws& W, EndsGeo& g, hipStream_t st) {
+          char* ws, const Ws& W, EndsGeo& g, hipStream_t st, int nt_min = -1) {
+  if (nt_min < 0) nt_min = s.T + 1;
   if (!n_train || !n_feat) return fail(TFM_ERR_POINTER, "n_train or n_feat is null");
   std::vector<int32_t> blob((size_t)s.B * 4);
   int64_t test0 = 0;
   const int mmax = s.C < s.F ? s.C : s.F;
   for (int b = 0; b < s.B; ++b) {
-    if (n_train[b] < s.T + 1 || n_train[b] > s.R)
-      return fail(TFM_ERR_NTRAIN, "n_train[%d]=%d outside [T+1=%d, R=%d]", b, n_train[b],
-                  s.T + 1, s.R);
+    if (n_train[b] < nt_min || n_train[b] > s.R)
+      return fail(TFM_ERR_NTRAIN, "n_train[%d]=%d outside [%d, R=%d]", b, n_train[b], nt_min,
+                  s.R);
     if (n_feat[b] < 1 || n_feat[b] > mmax)
       return fail(TFM_ERR_DIMS, "n_feat[%d]=%d outside [1, min(C, F)=%d]", b, n_feat[b], mmax);
     if (n_class && (n_class[b] < 1 || n_class[b] > s.K))
@@ -299,7 +302,7 @@ int tfm_decode_fwd(const tfm_dims* dims, const tfm_ends* ends, const int32_t* n_
   hipStream_t st = (hipStream_t)stream;
   char* ws = (char*)workspace;
   EndsGeo g;
-  rc = setup(s, n_train, n_feat, nullptr, ws, W, g, st);
+  rc = setup(s, n_train, n_feat, nullptr, ws, W, g, st, 0);
   if (rc) return rc;
   return decoder_forward(s, g, Y, params, logits, ws, W, st);
 }

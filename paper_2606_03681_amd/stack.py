@@ -304,3 +304,90 @@ class Optimizer:
         for y, g, z, v, segs in self.vectors:
             if segs:
                 tfm.sfadamw_step(self.hp, self.t, segs, y, z, v, g, self.scale)
+
+
+class InferModel:
+    """Evaluation of whole tables through the forward-only path: the encoders build the stack
+    input of every row (the thinking-row table fills rows [0, T)), the context rows — rows
+    [0, max n_train), which hold every labelled row — run through every layer once and leave
+    key/value caches, the remaining rows run through every layer in chunks of unlabelled rows
+    against those caches, and the decoder turns the outputs of each dataset's unlabelled rows
+    into logits.  Allocation, call order and the row order of the result only."""
+
+    def __init__(self, dims, ends, n_train, n_feat, params, ends_params, table=None,
+                 chunk=256, device="cuda", decay_base=0.95):
+        if dims.dtype != tfm.TFM_BF16:
+            raise ValueError("the forward-only path runs in bfloat16")
+        self.dims, self.ends = dims, ends
+        self.n_train = np.ascontiguousarray(n_train, dtype=np.int32)
+        self.n_feat = np.ascontiguousarray(n_feat, dtype=np.int32)
+        B, R, C, E = dims.B, dims.R, dims.C, dims.E
+        self.cell_mask = np.zeros((B, C + 1), np.uint8)
+        for b, m in enumerate(self.n_feat):
+            self.cell_mask[b, :m] = 1
+        self.cell_mask[:, C] = 1
+        self.Rc = int(self.n_train.max())
+        self.chunk = max(1, int(chunk))
+        self.spans = [(a, min(a + self.chunk, R)) for a in range(self.Rc, R, self.chunk)]
+        dc = tfm.tfm_dims.from_buffer_copy(dims)
+        dc.R = self.Rc
+        self.ctx_dims = dc
+        self.stack = InferStack(dc, self.n_train, self.cell_mask, params,
+                                max_query_rows=self.chunk, device=device, decay_base=decay_base)
+        self.ends_params = ends_params if isinstance(ends_params, torch.Tensor) else \
+            torch.from_numpy(np.ascontiguousarray(ends_params, dtype=np.float32)).to(device)
+        self.table = None
+        if ends.T:
+            self.table = table if isinstance(table, torch.Tensor) else \
+                torch.from_numpy(np.ascontiguousarray(table, dtype=np.float32)).to(device)
+            self.think_ws = torch.empty(tfm.workspace_bytes(dims), dtype=torch.uint8,
+                                        device=device)
+        # the decoder calls see tables without thinking rows (T does not enter decoding)
+        self.dec_ends = tfm.tfm_ends.from_buffer_copy(ends)
+        self.dec_ends.T = 0
+        wb = max(tfm.ends_workspace_bytes(dims, ends), tfm.ends_workspace_bytes(dims, self.dec_ends))
+        self.ends_ws = torch.empty(wb, dtype=torch.uint8, device=device)
+        self.X = torch.empty((B, R, C + 1, E), dtype=torch.bfloat16, device=device)
+        self.xq = torch.empty(B * self.chunk * (C + 1) * E, dtype=torch.bfloat16, device=device)
+        self.K = ends.K
+        self.device = device
+
+    def predict(self, x, labels):
+        """x: device float32 [B, R-T, F]; labels: device int32 [B, R-T] (the labelled rows'
+        entries are read).  Returns logits [T_test, K] of the unlabelled rows in (dataset, row)
+        order, as tfm_decode_loss orders them."""
+        d, e = self.dims, self.ends
+        B, C, E = d.B, d.C, d.E
+        if e.T:
+            tfm.thinking_rows_fwd(d, self.n_train, self.cell_mask, e.T, self.table, self.X,
+                                  self.think_ws)
+        tfm.encode_fwd(d, e, self.n_train, self.n_feat, x, labels, self.ends_params, self.X,
+                       self.ends_ws)
+        Xc = self.X[:, :self.Rc].contiguous()
+        parts = []  # (first row, per-dataset row counts, logits of the call)
+        Yc = self.stack.context(Xc)
+        nctx = self.Rc - self.n_train
+        lg = torch.empty((max(int(nctx.sum()), 1), self.K), device=self.device)
+        if nctx.sum() > 0:
+            tfm.decode_fwd(self.ctx_dims, self.dec_ends, self.n_train, self.n_feat, Yc,
+                           self.ends_params, lg, self.ends_ws)
+        parts.append((nctx, lg))
+        for a, b in self.spans:
+            Rq = b - a
+            xq = self.xq[:B * Rq * (C + 1) * E].view(B, Rq, C + 1, E)
+            xq.copy_(self.X[:, a:b])
+            Yq = self.stack.query(xq)
+            dq = tfm.tfm_dims.from_buffer_copy(d)
+            dq.R = Rq
+            lq = torch.empty((B * Rq, self.K), device=self.device)
+            tfm.decode_fwd(dq, self.dec_ends, np.zeros(B, np.int32), self.n_feat, Yq,
+                           self.ends_params, lq, self.ends_ws)
+            parts.append((np.full(B, Rq), lq))
+        # (dataset, row) order: dataset b's rows come from the context call, then each chunk
+        out = []
+        offs = [np.concatenate([[0], np.cumsum(cnt)]) for cnt, _ in parts]
+        for b in range(B):
+            for (cnt, lgp), off in zip(parts, offs):
+                if cnt[b]:
+                    out.append(lgp[off[b]:off[b] + cnt[b]])
+        return torch.cat(out) if out else torch.empty((0, self.K), device=self.device)

@@ -435,3 +435,30 @@ def test_training_step_optimizer_against_oracle(name, T):
             _say(f"[train] {name} step {step} vector {i}: update err {err:.3g} (bound {tol:.3g})")
             assert err <= tol, (step, i, err, tol)
             assert np.abs(a - b).max() > 0
+
+
+# ---- evaluation: encoders, forward-only stack and decoder -------------------------------------
+
+@pytest.mark.parametrize("name,T,chunk,n_train", [("d16-bf16", 0, 11, None),
+                                                  ("prenorm-small-bf16", 4, 64,
+                                                   [150, 120, 5, 199])])
+def test_infer_model_matches_the_training_forward(name, T, chunk, n_train):
+    """Logits of the forward-only path (context rows once, unlabelled rows in chunks) equal,
+    bit for bit, the decoder applied to the training forward's output."""
+    import torch
+    from paper_2606_03681_amd import tfm
+    from paper_2606_03681_amd.stack import InferModel, TrainStep
+    w, e = _setup(name, T=T, n_train=n_train)
+    dims, en = _dims(w), _ends(e)
+    x, lab = _dev(e.x), _dev(e.labels)
+    ts = TrainStep(dims, en, w.n_train, e.n_feat, e.n_class, w.params, e.params, e.table)
+    ts.run(x, lab)
+    ntest = int((w.cfg["R"] - w.n_train).sum())
+    ref = torch.empty((ntest, e.K), device="cuda")
+    tfm.decode_fwd(dims, en, w.n_train, e.n_feat, ts.Y, ts.ends_params, ref, ts.ends_ws)
+    im = InferModel(dims, en, w.n_train, e.n_feat, w.params, e.params, e.table, chunk=chunk)
+    got = im.predict(x, lab)
+    torch.cuda.synchronize()
+    _say(f"[infer-model] {name}: {ntest} rows, {len(im.spans)} query chunks")
+    assert got.shape == ref.shape
+    assert torch.equal(got, ref)
