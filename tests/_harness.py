@@ -4,6 +4,7 @@ and through the float64 oracle on the CPU, and compare."""
 import numpy as np
 
 import oracle
+from oracle import ends as oe
 from paper_2606_03681_amd import workloads as wl
 
 TOL = {"f32": 1e-4, "bf16": 2e-2}
@@ -128,3 +129,97 @@ def oracle_rows(Xb, mask_b, P, heads, n, rows_train, rows_test, dYq=None, block=
     else:
         dz, g = oracle.dataset_backward(dYq, c, P, heads)
     return Y, dz, g, act, keep
+
+
+# ---- the stack's two ends and a whole training step ---------------------------------------
+
+def ends_setup(name, T=None, G=None, mean=None, dtype=None, n_train=None):
+    """A workload (its stack parameters and train prefixes, T thinking rows if given, at least
+    one labelled data row per dataset) and the inputs of its two ends."""
+    w = wl.make_workload(name, with_dY=False)
+    cfg = dict(w.cfg)
+    if T is not None:
+        cfg["thinking"] = T
+    if dtype is not None:
+        cfg["dtype"] = dtype
+    w.cfg = cfg
+    T = cfg.get("thinking", 0)
+    if n_train is not None:
+        w.n_train = np.asarray(n_train, np.int32)
+    w.n_train = np.maximum(w.n_train, T + 1).astype(np.int32)
+    e = wl.make_ends_inputs(w, G=G, mean=mean)
+    return w, e
+
+
+def ends_dims(w):
+    from paper_2606_03681_amd import tfm
+    return tfm.make_dims(dtype=w.dtype, block=w.block,
+                         **{k: v for k, v in w.dims.items() if k != "dtype"})
+
+
+def ends_struct(e):
+    from paper_2606_03681_amd import tfm
+    return tfm.make_ends(e.G, e.offsets, e.F, e.T, e.Hd, e.K, e.mean)
+
+
+def to_dev(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def ends_oracle_params(w, e):
+    return oe.unpack_ends_params(e.params.astype(np.float64), w.cfg["E"], e.G, e.Hd, e.K)
+
+
+def full_labels(w, e):
+    """Labels aligned with the rows of the stack input (thinking rows get 0, never read)."""
+    y = np.zeros((len(w.n_train), w.cfg["R"]))
+    y[:, e.T:] = e.labels
+    return y
+
+
+def oracle_encode(w, e, b=None):
+    sl = slice(None) if b is None else slice(b, b + 1)
+    return oe.encode_forward(e.x[sl], e.labels[sl].astype(np.float64),
+                             (w.n_train - e.T)[sl], e.n_feat[sl], w.cfg["C"], e.offsets,
+                             ends_oracle_params(w, e))
+
+
+def oracle_train_step(w, e):
+    """The oracle's training step: encoders (and thinking rows), the stack, the decoder and loss,
+    and the backward pass.  Returns (loss, packed block gradients, ends gradients, dtable)."""
+    T, C = e.T, w.cfg["C"]
+    P = ends_oracle_params(w, e)
+    Xd, _, cache = oracle_encode(w, e)
+    X = oracle.thinking_rows_forward(Xd, e.table.astype(np.float64), e.cell_mask) if T else Xd
+    Ps = oracle_params(w)
+    heads = w.cfg["heads"]
+    if w.block == "pre":
+        Y, caches = oracle.prenorm_stack_forward(X, Ps, w.n_train, e.cell_mask, heads)
+    else:
+        Y, caches = oracle.stack_forward(X, Ps, w.n_train, e.cell_mask, heads)
+    mode = "mean" if e.mean else "target"
+    loss, dY, dP, _ = oe.decode_loss(Y, full_labels(w, e), w.n_train, e.n_feat, e.n_class, C,
+                                     P, mode)
+    if w.block == "pre":
+        dX, grads = oracle.prenorm_stack_backward(dY, caches)
+        grads = [oracle.pack_prenorm_params(g) for g in grads]
+    else:
+        dX, grads = oracle.stack_backward(dY, caches)
+        grads = [oracle.pack_params(g) for g in grads]
+    dtable = None
+    if T:
+        dX, dtable = oracle.thinking_rows_backward(dX, e.cell_mask, T)
+    dP.update(oe.encode_backward(dX, cache))
+    return loss, grads, dP, dtable
+
+
+def gpu_train_step(w, e):
+    """The same step on the GPU (stack.TrainStep); returns the step object and the loss."""
+    import torch
+    from paper_2606_03681_amd.stack import TrainStep
+    ts = TrainStep(ends_dims(w), ends_struct(e), w.n_train, e.n_feat, e.n_class, w.params,
+                   e.params, e.table)
+    loss = ts.run(to_dev(e.x), to_dev(e.labels))
+    torch.cuda.synchronize()
+    return ts, float(loss.item())

@@ -14,7 +14,10 @@ from oracle import ends as oe
 from paper_2606_03681_amd import workloads as wl
 from paper_2606_03681_amd.stack import to_device
 
-from _harness import TOL, nerr, oracle_params
+from _harness import (TOL, nerr, ends_setup as _setup, ends_dims as _dims,
+                      ends_struct as _ends, to_dev as _dev, ends_oracle_params as _oparams,
+                      full_labels as _full_labels, oracle_encode as _oracle_encode,
+                      oracle_train_step as _oracle_step, gpu_train_step as _gpu_step)
 
 pytestmark = pytest.mark.gpu
 
@@ -32,61 +35,11 @@ def _gpu():
     tfm.lib()
 
 
-def _setup(name, T=None, G=None, mean=None, dtype=None, n_train=None):
-    w = wl.make_workload(name, with_dY=False)
-    cfg = dict(w.cfg)
-    if T is not None:
-        cfg["thinking"] = T
-    if dtype is not None:
-        cfg["dtype"] = dtype
-    w.cfg = cfg
-    T = cfg.get("thinking", 0)
-    if n_train is not None:
-        w.n_train = np.asarray(n_train, np.int32)
-    w.n_train = np.maximum(w.n_train, T + 1).astype(np.int32)
-    e = wl.make_ends_inputs(w, G=G, mean=mean)
-    return w, e
-
-
-def _dims(w):
-    from paper_2606_03681_amd import tfm
-    return tfm.make_dims(dtype=w.dtype, block=w.block,
-                         **{k: v for k, v in w.dims.items() if k != "dtype"})
-
-
-def _ends(e):
-    from paper_2606_03681_amd import tfm
-    return tfm.make_ends(e.G, e.offsets, e.F, e.T, e.Hd, e.K, e.mean)
-
-
-def _dev(a):
-    import torch
-    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
-
-
 def _storage(t, dtype):
     import torch
     if dtype == "f32":
         return t.detach().cpu().numpy()
     return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
-
-
-def _oparams(w, e):
-    return oe.unpack_ends_params(e.params.astype(np.float64), w.cfg["E"], e.G, e.Hd, e.K)
-
-
-def _full_labels(w, e):
-    """Labels aligned with the rows of the stack input (thinking rows get 0, never read)."""
-    y = np.zeros((len(w.n_train), w.cfg["R"]))
-    y[:, e.T:] = e.labels
-    return y
-
-
-def _oracle_encode(w, e, b=None):
-    sl = slice(None) if b is None else slice(b, b + 1)
-    return oe.encode_forward(e.x[sl], e.labels[sl].astype(np.float64),
-                             (w.n_train - e.T)[sl], e.n_feat[sl], w.cfg["C"], e.offsets,
-                             _oparams(w, e))
 
 
 def _ws(dims, en):
@@ -240,43 +193,6 @@ def test_ends_bitwise_deterministic():
 
 
 # ---- a whole training step ---------------------------------------------------------------------
-
-def _oracle_step(w, e):
-    T, C = e.T, w.cfg["C"]
-    P = _oparams(w, e)
-    Xd, _, cache = _oracle_encode(w, e)
-    X = oracle.thinking_rows_forward(Xd, e.table.astype(np.float64), e.cell_mask) if T else Xd
-    Ps = oracle_params(w)
-    heads = w.cfg["heads"]
-    if w.block == "pre":
-        Y, caches = oracle.prenorm_stack_forward(X, Ps, w.n_train, e.cell_mask, heads)
-    else:
-        Y, caches = oracle.stack_forward(X, Ps, w.n_train, e.cell_mask, heads)
-    mode = "mean" if e.mean else "target"
-    loss, dY, dP, _ = oe.decode_loss(Y, _full_labels(w, e), w.n_train, e.n_feat, e.n_class, C,
-                                     P, mode)
-    if w.block == "pre":
-        dX, grads = oracle.prenorm_stack_backward(dY, caches)
-        grads = [oracle.pack_prenorm_params(g) for g in grads]
-    else:
-        dX, grads = oracle.stack_backward(dY, caches)
-        grads = [oracle.pack_params(g) for g in grads]
-    dtable = None
-    if T:
-        dX, dtable = oracle.thinking_rows_backward(dX, e.cell_mask, T)
-    dP.update(oe.encode_backward(dX, cache))
-    return loss, grads, dP, dtable
-
-
-def _gpu_step(w, e):
-    import torch
-    from paper_2606_03681_amd.stack import TrainStep
-    ts = TrainStep(_dims(w), _ends(e), w.n_train, e.n_feat, e.n_class, w.params, e.params,
-                   e.table)
-    loss = ts.run(_dev(e.x), _dev(e.labels))
-    torch.cuda.synchronize()
-    return ts, float(loss.item())
-
 
 STEP_CASES = [("d64-f32", 0, None), ("ragged-small-f32", 2, None), ("d16-bf16", 0, None),
               ("prenorm-small-bf16", 4, None), ("prenorm-d64-bf16", 6, None)]
