@@ -378,3 +378,47 @@ def test_infer_model_matches_the_training_forward(name, T, chunk, n_train):
     _say(f"[infer-model] {name}: {ntest} rows, {len(im.spans)} query chunks")
     assert got.shape == ref.shape
     assert torch.equal(got, ref)
+
+
+def test_ends_at_the_envelope_limits():
+    """The largest group (8 shifts), the most decoder outputs (64 classes), 255 feature cells
+    and a table whose feature count is 1; encoders and decoder against the oracle."""
+    import torch
+    from paper_2606_03681_amd import tfm
+    rng = np.random.default_rng(31)
+    B, R, C, E, Hd, K, G = 2, 24, 255, 64, 48, 64, 8
+    offs = (0, 1, 3, 7, 12, 20, 30, 44)
+    n_train = np.array([17, 3], np.int32)
+    n_feat = np.array([255, 1], np.int32)
+    n_class = np.array([64, 2], np.int32)
+    x = rng.normal(size=(B, R, C)).astype(np.float32)
+    lab = np.stack([rng.integers(0, n_class[b], R) for b in range(B)]).astype(np.int32)
+    P = rng.normal(0, 0.3, oe.ends_param_count(E, G, Hd, K)).astype(np.float32)
+    dims = tfm.make_dims(B, R, C, E, 2, 128, "f32")
+    en = tfm.make_ends(G, offs, C, 0, Hd, K, 1)
+    ws = torch.empty(tfm.ends_workspace_bytes(dims, en), dtype=torch.uint8, device="cuda")
+    X = torch.empty((B, R, C + 1, E), device="cuda")
+    tfm.encode_fwd(dims, en, n_train, n_feat, _dev(x), _dev(lab), _dev(P), X, ws)
+    Po = oe.unpack_ends_params(P.astype(np.float64), E, G, Hd, K)
+    Xr, mask, cache = oe.encode_forward(x, lab.astype(np.float64), n_train, n_feat, C, offs, Po)
+    assert nerr(X.cpu().numpy(), Xr) <= TOL["f32"]
+    Y = torch.randn((B, R, C + 1, E), device="cuda")
+    loss = torch.empty(4, device="cuda")
+    dY = torch.empty_like(Y)
+    grads = torch.zeros(P.size, device="cuda")
+    lg = torch.empty((int((R - n_train).sum()), K), device="cuda")
+    tfm.decode_loss(dims, en, n_train, n_feat, n_class, _dev(lab), Y, _dev(P), loss, lg, dY,
+                    grads, False, ws)
+    dXs = torch.randn((B, R, C + 1, E), device="cuda")
+    tfm.encode_bwd(dims, en, n_train, n_feat, _dev(x), _dev(lab), dXs, grads, False, ws)
+    torch.cuda.synchronize()
+    Yh = Y.double().cpu().numpy()
+    rl, rdY, rdP, rlg = oe.decode_loss(Yh, lab.astype(np.float64), n_train, n_feat, n_class, C,
+                                       Po, "mean")
+    rdP.update(oe.encode_backward(dXs.double().cpu().numpy(), cache))
+    assert abs(float(loss[0].item()) - rl) <= TOL["f32"] * abs(rl)
+    assert nerr(lg.double().cpu().numpy(), rlg) <= TOL["f32"]
+    assert nerr(dY.double().cpu().numpy(), rdY) <= TOL["f32"]
+    got = oe.unpack_ends_params(grads.double().cpu().numpy(), E, G, Hd, K)
+    for k in oe.ENDS_PARAM_ORDER:
+        assert nerr(got[k], rdP[k]) <= TOL["f32"], k

@@ -131,3 +131,51 @@ def test_muon_against_oracle(count, rows, cols):
              f"update {eO:.3g}")
         assert eW <= TOL and eb <= TOL
         assert eO <= TOL  # the update itself, recovered through a float32 difference
+
+
+@pytest.mark.parametrize("count,rows,cols", [(1, 1, 1), (3, 1, 40), (2, 40, 1), (1, 300, 7)])
+def test_muon_degenerate_shapes(count, rows, cols):
+    """1 x 1 matrices (the map drives a scalar toward sign), single rows and columns (the map
+    normalises a vector), and a strongly tall matrix."""
+    import torch
+    from paper_2606_03681_amd import tfm
+    rng = np.random.default_rng(count * 100 + rows + cols)
+    W0 = rng.normal(0, 0.05, size=(count, rows, cols)).astype(np.float32)
+    G = rng.normal(size=(count, rows, cols)).astype(np.float32)
+    Wd, Gd = _dev(W0.reshape(-1)), _dev(G.reshape(-1))
+    bd = torch.zeros(count * rows * cols, device="cuda")
+    nel = rows * cols
+    hp = tfm.tfm_muon(0.02, 0.95, 0.1, 1, 5)
+    ws = torch.empty(tfm.muon_workspace_bytes(count, rows, cols), dtype=torch.uint8,
+                     device="cuda")
+    tfm.muon_step(hp, rows, cols, [Wd.data_ptr() + 4 * i * nel for i in range(count)],
+                  [Gd.data_ptr() + 4 * i * nel for i in range(count)],
+                  [bd.data_ptr() + 4 * i * nel for i in range(count)], None, ws)
+    W, _ = optim.muon_step(W0.astype(np.float64), G.astype(np.float64),
+                           np.zeros((count, rows, cols)), 0.02, 0.95, 0.1)
+    torch.cuda.synchronize()
+    got = Wd.cpu().numpy().reshape(count, rows, cols).astype(np.float64)
+    e = nerr(got, W)
+    _say(f"[optim] muon degenerate {count}x{rows}x{cols}: W {e:.3g}")
+    assert e <= TOL
+
+
+def test_sfadamw_long_warmup_schedule_scalars():
+    """The step scalars come from a closed form of sum_{i<=t} s_i^2: check them deep into and
+    past a long warm-up against the oracle run step by step."""
+    import torch
+    from paper_2606_03681_amd import tfm
+    rng = np.random.default_rng(12)
+    n = 64
+    y0 = rng.normal(size=n).astype(np.float32)
+    hp = tfm.tfm_sfadamw(3e-3, 0.9, 0.999, 1e-8, 0.01, 40)
+    y, z, v = _dev(y0), _dev(y0), torch.zeros(n, device="cuda")
+    opt = optim.ScheduleFreeAdamW(y0.astype(np.float64), 3e-3, weight_decay=0.01, warmup=40)
+    for t in range(1, 61):
+        g = rng.normal(size=n).astype(np.float32)
+        tfm.sfadamw_step(hp, t, [(0, n)], y, z, v, _dev(g))
+        ref = opt.step(g.astype(np.float64))
+    torch.cuda.synchronize()
+    e = nerr(y.cpu().numpy(), ref)
+    _say(f"[optim] sfadamw 60 steps, warm-up 40: y {e:.3g}")
+    assert e <= TOL
