@@ -119,7 +119,8 @@ int tfm_layer_bwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* c
  * prepended along the row axis, broadcast over the cell columns and counted as train rows.
  * dims, n_train and cell_mask describe the stack input X[B][R][C+1][E] whose rows [0, T) are the
  * thinking rows (n_train includes them, 1 <= T <= min(n_train)); workspace is a
- * tfm_layer_workspace_bytes() scratch (it holds the column map).
+ * tfm_layer_workspace_bytes() or tfm_infer_workspace_bytes() scratch (only its leading bytes
+ * are used: the column map).
  *
  * tfm_thinking_rows_fwd writes table[T][E] (device, float32, rounded to dims->dtype) into rows
  * [0, T) of every active cell column of X and 0 into rows [0, T) of inactive columns; other rows

@@ -150,9 +150,9 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
   gload(0);
   sstore(0);
   lds_barrier();
-  // two chunks per iteration, so every LDS buffer offset is a constant
+  // one query chunk into LDS buffer b (a constant when bc is an integral_constant)
   auto step = [&](int ic, auto bc) __attribute__((always_inline)) {
-    constexpr int b = decltype(bc)::value;
+    const int b = (int)bc;
     if (ic + 1 < NCH) gload((ic + 1) * QC);
     // S = Q K^T, dP = dO V^T per (query block, key block); lane: queries qb*16 + 4*lg + i
     uint32_t pw[2][4][2], sw[2][4][2];
@@ -196,10 +196,16 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
     if (ic + 1 < NCH) sstore(b ^ 1);
     lds_barrier();
   };
-  for (int ic = 0; ic < NCH; ic += 2) {
-    step(ic, std::integral_constant<int, 0>{});
-    if (ic + 1 >= NCH) break;
-    step(ic + 1, std::integral_constant<int, 1>{});
+  if constexpr (D <= 32) {
+    // two chunks per iteration, so every LDS buffer offset is a constant
+    for (int ic = 0; ic < NCH; ic += 2) {
+      step(ic, std::integral_constant<int, 0>{});
+      if (ic + 1 >= NCH) break;
+      step(ic + 1, std::integral_constant<int, 1>{});
+    }
+  } else {
+    // at d = 64 a doubled body needs more than 256 VGPRs (one wave per SIMD): keep one
+    for (int ic = 0; ic < NCH; ++ic) step(ic, ic & 1);
   }
   // lane: dims db*16 + 4*lg + i of key kw0 + kb*16 + c
 #pragma unroll

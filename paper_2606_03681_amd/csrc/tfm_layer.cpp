@@ -1103,10 +1103,11 @@ static int thinking_setup(const tfm_dims* dims, const int32_t* n_train, const ui
   int rc = check_dims(dims, d);
   if (rc) return rc;
   if (!aligned(workspace)) return fail(TFM_ERR_POINTER, "workspace must be 16-byte aligned");
-  const WsLayout W = ws_layout(d);
-  if (workspace_bytes < W.total)
-    return fail(TFM_ERR_BUFFER, "workspace has %zu bytes, %zu required", workspace_bytes,
-                W.total);
+  // only the column map is used: it leads both the training and the forward-only workspaces
+  Arena a;
+  const MetaOff M = take_meta(d, a);
+  if (workspace_bytes < a.off)
+    return fail(TFM_ERR_BUFFER, "workspace has %zu bytes, %zu required", workspace_bytes, a.off);
   Plan P;
   rc = make_plan(d, n_train, cell_mask, P);
   if (rc) return rc;
@@ -1114,7 +1115,7 @@ static int thinking_setup(const tfm_dims* dims, const int32_t* n_train, const ui
     if (T < 1 || T > n_train[b])
       return fail(TFM_ERR_DIMS, "T=%d thinking rows outside [1, n_train[%d]=%d]", T, b,
                   n_train[b]);
-  return setup_geo(d, P, (char*)workspace, W.meta, g, s);
+  return setup_geo(d, P, (char*)workspace, M, g, s);
 }
 
 int tfm_thinking_rows_fwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* cell_mask,

@@ -340,8 +340,6 @@ class InferModel:
         if ends.T:
             self.table = table if isinstance(table, torch.Tensor) else \
                 torch.from_numpy(np.ascontiguousarray(table, dtype=np.float32)).to(device)
-            self.think_ws = torch.empty(tfm.workspace_bytes(dims), dtype=torch.uint8,
-                                        device=device)
         # the decoder calls see tables without thinking rows (T does not enter decoding)
         self.dec_ends = tfm.tfm_ends.from_buffer_copy(ends)
         self.dec_ends.T = 0
@@ -360,7 +358,7 @@ class InferModel:
         B, C, E = d.B, d.C, d.E
         if e.T:
             tfm.thinking_rows_fwd(d, self.n_train, self.cell_mask, e.T, self.table, self.X,
-                                  self.think_ws)
+                                  self.stack.workspace)
         tfm.encode_fwd(d, e, self.n_train, self.n_feat, x, labels, self.ends_params, self.X,
                        self.ends_ws)
         Xc = self.X[:, :self.Rc].contiguous()
