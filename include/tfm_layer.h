@@ -40,7 +40,8 @@
  * tfm_last_error() describes it.
  *
  * Supported envelope: B >= 1, R >= 1, 0 <= C <= 255, heads >= 1, d = E/heads in {16, 32, 64},
- * 32 <= E <= 256 with E % 32 == 0, 32 <= H <= 1024 with H % 32 == 0.
+ * 32 <= E <= 256 with E % 32 == 0, 32 <= H <= 1024 with H % 32 == 0, at most 2^26 cells
+ * B*R*(C+1) in all, and R*(C+1)*E <= 715,827,882 (one dataset's bfloat16 Q|K|V under 4 GiB).
  *
  * Pre-norm block (dims->block == TFM_BLOCK_PRENORM): the block of the paper's current best
  * record (Sec. 5 "Residual Decay" and "RMSNorm, Thinking Rows", the Fig. 4 caption, App. B.6,

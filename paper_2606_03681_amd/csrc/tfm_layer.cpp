@@ -6,6 +6,7 @@
 
 #include <cmath>
 #include <cstdarg>
+#include <cstdint>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -67,6 +68,11 @@ int check_dims(const tfm_dims* p, Dims& d) {
   if (d.Nmax > kMaxCells)
     return fail(TFM_ERR_DIMS, "B*R*(C+1)=%lld cells exceeds %lld", (long long)d.Nmax,
                 (long long)kMaxCells);
+  // the attention kernels address one dataset's bf16 Q|K|V [C+1][R][3E] through 32-bit
+  // buffer offsets
+  if ((int64_t)d.R * d.S * 3 * d.E * 2 > (int64_t)UINT32_MAX)
+    return fail(TFM_ERR_DIMS, "R*(C+1)*E=%lld: one dataset's Q|K|V would exceed 4 GiB",
+                (long long)d.R * d.S * d.E);
   d.tsz = d.dtype == TFM_F32 ? 4 : 2;
   d.words = (d.S + 31) / 32;
   d.block = p->block;

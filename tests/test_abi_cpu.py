@@ -74,6 +74,8 @@ def test_sizes_positive_and_grow_with_batch():
     (dict(block="pre", dtype="bf16", E=96, heads=3), -1),          # ... and E in {64,...,256}
     (dict(block="pre", dtype="bf16", H=96), -1),                   # ... and H % E == 0
     (dict(block="pre", dtype="bf16", decay=float("nan")), -1),
+    (dict(B=1, R=1 << 20, C=15, E=256, heads=4), -1),          # one dataset's Q|K|V > 4 GiB
+    (dict(B=20, R=1 << 20, C=3), -1),                          # more than 2^26 cells
 ])
 def test_invalid_dims_rejected(kw, code):
     d = _dims(**kw)
