@@ -137,8 +137,7 @@ __global__ __launch_bounds__(256) void k_feat_attn_fwd(Geo g, const bf16* __rest
         }
       }
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    mx = rows4_max(mx);
     const float mb = -mx * c2;
     float l = 0.f;
 #pragma unroll
@@ -152,8 +151,7 @@ __global__ __launch_bounds__(256) void k_feat_attn_fwd(Geo g, const bf16* __rest
       } else {
         s[kb] = zero4();
       }
-    l += __shfl_xor(l, 16, 64);
-    l += __shfl_xor(l, 32, 64);
+    l = rows4_sum(l);
     f32x4 oacc[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db) oacc[db] = zero4();
@@ -233,8 +231,7 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
 #pragma unroll
   for (int kb = 0; kb < NKB; ++kb)
     if (kb < nks) {
-      dq[kb] += __shfl_xor(dq[kb], 16, 64);
-      dq[kb] += __shfl_xor(dq[kb], 32, 64);
+      dq[kb] = rows4_sum(dq[kb]);
       if (lg == 0) {
         Lr[w][kb * 16 + c] = nbq[kb];
         Dr[w][kb * 16 + c] = dq[kb];

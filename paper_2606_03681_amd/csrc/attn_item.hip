@@ -148,8 +148,7 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
       for (int kb = 1; kb < 4; ++kb)
         mx = fmaxf(mx, fmaxf(fmaxf(sc[kb][qb][0], sc[kb][qb][1]),
                              fmaxf(sc[kb][qb][2], sc[kb][qb][3])));
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      mx = rows4_max(mx);
       // first tile: ref = the tile maximum; later: raise ref by the excess when it is large
       const bool first = ref[qb] == -INFINITY;
       if (__any(first || mx > slack)) {

@@ -274,8 +274,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
     df[qb] = HF<D>::buf(rdO, qq * rowO, lg);
     const typename HF<D>::frag of = HF<D>::buf(rO, qq * rowO, lg);
     float dot = hf_dot<D>(df[qb], of);
-    dot += __shfl_xor(dot, 16, 64);
-    dot += __shfl_xor(dot, 32, 64);
+    dot = rows4_sum(dot);
     Dv[qb] = dot;
     nb[qb] = -bloadf(rL, qq * 4) * LOG2E;
     if (lg == 0 && (int)qq < R) Dbuf[prob * R + qq] = dot;

@@ -150,11 +150,8 @@ __global__ __launch_bounds__(512) void k_ln_out_bwd(Geo g, const bf16* __restric
         s1 += dy[j] * gm[j];
         s2 += dy[j] * gm[j] * x[j];
       }
-#pragma unroll
-      for (int o = 1; o < 32; o <<= 1) {
-        s1 += __shfl_xor(s1, o, 64);
-        s2 += __shfl_xor(s2, o, 64);
-      }
+      s1 = half32_sum(s1);
+      s2 = half32_sum(s2);
       const float m1 = s1 / E, m2 = s2 / E;
       if (ok[u] && act) {
         uint4 o;
@@ -235,8 +232,7 @@ __global__ __launch_bounds__(512) void k_rms_in(Geo g, const bf16* __restrict__ 
         x[j] = decay * bf2f(u4_elem(xv[u], j));
         ss += x[j] * x[j];
       }
-#pragma unroll
-      for (int o = 1; o < 32; o <<= 1) ss += __shfl_xor(ss, o, 64);
+      ss = half32_sum(ss);
       const float rs = 1.0f / sqrtf(ss / E + eps);
       if (ok[u] && l == 0) rstd[pc[u]] = rs;
       if (ok[u] && act) {

@@ -69,20 +69,6 @@ __device__ __forceinline__ int64_t row_addr(const Geo& g, int mode, int64_t m, i
   return mode == ROWS_NATIVE ? native_cell(g, m) * g.E : m * ld;
 }
 
-// Sum over the 16 lanes that share lane / 16.
-__device__ __forceinline__ float sum16(float v) {
-  v += __shfl_xor(v, 1, 64);
-  v += __shfl_xor(v, 2, 64);
-  v += __shfl_xor(v, 4, 64);
-  v += __shfl_xor(v, 8, 64);
-  return v;
-}
-// Sum over the 4 lanes that share lane % 16.
-__device__ __forceinline__ float sum4g(float v) {
-  v += __shfl_xor(v, 16, 64);
-  v += __shfl_xor(v, 32, 64);
-  return v;
-}
 __device__ __forceinline__ f32x4 unpack4(uint2 u) {
   f32x4 r;
   r[0] = __uint_as_float(u.x << 16);
@@ -531,7 +517,7 @@ __global__ __launch_bounds__(256, (gemm_half_tile<EPI, BN>() ? 3 : 2)) void k_ge
         const f32x4 v = f(i, j);
         sm += (v[0] + v[1]) + (v[2] + v[3]);
       }
-      sm = sum4g(sm);
+      sm = rows4_sum(sm);
       if (lg == 0) red[wn][rloc(i)] = sm;
     }
     lds_barrier();
@@ -608,7 +594,7 @@ __global__ __launch_bounds__(256, (gemm_half_tile<EPI, BN>() ? 3 : 2)) void k_ge
       }
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const float t1 = sum16(s1[q]), t2 = sum16(s2[q]);
+        const float t1 = row16_sum(s1[q]), t2 = row16_sum(s2[q]);
         if (lr == 0) {
           cred[0][wm][cb0 + j * 16 + q] = t1;
           cred[1][wm][cb0 + j * 16 + q] = t2;
@@ -688,7 +674,7 @@ __global__ __launch_bounds__(256, (gemm_half_tile<EPI, BN>() ? 3 : 2)) void k_ge
       for (int i = 0; i < MI; ++i) s1 += acc[i][j] * tile4(i, j) * rsi[i];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const float t1 = sum16(s1[q]);
+        const float t1 = row16_sum(s1[q]);
         if (lr == 0) cred[0][wm][cb0 + j * 16 + q] = t1;
       }
     }

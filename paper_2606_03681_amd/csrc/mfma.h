@@ -110,6 +110,48 @@ __device__ __forceinline__ uint16_t u4_elem(const uint4& u, int j) {
   return (uint16_t)((j & 1) ? (w >> 16) : (w & 0xffffu));
 }
 
+// Cross-lane sums and maxima that stay in the VALU (no LDS permute).  Within a 16-lane row:
+// DPP moves pair lanes i ^ 1 and i ^ 2 (quad permutes), then the half-row mirror and the row
+// mirror pair the same groups of four and eight lanes as i ^ 4 and i ^ 8 would.  Across the
+// four rows: the row swaps of gfx950 (rows 0 <-> 1 and 2 <-> 3, then the two halves).  Every
+// lane of the group ends with the same value, added in the same tree as an xor butterfly.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+// Sum over the 16 lanes of the lane's row (lanes sharing lane / 16).
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_mov<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+  v += dpp_mov<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+  v += dpp_mov<0x141>(v);  // row_half_mirror
+  v += dpp_mov<0x140>(v);  // row_mirror
+  return v;
+}
+// Sum over the 32 lanes of the lane's half-wave (lanes sharing lane / 32).
+__device__ __forceinline__ float half32_sum(float v) {
+  v = row16_sum(v);
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return __uint_as_float(a[0]) + __uint_as_float(a[1]);
+}
+// Sum and maximum over the 4 lanes that share lane % 16 (one per row).
+__device__ __forceinline__ float rows4_sum(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  v = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+__device__ __forceinline__ float rows4_max(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
 __device__ __forceinline__ float wave_reduce_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

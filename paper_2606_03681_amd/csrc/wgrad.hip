@@ -287,8 +287,7 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
 #pragma unroll
     for (int i = 0; i < NBW; ++i) {
       float t = bacc[i];
-      t += __shfl_xor(t, 16, 64);
-      t += __shfl_xor(t, 32, 64);
+      t = rows4_sum(t);
       if (lg == 0) a.bpart[zb * a.N + n0 + wn * (BN / 2) + i * 16 + c] = t;
     }
   }
