@@ -212,7 +212,33 @@ def _feature_attention_backward(da, z, c, P, heads, row_chunk=128):
     return dz, g
 
 
-def _item_attention(h, P, heads, n_train, qrows, col_chunk=4):
+# Worker threads over the (column, head) problems of item-axis attention.  Execution only: each
+# problem is computed by the same calls whatever the count (numpy releases the interpreter lock
+# in its kernels, so the problems of large workloads run on several cores), and every problem
+# writes its own slice of the result.
+_WORKERS = 1
+
+
+def set_workers(n):
+    """Number of threads that evaluate item-axis attention problems (default 1)."""
+    global _WORKERS
+    _WORKERS = max(1, int(n))
+
+
+def _each_problem(fn, S, heads):
+    """fn(c, j) for every column c < S and head j < heads."""
+    items = [(c, j) for c in range(S) for j in range(heads)]
+    if _WORKERS <= 1 or len(items) <= 1:
+        for c, j in items:
+            fn(c, j)
+        return
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(_WORKERS) as ex:
+        for f in [ex.submit(fn, c, j) for c, j in items]:
+            f.result()
+
+
+def _item_attention(h, P, heads, n_train, qrows):
     """Item-axis attention down each column: every query row of a column attends to the rows
     t < n_train of the same column.  h: (R, S, E).  Keys and values are computed for the train
     rows only; queries for the rows listed in qrows (all rows in the plain layer).  Returns the
@@ -223,17 +249,19 @@ def _item_attention(h, P, heads, n_train, qrows, col_chunk=4):
     q = zt[:, qrows] @ W[:E].T + b[:E]                         # query rows
     k = zt[:, :n_train] @ W[E:2 * E].T + b[E:2 * E]            # train rows only
     v = zt[:, :n_train] @ W[2 * E:].T + b[2 * E:]
-    o = np.empty_like(q)
-    for c0 in range(0, zt.shape[0], col_chunk):
-        sl = slice(c0, c0 + col_chunk)
-        o[sl] = merge_heads(attention(split_heads(q[sl], heads), split_heads(k[sl], heads),
-                                      split_heads(v[sl], heads)))
-    o = np.swapaxes(o, 0, 1)                                   # (len(qrows), S, E)
+    qh, kh, vh = split_heads(q, heads), split_heads(k, heads), split_heads(v, heads)
+    oh = np.empty_like(qh)                                     # (S, heads, len(qrows), d)
+
+    def one(c, j):
+        oh[c, j] = attention(qh[c, j], kh[c, j], vh[c, j])
+
+    _each_problem(one, zt.shape[0], heads)
+    o = np.swapaxes(merge_heads(oh), 0, 1)                     # (len(qrows), S, E)
     a = o @ P["Wo_i"].T + P["bo_i"]
     return a, {"q": q, "k": k, "v": v, "o": o}
 
 
-def _item_attention_backward(da, h, c, P, heads, n_train, qrows, col_chunk=4):
+def _item_attention_backward(da, h, c, P, heads, n_train, qrows):
     """Gradient of _item_attention; da: (len(qrows), S, E).  Returns dh for all R rows."""
     E = h.shape[-1]
     W = P["Wqkv_i"]
@@ -241,16 +269,16 @@ def _item_attention_backward(da, h, c, P, heads, n_train, qrows, col_chunk=4):
     g["Wo_i"] = outer_sum(da, c["o"])
     g["bo_i"] = da.sum(axis=(0, 1))
     dot = np.swapaxes(da @ P["Wo_i"], 0, 1)                    # (S, len(qrows), E)
-    dq = np.empty_like(c["q"])
-    dk = np.empty_like(c["k"])
-    dv = np.empty_like(c["v"])
-    for c0 in range(0, dot.shape[0], col_chunk):
-        sl = slice(c0, c0 + col_chunk)
-        a, b_, v_ = attention_backward(split_heads(c["q"][sl], heads),
-                                       split_heads(c["k"][sl], heads),
-                                       split_heads(c["v"][sl], heads),
-                                       split_heads(dot[sl], heads))
-        dq[sl], dk[sl], dv[sl] = merge_heads(a), merge_heads(b_), merge_heads(v_)
+    qh, kh, vh = split_heads(c["q"], heads), split_heads(c["k"], heads), split_heads(c["v"], heads)
+    doh = split_heads(dot, heads)
+    dqh, dkh, dvh = np.empty_like(qh), np.empty_like(kh), np.empty_like(vh)
+
+    def one(cc, j):
+        dqh[cc, j], dkh[cc, j], dvh[cc, j] = attention_backward(qh[cc, j], kh[cc, j], vh[cc, j],
+                                                                doh[cc, j])
+
+    _each_problem(one, dot.shape[0], heads)
+    dq, dk, dv = merge_heads(dqh), merge_heads(dkh), merge_heads(dvh)
     zt = np.swapaxes(h, 0, 1)
     ztr = zt[:, :n_train]
     g["Wqkv_i"] = np.concatenate([
