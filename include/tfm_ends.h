@@ -2,7 +2,7 @@
  * tfm_ends.h — C ABI of the two ends of the stack on MI355X (gfx950): the encoders that turn a
  * batch of tables into the stack input, and the decoder with the cross-entropy loss that turns
  * the stack output into the training loss (paper "Speedrunning Tabular Foundation Model
- * Pretraining", Fig. 3 and Fig. 4 captions, Tab. 7, App. "Repeated Feature Grouping" and
+ * Pretraining", Fig. 3 and Fig. 4 captions, Tab. 5, App. "Repeated Feature Grouping" and
  * "Autoresearch").  With tfm_layer.h this covers a whole training step:
  *
  *     X  = encode(x, labels)             tfm_encode_fwd   (+ tfm_thinking_rows_fwd)

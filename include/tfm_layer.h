@@ -45,7 +45,7 @@
  *
  * Pre-norm block (dims->block == TFM_BLOCK_PRENORM): the block of the paper's current best
  * record (Sec. 5 "Residual Decay" and "RMSNorm, Thinking Rows", the Fig. 4 caption, App. B.6,
- * Tab. 7), with c = dims->decay (0.95^i for block i of a stack):
+ * Tab. 5), with c = dims->decay (0.95^i for block i of a stack):
  *
  *     X' = c X
  *     H1 = X' + FeatureAttention(RMS1(X'))
@@ -116,7 +116,7 @@ int tfm_layer_bwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* c
                   const void* dY, void* dX, float* grads, int accumulate,
                   void* workspace, size_t workspace_bytes, void* stream);
 
-/* Thinking rows (Sec. 5 "RMSNorm, Thinking Rows", App. B.6, Tab. 7): learned E-vectors
+/* Thinking rows (Sec. 5 "RMSNorm, Thinking Rows", App. B.6, Tab. 5): learned E-vectors
  * prepended along the row axis, broadcast over the cell columns and counted as train rows.
  * dims, n_train and cell_mask describe the stack input X[B][R][C+1][E] whose rows [0, T) are the
  * thinking rows (n_train includes them, 1 <= T <= min(n_train)); workspace is a

@@ -1,7 +1,7 @@
 /*
  * tfm_optim.h — C ABI of the optimiser step on MI355X (gfx950) (paper "Speedrunning Tabular
  * Foundation Model Pretraining", Sec. 5 "Muon Optimizer" and "Batched Muon, Compile", App.
- * "Muon Optimizer", "Batched Muon, Compile", "LAWA, AdamW Weight Decay", Tab. 7): clipping of the
+ * "Muon Optimizer", "Batched Muon, Compile", "LAWA, AdamW Weight Decay", Tab. 5): clipping of the
  * gradients by their global norm, Muon on the hidden weight matrices of the blocks with the
  * Newton–Schulz iteration batched over equally shaped matrices (the Q, K and V matrices of a
  * block, and the same matrices of every block), and schedule-free AdamW on the other parameters.
@@ -22,7 +22,7 @@
 extern "C" {
 #endif
 
-/* ---- gradient clipping (Tab. 7 "Gradient clip") --------------------------------------------
+/* ---- gradient clipping (Tab. 5 "Gradient clip") --------------------------------------------
  * norm = the L2 norm of the concatenation of nvec gradient arrays grads[i] (counts[i] floats
  * each; host arrays of device pointers and counts, nvec in [1, 1024]); scale = min(1, max_norm /
  * (norm + 1e-6)), the factor the optimisers below take as grad_scale.  scale and norm (nullable)
@@ -32,7 +32,7 @@ int tfm_clip_scale(int32_t nvec, const float* const* grads, const int64_t* count
                    float* scale, float* norm, void* workspace, size_t workspace_bytes,
                    void* stream);
 
-/* ---- schedule-free AdamW (App. "Baseline": the baseline's optimiser; Tab. 7) ----------------
+/* ---- schedule-free AdamW (App. "Baseline": the baseline's optimiser; Tab. 5) ----------------
  * One step t >= 1 of schedule-free AdamW (Defazio et al. 2024, AdamW form) on the entries of the
  * nseg segments [seg_off[k], seg_off[k] + seg_len[k]) (host int64 arrays, nseg in [1, 64],
  * segments disjoint) of the vectors y (the model's parameters, where the gradient was taken),

@@ -12,7 +12,7 @@ What it computes (paper: "Speedrunning Tabular Foundation Model Pretraining"):
   feature cells then the target cell of each row) and, after the stack, the test rows' outputs
   go to the decoder.
 * App. "Repeated Feature Grouping": with m feature columns, cell j encodes the columns at
-  positions (j + o) mod m for o in the group's offsets, (0, 1, 3) for groups of three; Tab. 7
+  positions (j + o) mod m for o in the group's offsets, (0, 1, 3) for groups of three; Tab. 5
   uses groups of five, whose offsets the paper does not give (the caller passes them).
 * Fig. 4 caption and App. "Autoresearch": the current best record decodes the mean over the
   feature cells of each test row instead of its target cell.

@@ -7,7 +7,7 @@ and the CPU-baseline leg of the benchmark may import it, and it imports nothing 
 package.
 
 What the paper fixes (Sec. 5 "Muon Optimizer", "Batched Muon, Compile"; App. "Muon Optimizer",
-"Batched Muon, Compile"; Tab. 7): Muon updates the two-dimensional hidden weight matrices of the
+"Batched Muon, Compile"; Tab. 5): Muon updates the two-dimensional hidden weight matrices of the
 blocks and schedule-free AdamW everything else; the Muon learning rate is 0.1 x the AdamW one,
 its momentum 0.96 and its weight decay 0.1 in the current best record; AdamW weight decay 0 in
 the baseline and 0.01 in the record; gradients are clipped to a global norm of 1.0 (baseline)

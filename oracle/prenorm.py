@@ -8,12 +8,12 @@ package.
 What it computes (paper: "Speedrunning Tabular Foundation Model Pretraining"):
 
 * Sec. 5 "Residual Decay": the input of block i is multiplied by 0.95^i before the block
-  (Tab. 7 "Residual decay 0.95"; Fig. 4 caption).
+  (Tab. 5 "Residual decay 0.95"; Fig. 4 caption).
 * Sec. 5 "SDPA, bf16, Learning Rate, Width" and the Fig. 4 caption: the norms move in front of
   the attention and MLP sub-layers (pre-norm).
 * Sec. 5 "RMSNorm, Thinking Rows" and App. B.6: RMSNorm replaces all three LayerNorms.
-* Tab. 7: embedding 256, 4 heads (head dim 64), MLP hidden 768.
-* Thinking rows (App. B.6, Tab. 7): learnable E-vectors prepended along the row axis,
+* Tab. 5: embedding 256, 4 heads (head dim 64), MLP hidden 768.
+* Thinking rows (App. B.6, Tab. 5): learnable E-vectors prepended along the row axis,
   broadcast over the columns and counted as train rows.  Inside a block they are ordinary train
   rows; `thinking_rows_forward/backward` give the broadcast and its gradient.
 

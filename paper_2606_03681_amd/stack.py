@@ -216,7 +216,7 @@ class TrainStep:
         return self.loss[:1]
 
 
-# Optimiser settings of Tab. 7 (baseline / current best record); b1, b2, eps and the absent
+# Optimiser settings of Tab. 5 (baseline / current best record); b1, b2, eps and the absent
 # warm-up are the schedule-free defaults.
 OPTIM_BASELINE = dict(lr=1e-4, adamw_wd=0.0, clip=1.0, muon=False)
 OPTIM_RECORD = dict(lr=1e-3, adamw_wd=0.01, clip=2.0, muon=True, muon_lr_ratio=0.1,

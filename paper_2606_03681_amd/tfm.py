@@ -11,7 +11,9 @@ import os
 
 import numpy as np
 
-_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtfmlayer.so")
+# TFM_LIB may name another build of the same library (the host-sanitizer build of build.py)
+_LIB_PATH = os.environ.get("TFM_LIB") or \
+    os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtfmlayer.so")
 _lib = None
 
 TFM_F32, TFM_BF16 = 0, 1

@@ -102,11 +102,23 @@ TEST_CONFIGS = {
                                n_train=(1, 200), C=20, active=(0, 20), mask="random", E=64,
                                heads=2, H=192, layers=2, cells="normal", weights="xavier_bias",
                                block="pre"),
+    # rows wider than the matrix-core feature attention takes (more than 128 cells at d = 32,
+    # more than 64 at d = 64): the bfloat16 feature attention runs on the vector kernels
+    "wide-d32-bf16": dict(name="wide-d32-bf16", dtype="bf16", B=3, R=128, n_train=(1, 128),
+                          C=150, active=(100, 150), mask="random", E=64, heads=2, H=128,
+                          layers=1, cells="normal", weights="xavier_bias"),
+    "wide-d64-bf16": dict(name="wide-d64-bf16", dtype="bf16", B=3, R=40, n_train=(1, 40),
+                          C=90, active=(60, 90), mask="random", E=128, heads=2, H=256,
+                          layers=1, cells="normal", weights="xavier_bias"),
+    "wide-prenorm-d64-bf16": dict(name="wide-prenorm-d64-bf16", dtype="bf16", B=3, R=128,
+                                  n_train=(1, 128), C=90, active=(60, 90), mask="random",
+                                  E=128, heads=2, H=256, layers=2, cells="normal",
+                                  weights="xavier_bias", block="pre"),
 }
 
 
 # Workloads of the widened scope (not parity configurations of the baseline block).
-#   record9-bf16: the current best record's block (Tab. 7): pre-norm RMSNorm, residual decay,
+#   record9-bf16: the current best record's block (Tab. 5): pre-norm RMSNorm, residual decay,
 #   E = 256 with 4 heads of 64, MLP 768, 5 blocks; 1000 data rows plus 24 thinking rows
 #   prepended as train rows (750 labelled data rows); 20 features, the most the pretraining
 #   prior draws (Sec. 4.1), and repeated grouping makes one group of 5 per feature column, so
@@ -394,7 +406,7 @@ def make_ends_inputs(w, seed=None, G=None, mean=None, K=10, Hd=None, bias_scale=
     dataset's classes (2..K unless n_class is given), Xavier-uniform weights, N(0, bias_scale^2)
     biases, a N(0, 1) thinking-row table.  Defaults follow the block: the post-norm baseline
     encodes single features and decodes the target cell; the pre-norm record groups 5 features
-    and decodes the feature mean (Tab. 7).  The feature count of a dataset is its workload's
+    and decodes the feature mean (Tab. 5).  The feature count of a dataset is its workload's
     when the workload's mask is a prefix mask, else drawn from [1, C]."""
     cfg = w.cfg
     pre = cfg.get("block", "post") == "pre"

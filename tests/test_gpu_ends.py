@@ -297,7 +297,7 @@ OPT_CASES = [("d64-f32", 0), ("ragged-small-f32", 2), ("prenorm-small-bf16", 4)]
 
 @pytest.mark.parametrize("name,T", OPT_CASES)
 def test_training_step_optimizer_against_oracle(name, T):
-    """Two training steps with the optimiser of Tab. 7 (baseline settings for the post-norm
+    """Two training steps with the optimiser of Tab. 5 (baseline settings for the post-norm
     block, the record's Muon + schedule-free AdamW for the pre-norm one).  The oracle's clip,
     Muon and schedule-free AdamW, fed the gradients the GPU step produced, must give the same
     parameter changes: this checks which parameters go to which optimiser, the clip over every

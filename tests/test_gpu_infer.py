@@ -60,7 +60,8 @@ def _oracle_forward(w, X, n_train):
 
 
 @pytest.mark.parametrize("name", ["ragged-small-bf16", "d16-bf16", "d64-bf16",
-                                  "prenorm-small-bf16", "prenorm-d64-bf16"])
+                                  "prenorm-small-bf16", "prenorm-d64-bf16", "wide-d32-bf16",
+                                  "wide-prenorm-d64-bf16"])
 def test_context_and_query_chunks(name):
     import torch
     from paper_2606_03681_amd.stack import InferStack, to_device
