@@ -23,6 +23,15 @@ hipError_t launch_item_attn_dkdv(const Geo& g, const bf16* q, const bf16* k, con
                                  const bf16* o, const bf16* dout, const float* lse,
                                  const float* Dbuf, bf16* dk, bf16* dv, hipStream_t s);
 
+// The same backward in one launch for train prefixes of at most 768 rows at d in {16, 32}
+// (item_attn_bwd_fused_ok): one workgroup per (column, head) problem computes P and dS once per
+// score and writes dq, dk and dv; nmax is the longest train prefix of the launch.
+bool item_attn_bwd_fused_ok(const Geo& g, int nmax);
+hipError_t launch_item_attn_bwd_fused(const Geo& g, int nmax, const bf16* q, const bf16* k,
+                                      const bf16* v, const bf16* o, const bf16* dout,
+                                      const float* lse, bf16* dq, bf16* dk, bf16* dv,
+                                      hipStream_t s);
+
 // Feature-axis attention (cells of a row, per head).  qkv cell-major [cell][3E]; o, dout
 // cell-major [cell][E]; lse [cell][heads]; dqkv cell-major [cell][3E].  Requires
 // feat_attn_mfma_ok(g) (at most 128 active cells per row, 32-bit row offsets).

@@ -39,6 +39,10 @@ __device__ __forceinline__ bf16x8 cat8(uint2 lo, uint2 hi) {
   return *reinterpret_cast<bf16x8*>(&u);
 }
 
+// Makes this wave's LDS writes visible to its own later LDS reads (and its reads complete before
+// it overwrites what they read); no workgroup barrier.
+__device__ __forceinline__ void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
 __device__ __forceinline__ bf16x8 pack8(const f32x4& a, const f32x4& b) {
   uint4 u = make_uint4(pack2(a[0], a[1]), pack2(a[2], a[3]), pack2(b[0], b[1]),
                        pack2(b[2], b[3]));
@@ -374,6 +378,291 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
       *reinterpret_cast<uint2*>(dq + (prob * R + qq) * D + db * 16 + lg * 4) = u;
     }
   }
+}
+
+// =============================================================================== fused
+// One workgroup per (column, head) problem whose train prefix has at most 8 * 16 * NKB rows
+// (NKB <= 6):
+// 8 waves, wave w owns the keys [w KW, (w + 1) KW), KW = 16 NKB, and every wave walks all query
+// rows in chunks of 32 (Q, dO, D and the LSE of a chunk staged once in LDS for all waves).  Per
+// chunk and wave, in the key-major layout of the dK/dV kernel above:
+//   S = Q K^T, dP = dO V^T  (seeded with -lse log2 e and -D),  P = exp2(S),  dS = P (dP - D)
+//   dV^T += dO^T P,  dK^T += Q^T dS                     (registers, across every chunk)
+//   dQ_w = dS K over the wave's own keys: dS goes through the wave's LDS tile [key][query]
+//          (8-byte row writes), read back transposed as the A operand; K^T fragments are
+//          built once from an LDS copy of the wave's keys
+// then the eight dQ_w of the chunk are added in wave order through LDS and stored.  P and dS
+// are computed once per score (the two-kernel form computes them in both kernels), and every
+// output element is summed in a fixed order, so results are bitwise reproducible.
+template <int D, int NKB>
+__global__ __launch_bounds__(512) void k_item_attn_bwd_fused(Geo g, const bf16* __restrict__ q,
+                                                             const bf16* __restrict__ k,
+                                                             const bf16* __restrict__ v,
+                                                             const bf16* __restrict__ o,
+                                                             const bf16* __restrict__ dout,
+                                                             const float* __restrict__ lse,
+                                                             bf16* __restrict__ dq,
+                                                             bf16* __restrict__ dk,
+                                                             bf16* __restrict__ dv, int per_xcd) {
+  constexpr int W = 8;                 // waves
+  constexpr int QC = 32;               // queries per chunk (two 16-query blocks)
+  constexpr int KW = 16 * NKB;         // keys per wave
+  constexpr int DB = D / 16;
+  constexpr int CPR = D / 8;           // 16-byte chunks per row of d values
+  constexpr int RS = tr_stride<D>();   // LDS row stride of Q / dO and of the key copy
+  constexpr int DSS = 48;              // dS^T tile [key][32 queries]: 96-byte rows (see ld_tr8)
+  constexpr int PQS = QC + 4;          // dQ partial [d][query] floats: 144-byte rows
+  constexpr int T1 = KW * DSS * 2, T2 = D * PQS * 4, T3 = KW * RS * 2;
+  constexpr int REG = (T1 > T2 ? (T1 > T3 ? T1 : T3) : (T2 > T3 ? T2 : T3));
+  constexpr int VS = D + 8;             // the wave's value rows: 16-byte reads conflict-free
+  static_assert(NKB % 2 == 0, "keys per wave must fill 32-key steps");
+  __shared__ __attribute__((aligned(16))) bf16 Qs[2][QC * RS];
+  __shared__ __attribute__((aligned(16))) bf16 dOs[2][QC * RS];
+  __shared__ __attribute__((aligned(16))) float Lq[2][QC];
+  __shared__ __attribute__((aligned(16))) float Dq[2][QC];
+  __shared__ __attribute__((aligned(16))) char wreg[W][REG];
+  __shared__ __attribute__((aligned(16))) bf16 Vw[W][KW * VS];
+
+  // problems of one XCD are consecutive (the heads of a column share their O / dO rows in L2)
+  const int bid = blockIdx.x;
+  const int64_t prob = (int64_t)(bid & 7) * per_xcd + (bid >> 3);
+  if (prob >= (int64_t)g.NC * g.heads) return;
+  const int64_t col = prob / g.heads;
+  const int head = (int)(prob - col * g.heads);
+  const int n = g.col_ntr[col];
+  const int R = g.R, E = g.E;
+  const int nact = (n + KW - 1) / KW < W ? (n + KW - 1) / KW : W;  // waves that own keys
+
+  const uint32_t rowQ = D * 2, rowO = (uint32_t)E * 2;
+  const rsrc_t rQ = make_rsrc(q + prob * R * D, (uint32_t)R * rowQ);
+  const rsrc_t rK = make_rsrc(k + prob * R * D, (uint32_t)n * rowQ);
+  const rsrc_t rV = make_rsrc(v + prob * R * D, (uint32_t)n * rowQ);
+  const uint32_t obytes = (uint32_t)(R - 1) * rowO + rowQ;
+  const rsrc_t rO = make_rsrc(o + col * R * (int64_t)E + head * D, obytes);
+  const rsrc_t rdO = make_rsrc(dout + col * R * (int64_t)E + head * D, obytes);
+  const rsrc_t rL = make_rsrc(lse + prob * R, (uint32_t)R * 4);
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int c = lane & 15, lg = lane >> 4;
+  const float tau = 1.0f / sqrtf((float)D);
+  const bool active = w < nact;
+  const int kw0 = w * KW;
+  typedef typename HF<D>::frag frag;
+
+  // the wave's keys (lane: key kw0 + kb*16 + c) in registers, its values in LDS; keys past n
+  // read K = V = 0: their dK, dV are never stored and they add K = 0 to dQ, so no key masking
+  // is needed
+  frag kf[NKB];
+  bf16x8 ktf[NKB / 2][DB];  // K as the B operand of dS K: dims db*16 + c, keys of a 32-key step
+  f32x4 dkt[NKB][DB], dvt[NKB][DB];
+  bf16* vw = Vw[w];
+#pragma unroll
+  for (int kb = 0; kb < NKB; ++kb) {
+#pragma unroll
+    for (int db = 0; db < DB; ++db) dkt[kb][db] = dvt[kb][db] = zero4();
+    const uint32_t key = (uint32_t)(kw0 + kb * 16 + c);
+    kf[kb] = HF<D>::buf(rK, key * rowQ, lg);
+    const frag vv = HF<D>::buf(rV, key * rowQ, lg);
+    *reinterpret_cast<frag*>(&vw[(kb * 16 + c) * VS + lg * HF<D>::EPL]) = vv;
+  }
+  {
+    bf16* kst = reinterpret_cast<bf16*>(wreg[w]);  // [KW][RS] row-major copy of the keys
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb)
+      *reinterpret_cast<frag*>(&kst[(kb * 16 + c) * RS + lg * HF<D>::EPL]) = kf[kb];
+    wave_lds_sync();
+#pragma unroll
+    for (int ks = 0; ks < NKB / 2; ++ks)
+#pragma unroll
+      for (int db = 0; db < DB; ++db) ktf[ks][db] = ld_tr8(&kst[ks * 32 * RS], RS, db * 16, lane);
+    wave_lds_sync();
+  }
+
+  // staging of a query chunk: threads [0, 128) move Q, threads [128, 256) move dO and read O
+  // for D = rowsum(dO o O) (the CPR threads of a query are adjacent lanes); queries past R read
+  // Q = dO = O = lse = 0 (P = 1 there, but dO and dS vanish and their dQ is not stored)
+  constexpr int NIT = QC * CPR;  // items per tensor (<= 128)
+  const bool qthr = tid < NIT, othr = tid >= 128 && tid < 128 + NIT;
+  const int it = qthr ? tid : tid - 128;
+  const int iq = it / CPR, id0 = (it % CPR) * 8;
+  uint4 rq = make_uint4(0, 0, 0, 0), rdo = rq, ro = rq;
+  float rl = 0.f;
+  auto gload = [&](int q0) {
+    const uint32_t qg = (uint32_t)(q0 + iq);
+    if (qthr) rq = bload16(rQ, qg * rowQ + id0 * 2);
+    if (othr) {
+      rdo = bload16(rdO, qg * rowO + id0 * 2);
+      ro = bload16(rO, qg * rowO + id0 * 2);
+      if (id0 == 0) rl = bloadf(rL, qg * 4);
+    }
+  };
+  auto sstore = [&](int b) {
+    if (qthr) stu4(&Qs[b][iq * RS + id0], rq);
+    if (tid >= 128 && tid < 256) {  // whole waves: the lane sums below see only their own
+      float dd = 0.f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) dd = fmaf(bf2f(u4_elem(rdo, j)), bf2f(u4_elem(ro, j)), dd);
+      dd += dpp_mov<0xB1>(dd);                  // lanes of a query: 4 (d = 32) or 2 (d = 16)
+      if (CPR == 4) dd += dpp_mov<0x4E>(dd);
+      if (othr) {
+        stu4(&dOs[b][iq * RS + id0], rdo);
+        if (id0 == 0) {
+          Dq[b][iq] = -dd;
+          Lq[b][iq] = -rl * LOG2E;
+        }
+      }
+    }
+  };
+
+  const int NCH = (R + QC - 1) / QC;
+  gload(0);
+  sstore(0);
+  lds_barrier();
+  constexpr float kLn2 = 0.69314718055994531f;
+  for (int ic = 0; ic < NCH; ++ic) {
+    const int b = ic & 1;
+    if (ic + 1 < NCH) gload((ic + 1) * QC);
+    if (active) {
+      frag qa[2], da[2];
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb) {
+        qa[qb] = HF<D>::lds(&Qs[b][(qb * 16 + c) * RS], lg);
+        da[qb] = HF<D>::lds(&dOs[b][(qb * 16 + c) * RS], lg);
+      }
+      bf16x8 qt[DB], dot[DB];
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        qt[db] = ld_tr8(Qs[b], RS, db * 16, lane);
+        dot[db] = ld_tr8(dOs[b], RS, db * 16, lane);
+      }
+      bf16* dst = reinterpret_cast<bf16*>(wreg[w]);  // dS^T tile [KW][DSS]
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) {
+        const frag vfk = HF<D>::lds(&vw[(kb * 16 + c) * VS], lg);
+        uint32_t pw[2][2], sw[2][2];
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          const f32x4 nl = *reinterpret_cast<const f32x4*>(&Lq[b][qb * 16 + lg * 4]);
+          const f32x4 nd = *reinterpret_cast<const f32x4*>(&Dq[b][qb * 16 + lg * 4]);
+          const f32x4 sc = HF<D>::mma(qa[qb], kf[kb], nl);   // S log2(e) - lse log2(e)
+          const f32x4 dp = HF<D>::mma(da[qb], vfk, nd);      // dP - D
+          const float p0 = exp2_hw(sc[0]), p1 = exp2_hw(sc[1]);
+          const float p2 = exp2_hw(sc[2]), p3 = exp2_hw(sc[3]);
+          pw[qb][0] = pack2(p0, p1);
+          pw[qb][1] = pack2(p2, p3);
+          sw[qb][0] = pack2(p0 * dp[0], p1 * dp[1]);
+          sw[qb][1] = pack2(p2 * dp[2], p3 * dp[3]);
+        }
+        const bf16x8 pf = cat8(make_uint2(pw[0][0], pw[0][1]), make_uint2(pw[1][0], pw[1][1]));
+        const bf16x8 sf = cat8(make_uint2(sw[0][0], sw[0][1]), make_uint2(sw[1][0], sw[1][1]));
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          dvt[kb][db] = mfma16(dot[db], pf, dvt[kb][db]);
+          dkt[kb][db] = mfma16(qt[db], sf, dkt[kb][db]);
+        }
+        // dS^T rows: key kb*16 + c, queries qb*16 + 4 lg .. + 3
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb)
+          *reinterpret_cast<uint2*>(&dst[(kb * 16 + c) * DSS + qb * 16 + 4 * lg]) =
+              make_uint2(sw[qb][0], sw[qb][1]);
+      }
+      wave_lds_sync();
+      // dQ_w[q][d] = sum over the wave's keys of dS[q][key] K[key][d]
+      f32x4 dqp[2][DB];
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int db = 0; db < DB; ++db) dqp[qb][db] = zero4();
+#pragma unroll
+      for (int ks = 0; ks < NKB / 2; ++ks)
+#pragma unroll
+        for (int qb = 0; qb < 2; ++qb) {
+          const bf16x8 af = ld_tr8(&dst[ks * 32 * DSS], DSS, qb * 16, lane);
+#pragma unroll
+          for (int db = 0; db < DB; ++db) dqp[qb][db] = mfma16(af, ktf[ks][db], dqp[qb][db]);
+        }
+      wave_lds_sync();  // the tile is read before the partial overwrites it
+      // lane: dQ_w[q = qb*16 + 4 lg + i][d = db*16 + c] -> partial [d][q]
+      float* pq = reinterpret_cast<float*>(wreg[w]);
+#pragma unroll
+      for (int qb = 0; qb < 2; ++qb)
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          *reinterpret_cast<f32x4*>(&pq[(db * 16 + c) * PQS + qb * 16 + 4 * lg]) = dqp[qb][db];
+    }
+    if (ic + 1 < NCH) sstore(b ^ 1);
+    lds_barrier();
+    // dQ of the chunk: the partials of the active waves added in wave order, two dims a thread
+    if (tid < QC * D / 2) {
+      const int qq = tid / (D / 2), d0 = 2 * (tid % (D / 2));
+      float s0 = 0.f, s1 = 0.f;
+      for (int w2 = 0; w2 < nact; ++w2) {
+        const float* pq = reinterpret_cast<const float*>(wreg[w2]);
+        s0 += pq[d0 * PQS + qq];
+        s1 += pq[(d0 + 1) * PQS + qq];
+      }
+      const int qg = ic * QC + qq;
+      if (qg < R)
+        *reinterpret_cast<uint32_t*>(dq + (prob * R + qg) * D + d0) = pack2(s0 * kLn2, s1 * kLn2);
+    }
+    lds_barrier();
+  }
+  // lane: dims db*16 + 4*lg + i of key kw0 + kb*16 + c
+  if (!active) return;
+#pragma unroll
+  for (int kb = 0; kb < NKB; ++kb) {
+    const int key = kw0 + kb * 16 + c;
+    if (key >= n) continue;
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const uint2 a = make_uint2(pack2(dkt[kb][db][0] * tau, dkt[kb][db][1] * tau),
+                                 pack2(dkt[kb][db][2] * tau, dkt[kb][db][3] * tau));
+      const uint2 bb = make_uint2(pack2(dvt[kb][db][0], dvt[kb][db][1]),
+                                  pack2(dvt[kb][db][2], dvt[kb][db][3]));
+      *reinterpret_cast<uint2*>(dk + (prob * R + key) * D + db * 16 + lg * 4) = a;
+      *reinterpret_cast<uint2*>(dv + (prob * R + key) * D + db * 16 + lg * 4) = bb;
+    }
+  }
+}
+
+// Key blocks of 16 per wave of the fused backward for train prefixes of at most nmax rows;
+// 0 where it does not apply (d = 64, or more than 768 train rows: the keys' dK / dV
+// accumulators and fragments would not fit the registers of two waves per SIMD).
+static int fused_nkb(int d, int nmax) {
+  if (d != 16 && d != 32) return 0;
+  if (nmax <= 256) return 2;
+  if (nmax <= 512) return 4;
+  if (nmax <= 768) return 6;
+  return 0;
+}
+
+bool item_attn_bwd_fused_ok(const Geo& g, int nmax) { return fused_nkb(g.d, nmax) > 0; }
+
+template <int D>
+static hipError_t fused_d(const Geo& g, int nkb, unsigned grid, int per, const bf16* q,
+                          const bf16* k, const bf16* v, const bf16* o, const bf16* dout,
+                          const float* lse, bf16* dq, bf16* dk, bf16* dv, hipStream_t s) {
+  switch (nkb) {
+    case 2: k_item_attn_bwd_fused<D, 2><<<grid, 512, 0, s>>>(g, q, k, v, o, dout, lse, dq, dk, dv, per); break;
+    case 4: k_item_attn_bwd_fused<D, 4><<<grid, 512, 0, s>>>(g, q, k, v, o, dout, lse, dq, dk, dv, per); break;
+    case 6: k_item_attn_bwd_fused<D, 6><<<grid, 512, 0, s>>>(g, q, k, v, o, dout, lse, dq, dk, dv, per); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_item_attn_bwd_fused(const Geo& g, int nmax, const bf16* q, const bf16* k,
+                                      const bf16* v, const bf16* o, const bf16* dout,
+                                      const float* lse, bf16* dq, bf16* dk, bf16* dv,
+                                      hipStream_t s) {
+  const int nkb = fused_nkb(g.d, nmax);
+  if (nkb == 0) return hipErrorInvalidValue;
+  const int64_t P = (int64_t)g.NC * g.heads;
+  if (P == 0) return hipSuccess;
+  const int per = (int)((P + 7) / 8);
+  const unsigned grid = (unsigned)(8 * per);
+  if (g.d == 16) return fused_d<16>(g, nkb, grid, per, q, k, v, o, dout, lse, dq, dk, dv, s);
+  return fused_d<32>(g, nkb, grid, per, q, k, v, o, dout, lse, dq, dk, dv, s);
 }
 
 hipError_t launch_item_attn_dq(const Geo& g, const bf16* q, const bf16* k, const bf16* v,

@@ -36,6 +36,7 @@ struct Geo {
   // train-prefix length of the column's dataset.
   const int64_t* col_cell0;  // [NC]
   const int32_t* col_ntr;    // [NC]
+  int32_t nmax;              // longest train prefix over the datasets
 };
 
 __host__ __device__ inline int64_t native_cell(const Geo& g, int64_t p) {

@@ -257,6 +257,7 @@ bool aligned(const void* p) { return p && ((uintptr_t)p % 16) == 0; }
 // ---- per-call plan ---------------------------------------------------------------------------
 struct Plan {
   int NC = 0;
+  int nmax = 0;  // longest train prefix
   std::vector<int32_t> blob;
 };
 
@@ -281,6 +282,7 @@ int make_plan(const Dims& d, const int32_t* n_train, const uint8_t* mask, Plan& 
         e[3 + (c >> 5)] |= (int32_t)(1u << (c & 31));
       }
     e[0] = n_train[b];
+    if (n_train[b] > P.nmax) P.nmax = n_train[b];
     e[1] = col;
     e[2] = cnt;
     col += cnt;
@@ -308,6 +310,7 @@ int setup_geo(const Dims& d, const Plan& P, char* ws, const MetaOff& W, tfm::Geo
   int32_t* blob = (int32_t*)(ws + W.blob);
   g.B = d.B; g.R = d.R; g.S = d.S; g.E = d.E; g.heads = d.heads; g.d = d.d; g.H = d.H;
   g.NC = P.NC;
+  g.nmax = P.nmax;
   g.N = (int64_t)P.NC * d.R;
   g.ds = (const tfm::DsInfo*)(ws + W.ds);
   g.col_ds = (const int32_t*)(ws + W.col_ds);
@@ -677,8 +680,14 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   const T* oi = (const T*)(sv + S.oi);
   const float* lsei = (const float*)(sv + S.lsei);
   float* Dq = (float*)(ws + W.D);
-  STEP("item_attn_dq/mfma", launch_item_attn_dq(g, qi, ki, vi, oi, doi, lsei, Dq, dq, s));
-  STEP("item_attn_dkdv/mfma", launch_item_attn_dkdv(g, qi, ki, vi, oi, doi, lsei, Dq, dk, dv, s));
+  if (item_attn_bwd_fused_ok(g, g.nmax)) {
+    STEP("item_attn_bwd/mfma",
+         launch_item_attn_bwd_fused(g, g.nmax, qi, ki, vi, oi, doi, lsei, dq, dk, dv, s));
+  } else {
+    STEP("item_attn_dq/mfma", launch_item_attn_dq(g, qi, ki, vi, oi, doi, lsei, Dq, dq, s));
+    STEP("item_attn_dkdv/mfma",
+         launch_item_attn_dkdv(g, qi, ki, vi, oi, doi, lsei, Dq, dk, dv, s));
+  }
   CHK(G.run(dq, 3 * E, h1, E, ROWS_COMPACT, o.Wqkv_i, o.bqkv_i, dk, dv));
   // dZ1 = LN1'(dZ2 + dQKV_i Wqkv_i), the gradients read head-major in place
   a = gemm_base(g, N, E, 3 * E, EPI_LN_BWD);
@@ -826,8 +835,14 @@ int bwd_pre(const Dims& d, const tfm::Geo& g, const float* prm, const char* sv,
   const T* oi = (const T*)(sv + S.oi);
   const float* lsei = (const float*)(sv + S.lsei);
   float* Dq = (float*)(ws + W.D);
-  STEP("item_attn_dq/mfma", launch_item_attn_dq(g, qi, ki, vi, oi, doi, lsei, Dq, dq, s));
-  STEP("item_attn_dkdv/mfma", launch_item_attn_dkdv(g, qi, ki, vi, oi, doi, lsei, Dq, dk, dv, s));
+  if (item_attn_bwd_fused_ok(g, g.nmax)) {
+    STEP("item_attn_bwd/mfma",
+         launch_item_attn_bwd_fused(g, g.nmax, qi, ki, vi, oi, doi, lsei, dq, dk, dv, s));
+  } else {
+    STEP("item_attn_dq/mfma", launch_item_attn_dq(g, qi, ki, vi, oi, doi, lsei, Dq, dq, s));
+    STEP("item_attn_dkdv/mfma",
+         launch_item_attn_dkdv(g, qi, ki, vi, oi, doi, lsei, Dq, dk, dv, s));
+  }
   CHK(G.run(dq, 3 * E, (const T*)(sv + S.r2), E, ROWS_COMPACT, o.Wqkv_i, o.bqkv_i, dk, dv));
   // dh1 = dh2 + RMS2'(dQKV_i Wqkv_i), the gradients read head-major in place
   a = gemm_base(g, N, E, 3 * E, EPI_RMS_BWD);
