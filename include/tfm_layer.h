@@ -116,6 +116,26 @@ int tfm_layer_bwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* c
                   const void* dY, void* dX, float* grads, int accumulate,
                   void* workspace, size_t workspace_bytes, void* stream);
 
+/* Allocation-free forward, for callers that cannot allocate device memory or pass a workspace
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid allocation).  Same
+ * arguments and results as tfm_layer_fwd (Y and saved bit for bit; saved feeds tfm_layer_bwd as
+ * usual) without the workspace: the call's scratch (the active-cell plan and the bfloat16 copies
+ * of the weights) lives in a device array the library owns, TFM_NOALLOC_SCRATCH_BYTES on each
+ * GPU it runs on, held until the process ends.  The call allocates nothing and calls no
+ * allocating routine.
+ *
+ * Limits: TFM_BF16 with E in {64, 128, 192, 256} and H a multiple of E (either block); dims whose
+ * scratch exceeds TFM_NOALLOC_SCRATCH_BYTES (the bf16 weights, 2 (8E^2 + 2EH) bytes, plus about
+ * 24 B (C+1) + 28 + 4 ceil((C+1)/32) bytes per dataset) return TFM_ERR_BUFFER; a stream of another
+ * device than the current one returns TFM_ERR_HIP.  The array is shared by every call on one
+ * GPU and keeps the last call's contents (nothing in it needs to start at zero: each call
+ * rewrites what it reads), so calls that overlap on one GPU (concurrent streams, or threads)
+ * race: the caller serialises them. */
+#define TFM_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+int tfm_layer_fwd_noalloc(const tfm_dims* dims, const int32_t* n_train, const uint8_t* cell_mask,
+                          const void* X, const float* params, void* Y, void* saved,
+                          size_t saved_bytes, void* stream);
+
 /* Thinking rows (Sec. 5 "RMSNorm, Thinking Rows", App. B.6, Tab. 5): learned E-vectors
  * prepended along the row axis, broadcast over the cell columns and counted as train rows.
  * dims, n_train and cell_mask describe the stack input X[B][R][C+1][E] whose rows [0, T) are the

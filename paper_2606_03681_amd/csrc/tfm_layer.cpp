@@ -16,6 +16,7 @@
 #include "attn.h"
 #include "fast.h"
 #include "prof.h"
+#include "static_scratch.h"
 
 namespace {
 
@@ -1114,6 +1115,52 @@ int tfm_layer_bwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* c
   return bwd_simple<tfm::bf16>(d, g, (const tfm::bf16*)X, params, (const char*)saved, S,
                                (const tfm::bf16*)dY, (tfm::bf16*)dX, grads, accumulate, ws, W,
                                s);
+}
+
+// Allocation-free forward: the plan and the bf16 weights in the library's static scratch.
+int tfm_layer_fwd_noalloc(const tfm_dims* dims, const int32_t* n_train, const uint8_t* cell_mask,
+                          const void* X, const float* params, void* Y, void* saved,
+                          size_t saved_bytes, void* stream) {
+  Dims d;
+  int rc = check_dims(dims, d);
+  if (rc) return rc;
+  if (!infer_eligible(d))
+    return fail(TFM_ERR_DIMS, "tfm_layer_fwd_noalloc needs TFM_BF16, E in {64, 128, 192, 256} "
+                              "and H a multiple of E");
+  if (!aligned(X) || !aligned(params) || !aligned(Y) || !aligned(saved))
+    return fail(TFM_ERR_POINTER, "X, params, Y and saved must be non-null and 16-byte aligned");
+  Arena a;
+  const MetaOff M = take_meta(d, a);
+  const tfm::WOff wo = tfm::weight_offsets(d.E, d.H);
+  const size_t w_off = a.take((size_t)wo.total * 2);
+  const size_t wt_off = a.take((size_t)wo.total * 2);
+  if (a.off > tfm::kStaticScratchBytes)
+    return fail(TFM_ERR_BUFFER, "these dims need %zu bytes of library scratch; the maximum is "
+                                "%zu (TFM_NOALLOC_SCRATCH_BYTES)", a.off,
+                tfm::kStaticScratchBytes);
+  if (saved_bytes < saved_total(d))
+    return fail(TFM_ERR_BUFFER, "saved buffer has %zu bytes, %zu required", saved_bytes,
+                saved_total(d));
+  Plan P;
+  rc = make_plan(d, n_train, cell_mask, P);
+  if (rc) return rc;
+  hipStream_t s = (hipStream_t)stream;
+  void* base = nullptr;
+  HIPCHK(tfm::static_scratch(s, &base));
+  char* ws = (char*)base;
+  tfm::Geo g;
+  rc = setup_geo(d, P, ws, M, g, s);
+  if (rc) return rc;
+  FastWs f{};
+  f.wo = wo;
+  f.w = (tfm::bf16*)(ws + w_off);
+  f.wt = (tfm::bf16*)(ws + wt_off);
+  char* sv = (char*)saved;
+  if (d.block == TFM_BLOCK_PRENORM)
+    return fwd_pre(d, g, (const tfm::bf16*)X, params, (tfm::bf16*)Y,
+                   bufs_from_pre_saved(sv, pre_saved_layout(d)), f, s);
+  return fwd_fast(d, g, (const tfm::bf16*)X, params, (tfm::bf16*)Y,
+                  bufs_from_saved(sv, saved_layout(d)), f, s);
 }
 
 // Shared checks of the thinking-row calls (the dims, the workspace that holds the column map,

@@ -23,7 +23,8 @@ ERRORS = {
     -5: "TFM_ERR_POINTER", -6: "TFM_ERR_HIP", -7: "TFM_ERR_BUFFER",
 }
 EXPORTS = ("tfm_layer_param_count", "tfm_layer_saved_bytes", "tfm_layer_workspace_bytes",
-           "tfm_layer_fwd", "tfm_layer_bwd", "tfm_thinking_rows_fwd", "tfm_thinking_rows_bwd",
+           "tfm_layer_fwd", "tfm_layer_fwd_noalloc", "tfm_layer_bwd", "tfm_thinking_rows_fwd",
+           "tfm_thinking_rows_bwd",
            "tfm_infer_workspace_bytes", "tfm_infer_cache_bytes", "tfm_layer_fwd_context",
            "tfm_layer_fwd_query", "tfm_last_error", "tfm_prof_enable", "tfm_prof_collect",
            "tfm_prof_step", "tfm_ends_param_count", "tfm_ends_workspace_bytes", "tfm_encode_fwd",
@@ -91,6 +92,8 @@ def lib():
         L.tfm_last_error.argtypes = []
         L.tfm_layer_fwd.restype = i32
         L.tfm_layer_fwd.argtypes = [P(tfm_dims), vp, vp, vp, vp, vp, vp, sz, vp, sz, vp]
+        L.tfm_layer_fwd_noalloc.restype = i32
+        L.tfm_layer_fwd_noalloc.argtypes = [P(tfm_dims), vp, vp, vp, vp, vp, vp, sz, vp]
         L.tfm_layer_bwd.restype = i32
         L.tfm_layer_bwd.argtypes = [P(tfm_dims), vp, vp, vp, vp, vp, sz, vp, vp, vp, i32, vp,
                                     sz, vp]
@@ -199,6 +202,17 @@ def layer_fwd(dims, n_train, cell_mask, X, params, Y, saved, workspace, stream=N
                              _ptr(saved), saved.numel() * saved.element_size(),
                              _ptr(workspace), workspace.numel() * workspace.element_size(),
                              _stream(stream))
+    _check(rc)
+
+
+def layer_fwd_noalloc(dims, n_train, cell_mask, X, params, Y, saved, stream=None):
+    """tfm_layer_fwd_noalloc: tfm_layer_fwd with its scratch in the library's own device array
+    (no workspace argument; calls on one GPU must not overlap)."""
+    nt, ntp = _host(n_train, np.int32)
+    cm, cmp_ = _host(cell_mask, np.uint8)
+    rc = lib().tfm_layer_fwd_noalloc(ctypes.byref(dims), ntp, cmp_, _ptr(X), _ptr(params),
+                                     _ptr(Y), _ptr(saved), saved.numel() * saved.element_size(),
+                                     _stream(stream))
     _check(rc)
 
 

@@ -357,3 +357,20 @@ def test_muon_arguments_rejected_before_launch():
     assert tfm.muon_workspace_bytes(16, 256, 256) > w1
     assert tfm.muon_workspace_bytes(1, 768, 256) == tfm.muon_workspace_bytes(1, 256, 768)
     assert tfm.muon_workspace_bytes(0, 8, 8) == 0
+
+
+def test_noalloc_forward_limits_rejected_before_launch():
+    """The allocation-free forward takes the bf16 matrix-core dims only, and rejects dims whose
+    scratch (the plan and the bf16 weights) exceeds the library's fixed array, before any HIP
+    call."""
+    p = 1 << 20
+    d = _dims()                                                   # float32: not supported
+    rc = tfm.lib().tfm_layer_fwd_noalloc(ctypes.byref(d), None, None, p, p, p, p, 1 << 40, None)
+    assert rc == -1 and "TFM_BF16" in tfm.last_error()
+    # 10,000 datasets of 256 cells per row: ~61 MB of per-column plan alone
+    d = _dims(B=10000, R=1, C=255, E=64, heads=2, H=128, dtype="bf16")
+    rc = tfm.lib().tfm_layer_fwd_noalloc(ctypes.byref(d), None, None, p, p, p, p, 1 << 40, None)
+    assert rc == -7 and "TFM_NOALLOC_SCRATCH_BYTES" in tfm.last_error()
+    d = _dims(dtype="bf16")
+    rc = tfm.lib().tfm_layer_fwd_noalloc(ctypes.byref(d), None, None, p, p, p, 0, 1 << 40, None)
+    assert rc == -5
