@@ -38,9 +38,10 @@ int tfm_clip_scale(int32_t nvec, const float* const* grads, const int64_t* count
  * segments disjoint) of the vectors y (the model's parameters, where the gradient was taken),
  * z (the base sequence, equal to y before the first step) and v (second moments, 0 before the
  * first step).  With g = grad_scale[0] * grad (grad_scale nullable = 1), s_t = lr min(1, t /
- * warmup) (1 without warm-up), gamma = s_t sqrt(1 - beta2^t) and c = s_t^2 / sum_{i<=t} s_i^2:
+ * warmup) (1 without warm-up), gamma_t = s_t sqrt(1 - beta2^t) and the averaging weight
+ * c = gamma_t^2 / sum_{i<=t} gamma_i^2 (Defazio et al.'s Algorithm 1):
  *     v <- beta2 v + (1 - beta2) g^2,   u = g / (sqrt(v) + eps) + weight_decay y,
- *     y <- y + c (z - y) + gamma (beta1 (1 - c) - 1) u,   z <- z - gamma u.
+ *     y <- y + c (z - y) + gamma_t (beta1 (1 - c) - 1) u,   z <- z - gamma_t u.
  * Entries outside the segments are not touched. */
 typedef struct {
   float lr, beta1, beta2, eps, weight_decay;

@@ -26,13 +26,13 @@ The algorithms themselves are the published ones, written here from their defini
   v_t = b2 v_{t-1} + (1 - b2) g_t^2; with the scheduled rate s_t = lr min(1, t / warmup) and the
   step rate gamma_t = s_t sqrt(1 - b2^t),
   z_{t+1} = z_t - gamma_t (g_t / (sqrt(v_t) + eps) + wd y_t);
-  x_{t+1} = (1 - c_{t+1}) x_t + c_{t+1} z_{t+1} with c_{t+1} = s_t^2 / sum_{i<=t} s_i^2.
+  x_{t+1} = (1 - c_{t+1}) x_t + c_{t+1} z_{t+1} with c_{t+1} = gamma_t^2 / sum_{i<=t} gamma_i^2
+  (the averaging weights are the squared step rates, bias correction included).
   Starting point x_1 = z_1 = y_1 = the initial parameters, v_0 = 0.
 
 Readings where the paper is silent are listed in the design doc: the Nesterov form and the momentum
 average (buf <- m buf + (1 - m) g, input (1 - m) g + m buf), the Frobenius-norm guard 1e-7, the
-bias correction sqrt(1 - b2^t) on the step (gradient and decay terms) but not on the averaging
-weights, b1 = 0.9, b2 = 0.999, eps = 1e-8, no warm-up unless given, and the clip factor
+b1 = 0.9, b2 = 0.999, eps = 1e-8, no warm-up unless given, and the clip factor
 min(1, max_norm / (norm + 1e-6)).
 """
 
@@ -93,7 +93,7 @@ class ScheduleFreeAdamW:
         self.lr, self.b1, self.b2, self.eps = lr, beta1, beta2, eps
         self.wd, self.warmup = weight_decay, warmup
         self.z_hist = [self.z.copy()]
-        self.sched_hist = []
+        self.gamma_hist = []
 
     @property
     def y(self):
@@ -108,9 +108,9 @@ class ScheduleFreeAdamW:
         self.v = self.b2 * self.v + (1.0 - self.b2) * g * g
         gamma = sched * np.sqrt(1.0 - self.b2 ** t)
         self.z = self.z - gamma * (g / (np.sqrt(self.v) + self.eps) + self.wd * y)
-        self.gsq += sched * sched
-        c = sched * sched / self.gsq
+        self.gsq += gamma * gamma
+        c = gamma * gamma / self.gsq
         self.x = (1.0 - c) * self.x + c * self.z
         self.z_hist.append(self.z.copy())
-        self.sched_hist.append(sched)
+        self.gamma_hist.append(gamma)
         return self.y

@@ -152,20 +152,26 @@ int tfm_sfadamw_step(const tfm_sfadamw* hp, int64_t t, int32_t nseg, const int64
     sg.off[k] = seg_off[k];
     sg.start[k + 1] = sg.start[k] + seg_len[k];
   }
-  // step scalars in double: s_t, sum_{i<=t} s_i^2, the averaging weight and the step rates
-  const double lr = hp->lr;
+  // step scalars in double: the scheduled rate s_t, the step rate gamma_t = s_t sqrt(1 - b2^t),
+  // the averaging weight c = gamma_t^2 / sum_{i<=t} gamma_i^2 and the y coefficient.  The sum
+  // runs term by term over the warm-up steps; past them s_i = lr and the tail is
+  // lr^2 ((t - w) - sum_{i=w+1}^{t} b2^i), the geometric part in closed form.
+  const double lr = hp->lr, b2 = hp->beta2;
   const int64_t w = hp->warmup;
   const double st_rate = w > 0 ? lr * std::min(1.0, (double)t / (double)w) : lr;
-  double ssum;
-  if (w > 0) {
-    const double k = (double)std::min<int64_t>(t, w);
-    ssum = lr * lr * k * (k + 1.0) * (2.0 * k + 1.0) / (6.0 * (double)w * (double)w);
-    if (t > w) ssum += lr * lr * (double)(t - w);
-  } else {
-    ssum = lr * lr * (double)t;
+  const int64_t kw = w > 0 ? std::min<int64_t>(t, w) : 0;
+  double gsum = 0.0;
+  for (int64_t i = 1; i <= kw; ++i) {
+    const double si = lr * (double)i / (double)w;
+    gsum += si * si * (1.0 - std::pow(b2, (double)i));
   }
-  const double c = ssum > 0.0 ? st_rate * st_rate / ssum : 1.0;
-  const double gamma = st_rate * std::sqrt(1.0 - std::pow((double)hp->beta2, (double)t));
+  if (t > kw) {
+    const double geo = b2 == 1.0 ? 0.0 : std::pow(b2, (double)(kw + 1)) *
+                                             (1.0 - std::pow(b2, (double)(t - kw))) / (1.0 - b2);
+    gsum += lr * lr * ((double)(t - kw) - (b2 == 1.0 ? (double)(t - kw) : geo));
+  }
+  const double gamma = st_rate * std::sqrt(1.0 - std::pow(b2, (double)t));
+  const double c = gsum > 0.0 ? gamma * gamma / gsum : 1.0;
   tfm::SfScalars sc;
   sc.beta2 = hp->beta2;
   sc.eps = hp->eps;

@@ -89,8 +89,8 @@ def _y_form(y0, grads, lr, b1, b2, eps, wd, warmup):
         v = b2 * v + (1 - b2) * g * g
         gamma = s * np.sqrt(1 - b2 ** t)
         u = g / (np.sqrt(v) + eps) + wd * y
-        ssum += s * s
-        c = s * s / ssum
+        ssum += gamma * gamma
+        c = gamma * gamma / ssum
         y = y + c * (z - y) + gamma * (b1 * (1 - c) - 1) * u
         z = z - gamma * u
         out.append(y.copy())
@@ -113,9 +113,29 @@ def test_schedule_free_x_is_the_weighted_average_of_z():
     opt = optim.ScheduleFreeAdamW(rng.normal(size=20), 3e-3, warmup=5)
     for g in rng.normal(size=(12, 20)):
         opt.step(g)
-    w = np.array(opt.sched_hist) ** 2
+    w = np.array(opt.gamma_hist) ** 2
     avg = (w[:, None] * np.array(opt.z_hist[1:])).sum(axis=0) / w.sum()
     assert np.allclose(opt.x, avg, rtol=1e-12, atol=1e-15)
+
+
+def test_schedule_free_averaging_weights_closed_form():
+    """Without warm-up gamma_t^2 = lr^2 (1 - b2^t), so the averaging weights are
+    c_{t+1} = (1 - b2^t) / (t - b2 (1 - b2^t) / (1 - b2)): 1, then 0.666556..., 0.499833...
+    at b2 = 0.999 (not 1/t, which a schedule without the bias correction would give).  With
+    b1 = 0, y is x, so x_{t+1} = (1 - c) x_t + c z_{t+1} can be checked step by step."""
+    rng = np.random.default_rng(12)
+    lr, b2 = 2e-2, 0.999
+    opt = optim.ScheduleFreeAdamW(rng.normal(size=8), lr, beta1=0.0, beta2=b2)
+    expected = [1.0, 0.6665555185, 0.4998333056]
+    for t in range(1, 7):
+        x_prev = opt.x.copy()
+        opt.step(rng.normal(size=8))
+        c = (1 - b2 ** t) / sum(1 - b2 ** i for i in range(1, t + 1))
+        closed = (1 - b2 ** t) / (t - b2 * (1 - b2 ** t) / (1 - b2))
+        assert abs(c - closed) < 1e-9
+        if t <= 3:
+            assert abs(c - expected[t - 1]) < 1e-9
+        assert np.allclose(opt.x, (1 - c) * x_prev + c * opt.z, rtol=1e-13, atol=1e-15)
 
 
 def test_schedule_free_without_momentum_is_bias_corrected_rmsprop():
