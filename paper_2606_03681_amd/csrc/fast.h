@@ -98,8 +98,14 @@ hipError_t launch_reduce_strided(int Z, int64_t count, int64_t stride, const flo
 hipError_t launch_zero_inactive(const Geo& g, bf16* native, hipStream_t s);
 
 // Weight gradient dW[n][k] = sum_m dY[m][n] X[m][k] (+ db[n] = sum_m dY[m][n]) over M cells,
-// split into chunks of WGRAD_CHUNK cells; partials land in part [Z][N][K] and bpart [Z][N].
-constexpr int WGRAD_CHUNK = 4096;
+// split into Z = wgrad_chunks(M) chunks of wgrad_chunk(M) cells (a multiple of 32, at most
+// WGRAD_CHUNK_MAX): M / 256 cells rounded up while that is at most WGRAD_CHUNK_MAX, so that
+// the workgroups of one tile fill the 256 compute units in whole rounds; partials land in part
+// [Z][N][K] and bpart [Z][N].  wgrad_max_chunks(Mmax) bounds Z for every M <= Mmax.
+constexpr int WGRAD_CHUNK_MAX = 8192;
+constexpr int WGRAD_SLOTS = 256;
+int64_t wgrad_chunk(int64_t M);
+int64_t wgrad_max_chunks(int64_t Mmax);
 struct WgradArgs {
   int64_t M;
   int N, K;

@@ -320,7 +320,7 @@ size_t fast_workspace_bytes(int B, int R, int S, int E, int heads, int H, bool b
   size_t bytes = 2 * (size_t)wo.total * 2 + 1024;   // w and wt
   bytes += (size_t)tiles * 2 * E * 4 + 256;         // LN-backward column partials
   const int64_t cells = (int64_t)B * R * S;
-  const int64_t zw = (cells + WGRAD_CHUNK - 1) / WGRAD_CHUNK;
+  const int64_t zw = wgrad_max_chunks(cells);
   const int64_t maxw = 3LL * E * E > (int64_t)H * E ? 3LL * E * E : (int64_t)H * E;
   const int64_t maxn = 3LL * E > H ? 3LL * E : H;
   bytes += (size_t)zw * maxw * 4 + 256;                // weight-gradient partials

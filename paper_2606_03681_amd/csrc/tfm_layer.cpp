@@ -509,7 +509,7 @@ FastWs fast_ws(const Dims& d, char* ws, const WsLayout& W) {
   p += align_up((size_t)f.wo.total * 2);
   f.lnpart = (float*)p;
   p += align_up((size_t)tfm::gemm_row_tiles(d.Nmax) * 2 * d.E * 4 + 256);
-  const int64_t zw = (d.Nmax + tfm::WGRAD_CHUNK - 1) / tfm::WGRAD_CHUNK;
+  const int64_t zw = tfm::wgrad_max_chunks(d.Nmax);
   const int64_t maxw = 3LL * d.E * d.E > (int64_t)d.H * d.E ? 3LL * d.E * d.E : (int64_t)d.H * d.E;
   f.wpart = (float*)p;
   p += align_up((size_t)zw * maxw * 4 + 256);

@@ -106,7 +106,7 @@ __device__ __forceinline__ void cur_advance(Cursor& c, const Geo& g, int64_t ld,
 // 512 threads = 8 waves in a 2 (n) x 4 (k) arrangement; tile BN x BK.  dY is in layout YM
 // (compact, native or head-major item gradients), X in layout XM (compact or native).  TBL: the
 // workgroup copies the metadata of the columns its chunk spans into LDS (requires R >= MS, so
-// that a chunk spans at most WGRAD_CHUNK / MS + 1 columns).
+// that a chunk spans at most WGRAD_CHUNK_MAX / MS + 1 columns).
 template <int BN, int BK, int YM, int XM, bool TBL>
 __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
   constexpr int NBW = BN / 32;      // 16-row blocks per wave along n (BN/2 rows)
@@ -135,7 +135,7 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
   const int64_t me = mb + a.chunk < a.M ? mb + a.chunk : a.M;
   const Geo& g = a.g;
 
-  constexpr int CT = WGRAD_CHUNK / MS + 2;
+  constexpr int CT = WGRAD_CHUNK_MAX / MS + 2;
   __shared__ int64_t tcell[TBL ? CT : 1];
   __shared__ int32_t tntr[TBL ? CT : 1];
   const int lo = TBL ? (int)(mb / g.R) : 0;
@@ -354,9 +354,22 @@ __global__ __launch_bounds__(256) void k_reduce_z(int Z, int zc, int64_t count, 
   }
 }
 
+int64_t wgrad_chunk(int64_t M) {
+  int64_t c = (M + WGRAD_SLOTS - 1) / WGRAD_SLOTS;
+  c = (c + MS - 1) / MS * MS;
+  if (c < MS) c = MS;
+  return c < WGRAD_CHUNK_MAX ? c : WGRAD_CHUNK_MAX;
+}
+
 int wgrad_chunks(int64_t M) {
-  int64_t z = (M + WGRAD_CHUNK - 1) / WGRAD_CHUNK;
+  const int64_t c = wgrad_chunk(M);
+  const int64_t z = (M + c - 1) / c;
   return (int)(z < 1 ? 1 : z);
+}
+
+int64_t wgrad_max_chunks(int64_t Mmax) {
+  const int64_t big = (Mmax + WGRAD_CHUNK_MAX - 1) / WGRAD_CHUNK_MAX;
+  return big > WGRAD_SLOTS ? big : WGRAD_SLOTS;
 }
 
 template <int BN, int BK>
@@ -393,7 +406,7 @@ hipError_t launch_wgrad_mfma(const WgradArgs& a, hipStream_t s) {
   if (a.N % BN || a.K % BK) return hipErrorInvalidValue;
   const dim3 grid((unsigned)(((int64_t)Z + 7) / 8 * 8 * (a.N / BN) * (a.K / BK)));
   WgradArgs b = a;
-  b.chunk = WGRAD_CHUNK;
+  b.chunk = wgrad_chunk(a.M);
   switch (BN) {
     case 64: return wgrad_modes<64, 64>(b, grid, s);
     case 128: return wgrad_modes<128, 128>(b, grid, s);
