@@ -16,21 +16,25 @@ hipError_t launch_item_attn_fwd(const Geo& g, const bf16* q, const bf16* k, cons
 // Item-axis attention backward: dq, dk, dv head-major (dk, dv for train rows only).
 // Backward in two launches, dQ first: it also writes Dbuf ([problem][R] float32) with
 // D = rowsum(dO o O) per query row, which the dK/dV launch reads.
-hipError_t launch_item_attn_dq(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
-                               const bf16* o, const bf16* dout, const float* lse, float* Dbuf,
-                               bf16* dq, hipStream_t s);
-hipError_t launch_item_attn_dkdv(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
-                                 const bf16* o, const bf16* dout, const float* lse,
-                                 const float* Dbuf, bf16* dk, bf16* dv, hipStream_t s);
+// Both run over the problems of the columns in cl (every column when cl.cols is null).
+hipError_t launch_item_attn_dq(const Geo& g, const ColList& cl, const bf16* q, const bf16* k,
+                               const bf16* v, const bf16* o, const bf16* dout, const float* lse,
+                               float* Dbuf, bf16* dq, hipStream_t s);
+hipError_t launch_item_attn_dkdv(const Geo& g, const ColList& cl, const bf16* q, const bf16* k,
+                                 const bf16* v, const bf16* o, const bf16* dout,
+                                 const float* lse, const float* Dbuf, bf16* dk, bf16* dv,
+                                 hipStream_t s);
 
 // The same backward in one launch for train prefixes of at most 768 rows at d in {16, 32}
-// (item_attn_bwd_fused_ok): one workgroup per (column, head) problem computes P and dS once per
-// score and writes dq, dk and dv; nmax is the longest train prefix of the launch.
+// (item_attn_bwd_fused_ok): one workgroup per (column, head) problem of the columns in cl
+// computes P and dS once per score and writes dq, dk and dv; nmax is the longest train prefix
+// among those columns.
 bool item_attn_bwd_fused_ok(const Geo& g, int nmax);
-hipError_t launch_item_attn_bwd_fused(const Geo& g, int nmax, const bf16* q, const bf16* k,
-                                      const bf16* v, const bf16* o, const bf16* dout,
-                                      const float* lse, bf16* dq, bf16* dk, bf16* dv,
-                                      hipStream_t s);
+int item_attn_bwd_fused_max_rows(int d);
+hipError_t launch_item_attn_bwd_fused(const Geo& g, const ColList& cl, int nmax, const bf16* q,
+                                      const bf16* k, const bf16* v, const bf16* o,
+                                      const bf16* dout, const float* lse, bf16* dq, bf16* dk,
+                                      bf16* dv, hipStream_t s);
 
 // Feature-axis attention (cells of a row, per head).  qkv cell-major [cell][3E]; o, dout
 // cell-major [cell][E]; lse [cell][heads]; dqkv cell-major [cell][3E].  Requires

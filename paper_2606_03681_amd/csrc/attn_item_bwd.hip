@@ -61,7 +61,8 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
                                                         const float* __restrict__ lse,
                                                         const float* __restrict__ Dbuf,
                                                         bf16* __restrict__ dk,
-                                                        bf16* __restrict__ dv, int KT) {
+                                                        bf16* __restrict__ dv, int KT,
+                                                        ColList cl) {
   constexpr int QC = 64;          // queries per chunk
   constexpr int KW = 32;          // keys per wave (two 16-key blocks)
   constexpr int DB = D / 16;
@@ -74,11 +75,13 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
   __shared__ __attribute__((aligned(16))) float Lq[2][QC];
 
   const int bid = blockIdx.x;
-  const int64_t prob = (int64_t)((bid >> 3) / KT) * 8 + (bid & 7);
+  const int64_t pi = (int64_t)((bid >> 3) / KT) * 8 + (bid & 7);  // problem of the list
   const int kt = (bid >> 3) % KT;
-  if (prob >= (int64_t)g.NC * g.heads) return;
-  const int64_t col = prob / g.heads;
-  const int head = (int)(prob - col * g.heads);
+  if (pi >= (int64_t)cl.count * g.heads) return;
+  const int64_t ci = pi / g.heads;
+  const int head = (int)(pi - ci * g.heads);
+  const int64_t col = cl.cols ? cl.cols[ci] : ci;
+  const int64_t prob = col * g.heads + head;
   const int n = g.col_ntr[col];
   const int t0 = kt * 4 * KW;
   if (t0 >= n) return;
@@ -237,7 +240,8 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
                                                       const bf16* __restrict__ dout,
                                                       const float* __restrict__ lse,
                                                       float* __restrict__ Dbuf,
-                                                      bf16* __restrict__ dq, int QT) {
+                                                      bf16* __restrict__ dq, int QT,
+                                                      ColList cl) {
   constexpr int KTL = 64;         // keys per tile
   constexpr int DB = D / 16;
   constexpr int CPR = D / 8;
@@ -247,11 +251,13 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
   __shared__ __attribute__((aligned(16))) bf16 Vs[2][KTL * VS];
 
   const int bid = blockIdx.x;
-  const int64_t prob = (int64_t)((bid >> 3) / QT) * 8 + (bid & 7);
+  const int64_t pi = (int64_t)((bid >> 3) / QT) * 8 + (bid & 7);  // problem of the list
   const int qt = (bid >> 3) % QT;
-  if (prob >= (int64_t)g.NC * g.heads) return;
-  const int64_t col = prob / g.heads;
-  const int head = (int)(prob - col * g.heads);
+  if (pi >= (int64_t)cl.count * g.heads) return;
+  const int64_t ci = pi / g.heads;
+  const int head = (int)(pi - ci * g.heads);
+  const int64_t col = cl.cols ? cl.cols[ci] : ci;
+  const int64_t prob = col * g.heads + head;
   const int n = g.col_ntr[col];
   const int R = g.R, E = g.E;
 
@@ -403,7 +409,8 @@ __global__ __launch_bounds__(512) void k_item_attn_bwd_fused(Geo g, const bf16* 
                                                              const float* __restrict__ lse,
                                                              bf16* __restrict__ dq,
                                                              bf16* __restrict__ dk,
-                                                             bf16* __restrict__ dv, int per_xcd) {
+                                                             bf16* __restrict__ dv, int per_xcd,
+                                                             ColList cl) {
   constexpr int W = 8;                 // waves
   constexpr int QC = 32;               // queries per chunk (two 16-query blocks)
   constexpr int KW = 16 * NKB;         // keys per wave
@@ -423,12 +430,15 @@ __global__ __launch_bounds__(512) void k_item_attn_bwd_fused(Geo g, const bf16* 
   __shared__ __attribute__((aligned(16))) char wreg[W][REG];
   __shared__ __attribute__((aligned(16))) bf16 Vw[W][KW * VS];
 
-  // problems of one XCD are consecutive (the heads of a column share their O / dO rows in L2)
+  // problems of one XCD are consecutive in the list (the heads of a column share their O / dO
+  // rows in L2)
   const int bid = blockIdx.x;
-  const int64_t prob = (int64_t)(bid & 7) * per_xcd + (bid >> 3);
-  if (prob >= (int64_t)g.NC * g.heads) return;
-  const int64_t col = prob / g.heads;
-  const int head = (int)(prob - col * g.heads);
+  const int64_t pi = (int64_t)(bid & 7) * per_xcd + (bid >> 3);
+  if (pi >= (int64_t)cl.count * g.heads) return;
+  const int64_t ci = pi / g.heads;
+  const int head = (int)(pi - ci * g.heads);
+  const int64_t col = cl.cols ? cl.cols[ci] : ci;
+  const int64_t prob = col * g.heads + head;
   const int n = g.col_ntr[col];
   const int R = g.R, E = g.E;
   const int nact = (n + KW - 1) / KW < W ? (n + KW - 1) / KW : W;  // waves that own keys
@@ -638,62 +648,77 @@ static int fused_nkb(int d, int nmax) {
 
 bool item_attn_bwd_fused_ok(const Geo& g, int nmax) { return fused_nkb(g.d, nmax) > 0; }
 
+int item_attn_bwd_fused_max_rows(int d) { return fused_nkb(d, 1) > 0 ? 768 : 0; }
+
 template <int D>
-static hipError_t fused_d(const Geo& g, int nkb, unsigned grid, int per, const bf16* q,
-                          const bf16* k, const bf16* v, const bf16* o, const bf16* dout,
-                          const float* lse, bf16* dq, bf16* dk, bf16* dv, hipStream_t s) {
+static hipError_t fused_d(const Geo& g, const ColList& cl, int nkb, unsigned grid, int per,
+                          const bf16* q, const bf16* k, const bf16* v, const bf16* o,
+                          const bf16* dout, const float* lse, bf16* dq, bf16* dk, bf16* dv,
+                          hipStream_t s) {
   switch (nkb) {
-    case 2: k_item_attn_bwd_fused<D, 2><<<grid, 512, 0, s>>>(g, q, k, v, o, dout, lse, dq, dk, dv, per); break;
-    case 4: k_item_attn_bwd_fused<D, 4><<<grid, 512, 0, s>>>(g, q, k, v, o, dout, lse, dq, dk, dv, per); break;
-    case 6: k_item_attn_bwd_fused<D, 6><<<grid, 512, 0, s>>>(g, q, k, v, o, dout, lse, dq, dk, dv, per); break;
+    case 2:
+      k_item_attn_bwd_fused<D, 2><<<grid, 512, 0, s>>>(g, q, k, v, o, dout, lse, dq, dk, dv,
+                                                         per, cl);
+      break;
+    case 4:
+      k_item_attn_bwd_fused<D, 4><<<grid, 512, 0, s>>>(g, q, k, v, o, dout, lse, dq, dk, dv,
+                                                         per, cl);
+      break;
+    case 6:
+      k_item_attn_bwd_fused<D, 6><<<grid, 512, 0, s>>>(g, q, k, v, o, dout, lse, dq, dk, dv,
+                                                         per, cl);
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_item_attn_bwd_fused(const Geo& g, int nmax, const bf16* q, const bf16* k,
-                                      const bf16* v, const bf16* o, const bf16* dout,
-                                      const float* lse, bf16* dq, bf16* dk, bf16* dv,
-                                      hipStream_t s) {
+hipError_t launch_item_attn_bwd_fused(const Geo& g, const ColList& cl, int nmax, const bf16* q,
+                                      const bf16* k, const bf16* v, const bf16* o,
+                                      const bf16* dout, const float* lse, bf16* dq, bf16* dk,
+                                      bf16* dv, hipStream_t s) {
   const int nkb = fused_nkb(g.d, nmax);
   if (nkb == 0) return hipErrorInvalidValue;
-  const int64_t P = (int64_t)g.NC * g.heads;
+  const int64_t P = (int64_t)cl.count * g.heads;
   if (P == 0) return hipSuccess;
   const int per = (int)((P + 7) / 8);
   const unsigned grid = (unsigned)(8 * per);
-  if (g.d == 16) return fused_d<16>(g, nkb, grid, per, q, k, v, o, dout, lse, dq, dk, dv, s);
-  return fused_d<32>(g, nkb, grid, per, q, k, v, o, dout, lse, dq, dk, dv, s);
+  if (g.d == 16) return fused_d<16>(g, cl, nkb, grid, per, q, k, v, o, dout, lse, dq, dk, dv, s);
+  return fused_d<32>(g, cl, nkb, grid, per, q, k, v, o, dout, lse, dq, dk, dv, s);
 }
 
-hipError_t launch_item_attn_dq(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
-                               const bf16* o, const bf16* dout, const float* lse, float* Dbuf,
-                               bf16* dq, hipStream_t s) {
-  const int64_t P = (int64_t)g.NC * g.heads;
+hipError_t launch_item_attn_dq(const Geo& g, const ColList& cl, const bf16* q, const bf16* k,
+                               const bf16* v, const bf16* o, const bf16* dout, const float* lse,
+                               float* Dbuf, bf16* dq, hipStream_t s) {
+  const int64_t P = (int64_t)cl.count * g.heads;
+  if (P == 0) return hipSuccess;
   const int QT = (g.R + 127) / 128;
   const unsigned grid = (unsigned)((P + 7) / 8 * 8 * QT);
   if (g.d == 16)
-    k_item_attn_dq<16><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dq, QT);
+    k_item_attn_dq<16><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dq, QT, cl);
   else if (g.d == 32)
-    k_item_attn_dq<32><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dq, QT);
+    k_item_attn_dq<32><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dq, QT, cl);
   else if (g.d == 64)
-    k_item_attn_dq<64><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dq, QT);
+    k_item_attn_dq<64><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dq, QT, cl);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
 }
 
-hipError_t launch_item_attn_dkdv(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
-                                 const bf16* o, const bf16* dout, const float* lse,
-                                 const float* Dbuf, bf16* dk, bf16* dv, hipStream_t s) {
-  const int64_t P = (int64_t)g.NC * g.heads;
+hipError_t launch_item_attn_dkdv(const Geo& g, const ColList& cl, const bf16* q, const bf16* k,
+                                 const bf16* v, const bf16* o, const bf16* dout,
+                                 const float* lse, const float* Dbuf, bf16* dk, bf16* dv,
+                                 hipStream_t s) {
+  const int64_t P = (int64_t)cl.count * g.heads;
+  if (P == 0) return hipSuccess;
   const int KT = (g.R + 127) / 128;
   const unsigned grid = (unsigned)((P + 7) / 8 * 8 * KT);
   if (g.d == 16)
-    k_item_attn_dkdv<16><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dk, dv, KT);
+    k_item_attn_dkdv<16><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dk, dv, KT, cl);
   else if (g.d == 32)
-    k_item_attn_dkdv<32><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dk, dv, KT);
+    k_item_attn_dkdv<32><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dk, dv, KT, cl);
   else if (g.d == 64)
-    k_item_attn_dkdv<64><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dk, dv, KT);
+    k_item_attn_dkdv<64><<<grid, 256, 0, s>>>(g, q, k, v, o, dout, lse, Dbuf, dk, dv, KT, cl);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

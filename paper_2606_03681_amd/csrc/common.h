@@ -39,6 +39,13 @@ struct Geo {
   int32_t nmax;              // longest train prefix over the datasets
 };
 
+// A subset of the active columns in a chosen order: column cols[i] for i < count; cols null
+// means every column in order (count = NC).
+struct ColList {
+  const int32_t* cols;
+  int32_t count;
+};
+
 __host__ __device__ inline int64_t native_cell(const Geo& g, int64_t p) {
   int64_t col = p / g.R;
   int64_t r = p - col * g.R;

@@ -67,21 +67,25 @@ hipError_t launch_reduce_strided(int Z, int64_t count, int64_t stride, const flo
   return hipGetLastError();
 }
 
-// One thread per native cell; inactive cells get E zeros (16-byte stores).
+// One wave per native row (b, r): the row's S cells are S * E contiguous elements, written in
+// 16-byte pieces with consecutive lanes on consecutive pieces, zero where the piece's cell is
+// inactive.  Rows of datasets with every cell active leave at once.
 __global__ void k_zero_inactive(Geo g, bf16* __restrict__ x) {
-  int64_t cell = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (cell >= (int64_t)g.B * g.R * g.S) return;
-  int c = (int)(cell % g.S);
-  int b = (int)(cell / ((int64_t)g.R * g.S));
-  if (g.colmap[b * g.S + c] >= 0) return;
-  uint4 z = make_uint4(0, 0, 0, 0);
-  uint4* p = reinterpret_cast<uint4*>(x + cell * g.E);
-  for (int i = 0; i < g.E / 8; ++i) p[i] = z;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= (int64_t)g.B * g.R) return;
+  const int b = (int)(row / g.R);
+  if (g.ds[b].S == g.S) return;
+  const int lane = threadIdx.x & 63, per = g.E / 8;
+  const int32_t* cm = g.colmap + (int64_t)b * g.S;
+  uint4* p = reinterpret_cast<uint4*>(x + row * g.S * g.E);
+  const uint4 z = make_uint4(0, 0, 0, 0);
+  for (int i = lane; i < g.S * per; i += 64)
+    if (cm[i / per] < 0) p[i] = z;
 }
 
 hipError_t launch_zero_inactive(const Geo& g, bf16* native, hipStream_t s) {
-  int64_t n = (int64_t)g.B * g.R * g.S;
-  k_zero_inactive<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(g, native);
+  const int64_t rows = (int64_t)g.B * g.R;
+  k_zero_inactive<<<(unsigned)((rows + 3) / 4), 256, 0, s>>>(g, native);
   return hipGetLastError();
 }
 

@@ -8,7 +8,9 @@
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
+#include <algorithm>
 #include <cstring>
+#include <numeric>
 #include <string>
 #include <vector>
 
@@ -128,7 +130,7 @@ struct Arena {
 
 // Offsets of the device copy of the plan inside a workspace.
 struct MetaOff {
-  size_t blob, ds, col_ds, col_c, colmap, col_cell0, col_ntr;
+  size_t blob, ds, col_ds, col_c, colmap, col_cell0, col_ntr, cord;
 };
 
 MetaOff take_meta(const Dims& d, Arena& a) {
@@ -140,6 +142,7 @@ MetaOff take_meta(const Dims& d, Arena& a) {
   L.colmap = a.take((size_t)d.B * d.S * 4);
   L.col_cell0 = a.take((size_t)d.B * d.S * 8);
   L.col_ntr = a.take((size_t)d.B * d.S * 4);
+  L.cord = a.take((size_t)d.B * d.S * 4);
   return L;
 }
 
@@ -324,6 +327,56 @@ int setup_geo(const Dims& d, const Plan& P, char* ws, const MetaOff& W, tfm::Geo
                                  (int32_t*)(ws + W.col_ds), (int32_t*)(ws + W.col_c),
                                  (int32_t*)(ws + W.colmap), (int64_t*)(ws + W.col_cell0),
                                  (int32_t*)(ws + W.col_ntr), s));
+  return TFM_OK;
+}
+
+// Item-attention backward on the MFMA path.  The columns of datasets whose train prefix fits
+// the one-kernel form go through it, the others through the dQ and dK/dV kernels; within each
+// group the columns of longer prefixes come first, so the largest problems start earliest and
+// the launches end evenly.  The column order is uploaded only when it is not the natural one.
+int item_attn_bwd(const Dims& d, const tfm::Geo& g, const Plan& P, char* ws, const MetaOff& M,
+                  const tfm::bf16* qi, const tfm::bf16* ki, const tfm::bf16* vi,
+                  const tfm::bf16* oi, const tfm::bf16* doi, const float* lsei, float* Dq,
+                  tfm::bf16* dq, tfm::bf16* dk, tfm::bf16* dv, hipStream_t s) {
+  using namespace tfm;
+  const int fmax = item_attn_bwd_fused_max_rows(d.d);
+  const int stride = 3 + d.words;
+  std::vector<int> order(d.B);
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
+    return P.blob[(size_t)x * stride] > P.blob[(size_t)y * stride];
+  });
+  std::vector<int32_t> cols;
+  cols.reserve(P.NC);
+  int nF = 0, nmaxF = 0;
+  for (int pass = 0; pass < 2; ++pass)
+    for (int b : order) {
+      const int32_t* e = &P.blob[(size_t)b * stride];
+      const bool fused = e[0] <= fmax;
+      if (fused != (pass == 0)) continue;
+      for (int k = 0; k < e[2]; ++k) cols.push_back(e[1] + k);
+      if (fused) {
+        nF += e[2];
+        nmaxF = std::max(nmaxF, e[0]);
+      }
+    }
+  bool natural = nF == 0 || nF == P.NC;  // a single group in the natural column order
+  for (int i = 0; i < P.NC && natural; ++i) natural = cols[i] == i;
+  int32_t* dcols = nullptr;
+  if (!natural) {
+    dcols = (int32_t*)(ws + M.cord);
+    HIPCHK(launch_upload(cols.data(), P.NC, dcols, s));
+  }
+  const ColList F{dcols, nF};
+  const ColList T{dcols ? dcols + nF : nullptr, P.NC - nF};
+  if (nF > 0)
+    STEP("item_attn_bwd/mfma",
+         launch_item_attn_bwd_fused(g, F, nmaxF, qi, ki, vi, oi, doi, lsei, dq, dk, dv, s));
+  if (nF < P.NC) {
+    STEP("item_attn_dq/mfma", launch_item_attn_dq(g, T, qi, ki, vi, oi, doi, lsei, Dq, dq, s));
+    STEP("item_attn_dkdv/mfma",
+         launch_item_attn_dkdv(g, T, qi, ki, vi, oi, doi, lsei, Dq, dk, dv, s));
+  }
   return TFM_OK;
 }
 
@@ -628,9 +681,10 @@ struct FastGrads {
   }
 };
 
-int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* prm,
-             const char* sv, const SavedLayout& S, const tfm::bf16* dY, tfm::bf16* dX,
-             float* grads, int accumulate, char* ws, const WsLayout& W, hipStream_t s) {
+int bwd_fast(const Dims& d, const tfm::Geo& g, const Plan& P, const tfm::bf16* X,
+             const float* prm, const char* sv, const SavedLayout& S, const tfm::bf16* dY,
+             tfm::bf16* dX, float* grads, int accumulate, char* ws, const WsLayout& W,
+             hipStream_t s) {
   using namespace tfm;
   typedef tfm::bf16 T;
   const POff o = param_offsets(d.E, d.H);
@@ -681,14 +735,7 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   const T* oi = (const T*)(sv + S.oi);
   const float* lsei = (const float*)(sv + S.lsei);
   float* Dq = (float*)(ws + W.D);
-  if (item_attn_bwd_fused_ok(g, g.nmax)) {
-    STEP("item_attn_bwd/mfma",
-         launch_item_attn_bwd_fused(g, g.nmax, qi, ki, vi, oi, doi, lsei, dq, dk, dv, s));
-  } else {
-    STEP("item_attn_dq/mfma", launch_item_attn_dq(g, qi, ki, vi, oi, doi, lsei, Dq, dq, s));
-    STEP("item_attn_dkdv/mfma",
-         launch_item_attn_dkdv(g, qi, ki, vi, oi, doi, lsei, Dq, dk, dv, s));
-  }
+  CHK(item_attn_bwd(d, g, P, ws, W.meta, qi, ki, vi, oi, doi, lsei, Dq, dq, dk, dv, s));
   CHK(G.run(dq, 3 * E, h1, E, ROWS_COMPACT, o.Wqkv_i, o.bqkv_i, dk, dv));
   // dZ1 = LN1'(dZ2 + dQKV_i Wqkv_i), the gradients read head-major in place
   a = gemm_base(g, N, E, 3 * E, EPI_LN_BWD);
@@ -788,7 +835,7 @@ int fwd_pre(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* p
   return TFM_OK;
 }
 
-int bwd_pre(const Dims& d, const tfm::Geo& g, const float* prm, const char* sv,
+int bwd_pre(const Dims& d, const tfm::Geo& g, const Plan& P, const float* prm, const char* sv,
             const PreSaved& S, const tfm::bf16* dY, tfm::bf16* dX, float* grads, int accumulate,
             char* ws, const WsLayout& W, hipStream_t s) {
   using namespace tfm;
@@ -836,14 +883,7 @@ int bwd_pre(const Dims& d, const tfm::Geo& g, const float* prm, const char* sv,
   const T* oi = (const T*)(sv + S.oi);
   const float* lsei = (const float*)(sv + S.lsei);
   float* Dq = (float*)(ws + W.D);
-  if (item_attn_bwd_fused_ok(g, g.nmax)) {
-    STEP("item_attn_bwd/mfma",
-         launch_item_attn_bwd_fused(g, g.nmax, qi, ki, vi, oi, doi, lsei, dq, dk, dv, s));
-  } else {
-    STEP("item_attn_dq/mfma", launch_item_attn_dq(g, qi, ki, vi, oi, doi, lsei, Dq, dq, s));
-    STEP("item_attn_dkdv/mfma",
-         launch_item_attn_dkdv(g, qi, ki, vi, oi, doi, lsei, Dq, dk, dv, s));
-  }
+  CHK(item_attn_bwd(d, g, P, ws, W.meta, qi, ki, vi, oi, doi, lsei, Dq, dq, dk, dv, s));
   CHK(G.run(dq, 3 * E, (const T*)(sv + S.r2), E, ROWS_COMPACT, o.Wqkv_i, o.bqkv_i, dk, dv));
   // dh1 = dh2 + RMS2'(dQKV_i Wqkv_i), the gradients read head-major in place
   a = gemm_base(g, N, E, 3 * E, EPI_RMS_BWD);
@@ -1104,13 +1144,13 @@ int tfm_layer_bwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* c
   rc = setup_geo(d, P, ws, W.meta, g, s);
   if (rc) return rc;
   if (d.block == TFM_BLOCK_PRENORM)
-    return bwd_pre(d, g, params, (const char*)saved, pre_saved_layout(d), (const tfm::bf16*)dY,
-                   (tfm::bf16*)dX, grads, accumulate, ws, W, s);
+    return bwd_pre(d, g, P, params, (const char*)saved, pre_saved_layout(d),
+                   (const tfm::bf16*)dY, (tfm::bf16*)dX, grads, accumulate, ws, W, s);
   if (d.dtype == TFM_F32)
     return bwd_simple<float>(d, g, (const float*)X, params, (const char*)saved, S,
                              (const float*)dY, (float*)dX, grads, accumulate, ws, W, s);
   if (fast_eligible(d))
-    return bwd_fast(d, g, (const tfm::bf16*)X, params, (const char*)saved, S,
+    return bwd_fast(d, g, P, (const tfm::bf16*)X, params, (const char*)saved, S,
                     (const tfm::bf16*)dY, (tfm::bf16*)dX, grads, accumulate, ws, W, s);
   return bwd_simple<tfm::bf16>(d, g, (const tfm::bf16*)X, params, (const char*)saved, S,
                                (const tfm::bf16*)dY, (tfm::bf16*)dX, grads, accumulate, ws, W,

@@ -102,6 +102,11 @@ TEST_CONFIGS = {
                                n_train=(1, 200), C=20, active=(0, 20), mask="random", E=64,
                                heads=2, H=192, layers=2, cells="normal", weights="xavier_bias",
                                block="pre"),
+    # train prefixes on both sides of the one-kernel item-attention backward's limit (768
+    # rows): its columns and those of the two-kernel form run in separate launches
+    "mixed-prefix-bf16": dict(name="mixed-prefix-bf16", dtype="bf16", B=5, R=1000,
+                              n_train=(600, 1000), C=6, active=(1, 6), mask="random", E=192,
+                              heads=6, H=384, layers=1, cells="normal", weights="xavier_bias"),
     # rows wider than the matrix-core feature attention takes (more than 128 cells at d = 32,
     # more than 64 at d = 64): the bfloat16 feature attention runs on the vector kernels
     "wide-d32-bf16": dict(name="wide-d32-bf16", dtype="bf16", B=3, R=128, n_train=(1, 128),
