@@ -33,10 +33,13 @@ PEAK_TFLOPS = {"mfma_bf16": 2516.6, "mfma_f32": 157.3, "alu_f32": 157.3}
 HBM_PEAK_GBS = 8000.0
 
 
-def step_flops(w):
-    """Algorithmic matmul flops of one launch of each step (per layer), for the whole batch."""
+def step_flops(w, fused_rows=0):
+    """Algorithmic matmul flops of one launch of each step (per layer), for the whole batch.
+    fused_rows: the longest train prefix whose item-attention backward runs as the one-kernel
+    step item_attn_bwd (tfm_prof_item_bwd_fused_rows); the columns of longer prefixes run as
+    item_attn_dq and item_attn_dkdv, so each step is priced for the columns it runs."""
     R, E, H = w.cfg["R"], w.cfg["E"], w.cfg["H"]
-    lin = kv = fa = ia = 0
+    kv = fa = ia = ia_one = 0
     N = 0
     for b in range(len(w.n_train)):
         S = int(np.count_nonzero(w.cell_mask[b]))
@@ -45,14 +48,16 @@ def step_flops(w):
         kv += n * S * 4 * E * E
         fa += R * S * S * 4 * E
         ia += S * R * n * 4 * E
+        if n <= fused_rows:
+            ia_one += S * R * n * 4 * E
     f = {
         "feat_qkv": 6 * N * E * E, "feat_attn_fwd": fa, "feat_out": 2 * N * E * E,
         "item_qkv": 2 * N * E * E + kv, "item_attn_fwd": ia, "item_out": 2 * N * E * E,
         "mlp_up": 2 * N * E * H, "mlp_down": 2 * N * E * H,
-        "feat_attn_bwd": 2 * fa, "item_attn_bwd": 2 * ia,
-        # the MFMA path runs the item-attention backward as two kernels: dQ (dP and dQ
-        # products) and dK/dV (dV and dK products), one forward's worth of products each
-        "item_attn_dq": ia, "item_attn_dkdv": ia,
+        "feat_attn_bwd": 2 * fa, "item_attn_bwd": 2 * (ia_one if fused_rows else ia),
+        # the two-kernel item-attention backward: dQ (dP and dQ products) and dK/dV (dV and dK
+        # products), one forward's worth of products each over the columns it runs
+        "item_attn_dq": ia - ia_one, "item_attn_dkdv": ia - ia_one,
         "mlp_down_dx": 2 * N * E * H, "mlp_up_dx": 2 * N * E * H,
         "item_out_dx": 2 * N * E * E, "item_qkv_dx": 2 * N * E * E + kv,
         "feat_out_dx": 2 * N * E * E, "feat_qkv_dx": 6 * N * E * E,
@@ -91,10 +96,18 @@ def git_rev():
         return None
 
 
+# Query rows of the CPU-baseline sample: a dataset's rows up to this many (its outputs at those
+# rows, keys and values over its whole train prefix), so that the oracle's run stays in the
+# tens of seconds at the long-prefix workload.
+CPU_SAMPLE_ROWS = 1024
+
+
 def cpu_baseline(cfg_index, seed, forward_only=False):
-    """The float64 oracle, untuned, on a bounded sample of the same workload: one dataset
-    through one layer, forward and backward (or forward only), at the workload's full
-    per-dataset shape."""
+    """The float64 oracle, untuned, on a bounded sample of the same workload: dataset 0 through
+    one layer, forward and backward (or forward only), at the workload's per-dataset shape, its
+    outputs taken at the first CPU_SAMPLE_ROWS rows (all rows of every workload but the
+    many-rows one; a row's output needs the train prefix's keys and values, which are computed
+    whole)."""
     import oracle
     try:
         from threadpoolctl import threadpool_info
@@ -103,24 +116,29 @@ def cpu_baseline(cfg_index, seed, forward_only=False):
         threads = os.cpu_count()
     w = wl.make_workload(cfg_index, seed=seed, datasets=[0])
     E, H, heads = w.cfg["E"], w.cfg["H"], w.cfg["heads"]
-    X, dY = w.X64(), w.dY64()
+    R = w.cfg["R"]
+    act = np.flatnonzero(w.cell_mask[0])
+    z, dy = w.X64()[0][:, act], w.dY64()[0][:, act]
+    n = int(w.n_train[0])
+    q = np.arange(min(R, CPU_SAMPLE_ROWS))
     t0 = time.perf_counter()
     if w.block == "pre":
         P = oracle.unpack_prenorm_params(w.params64()[0], E, H)
-        _, cache = oracle.prenorm_layer_forward(X, P, w.n_train, w.cell_mask, heads, 1.0)
+        _, cache = oracle.prenorm_dataset_forward(z, P, heads, n, 1.0, query_rows=q)
         if not forward_only:
-            oracle.prenorm_layer_backward(dY, cache)
+            oracle.prenorm_dataset_backward(dy[q], cache, P, heads)
     else:
         P = oracle.unpack_params(w.params64()[0], E, H)
-        _, cache = oracle.layer_forward(X, P, w.n_train, w.cell_mask, heads)
+        _, cache = oracle.dataset_forward(z, P, heads, n, query_rows=q)
         if not forward_only:
-            oracle.layer_backward(dY, cache)
+            oracle.dataset_backward(dy[q], cache, P, heads)
     dt = time.perf_counter() - t0
-    cells = int(w.cfg["R"] * np.count_nonzero(w.cell_mask[0]))
+    cells = int(len(q) * len(act))
     kind = "fwd" if forward_only else "fwd+bwd"
+    rows = f"all {R} rows" if len(q) == R else f"the first {len(q)} of its {R} rows"
     return {"value": cells / dt, "unit": "cells/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"dataset 0 of the workload, 1 layer {kind}, {cells} active cells, "
-                      f"{dt:.1f} s, host {platform.processor() or platform.machine()} "
+            "sample": f"dataset 0 of the workload, 1 layer {kind} at {rows} ({cells} active "
+                      f"cells), {dt:.1f} s, host {platform.processor() or platform.machine()} "
                       f"({os.cpu_count()} logical CPUs)"}
 
 
@@ -275,7 +293,9 @@ def main():
     roof = None
     steps_out = {}
     if prof:
-        fl = step_flops(w)
+        mfma_path = w.dtype == "bf16"
+        fl = step_flops(w, tfm.prof_item_bwd_fused_rows(cfg["E"] // cfg["heads"]) if mfma_path
+                        else 0)
         for name, (n, ms) in sorted(prof.items(), key=lambda kv: -kv[1][1]):
             steps_out[name] = {"launches": n, "avg_ms": round(ms / n, 5),
                                "share": round(ms / (prof_ms or 1), 4)}

@@ -27,6 +27,13 @@ int tfm_prof_collect(void);
  * summed duration in milliseconds.  Returns 0, or -1 if i is out of range. */
 int tfm_prof_step(int i, const char** name, long long* launches, double* total_ms);
 
+/* Attribution of the item-attention backward to steps, for tools that price each step: on the
+ * bfloat16 MFMA path the columns whose train prefix has at most this many rows run in the
+ * one-kernel backward (step "item_attn_bwd"); longer prefixes run in the two-kernel form
+ * (steps "item_attn_dq" and "item_attn_dkdv").  Returns 0 when head_dim has no one-kernel form.
+ * Pure host function: no device, no side effects. */
+int tfm_prof_item_bwd_fused_rows(int head_dim);
+
 #ifdef __cplusplus
 }
 #endif

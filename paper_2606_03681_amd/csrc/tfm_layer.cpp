@@ -1,6 +1,7 @@
 // Host side of the C ABI declared in include/tfm_layer.h: argument validation, the
 // active-cell plan, buffer layouts and the launch sequences of the forward and backward pass.
 #include "tfm_layer.h"
+#include "tfm_prof.h"
 
 #include <hip/hip_runtime.h>
 
@@ -309,6 +310,12 @@ int make_plan(const Dims& d, const int32_t* n_train, const uint8_t* mask, Plan& 
     tfm::prof_end(s);                \
   } while (0)
 
+#define STEP_ERR(...)                \
+  do {                               \
+    const int rc_ = (__VA_ARGS__);   \
+    if (rc_ != TFM_OK) return rc_;   \
+  } while (0)
+
 int setup_geo(const Dims& d, const Plan& P, char* ws, const MetaOff& W, tfm::Geo& g,
               hipStream_t s) {
   int32_t* blob = (int32_t*)(ws + W.blob);
@@ -607,6 +614,21 @@ FwdBufs bufs_from_saved(char* sv, const SavedLayout& S) {
   return b;
 }
 
+// Feature Q|K|V (projection of the layer input x, rows per xmode), then the feature attention.
+int feat_fwd(const tfm::Geo& g, const tfm::bf16* x, int xmode, const float* bqkv,
+             const FwdBufs& b, const FastWs& f, hipStream_t s) {
+  using namespace tfm;
+  GemmArgs a = gemm_base(g, g.N, 3 * g.E, g.E, EPI_BIAS);
+  a.A = x; a.amode = xmode; a.lda = g.E;
+  a.Bt = f.w + f.wo.qkv_f; a.bias = bqkv; a.out = b.qkvf; a.ldo = 3 * g.E;
+  STEP("feat_qkv/mfma", launch_gemm(a, s));
+  if (feat_attn_mfma_ok(g))
+    STEP("feat_attn_fwd/mfma", launch_feat_attn_fwd(g, b.qkvf, b.of, b.lsef, s));
+  else
+    STEP("feat_attn_fwd/valu", launch_feat_attn_fwd_simple<bf16>(g, b.qkvf, b.of, b.lsef, s));
+  return TFM_OK;
+}
+
 int fwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* prm,
              tfm::bf16* Y, const FwdBufs& b, const FastWs& f, hipStream_t s) {
   using namespace tfm;
@@ -614,17 +636,10 @@ int fwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   const int E = d.E, H = d.H;
   const int64_t N = g.N;
   STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, s));
-  // feature Q|K|V from the native cells
-  GemmArgs a = gemm_base(g, N, 3 * E, E, EPI_BIAS);
-  a.A = X; a.amode = ROWS_NATIVE; a.lda = E;
-  a.Bt = f.w + f.wo.qkv_f; a.bias = prm + o.bqkv_f; a.out = b.qkvf; a.ldo = 3 * E;
-  STEP("feat_qkv/mfma", launch_gemm(a, s));
-  if (feat_attn_mfma_ok(g))
-    STEP("feat_attn_fwd/mfma", launch_feat_attn_fwd(g, b.qkvf, b.of, b.lsef, s));
-  else
-    STEP("feat_attn_fwd/valu", launch_feat_attn_fwd_simple<bf16>(g, b.qkvf, b.of, b.lsef, s));
+  // feature Q|K|V from the native cells, and the feature attention
+  STEP_ERR(feat_fwd(g, X, ROWS_NATIVE, prm + o.bqkv_f, b, f, s));
   // H1 = LN1(X + O_f Wo_f^T + bo_f)
-  a = gemm_base(g, N, E, E, EPI_LN);
+  GemmArgs a = gemm_base(g, N, E, E, EPI_LN);
   a.A = b.of; a.lda = E; a.Bt = f.w + f.wo.o_f; a.bias = prm + o.bo_f;
   a.resid = X; a.rmode = ROWS_NATIVE; a.gamma = prm + o.g1; a.beta = prm + o.be1;
   a.out = b.h1; a.omode = ROWS_COMPACT; a.xhat = b.xh1; a.rstd = b.rs1;
@@ -793,16 +808,9 @@ int fwd_pre(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* p
   STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, s));
   // x' = decay X, r1 = RMS1(x')
   STEP("rms_in/hbm", launch_rms_in(g, X, d.decay, prm + o.g1, kRmsEps, b.xs, b.r1, b.rs1, s));
-  GemmArgs a = gemm_base(g, N, 3 * E, E, EPI_BIAS);
-  a.A = b.r1; a.lda = E; a.Bt = f.w + f.wo.qkv_f; a.bias = prm + o.bqkv_f; a.out = b.qkvf;
-  a.ldo = 3 * E;
-  STEP("feat_qkv/mfma", launch_gemm(a, s));
-  if (feat_attn_mfma_ok(g))
-    STEP("feat_attn_fwd/mfma", launch_feat_attn_fwd(g, b.qkvf, b.of, b.lsef, s));
-  else
-    STEP("feat_attn_fwd/valu", launch_feat_attn_fwd_simple<bf16>(g, b.qkvf, b.of, b.lsef, s));
+  STEP_ERR(feat_fwd(g, b.r1, ROWS_COMPACT, prm + o.bqkv_f, b, f, s));
   // h1 = x' + O_f Wo_f^T + bo_f, r2 = RMS2(h1)
-  a = gemm_base(g, N, E, E, EPI_RMS);
+  GemmArgs a = gemm_base(g, N, E, E, EPI_RMS);
   a.A = b.of; a.lda = E; a.Bt = f.w + f.wo.o_f; a.bias = prm + o.bo_f;
   a.resid = b.xs; a.rmode = ROWS_COMPACT; a.rscale = 1.0f; a.gamma = prm + o.g2;
   a.eps = kRmsEps; a.out = b.h1; a.out2 = b.r2; a.rstd = b.rs2;
@@ -1077,6 +1085,10 @@ size_t tfm_layer_workspace_bytes(const tfm_dims* dims) {
 }
 
 const char* tfm_last_error(void) { return g_err.c_str(); }
+
+int tfm_prof_item_bwd_fused_rows(int head_dim) {
+  return tfm::item_attn_bwd_fused_max_rows(head_dim);
+}
 
 int tfm_layer_fwd(const tfm_dims* dims, const int32_t* n_train, const uint8_t* cell_mask,
                   const void* X, const float* params, void* Y, void* saved, size_t saved_bytes,

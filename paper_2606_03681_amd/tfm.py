@@ -27,7 +27,7 @@ EXPORTS = ("tfm_layer_param_count", "tfm_layer_saved_bytes", "tfm_layer_workspac
            "tfm_thinking_rows_bwd",
            "tfm_infer_workspace_bytes", "tfm_infer_cache_bytes", "tfm_layer_fwd_context",
            "tfm_layer_fwd_query", "tfm_last_error", "tfm_prof_enable", "tfm_prof_collect",
-           "tfm_prof_step", "tfm_ends_param_count", "tfm_ends_workspace_bytes", "tfm_encode_fwd",
+           "tfm_prof_step", "tfm_prof_item_bwd_fused_rows", "tfm_ends_param_count", "tfm_ends_workspace_bytes", "tfm_encode_fwd",
            "tfm_encode_bwd", "tfm_decode_fwd", "tfm_decode_loss", "tfm_clip_workspace_bytes",
            "tfm_clip_scale", "tfm_sfadamw_step", "tfm_muon_workspace_bytes", "tfm_muon_step")
 
@@ -139,6 +139,8 @@ def lib():
         L.tfm_prof_step.restype = i32
         L.tfm_prof_step.argtypes = [i32, P(ctypes.c_char_p), P(ctypes.c_longlong),
                                     P(ctypes.c_double)]
+        L.tfm_prof_item_bwd_fused_rows.restype = i32
+        L.tfm_prof_item_bwd_fused_rows.argtypes = [i32]
         _lib = L
     return _lib
 
@@ -386,6 +388,12 @@ def muon_step(hp, rows, cols, W, G, buf, grad_scale, workspace, stream=None):
 def prof_enable(on=True):
     """Turns per-step HIP-event timing of the library's launches on or off (tfm_prof.h)."""
     _check(lib().tfm_prof_enable(int(bool(on))))
+
+
+def prof_item_bwd_fused_rows(head_dim):
+    """Longest train prefix whose item-attention backward runs as the one-kernel step
+    "item_attn_bwd" at this head dimension (0: never); see tfm_prof.h."""
+    return int(lib().tfm_prof_item_bwd_fused_rows(int(head_dim)))
 
 
 def prof_collect():
