@@ -5,16 +5,18 @@
 // p = (col0 + k) * R + r, so they are R * 3E elements apart in the Q|K|V buffer; a buffer
 // resource based at the row's first cell with S_b cells in range returns zeros past the last
 // active cell, which pads the cell count to whole 16-cell MFMA blocks.  Every operand fragment
-// of the pair is loaded once, at the start (a single memory round trip per wave); the
-// transposed LDS tiles the products need are written from those registers.
+// of the pair is loaded once, at the start (a single memory round trip per wave); the operands
+// whose contraction runs over cells are written from those registers into row-major LDS tiles
+// and read back transposed.
 //
 // Forward, per 16-query block: S^T = K Q^T (keys x queries), a softmax over all keys at once
-// (no online rescaling: the row fits), and O^T = V^T P^T with V^T in the wave's LDS.
+// (no online rescaling: the row fits), and O^T = V^T P^T with V in the wave's LDS.
 //
 // Backward, two sweeps (probabilities recomputed from the saved log-sum-exp):
-//   query-major:  dS^T = P^T (dP^T - D),  dQ^T = K^T dS^T             (K^T in LDS)
-//   key-major:    dS = P (dP - D),  dV^T += dO^T P,  dK^T += Q^T dS    (Q^T, dO^T in LDS)
-// so that every product's fragment comes from the lane's own registers or an 8-byte LDS read.
+//   query-major:  dS^T = P^T (dP^T - D),  dQ^T = K^T dS^T             (K in LDS)
+//   key-major:    dS = P (dP - D),  dV^T += dO^T P,  dK^T += Q^T dS    (Q, dO in LDS)
+// so that every product's fragment comes from the lane's own registers or a transposed LDS
+// read.
 #include <math.h>
 
 #include "attn.h"
@@ -30,15 +32,6 @@ constexpr float LOG2E = 1.4426950408889634f;
 // Makes this wave's LDS writes visible to its own later LDS reads (no workgroup barrier: each
 // wave owns its LDS region).
 __device__ __forceinline__ void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
-
-__device__ __forceinline__ bf16x8 cat8(uint2 lo, uint2 hi) {
-  uint4 u = make_uint4(lo.x, lo.y, hi.x, hi.y);
-  return *reinterpret_cast<bf16x8*>(&u);
-}
-
-__device__ __forceinline__ bf16x8 ld_perm(const bf16* p) {
-  return cat8(*reinterpret_cast<const uint2*>(p), *reinterpret_cast<const uint2*>(p + 16));
-}
 
 __device__ __forceinline__ bf16x8 pack8(const f32x4& a, const f32x4& b) {
   uint4 u = make_uint4(pack2(a[0], a[1]), pack2(a[2], a[3]), pack2(b[0], b[1]),
@@ -64,18 +57,52 @@ __device__ __forceinline__ bool pair_of(const Geo& g, int64_t t, Pair& p) {
   return true;
 }
 
-// Write the row-role fragments fr[kb] (lane: cell kb*16 + c) transposed into dst[d][TSF] for
-// the first nks of the NKB 16-cell blocks.
-template <int D, int NKB, int TSF>
-__device__ __forceinline__ void stage_frag(const typename HF<D>::frag* fr, int nks, int c,
-                                           int lg, bf16* dst) {
+// Row-major [cell][d] LDS tiles, read back transposed by ds_read_b64_tr_b16 (lds_read_tr16).
+// A transposed read lets every lane of a 32-lane half name 8 bytes of rows r .. r + 7 at one
+// 32-byte column chunk; rows are d * 2 bytes long with no padding, and the 32-byte chunks of
+// row r are XOR-rotated so that those 8 rows land on 8 distinct groups of 8 banks:
+//   d = 16: one chunk per row, rows 8 apart already distinct;
+//   d = 32: chunk ^ ((r >> 2) & 1)   (rows r and r + 4 share banks otherwise);
+//   d = 64: chunk ^ ((r >> 1) & 3)   (rows r, r + 2, r + 4, r + 6 share banks otherwise).
+template <int D>
+__device__ __forceinline__ int chunk_swz(int r) {
+  return D == 16 ? 0 : (D == 32 ? (r >> 2) & 1 : (r >> 1) & 3);
+}
+
+// Store the row-role fragments fr[kb] (lane (lg, c): cell kb*16 + c, the HF<D> dims of lg) of
+// the first nks 16-cell blocks into the row-major tile.
+template <int D, int NKB>
+__device__ __forceinline__ void put_rows(const typename HF<D>::frag* fr, int nks, int c, int lg,
+                                         bf16* tile) {
 #pragma unroll
   for (int kb = 0; kb < NKB; ++kb)
     if (kb < nks) {
-#pragma unroll
-      for (int j = 0; j < HF<D>::EPL; ++j)
-        dst[HF<D>::dim(lg, j) * TSF + kb * 16 + c] = HF<D>::elem(fr[kb], j);
+      const int r = kb * 16 + c;
+      bf16* row = tile + r * D;
+      const int z = chunk_swz<D>(r);
+      if constexpr (D == 16) {
+        *reinterpret_cast<uint2*>(row + 4 * lg) = *reinterpret_cast<const uint2*>(&fr[kb]);
+      } else if constexpr (D == 32) {
+        *reinterpret_cast<uint4*>(row + ((lg >> 1) ^ z) * 16 + (lg & 1) * 8) =
+            *reinterpret_cast<const uint4*>(&fr[kb]);
+      } else {
+        *reinterpret_cast<uint4*>(row + ((lg >> 1) ^ z) * 16 + (lg & 1) * 8) =
+            *reinterpret_cast<const uint4*>(&fr[kb].lo);
+        *reinterpret_cast<uint4*>(row + ((2 + (lg >> 1)) ^ z) * 16 + (lg & 1) * 8) =
+            *reinterpret_cast<const uint4*>(&fr[kb].hi);
+      }
     }
+}
+
+// MFMA operand whose k positions run down the tile's cells: lane (g, c) receives dim
+// db*16 + c of cells 32 ks + {4g .. 4g+3} (slots 0-3) and 32 ks + 16 + {4g .. 4g+3} (slots
+// 4-7), the k order of two packed 16-cell score blocks (pack8).
+template <int D>
+__device__ __forceinline__ bf16x8 get_cols(const bf16* tile, int ks, int db, int lane) {
+  const int r = ks * 32 + (lane >> 2);
+  const bf16* p = tile + r * D + ((db ^ chunk_swz<D>(r)) * 16) + 4 * (lane & 3);
+  const bf16x4 lo = lds_read_tr16(p), hi = lds_read_tr16(p + 16 * D);
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
 }  // namespace
@@ -87,8 +114,7 @@ __global__ __launch_bounds__(256) void k_feat_attn_fwd(Geo g, const bf16* __rest
                                                        float* __restrict__ lse) {
   constexpr int DB = D / 16;
   constexpr int NKB = SM / 16;   // 16-cell blocks of the longest row handled
-  constexpr int TSF = SM + 8;    // LDS row stride of the transposed tiles (elements)
-  __shared__ __attribute__((aligned(16))) bf16 Vt[4][D * TSF];
+  __shared__ __attribute__((aligned(16))) bf16 Vs[4][SM * D];  // per wave: V, [cell][d]
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int c = lane & 15, lg = lane >> 4;
   Pair pr;
@@ -100,7 +126,7 @@ __global__ __launch_bounds__(256) void k_feat_attn_fwd(Geo g, const bf16* __rest
   const uint32_t oq = pr.head * D * 2, ok = (E + pr.head * D) * 2, ov = (2 * E + pr.head * D) * 2;
   const float c2 = LOG2E / sqrtf((float)D);
 
-  bf16* vt = Vt[w];
+  bf16* vt = Vs[w];
   const int nks = (nkb + 1) & ~1;  // staged blocks: whole pairs of 16-cell blocks
   typedef typename HF<D>::frag frag;
   frag kf[NKB], qf[NKB];
@@ -114,7 +140,7 @@ __global__ __launch_bounds__(256) void k_feat_attn_fwd(Geo g, const bf16* __rest
         vf[kb] = HF<D>::buf(rq, row + ov, lg);
         qf[kb] = HF<D>::buf(rq, row + oq, lg);
       }
-    stage_frag<D, NKB, TSF>(vf, nks, c, lg, vt);
+    put_rows<D, NKB>(vf, nks, c, lg, vt);
   }
   wave_lds_sync();
 
@@ -130,11 +156,13 @@ __global__ __launch_bounds__(256) void k_feat_attn_fwd(Geo g, const bf16* __rest
     for (int kb = 0; kb < NKB; ++kb) {
       if (kb < nkb) {
         s[kb] = HF<D>::mma(kf[kb], qf[qb]);
+        if (kb == nkb - 1) {  // keys past the row's last cell (only the last block has any)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          if (kb * 16 + lg * 4 + i >= S) s[kb][i] = -INFINITY;
-          mx = fmaxf(mx, s[kb][i]);
+          for (int i = 0; i < 4; ++i)
+            if (kb * 16 + lg * 4 + i >= S) s[kb][i] = -INFINITY;
         }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[kb][i]);
       }
     }
     mx = rows4_max(mx);
@@ -161,7 +189,7 @@ __global__ __launch_bounds__(256) void k_feat_attn_fwd(Geo g, const bf16* __rest
         const bf16x8 pf = pack8(s[2 * ks], s[2 * ks + 1]);
 #pragma unroll
         for (int db = 0; db < DB; ++db)
-          oacc[db] = mfma16(ld_perm(&vt[(db * 16 + c) * TSF + ks * 32 + lg * 4]), pf, oacc[db]);
+          oacc[db] = mfma16(get_cols<D>(vt, ks, db, lane), pf, oacc[db]);
       }
     }
     const int qq = qb * 16 + c;
@@ -187,9 +215,8 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
                                                        bf16* __restrict__ dqkv) {
   constexpr int DB = D / 16;
   constexpr int NKB = SM / 16;   // 16-cell blocks of the longest row handled
-  constexpr int TSF = SM + 8;    // LDS row stride of the transposed tiles (elements)
-  // per wave: sweep 1 uses [0, D*TSF) for K^T; sweep 2 uses Q^T then dO^T
-  __shared__ __attribute__((aligned(16))) bf16 T[4][2 * D * TSF];
+  // per wave, [cell][d] tiles: sweep 1 uses the first for K; sweep 2 holds Q and dO
+  __shared__ __attribute__((aligned(16))) bf16 T[4][2 * SM * D];
   __shared__ __attribute__((aligned(16))) float Lr[4][SM];
   __shared__ __attribute__((aligned(16))) float Dr[4][SM];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -207,7 +234,7 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
   const float c2 = LOG2E / sqrtf((float)D);
   const float tau = 1.0f / sqrtf((float)D);
   bf16* t0 = T[w];
-  bf16* t1 = T[w] + D * TSF;
+  bf16* t1 = T[w] + SM * D;
   bf16* drow = dqkv + pr.cell0 * 3 * E + pr.head * D;
   const uint64_t dcs = (uint64_t)g.R * 3 * E;  // elements between cells in dQKV
 
@@ -237,7 +264,7 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
         Dr[w][kb * 16 + c] = dq[kb];
       }
     }
-  stage_frag<D, NKB, TSF>(kf, nks, c, lg, t0);  // K^T
+  put_rows<D, NKB>(kf, nks, c, lg, t0);  // K
   wave_lds_sync();
 
   // ---- sweep 1 (query-major): dQ^T = K^T dS^T, one pair of key blocks (32 keys) at a time
@@ -258,12 +285,16 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
         if (kb < nkb) {
           const f32x4 s = HF<D>::mma(kf[kb], qf[qb]);
           const f32x4 dp = HF<D>::mma(vf[kb], df[qb]);
+          f32x4 p;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            float p = exp2_hw(fmaf(s[i], c2, nbq[qb]));
-            if (kb * 16 + lg * 4 + i >= S) p = 0.f;
-            ds[h][i] = p * (dp[i] - dq[qb]);
+          for (int i = 0; i < 4; ++i) p[i] = exp2_hw(fmaf(s[i], c2, nbq[qb]));
+          if (kb == nkb - 1) {  // keys past the row's last cell
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (kb * 16 + lg * 4 + i >= S) p[i] = 0.f;
           }
+#pragma unroll
+          for (int i = 0; i < 4; ++i) ds[h][i] = p[i] * (dp[i] - dq[qb]);
         } else {
           ds[h] = zero4();
         }
@@ -271,7 +302,7 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
       const bf16x8 sf = pack8(ds[0], ds[1]);
 #pragma unroll
       for (int db = 0; db < DB; ++db)
-        acc[db] = mfma16(ld_perm(&t0[(db * 16 + c) * TSF + ks * 32 + lg * 4]), sf, acc[db]);
+        acc[db] = mfma16(get_cols<D>(t0, ks, db, lane), sf, acc[db]);
     }
     if (qq < S) {
 #pragma unroll
@@ -284,8 +315,8 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
   }
   wave_lds_sync();
   // ---- sweep 2 (key-major): dV^T += dO^T P, dK^T += Q^T dS over all query blocks
-  stage_frag<D, NKB, TSF>(qf, nks, c, lg, t0);  // Q^T
-  stage_frag<D, NKB, TSF>(df, nks, c, lg, t1);  // dO^T
+  put_rows<D, NKB>(qf, nks, c, lg, t0);  // Q
+  put_rows<D, NKB>(df, nks, c, lg, t1);  // dO
   wave_lds_sync();
 #pragma unroll
   for (int kb = 0; kb < NKB; ++kb) {
@@ -306,19 +337,21 @@ __global__ __launch_bounds__(256) void k_feat_attn_bwd(Geo g, const bf16* __rest
           const float4 d4 = *reinterpret_cast<const float4*>(&Dr[w][qb * 16 + lg * 4]);
           const float lv[4] = {l4.x, l4.y, l4.z, l4.w}, dv4[4] = {d4.x, d4.y, d4.z, d4.w};
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const bool qok = qb * 16 + lg * 4 + i < S;
-            p[h][i] = qok ? exp2_hw(fmaf(s[i], c2, lv[i])) : 0.f;
-            dsv[h][i] = p[h][i] * (dp[i] - dv4[i]);
+          for (int i = 0; i < 4; ++i) p[h][i] = exp2_hw(fmaf(s[i], c2, lv[i]));
+          if (qb >= nkb - 1) {  // queries past the row's last cell (and the zero block after)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (qb * 16 + lg * 4 + i >= S) p[h][i] = 0.f;
           }
+#pragma unroll
+          for (int i = 0; i < 4; ++i) dsv[h][i] = p[h][i] * (dp[i] - dv4[i]);
         }
         const bf16x8 pf = pack8(p[0], p[1]);
         const bf16x8 sf = pack8(dsv[0], dsv[1]);
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const int row = (db * 16 + c) * TSF + ks * 32 + lg * 4;
-          dvt[db] = mfma16(ld_perm(&t1[row]), pf, dvt[db]);
-          dkt[db] = mfma16(ld_perm(&t0[row]), sf, dkt[db]);
+          dvt[db] = mfma16(get_cols<D>(t1, ks, db, lane), pf, dvt[db]);
+          dkt[db] = mfma16(get_cols<D>(t0, ks, db, lane), sf, dkt[db]);
         }
       }
     }
