@@ -386,6 +386,30 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
   }
 }
 
+// The fused kernel's 64-byte LDS rows (the dS tile of 32 queries, the values at d = 32): the two
+// 16-byte halves of each 32-byte chunk and the two chunks are swapped by bits 1 and 2 of the
+// row, which makes both its 16-byte row accesses (16 rows, one column, per instruction) and its
+// transposed reads (8 rows of one 32-byte chunk per half-wave) free of bank conflicts.
+__device__ __forceinline__ int row64_swz(int r, int byte) {
+  return byte ^ (((r >> 1) & 1) << 4) ^ (((r >> 2) & 1) << 5);
+}
+
+// The dS tile holds, in row `key`, the 32 queries of a chunk in the lane order of the score
+// blocks: byte 16 g + 8 qb holds queries qb*16 + 4g .. + 3, so the 8 values of one lane (its
+// two 16-query blocks) are one 16-byte write.  Transposed read (ds_read_b64_tr_b16) of key
+// rows kr0 + {4g .. 4g+3, 16 + 4g .. 16 + 4g+3} (kr0 a multiple of 32): lane (g, c) receives
+// query qb*16 + c.  off is the lane's byte offset for kr0 = 0 (ds_tile_off), which the swizzle
+// leaves unchanged by multiples of 8 rows.
+__device__ __forceinline__ int ds_tile_off(int lane, int qb) {
+  const int r = lane >> 2;
+  return r * 64 + row64_swz(r, 16 * (lane & 3) + 8 * qb);
+}
+__device__ __forceinline__ bf16x8 ds_tile_tr(const bf16* T, int kr0, int off) {
+  const bf16* p = T + (kr0 * 64 + off) / 2;
+  const bf16x4 lo = lds_read_tr16(p), hi = lds_read_tr16(p + 16 * 32);
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
 // =============================================================================== fused
 // One workgroup per (column, head) problem whose train prefix has at most 8 * 16 * NKB rows
 // (NKB <= 6):
@@ -394,9 +418,9 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
 // chunk and wave, in the key-major layout of the dK/dV kernel above:
 //   S = Q K^T, dP = dO V^T  (seeded with -lse log2 e and -D),  P = exp2(S),  dS = P (dP - D)
 //   dV^T += dO^T P,  dK^T += Q^T dS                     (registers, across every chunk)
-//   dQ_w = dS K over the wave's own keys: dS goes through the wave's LDS tile [key][query]
-//          (8-byte row writes), read back transposed as the A operand; K^T fragments are
-//          built once from an LDS copy of the wave's keys
+//   dQ_w^T = K^T dS^T over the wave's own keys: dS goes through the wave's LDS tile
+//          [key][query] (one 16-byte row write per key block), read back transposed as the B
+//          operand; K^T fragments are built once from an LDS copy of the wave's keys
 // then the eight dQ_w of the chunk are added in wave order through LDS and stored.  P and dS
 // are computed once per score (the two-kernel form computes them in both kernels), and every
 // output element is summed in a fixed order, so results are bitwise reproducible.
@@ -417,11 +441,11 @@ __global__ __launch_bounds__(512) void k_item_attn_bwd_fused(Geo g, const bf16* 
   constexpr int DB = D / 16;
   constexpr int CPR = D / 8;           // 16-byte chunks per row of d values
   constexpr int RS = tr_stride<D>();   // LDS row stride of Q / dO and of the key copy
-  constexpr int DSS = 48;              // dS^T tile [key][32 queries]: 96-byte rows (see ld_tr8)
-  constexpr int PQS = QC + 4;          // dQ partial [d][query] floats: 144-byte rows
-  constexpr int T1 = KW * DSS * 2, T2 = D * PQS * 4, T3 = KW * RS * 2;
+  constexpr int PQS = D + 4;           // dQ partial [query][d] floats: rows of 16 mod 32 bytes
+  constexpr int T1 = KW * 64, T2 = QC * PQS * 4, T3 = KW * RS * 2;  // dS tile: 64-byte rows
   constexpr int REG = (T1 > T2 ? (T1 > T3 ? T1 : T3) : (T2 > T3 ? T2 : T3));
-  constexpr int VS = D + 8;             // the wave's value rows: 16-byte reads conflict-free
+  // the wave's value rows: 64-byte swizzled rows at d = 32 (row64_swz), padded at d = 16
+  constexpr int VS = D == 32 ? 32 : D + 8;
   static_assert(NKB % 2 == 0, "keys per wave must fill 32-key steps");
   __shared__ __attribute__((aligned(16))) bf16 Qs[2][QC * RS];
   __shared__ __attribute__((aligned(16))) bf16 dOs[2][QC * RS];
@@ -463,9 +487,13 @@ __global__ __launch_bounds__(512) void k_item_attn_bwd_fused(Geo g, const bf16* 
   // read K = V = 0: their dK, dV are never stored and they add K = 0 to dQ, so no key masking
   // is needed
   frag kf[NKB];
-  bf16x8 ktf[NKB / 2][DB];  // K as the B operand of dS K: dims db*16 + c, keys of a 32-key step
+  bf16x8 ktf[NKB / 2][DB];  // K^T as the A operand of K^T dS^T: dims db*16 + c, 32-key steps
   f32x4 dkt[NKB][DB], dvt[NKB][DB];
   bf16* vw = Vw[w];
+  // the lane's byte offsets in 64-byte swizzled rows: its 16-byte piece of row c (+ 16 kb rows)
+  // and its transposed-read addresses in the dS tile
+  const int roff = c * 64 + row64_swz(c, 16 * lg);
+  const int toff0 = ds_tile_off(lane, 0), toff1 = ds_tile_off(lane, 1);
 #pragma unroll
   for (int kb = 0; kb < NKB; ++kb) {
 #pragma unroll
@@ -473,7 +501,11 @@ __global__ __launch_bounds__(512) void k_item_attn_bwd_fused(Geo g, const bf16* 
     const uint32_t key = (uint32_t)(kw0 + kb * 16 + c);
     kf[kb] = HF<D>::buf(rK, key * rowQ, lg);
     const frag vv = HF<D>::buf(rV, key * rowQ, lg);
-    *reinterpret_cast<frag*>(&vw[(kb * 16 + c) * VS + lg * HF<D>::EPL]) = vv;
+    const int vr = kb * 16 + c;
+    if constexpr (D == 32)
+      *reinterpret_cast<frag*>(&vw[kb * 16 * 32 + roff / 2]) = vv;
+    else
+      *reinterpret_cast<frag*>(&vw[vr * VS + lg * HF<D>::EPL]) = vv;
   }
   {
     bf16* kst = reinterpret_cast<bf16*>(wreg[w]);  // [KW][RS] row-major copy of the keys
@@ -545,10 +577,15 @@ __global__ __launch_bounds__(512) void k_item_attn_bwd_fused(Geo g, const bf16* 
         qt[db] = ld_tr8(Qs[b], RS, db * 16, lane);
         dot[db] = ld_tr8(dOs[b], RS, db * 16, lane);
       }
-      bf16* dst = reinterpret_cast<bf16*>(wreg[w]);  // dS^T tile [KW][DSS]
+      bf16* dst = reinterpret_cast<bf16*>(wreg[w]);  // dS tile [KW][32 queries]
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb) {
-        const frag vfk = HF<D>::lds(&vw[(kb * 16 + c) * VS], lg);
+        const int vr = kb * 16 + c;
+        frag vfk;
+        if constexpr (D == 32)
+          vfk = *reinterpret_cast<const frag*>(&vw[kb * 16 * 32 + roff / 2]);
+        else
+          vfk = HF<D>::lds(&vw[vr * VS], lg);
         uint32_t pw[2][2], sw[2][2];
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
@@ -570,14 +607,11 @@ __global__ __launch_bounds__(512) void k_item_attn_bwd_fused(Geo g, const bf16* 
           dvt[kb][db] = mfma16(dot[db], pf, dvt[kb][db]);
           dkt[kb][db] = mfma16(qt[db], sf, dkt[kb][db]);
         }
-        // dS^T rows: key kb*16 + c, queries qb*16 + 4 lg .. + 3
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
-          *reinterpret_cast<uint2*>(&dst[(kb * 16 + c) * DSS + qb * 16 + 4 * lg]) =
-              make_uint2(sw[qb][0], sw[qb][1]);
+        // dS row of key kb*16 + c: the lane's queries 4 lg .. + 3 of both 16-query blocks
+        *reinterpret_cast<bf16x8*>(&dst[kb * 16 * 32 + roff / 2]) = sf;
       }
       wave_lds_sync();
-      // dQ_w[q][d] = sum over the wave's keys of dS[q][key] K[key][d]
+      // dQ_w^T[d][q] = sum over the wave's keys of K[key][d] dS[q][key]
       f32x4 dqp[2][DB];
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb)
@@ -587,18 +621,18 @@ __global__ __launch_bounds__(512) void k_item_attn_bwd_fused(Geo g, const bf16* 
       for (int ks = 0; ks < NKB / 2; ++ks)
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) {
-          const bf16x8 af = ld_tr8(&dst[ks * 32 * DSS], DSS, qb * 16, lane);
+          const bf16x8 bq = ds_tile_tr(dst, ks * 32, qb ? toff1 : toff0);
 #pragma unroll
-          for (int db = 0; db < DB; ++db) dqp[qb][db] = mfma16(af, ktf[ks][db], dqp[qb][db]);
+          for (int db = 0; db < DB; ++db) dqp[qb][db] = mfma16(ktf[ks][db], bq, dqp[qb][db]);
         }
       wave_lds_sync();  // the tile is read before the partial overwrites it
-      // lane: dQ_w[q = qb*16 + 4 lg + i][d = db*16 + c] -> partial [d][q]
+      // lane: dQ_w[q = qb*16 + c][d = db*16 + 4 lg + i] -> partial [q][d]
       float* pq = reinterpret_cast<float*>(wreg[w]);
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb)
 #pragma unroll
         for (int db = 0; db < DB; ++db)
-          *reinterpret_cast<f32x4*>(&pq[(db * 16 + c) * PQS + qb * 16 + 4 * lg]) = dqp[qb][db];
+          *reinterpret_cast<f32x4*>(&pq[(qb * 16 + c) * PQS + db * 16 + 4 * lg]) = dqp[qb][db];
     }
     if (ic + 1 < NCH) sstore(b ^ 1);
     lds_barrier();
@@ -607,9 +641,10 @@ __global__ __launch_bounds__(512) void k_item_attn_bwd_fused(Geo g, const bf16* 
       const int qq = tid / (D / 2), d0 = 2 * (tid % (D / 2));
       float s0 = 0.f, s1 = 0.f;
       for (int w2 = 0; w2 < nact; ++w2) {
-        const float* pq = reinterpret_cast<const float*>(wreg[w2]);
-        s0 += pq[d0 * PQS + qq];
-        s1 += pq[(d0 + 1) * PQS + qq];
+        const float2 pv =
+            *reinterpret_cast<const float2*>(reinterpret_cast<const float*>(wreg[w2]) + qq * PQS + d0);
+        s0 += pv.x;
+        s1 += pv.y;
       }
       const int qg = ic * QC + qq;
       if (qg < R)
