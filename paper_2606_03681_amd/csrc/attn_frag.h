@@ -106,4 +106,23 @@ constexpr int tr_stride() {
   return D <= 32 ? 48 : 80;
 }
 
+// LDS tiles of 64-byte rows (32 bf16: d = 32, or 32 queries): the two 16-byte halves of each
+// 32-byte chunk and the two chunks are swapped by bits 1 and 2 of the row.  Measured on this
+// LDS, that makes 16-byte row accesses (16 rows, one column, per instruction) and transposed
+// reads (8 rows of one 32-byte chunk per half-wave) free of bank conflicts, where padded rows
+// serve one of the two at best.  Returns the physical byte offset within row r.
+__device__ __forceinline__ int row64_swz(int r, int byte) {
+  return byte ^ (((r >> 1) & 1) << 4) ^ (((r >> 2) & 1) << 5);
+}
+
+// Transposed read (ds_read_b64_tr_b16) of a row64 tile: off is the lane's byte offset of row
+// lane / 4 (row64_swz applied; unchanged by multiples of 8 rows), T the tile's first row of the
+// 32-row step.  Lane (g, c) receives the column the offset names, of rows {4g .. 4g+3} (slots
+// 0-3) and 16 + {4g .. 4g+3} (slots 4-7).
+__device__ __forceinline__ bf16x8 tr8_row64(const bf16* T, int off) {
+  const bf16* p = T + off / 2;
+  const bf16x4 lo = lds_read_tr16(p), hi = lds_read_tr16(p + 16 * 32);
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
 }  // namespace tfm

@@ -5,8 +5,8 @@
 // are never materialised and the only masking is inside the last, partial key tile.
 //
 // One workgroup = 4 waves = 128 queries of one problem; each wave owns 32 queries (two 16-query
-// MFMA blocks).  Key tiles of 64 keys are staged in LDS (K as [key][d], V transposed as [d][key])
-// with double buffering and shared by the 4 waves.  Per tile a wave computes S^T = K Q^T
+// MFMA blocks).  Key tiles of 64 keys are staged in LDS (K and V as [key][d]; V is read back
+// transposed) with double buffering and shared by the 4 waves.  Per tile a wave computes S^T = K Q^T
 // (keys x queries, so that a lane holds 4 keys of one query), the online softmax in the exp2
 // domain with the scale folded into one FMA, and O^T += V^T P^T where the D tile of S^T is
 // reused directly as the B operand (the k positions of V^T are permuted to match).
@@ -39,8 +39,12 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
                                                        bf16* __restrict__ o,
                                                        float* __restrict__ lse, int QT,
                                                        int kR) {
-  constexpr int KS = D + 8;   // LDS row stride of K (elements; conflict-free 16-byte reads)
-  constexpr int VS = tr_stride<D>();  // LDS row stride of V (conflict-free transpose reads)
+  // d = 32: K and V rows of 64 bytes, swizzled (row64_swz); otherwise padded rows
+  constexpr bool SW = D == 32;
+  // LDS row stride of K (elements): 16-byte row reads are conflict-free at strides of an odd
+  // multiple of 32 bytes (d = 64: 160 bytes)
+  constexpr int KS = SW ? 32 : (D == 64 ? tr_stride<D>() : D + 8);
+  constexpr int VS = SW ? 32 : tr_stride<D>();     // LDS row stride of V
   constexpr int DB = D / 16;  // 16-wide dim blocks
   constexpr int CPR = D / 8;  // 16-byte chunks per key row
   __shared__ __attribute__((aligned(16))) bf16 Ks[2][KT * KS];
@@ -70,14 +74,18 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
     qf[qb] = qq < R ? HF<D>::glob(Qp + (int64_t)qq * D, lg) : HF<D>::zero();
   }
 
-  // staging: item it = tid + 256 i -> (key it / CPR, 16-byte chunk of its dims)
+  // staging: item it = tid + 256 i -> (key, 16-byte chunk of its dims): key it / CPR, chunk
+  // it % CPR; at d = 32 key (it % 16) + 16 (it / 64), chunk (it / 16) % 4, so that each store
+  // instruction names one chunk of 16 rows (the conflict-free access of the swizzled rows)
   constexpr int NSI = (KT * CPR + 255) / 256;  // staging items per thread
   uint4 rk[NSI], rv[NSI];
+  auto item_key = [&](int it) { return SW ? (it & 15) + 16 * (it >> 6) : it / CPR; };
+  auto item_ch = [&](int it) { return SW ? (it >> 4) & 3 : it % CPR; };
   auto gload = [&](int t0) {
 #pragma unroll
     for (int i = 0; i < NSI; ++i) {
       const int it = tid + 256 * i;
-      const int t = t0 + it / CPR, ch = (it % CPR) * 8;
+      const int t = t0 + item_key(it), ch = item_ch(it) * 8;
       const bool ok = it < KT * CPR && t < n;
       rk[i] = ok ? ldu4(Kp + (int64_t)t * D + ch) : make_uint4(0, 0, 0, 0);
       rv[i] = ok ? ldu4(Vp + (int64_t)t * D + ch) : make_uint4(0, 0, 0, 0);
@@ -88,11 +96,23 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
     for (int i = 0; i < NSI; ++i) {
       const int it = tid + 256 * i;
       if (it >= KT * CPR) break;
-      const int key = it / CPR, ch = (it % CPR) * 8;
-      stu4(&Ks[buf][key * KS + ch], rk[i]);
-      stu4(&Vs[buf][key * VS + ch], rv[i]);
+      const int key = item_key(it), ch = item_ch(it);
+      if constexpr (SW) {
+        stu4(&Ks[buf][key * 32 + row64_swz(key, 16 * ch) / 2], rk[i]);
+        stu4(&Vs[buf][key * 32 + row64_swz(key, 16 * ch) / 2], rv[i]);
+      } else {
+        stu4(&Ks[buf][key * KS + ch * 8], rk[i]);
+        stu4(&Vs[buf][key * VS + ch * 8], rv[i]);
+      }
     }
   };
+  // d = 32: the lane's byte offsets in the swizzled rows: its K fragment piece of row c, and
+  // its transposed-read addresses of V (dims db*16 + c)
+  const int roff = c * 64 + row64_swz(c, 16 * lg);
+  int voff[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+    voff[db] = (lane >> 2) * 64 + row64_swz(lane >> 2, 32 * db + 8 * (lane & 3));
 
   // K arrives pre-multiplied by log2(e)/sqrt(d), so S^T = K Q^T is in the exp2 domain.  The MFMA
   // accumulators start at -ref, a running reference of the exponent per query, so they return
@@ -126,7 +146,11 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
     }
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb) {
-      const typename HF<D>::frag kf = HF<D>::lds(&Ks[cur][(kb * 16 + c) * KS], lg);
+      typename HF<D>::frag kf;
+      if constexpr (SW)
+        kf = *reinterpret_cast<const typename HF<D>::frag*>(&Ks[cur][kb * 16 * 32 + roff / 2]);
+      else
+        kf = HF<D>::lds(&Ks[cur][(kb * 16 + c) * KS], lg);
 #pragma unroll
       for (int qb = 0; qb < 2; ++qb) sc[kb][qb] = HF<D>::mma(kf, qf[qb], init[qb]);
     }
@@ -176,7 +200,8 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
     for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
-        const bf16x8 vf = ld_tr8(&Vs[cur][ks * 32 * VS], VS, db * 16, lane);
+        const bf16x8 vf = SW ? tr8_row64(&Vs[cur][ks * 32 * 32], voff[db])
+                             : ld_tr8(&Vs[cur][ks * 32 * VS], VS, db * 16, lane);
 #pragma unroll
         for (int qb = 0; qb < 2; ++qb) oacc[db][qb] = mfma16(vf, pf[qb][ks], oacc[db][qb]);
       }

@@ -386,14 +386,6 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
   }
 }
 
-// The fused kernel's 64-byte LDS rows (the dS tile of 32 queries, the values at d = 32): the two
-// 16-byte halves of each 32-byte chunk and the two chunks are swapped by bits 1 and 2 of the
-// row, which makes both its 16-byte row accesses (16 rows, one column, per instruction) and its
-// transposed reads (8 rows of one 32-byte chunk per half-wave) free of bank conflicts.
-__device__ __forceinline__ int row64_swz(int r, int byte) {
-  return byte ^ (((r >> 1) & 1) << 4) ^ (((r >> 2) & 1) << 5);
-}
-
 // The dS tile holds, in row `key`, the 32 queries of a chunk in the lane order of the score
 // blocks: byte 16 g + 8 qb holds queries qb*16 + 4g .. + 3, so the 8 values of one lane (its
 // two 16-query blocks) are one 16-byte write.  Transposed read (ds_read_b64_tr_b16) of key
@@ -405,9 +397,7 @@ __device__ __forceinline__ int ds_tile_off(int lane, int qb) {
   return r * 64 + row64_swz(r, 16 * (lane & 3) + 8 * qb);
 }
 __device__ __forceinline__ bf16x8 ds_tile_tr(const bf16* T, int kr0, int off) {
-  const bf16* p = T + (kr0 * 64 + off) / 2;
-  const bf16x4 lo = lds_read_tr16(p), hi = lds_read_tr16(p + 16 * 32);
-  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return tr8_row64(T + kr0 * 32, off);
 }
 
 // =============================================================================== fused
