@@ -706,6 +706,198 @@ __global__ __launch_bounds__(256, (gemm_half_tile<EPI, BN>() ? 3 : 2)) void k_ge
   }
 }
 
+
+// ============================================================== weight-resident persistent GEMM
+// For the bias-only products whose contraction is the embedding width (K = E = BN): the
+// workgroup's weight column tile (BN x K, at most 72 KB) lives in registers for the whole
+// launch, split over 8 waves (2 row groups x 4 column groups), and the workgroup walks a
+// sequence of 128-row tiles, streaming only A through an LDS ring of 8 KB stages that runs
+// across tile boundaries: the next tile's rows are in flight during this tile's epilogue, and
+// no LDS traffic is spent on B.  One workgroup per CU.  With several column tiles (N = 3E) the
+// workgroups of one row-tile sequence are placed on one XCD, so that A comes from HBM once and
+// then from that XCD's L2.  Epilogues: bias (EPI_BIAS) and head-major item Q|K|V
+// (EPI_ITEM_QKV).  The products and the epilogue arithmetic are those of k_gemm (same MFMA
+// order), so both kernels give identical results.  (The GELU epilogues stay on k_gemm: their
+// VALU work needs the overlap of several workgroups per CU.)
+template <int BN>
+struct WrShape {
+  static constexpr int WN = 4;                  // column waves
+  static constexpr int WM = 2;                  // row waves
+  static constexpr int BM = 128;
+  static constexpr int MI = BM / WM / 16;       // 16-row blocks per wave
+  static constexpr int NB = BN / WN / 16;       // 16-column blocks per wave
+  static constexpr int KT = BN / BK;            // k steps (K = BN)
+  static constexpr int NS = 8;                  // A stages in the ring (8 KB each)
+  static constexpr int TS = BN + 8;             // epilogue tile row stride (elements)
+  static constexpr int CPRW = BN / 8;           // 16-byte chunks per tile row
+  static constexpr int NCH = BM * CPRW / 512;   // chunks of one tile per thread
+};
+
+template <int BN, int EPI>
+__global__ __launch_bounds__(512, 1) void k_gemm_wr(GemmArgs a) {
+  typedef WrShape<BN> Sh;
+  constexpr int WN = Sh::WN, WM = Sh::WM, BM = Sh::BM, MI = Sh::MI, NB = Sh::NB, KT = Sh::KT;
+  constexpr int NS = Sh::NS, TS = Sh::TS, CPRW = Sh::CPRW, NCH = Sh::NCH;
+  constexpr int STAGE = BM * BK;
+  __shared__ __attribute__((aligned(16))) bf16 ring[NS * STAGE];
+  __shared__ __attribute__((aligned(16))) bf16 tile[BM * TS];
+  __shared__ __attribute__((aligned(16))) float cb[BN];
+  __shared__ int64_t rbase[BM];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int lr = lane & 15, lg = lane >> 4;
+  const Geo& g = a.g;
+  // workgroup -> (column tile, row-tile sequence); the NY column tiles of a sequence share an XCD
+  const int NY = a.N / BN;
+  const int xcd = (int)(blockIdx.x & 7), li = (int)(blockIdx.x >> 3);
+  const int gpx = (int)(gridDim.x >> 3) / NY;  // sequences per XCD
+  if (li >= gpx * NY) return;
+  const int by = li % NY;
+  const int64_t grp = (int64_t)xcd * gpx + li / NY, NG = 8 * (int64_t)gpx;
+  const int n0 = by * BN;
+  const int64_t MT = (a.M + BM - 1) / BM;
+  const int64_t ntile = grp < MT ? (MT - 1 - grp) / NG + 1 : 0;
+  if (ntile == 0) return;
+  const int64_t nst = ntile * KT;
+  const int part = EPI == EPI_ITEM_QKV ? n0 / g.E : 0;
+  const int pc0 = n0 - part * g.E;
+
+  // this wave's weight slice: output columns n0 + wn * BN / WN + j * 16 + lr, k 8 lg (+ 32 ks)
+  bf16x8 bfr[KT][NB];
+#pragma unroll
+  for (int ks = 0; ks < KT; ++ks)
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+      bfr[ks][j] = ld8(a.Bt + (int64_t)(n0 + wn * (BN / WN) + j * 16 + lr) * a.K + ks * BK + 8 * lg);
+  if (tid < BN) cb[tid] = a.bias ? a.bias[n0 + tid] : 0.f;
+
+  // A streaming: every thread moves one 16-byte piece per stage: row tid / 4 of the tile, k
+  // chunk kslot(row, tid % 4) (the layout k_gemm reads); a stage is one load of each thread,
+  // so that its completion can be awaited by count
+  const bf16* zero = reinterpret_cast<const bf16*>(&kZeroChunk);
+  const int ar = tid >> 2;
+  const int akc = kslot(ar, tid & 3);
+  int64_t iss_tile = -1;
+  const bf16* iss_row = zero;
+  auto issue = [&](int64_t st) {
+    const int64_t j = st / KT;
+    const int kt = (int)(st - j * KT);
+    if (j != iss_tile) {
+      iss_tile = j;
+      const int64_t am = (grp + j * NG) * BM + ar;
+      iss_row = am < a.M ? a.A + row_addr(g, a.amode, am, a.lda) + akc * 8 : nullptr;
+    }
+    lds_dma16(iss_row ? iss_row + kt * BK : zero, ring + (st % NS) * STAGE + wave * 512);
+  };
+  // NS - 1 stages ahead; past the last stage, loads of zeros into the free slots keep the
+  // count of younger loads that the waits below rely on
+#pragma unroll
+  for (int st = 0; st < NS - 1; ++st) {
+    if (st < nst) issue(st);
+    else lds_dma16(zero, ring + st * STAGE + wave * 512);
+  }
+
+  auto rloc = [&](int i) { return wm * (BM / WM) + i * 16 + lr; };
+  const int cb0 = wn * (BN / WN) + lg * 4;
+  // item K is stored pre-multiplied by log2(e)/sqrt(d), as k_gemm does
+  const float ksc =
+      EPI == EPI_ITEM_QKV && part == 1 ? 1.4426950408889634f / sqrtf((float)g.d) : 1.0f;
+
+  for (int64_t j = 0; j < ntile; ++j) {
+    const int64_t m0 = (grp + j * NG) * BM;
+    f32x4 acc[MI][NB];
+#pragma unroll
+    for (int i = 0; i < MI; ++i)
+#pragma unroll
+      for (int jj = 0; jj < NB; ++jj) acc[i][jj] = zero4();
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+      const int64_t st = j * KT + kt;
+      // stage st has landed once at most the NS - 2 stage loads issued after it are
+      // outstanding (loads complete in order; stores issued since only add younger ops)
+      asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(NS - 2) : "memory");
+      if (st + NS - 1 < nst) issue(st + NS - 1);
+      else  // a load into the free slot keeps the count of younger loads
+        lds_dma16(zero, ring + ((st + NS - 1) % NS) * STAGE + wave * 512);
+      const bf16* sa = ring + (st % NS) * STAGE;
+      bf16x8 af[MI];
+#pragma unroll
+      for (int i = 0; i < MI; ++i) {
+        const int r = rloc(i);
+        af[i] = ld8(&sa[r * BK + kslot(r, lg) * 8]);
+      }
+#pragma unroll
+      for (int i = 0; i < MI; ++i)
+#pragma unroll
+        for (int jj = 0; jj < NB; ++jj) acc[i][jj] = mfma16(bfr[kt][jj], af[i], acc[i][jj]);
+    }
+
+    // ---- epilogue: per-row destinations, then the tile through LDS in 16-byte row chunks
+    if (tid < BM) {
+      const int64_t m = m0 + tid;
+      int64_t off = -1;
+      if (m < a.M) {
+        if (EPI == EPI_ITEM_QKV) {
+          const int64_t col = m / g.R;
+          const int r = (int)(m - col * g.R);
+          if (part == 0 || r < g.col_ntr[col]) off = (col * g.heads * g.R + r) * (int64_t)g.d;
+        } else {
+          off = m * a.ldo + n0;
+        }
+      }
+      rbase[tid] = off;
+    }
+#pragma unroll
+    for (int jj = 0; jj < NB; ++jj) {
+      const float4 bb = *reinterpret_cast<const float4*>(&cb[cb0 + jj * 16]);
+      f32x4 b4;
+      b4[0] = bb.x; b4[1] = bb.y; b4[2] = bb.z; b4[3] = bb.w;
+#pragma unroll
+      for (int i = 0; i < MI; ++i) {
+        const f32x4 v = (acc[i][jj] + b4) * ksc;
+        *reinterpret_cast<uint2*>(&tile[rloc(i) * TS + cb0 + jj * 16]) =
+            make_uint2(pack2(v[0], v[1]), pack2(v[2], v[3]));
+      }
+    }
+    lds_barrier();
+    bf16* dst = EPI == EPI_ITEM_QKV ? (part == 0 ? a.out : (part == 1 ? a.out2 : a.out3)) : a.out;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int ch = tid + 512 * c;
+      const int row = ch / CPRW, cc = (ch % CPRW) * 8;
+      const int64_t off = rbase[row];
+      if (off < 0) continue;
+      int64_t o = off + cc;
+      if (EPI == EPI_ITEM_QKV) {
+        const int head = (pc0 + cc) / g.d, jd = pc0 + cc - head * g.d;
+        o = off + (int64_t)head * g.R * g.d + jd;
+      }
+      stu4(dst + o, ldu4(&tile[row * TS + cc]));
+    }
+  }
+}
+
+// The weight-resident kernel applies to K = E = BN <= 192 products with the bias or item
+// Q|K|V epilogue, A rows compact or native (at BN = 256 the weight slice leaves too few
+// registers); grid: one workgroup per CU.
+static bool gemm_wr_ok(const GemmArgs& a) {
+  const bool epi = a.epi == EPI_BIAS || a.epi == EPI_ITEM_QKV;
+  const bool mode = a.amode == ROWS_COMPACT || a.amode == ROWS_NATIVE;
+  return epi && mode && a.K == a.BN && a.N % a.BN == 0 && a.N / a.BN <= 32 &&
+         (a.BN == 64 || a.BN == 128 || a.BN == 192);
+}
+
+template <int BN>
+static hipError_t gemm_wr_dispatch(const GemmArgs& a, hipStream_t s) {
+  const unsigned grid = 256;
+  if (a.epi == EPI_BIAS)
+    k_gemm_wr<BN, EPI_BIAS><<<grid, 512, 0, s>>>(a);
+  else
+    k_gemm_wr<BN, EPI_ITEM_QKV><<<grid, 512, 0, s>>>(a);
+  return hipGetLastError();
+}
+
 template <int BN>
 static hipError_t gemm_dispatch(const GemmArgs& a, hipStream_t s) {
   // 128-row tiles (each weight tile staged through LDS serves twice the rows), except for the
@@ -760,6 +952,13 @@ int64_t gemm_tiles(int epi, int BN, int64_t M) {
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0) return hipSuccess;
   if (a.K % BK || a.N % a.BN) return hipErrorInvalidValue;
+  if (gemm_wr_ok(a)) {
+    switch (a.BN) {
+      case 64: return gemm_wr_dispatch<64>(a, s);
+      case 128: return gemm_wr_dispatch<128>(a, s);
+      default: return gemm_wr_dispatch<192>(a, s);
+    }
+  }
   switch (a.BN) {
     case 64: return gemm_dispatch<64>(a, s);
     case 128: return gemm_dispatch<128>(a, s);
