@@ -62,7 +62,7 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
   const bf16* Kp = k + prob * kR * D;  // keys and values: kR rows per problem
   const bf16* Vp = v + prob * kR * D;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
   const int c = lane & 15, lg = lane >> 4;
   const int qw0 = qt * QWG + wave * QWV;
 

@@ -97,7 +97,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dkdv(Geo g, const bf16* __res
   const rsrc_t rL = make_rsrc(lse + prob * R, (uint32_t)R * 4);
   const rsrc_t rD = make_rsrc(Dbuf + prob * R, (uint32_t)R * 4);
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int c = lane & 15, lg = lane >> 4;
   const float tau = 1.0f / sqrtf((float)D);
 
@@ -270,7 +270,7 @@ __global__ __launch_bounds__(256) void k_item_attn_dq(Geo g, const bf16* __restr
   const rsrc_t rdO = make_rsrc(dout + col * R * (int64_t)E + head * D, obytes);
   const rsrc_t rL = make_rsrc(lse + prob * R, (uint32_t)R * 4);
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int c = lane & 15, lg = lane >> 4;
   const int qw0 = qt * 128 + w * 32;
   // per query block: Q^T and dO^T fragments (B operands), D = rowsum(dO o O), -lse log2(e);
@@ -466,7 +466,7 @@ __global__ __launch_bounds__(512) void k_item_attn_bwd_fused(Geo g, const bf16* 
   const rsrc_t rdO = make_rsrc(dout + col * R * (int64_t)E + head * D, obytes);
   const rsrc_t rL = make_rsrc(lse + prob * R, (uint32_t)R * 4);
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int c = lane & 15, lg = lane >> 4;
   const float tau = 1.0f / sqrtf((float)D);
   const bool active = w < nact;

@@ -71,7 +71,7 @@ hipError_t launch_reduce_strided(int Z, int64_t count, int64_t stride, const flo
 // 16-byte pieces with consecutive lanes on consecutive pieces, zero where the piece's cell is
 // inactive.  Rows of datasets with every cell active leave at once.
 __global__ void k_zero_inactive(Geo g, bf16* __restrict__ x) {
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int64_t row = (int64_t)blockIdx.x * 4 + wave_id();
   if (row >= (int64_t)g.B * g.R) return;
   const int b = (int)(row / g.R);
   if (g.ds[b].S == g.S) return;

@@ -121,7 +121,7 @@ __global__ __launch_bounds__(256, (gemm_half_tile<EPI, BN>() ? 3 : 2)) void k_ge
   __shared__ int64_t rbase[BM];  // epilogue: per-row element offset for the current mode
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63, wave = wave_id();
   const int wm = wave >> 1, wn = wave & 1;
   const int lr = lane & 15, lg = lane >> 4;
   // Workgroup -> (row tile bx, column tile by).  The hardware deals consecutive workgroups
@@ -744,7 +744,7 @@ __global__ __launch_bounds__(512, 1) void k_gemm_wr(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) float cb[BN];
   __shared__ int64_t rbase[BM];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
   const int wm = wave / WN, wn = wave % WN;
   const int lr = lane & 15, lg = lane >> 4;
   const Geo& g = a.g;

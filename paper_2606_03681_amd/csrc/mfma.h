@@ -60,6 +60,12 @@ __device__ __forceinline__ bf16x8 ld_tr8(const bf16* T, int ls, int c0, int lane
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
+// Index of the calling wave in its workgroup, as a wave-uniform (scalar) value: values derived
+// from it (a wave's row, problem, key range) then stay in SGPRs and branches on them are scalar.
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+}
+
 // Round-to-nearest-even pack of two floats into two bf16 (low half = a): v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
   f32x2 v = {a, b};

@@ -118,7 +118,7 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 As[2][MS * LSA];
   __shared__ __attribute__((aligned(16))) bf16 Bs[2][MS * LSB];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int lg = lane >> 4, c = lane & 15;
   const int wn = w >> 2, wk = w & 3;
   // Workgroup -> (cell chunk z, n-tile, k-tile).  The hardware deals consecutive workgroups
