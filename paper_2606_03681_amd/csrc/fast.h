@@ -65,6 +65,9 @@ struct GemmArgs {
   const bf16* aux;
   float* part;  // EPI_LN_BWD: [row tiles][2][BN] partial sums (dgamma, dbeta);
                 //   EPI_RMS_BWD: [row tiles][BN] (dgamma)
+  const float* rgamma;  // EPI_LN: resid read as rgamma * resid + rbeta per column (null: as is)
+  const float* rbeta;
+  int xhat_out;  // EPI_LN: out receives x-hat (the normalised rows) instead of gamma x-hat + beta
   float rscale;  // EPI_RMS: factor on resid
   float oscale;  // EPI_RMS_BWD: factor on the output
   float eps;     // EPI_RMS, EPI_RMS_BWD: RMSNorm epsilon
@@ -83,13 +86,29 @@ int64_t gemm_tiles(int epi, int BN, int64_t M);
 // bf16 copies of the six weight matrices of one layer, as stored ([out][in]) and transposed.
 // Offsets (elements) inside w / wt follow the packed parameter order of the weights:
 // Wqkv_f, Wo_f, Wqkv_i, Wo_i, W1, W2.
+// bf16 weight copies (element offsets); fb: float32 folded biases (3E item Q|K|V, then H MLP
+// up), at element fb of the bf16 buffer
 struct WOff {
-  int64_t qkv_f, o_f, qkv_i, o_i, w1, w2, total;
+  int64_t qkv_f, o_f, qkv_i, o_i, w1, w2, fb, total;
 };
 WOff weight_offsets(int E, int H);
+// LayerNorm affines folded into the products that consume the normalised rows: the item Q|K|V
+// projection reads x-hat1 with weights Wqkv_i diag(g1) and bias bqkv_i + Wqkv_i be1, the MLP
+// up-projection x-hat2 with W1 diag(g2) and b1 + W1 be2 (null: no folding)
+struct WFold {
+  const float *g1, *be1, *bqkv_i, *g2, *be2, *b1;
+};
+// w: the six matrices in packed order (the fold applied to Wqkv_i and W1 when given, and the
+// folded biases written at fb); wt: each matrix transposed, never folded
 hipError_t launch_weight_prep(const float* params, int E, int H, bf16* w, bf16* wt,
-                              hipStream_t s);
+                              const WFold* fold, hipStream_t s);
 
+// Weight gradient of a product whose input was the folded x-hat (see WFold): with
+// h = gamma o x-hat + beta, dW[n][k] = (sum_z wpart)[n][k] gamma[k] + (sum_z bpart)[n] beta[k];
+// grad (N x K) = (accumulate ? grad : 0) + that, z ascending
+hipError_t launch_reduce_wfold(int Z, int N, int K, const float* wpart, const float* bpart,
+                               const float* gamma, const float* beta, float* grad,
+                               int accumulate, hipStream_t s);
 // grad[i] = (accumulate ? grad[i] : 0) + sum_z part[z * stride + i], z ascending
 hipError_t launch_reduce_strided(int Z, int64_t count, int64_t stride, const float* part,
                                  float* grad, int accumulate, hipStream_t s);

@@ -13,6 +13,7 @@ WOff weight_offsets(int E, int H) {
   o.o_i = x; x += (int64_t)E * E;
   o.w1 = x; x += (int64_t)H * E;
   o.w2 = x; x += (int64_t)E * H;
+  o.fb = (x + 7) / 8 * 8; x = o.fb + 2 * (3LL * E + H);
   o.total = x;
   return o;
 }
@@ -20,7 +21,8 @@ WOff weight_offsets(int E, int H) {
 // One thread per weight element: src (fp32, packed parameter order) -> w (same layout, bf16)
 // and wt (each matrix transposed, bf16).
 __global__ void k_weight_prep(const float* __restrict__ p, int E, int H, WOff wo,
-                              bf16* __restrict__ w, bf16* __restrict__ wt) {
+                              bf16* __restrict__ w, bf16* __restrict__ wt, WFold fold,
+                              int folded) {
   // packed parameter offsets of the six matrices
   const int64_t E2 = (int64_t)E * E;
   const int64_t src[6] = {0, 3 * E2 + 3 * E, 4 * E2 + 4 * E, 7 * E2 + 7 * E, 8 * E2 + 8 * E,
@@ -33,8 +35,10 @@ __global__ void k_weight_prep(const float* __restrict__ p, int E, int H, WOff wo
     int64_t n = (int64_t)rows[k] * cols[k];
     if (t < n) {
       int r = (int)(t / cols[k]), c = (int)(t % cols[k]);
-      uint16_t v = f2bf(p[src[k] + t]);
-      w[dst[k] + t] = v;
+      const float x = p[src[k] + t];
+      const uint16_t v = f2bf(x);
+      // the fold scales input column c of Wqkv_i by g1[c] and of W1 by g2[c]
+      w[dst[k] + t] = folded && (k == 2 || k == 4) ? f2bf(x * (k == 2 ? fold.g1 : fold.g2)[c]) : v;
       wt[dst[k] + (int64_t)c * rows[k] + r] = v;
       return;
     }
@@ -42,11 +46,57 @@ __global__ void k_weight_prep(const float* __restrict__ p, int E, int H, WOff wo
   }
 }
 
+// Folded biases, one thread per output: bqkv_i[n] + sum_k Wqkv_i[n][k] be1[k] for n < 3E, then
+// b1[m] + sum_k W1[m][k] be2[k]; float32, k ascending.
+__global__ void k_fold_bias(const float* __restrict__ p, int E, int H, WFold fold,
+                            float* __restrict__ fb) {
+  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= 3 * E + H) return;
+  const int64_t E2 = (int64_t)E * E;
+  const bool q = n < 3 * E;
+  const int m = q ? n : n - 3 * E;
+  const float* row = p + (q ? 4 * E2 + 4 * E : 8 * E2 + 8 * E) + (int64_t)m * E;
+  const float* be = q ? fold.be1 : fold.be2;
+  float acc = (q ? fold.bqkv_i : fold.b1)[m];
+  for (int k = 0; k < E; ++k) acc = fmaf(row[k], be[k], acc);
+  fb[n] = acc;
+}
+
 hipError_t launch_weight_prep(const float* params, int E, int H, bf16* w, bf16* wt,
-                              hipStream_t s) {
+                              const WFold* fold, hipStream_t s) {
   WOff wo = weight_offsets(E, H);
-  unsigned grid = (unsigned)((wo.total + 255) / 256);
-  k_weight_prep<<<grid, 256, 0, s>>>(params, E, H, wo, w, wt);
+  unsigned grid = (unsigned)((wo.fb + 255) / 256);
+  k_weight_prep<<<grid, 256, 0, s>>>(params, E, H, wo, w, wt, fold ? *fold : WFold{}, fold != nullptr);
+  if (fold) {
+    const int n = 3 * E + H;
+    k_fold_bias<<<(n + 255) / 256, 256, 0, s>>>(params, E, H, *fold,
+                                                reinterpret_cast<float*>(w + wo.fb));
+  }
+  return hipGetLastError();
+}
+
+__global__ void k_reduce_wfold(int Z, int N, int K, const float* __restrict__ wpart,
+                               const float* __restrict__ bpart, const float* __restrict__ gamma,
+                               const float* __restrict__ beta, float* __restrict__ grad,
+                               int accumulate) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t NK = (int64_t)N * K;
+  if (i >= NK) return;
+  const int n = (int)(i / K), k = (int)(i - (int64_t)n * K);
+  float sw = 0.f, sb = 0.f;
+  for (int z = 0; z < Z; ++z) {
+    sw += wpart[(int64_t)z * NK + i];
+    sb += bpart[(int64_t)z * N + n];
+  }
+  grad[i] = (accumulate ? grad[i] : 0.f) + fmaf(sw, gamma[k], sb * beta[k]);
+}
+
+hipError_t launch_reduce_wfold(int Z, int N, int K, const float* wpart, const float* bpart,
+                               const float* gamma, const float* beta, float* grad,
+                               int accumulate, hipStream_t s) {
+  const int64_t NK = (int64_t)N * K;
+  k_reduce_wfold<<<(unsigned)((NK + 255) / 256), 256, 0, s>>>(Z, N, K, wpart, bpart, gamma, beta,
+                                                              grad, accumulate);
   return hipGetLastError();
 }
 

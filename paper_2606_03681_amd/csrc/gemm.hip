@@ -117,7 +117,8 @@ __global__ __launch_bounds__(256, (gemm_half_tile<EPI, BN>() ? 3 : 2)) void k_ge
   float (*red)[BM] = reinterpret_cast<float (*)[BM]>(smem + TILE_BYTES);          // [2][BM]
   float (*cred)[2][BN] =
       reinterpret_cast<float (*)[2][BN]>(smem + TILE_BYTES + RED_BYTES);        // [2][2][BN]
-  __shared__ __attribute__((aligned(16))) float cpar[3][BN];  // bias, gamma, beta of the tile
+  // bias, gamma, beta of the tile; residual affine (EPI_LN)
+  __shared__ __attribute__((aligned(16))) float cpar[5][BN];
   __shared__ int64_t rbase[BM];  // epilogue: per-row element offset for the current mode
 
   const int tid = threadIdx.x;
@@ -221,6 +222,10 @@ __global__ __launch_bounds__(256, (gemm_half_tile<EPI, BN>() ? 3 : 2)) void k_ge
     if (EPI == EPI_LN || EPI == EPI_LN_BWD || EPI == EPI_RMS || EPI == EPI_RMS_BWD)
       cpar[1][tid] = a.gamma[tid];
     if (EPI == EPI_LN) cpar[2][tid] = a.beta[tid];
+    if (EPI == EPI_LN && a.rgamma) {
+      cpar[3][tid] = a.rgamma[tid];
+      cpar[4][tid] = a.rbeta[tid];
+    }
   }
 
   // ---- epilogue inputs (residual, x-hat, pre-activation) do not depend on the product: their
@@ -530,11 +535,20 @@ __global__ __launch_bounds__(256, (gemm_half_tile<EPI, BN>() ? 3 : 2)) void k_ge
   if (EPI == EPI_LN) {
     fill_tile(pin0);
     lds_barrier();
+    if (a.rgamma) {  // the residual arrives as x-hat of the previous norm: rgamma x-hat + rbeta
 #pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      const f32x4 b = par4(0, j);
+      for (int j = 0; j < NB; ++j) {
+        const f32x4 b = par4(0, j), rg = par4(3, j), rb = par4(4, j);
 #pragma unroll
-      for (int i = 0; i < MI; ++i) val[i][j] = acc[i][j] + b + tile4(i, j);
+        for (int i = 0; i < MI; ++i) val[i][j] = acc[i][j] + b + (rg * tile4(i, j) + rb);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const f32x4 b = par4(0, j);
+#pragma unroll
+        for (int i = 0; i < MI; ++i) val[i][j] = acc[i][j] + b + tile4(i, j);
+      }
     }
     float mean[MI], var[MI];
     row_sum([&](int i, int j) { return val[i][j]; }, mean);
@@ -550,12 +564,20 @@ __global__ __launch_bounds__(256, (gemm_half_tile<EPI, BN>() ? 3 : 2)) void k_ge
       for (int j = 0; j < NB; ++j) val[i][j] = (val[i][j] - mean[i]) * rs;
       if (a.rstd && wn == 0 && lg == 0 && m0 + rloc(i) < a.M) a.rstd[m0 + rloc(i)] = rs;
     }
-    // h = gamma * x-hat + beta -> out (omode); x-hat -> xhat (compact) unless xhat is null
+    // h = gamma * x-hat + beta -> out (omode), or x-hat itself when xhat_out; x-hat -> xhat
+    // (compact) unless xhat is null
+    if (a.xhat_out) {
 #pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      const f32x4 gm = par4(1, j), bt = par4(2, j);
+      for (int i = 0; i < MI; ++i)
 #pragma unroll
-      for (int i = 0; i < MI; ++i) put4(i, j, gm * val[i][j] + bt);
+        for (int j = 0; j < NB; ++j) put4(i, j, val[i][j]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        const f32x4 gm = par4(1, j), bt = par4(2, j);
+#pragma unroll
+        for (int i = 0; i < MI; ++i) put4(i, j, gm * val[i][j] + bt);
+      }
     }
     set_rows(a.omode, BN, -1);
     lds_barrier();

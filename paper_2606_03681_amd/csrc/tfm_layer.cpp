@@ -159,8 +159,11 @@ SavedLayout saved_layout(const Dims& d) {
   L.qkvf = a.take(N * 3 * E * t);
   L.of = a.take(N * E * t);
   L.lsef = a.take(N * d.heads * 4);
+  // the float32 path keeps H and x-hat of LN1 and LN2; the MFMA path keeps x-hat only, in the
+  // H slots (its LN1 / LN2 affines are folded into the consumers)
+  const size_t xhn = d.dtype == TFM_F32 ? N * E * t : 0;
   L.h1 = a.take(N * E * t);
-  L.xh1 = a.take(N * E * t);
+  L.xh1 = a.take(xhn);
   L.rs1 = a.take(N * 4);
   L.qi = a.take(N * E * t);
   L.ki = a.take(N * E * t);
@@ -168,7 +171,7 @@ SavedLayout saved_layout(const Dims& d) {
   L.oi = a.take(N * E * t);
   L.lsei = a.take(N * d.heads * 4);
   L.h2 = a.take(N * E * t);
-  L.xh2 = a.take(N * E * t);
+  L.xh2 = a.take(xhn);
   L.rs2 = a.take(N * 4);
   L.g = a.take(N * d.H * t);
   L.u = a.take(N * d.H * t);
@@ -590,11 +593,13 @@ tfm::GemmArgs gemm_base(const tfm::Geo& g, int64_t M, int N, int K, int epi) {
 
 // Buffers of one forward pass on the MFMA path.  The training forward points them into the
 // saved state; the forward-only calls point them into the workspace (reused where lifetimes
-// allow; the optional ones null) and into the caller's key/value cache.
+// allow; the optional ones null) and into the caller's key/value cache.  h1, h2: in the
+// post-norm block the x-hat of LN1 and LN2 (their affines are folded into the consumers); in
+// the pre-norm block the residual stream.
 struct FwdBufs {
   tfm::bf16 *qkvf = nullptr, *of = nullptr, *h1 = nullptr, *qi = nullptr, *ki = nullptr,
             *vi = nullptr, *oi = nullptr, *h2 = nullptr, *u = nullptr;
-  tfm::bf16 *xh1 = nullptr, *xh2 = nullptr, *xh3 = nullptr, *g = nullptr;  // optional
+  tfm::bf16 *xh3 = nullptr, *g = nullptr;  // optional
   tfm::bf16 *xs = nullptr, *r1 = nullptr, *r2 = nullptr, *r3 = nullptr;    // pre-norm block
   float *lsef = nullptr, *lsei = nullptr, *rs1 = nullptr, *rs2 = nullptr, *rs3 = nullptr;
   bool query = false;  // ki / vi hold the keys and values of a context call: project Q only
@@ -605,10 +610,10 @@ FwdBufs bufs_from_saved(char* sv, const SavedLayout& S) {
   typedef tfm::bf16 T;
   FwdBufs b;
   b.qkvf = (T*)(sv + S.qkvf); b.of = (T*)(sv + S.of); b.lsef = (float*)(sv + S.lsef);
-  b.h1 = (T*)(sv + S.h1); b.xh1 = (T*)(sv + S.xh1); b.rs1 = (float*)(sv + S.rs1);
+  b.h1 = (T*)(sv + S.h1); b.rs1 = (float*)(sv + S.rs1);
   b.qi = (T*)(sv + S.qi); b.ki = (T*)(sv + S.ki); b.vi = (T*)(sv + S.vi);
   b.oi = (T*)(sv + S.oi); b.lsei = (float*)(sv + S.lsei);
-  b.h2 = (T*)(sv + S.h2); b.xh2 = (T*)(sv + S.xh2); b.rs2 = (float*)(sv + S.rs2);
+  b.h2 = (T*)(sv + S.h2); b.rs2 = (float*)(sv + S.rs2);
   b.g = (T*)(sv + S.g); b.u = (T*)(sv + S.u); b.xh3 = (T*)(sv + S.xh3);
   b.rs3 = (float*)(sv + S.rs3);
   return b;
@@ -635,37 +640,44 @@ int fwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   const POff o = param_offsets(d.E, d.H);
   const int E = d.E, H = d.H;
   const int64_t N = g.N;
-  STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, s));
+  // H1 and H2 are kept as their x-hat only: the affines of LN1 and LN2 are folded into the
+  // products that read them (weights and biases) and into the residual reads
+  const WFold fold{prm + o.g1, prm + o.be1, prm + o.bqkv_i, prm + o.g2, prm + o.be2, prm + o.b1};
+  STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, &fold, s));
+  const float* fb = reinterpret_cast<const float*>(f.w + f.wo.fb);
   // feature Q|K|V from the native cells, and the feature attention
   STEP_ERR(feat_fwd(g, X, ROWS_NATIVE, prm + o.bqkv_f, b, f, s));
-  // H1 = LN1(X + O_f Wo_f^T + bo_f)
+  // x-hat1 of H1 = LN1(X + O_f Wo_f^T + bo_f)
   GemmArgs a = gemm_base(g, N, E, E, EPI_LN);
   a.A = b.of; a.lda = E; a.Bt = f.w + f.wo.o_f; a.bias = prm + o.bo_f;
   a.resid = X; a.rmode = ROWS_NATIVE; a.gamma = prm + o.g1; a.beta = prm + o.be1;
-  a.out = b.h1; a.omode = ROWS_COMPACT; a.xhat = b.xh1; a.rstd = b.rs1;
+  a.out = b.h1; a.omode = ROWS_COMPACT; a.xhat_out = 1; a.rstd = b.rs1;
   STEP("feat_out_ln1/mfma", launch_gemm(a, s));
-  // item Q (all rows), K, V (train rows), head-major; Q only when K/V come from a context call
+  // item Q (all rows), K, V (train rows), head-major, from x-hat1 with the folded weights;
+  // Q only when K/V come from a context call
   a = gemm_base(g, N, b.query ? E : 3 * E, E, EPI_ITEM_QKV);
-  a.A = b.h1; a.lda = E; a.Bt = f.w + f.wo.qkv_i; a.bias = prm + o.bqkv_i;
+  a.A = b.h1; a.lda = E; a.Bt = f.w + f.wo.qkv_i; a.bias = fb;
   a.out = b.qi; a.out2 = b.ki; a.out3 = b.vi;
   STEP("item_qkv/mfma", launch_gemm(a, s));
   STEP("item_attn_fwd/mfma",
        launch_item_attn_fwd(g, b.qi, b.ki, b.vi, b.oi, b.lsei, s, b.kR));
-  // H2 = LN2(H1 + O_i Wo_i^T + bo_i)
+  // x-hat2 of H2 = LN2(H1 + O_i Wo_i^T + bo_i), H1 = g1 x-hat1 + be1
   a = gemm_base(g, N, E, E, EPI_LN);
   a.A = b.oi; a.lda = E; a.Bt = f.w + f.wo.o_i; a.bias = prm + o.bo_i;
-  a.resid = b.h1; a.rmode = ROWS_COMPACT; a.gamma = prm + o.g2; a.beta = prm + o.be2;
-  a.out = b.h2; a.omode = ROWS_COMPACT; a.xhat = b.xh2; a.rstd = b.rs2;
+  a.resid = b.h1; a.rmode = ROWS_COMPACT; a.rgamma = prm + o.g1; a.rbeta = prm + o.be1;
+  a.gamma = prm + o.g2; a.beta = prm + o.be2;
+  a.out = b.h2; a.omode = ROWS_COMPACT; a.xhat_out = 1; a.rstd = b.rs2;
   STEP("item_out_ln2/mfma", launch_gemm(a, s));
-  // G = H2 W1^T + b1, U = GELU(G)
+  // G = H2 W1^T + b1 (from x-hat2, folded), U = GELU(G)
   a = gemm_base(g, N, H, E, EPI_GELU_FWD);
-  a.A = b.h2; a.lda = E; a.Bt = f.w + f.wo.w1; a.bias = prm + o.b1;
+  a.A = b.h2; a.lda = E; a.Bt = f.w + f.wo.w1; a.bias = fb + 3 * E;
   a.out = b.g; a.out2 = b.u; a.ldo = H;
   STEP("mlp_up/mfma", launch_gemm(a, s));
   // Y = LN3(H2 + U W2^T + b2), written to the native layout
   a = gemm_base(g, N, E, H, EPI_LN);
   a.A = b.u; a.lda = H; a.Bt = f.w + f.wo.w2; a.bias = prm + o.b2;
-  a.resid = b.h2; a.rmode = ROWS_COMPACT; a.gamma = prm + o.g3; a.beta = prm + o.be3;
+  a.resid = b.h2; a.rmode = ROWS_COMPACT; a.rgamma = prm + o.g2; a.rbeta = prm + o.be2;
+  a.gamma = prm + o.g3; a.beta = prm + o.be3;
   a.out = Y; a.omode = ROWS_NATIVE; a.xhat = b.xh3; a.rstd = b.rs3;
   STEP("mlp_down_ln3/mfma", launch_gemm(a, s));
   STEP("zero_inactive/hbm", launch_zero_inactive(g, Y, s));
@@ -680,17 +692,23 @@ struct FastGrads {
   int accumulate;
   hipStream_t s;
   // ymode: layout of dY (compact, native; head-major item gradients when dY2 is given)
+  // xg, xb: X is the x-hat of a norm with affine (xg, xb): the weight gradient is formed for
+  // h = xg o X + xb (launch_reduce_wfold)
   int run(const tfm::bf16* dY, int N, const tfm::bf16* X, int K, int xmode, size_t offW,
           size_t offb, const tfm::bf16* dY2 = nullptr, const tfm::bf16* dY3 = nullptr,
-          int ymode = tfm::ROWS_COMPACT) {
+          int ymode = tfm::ROWS_COMPACT, const float* xg = nullptr, const float* xb = nullptr) {
     tfm::WgradArgs a{};
     a.M = g.N; a.N = N; a.K = K; a.dY = dY; a.ldy = N; a.X = X; a.ldx = K; a.xmode = xmode;
     a.dY2 = dY2; a.dY3 = dY3; a.ymode = dY2 ? tfm::ROWS_ITEM_HM : ymode;
     a.part = f.wpart; a.bpart = f.bpart; a.g = g;
     const int Z = tfm::wgrad_chunks(g.N);
     STEP("wgrad/mfma", tfm::launch_wgrad_mfma(a, s));
-    STEP("reduce/hbm", tfm::launch_reduce_z(Z, (int64_t)N * K, (int64_t)N * K, f.wpart,
-                                            grads + offW, accumulate, s));
+    if (xg)
+      STEP("reduce/hbm", tfm::launch_reduce_wfold(Z, N, K, f.wpart, f.bpart, xg, xb,
+                                                  grads + offW, accumulate, s));
+    else
+      STEP("reduce/hbm", tfm::launch_reduce_z(Z, (int64_t)N * K, (int64_t)N * K, f.wpart,
+                                              grads + offW, accumulate, s));
     STEP("reduce/hbm", tfm::launch_reduce_z(Z, N, N, f.bpart, grads + offb, accumulate, s));
     return TFM_OK;
   }
@@ -708,14 +726,14 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const Plan& P, const tfm::bf16* X
   const int64_t N = g.N;
   const int tiles = (int)tfm::gemm_tiles(tfm::EPI_LN_BWD, E, N);
   FastGrads G{f, g, grads, accumulate, s};
-  STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, s));
+  STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, nullptr, s));
   T* dz3 = (T*)(ws + W.tb);
   T* dz2 = (T*)(ws + W.te);
   T* dz1 = (T*)(ws + W.tf);
   T* dgb = (T*)(ws + W.th1);
   T* dqkv = (T*)(ws + W.tqkv);
-  const T* h1 = (const T*)(sv + S.h1);
-  const T* h2 = (const T*)(sv + S.h2);
+  const T* xh1 = (const T*)(sv + S.h1);  // the forward keeps x-hat1 and x-hat2 only
+  const T* xh2 = (const T*)(sv + S.h2);
   // LN3 (from the native dY), with its gamma/beta column sums
   int nb = 0;
   STEP("ln3_bwd/hbm", launch_ln_out_bwd(g, dY, (const T*)(sv + S.xh3), (const float*)(sv + S.rs3),
@@ -728,10 +746,11 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const Plan& P, const tfm::bf16* X
   a.aux = (const T*)(sv + S.g);
   STEP("mlp_down_dx/mfma", launch_gemm(a, s));
   CHK(G.run(dz3, E, (const T*)(sv + S.u), H, ROWS_COMPACT, o.W2, o.b2));
-  CHK(G.run(dgb, H, h2, E, ROWS_COMPACT, o.W1, o.b1));
+  CHK(G.run(dgb, H, xh2, E, ROWS_COMPACT, o.W1, o.b1, nullptr, nullptr, ROWS_COMPACT,
+            prm + o.g2, prm + o.be2));
   // dZ2 = LN2'(dZ3 + dG W1)
   a = gemm_base(g, N, E, H, EPI_LN_BWD);
-  a.A = dgb; a.lda = H; a.Bt = f.wt + f.wo.w1; a.resid = dz3; a.aux = (const T*)(sv + S.xh2);
+  a.A = dgb; a.lda = H; a.Bt = f.wt + f.wo.w1; a.resid = dz3; a.aux = xh2;
   a.rstd_in = (const float*)(sv + S.rs2); a.gamma = prm + o.g2; a.out = dz2; a.part = f.lnpart;
   STEP("mlp_up_dx_ln2/mfma", launch_gemm(a, s));
   STEP("reduce/hbm", launch_reduce_z(tiles, 2 * E, 2 * E, f.lnpart, grads + o.g2, accumulate, s));
@@ -751,12 +770,13 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const Plan& P, const tfm::bf16* X
   const float* lsei = (const float*)(sv + S.lsei);
   float* Dq = (float*)(ws + W.D);
   CHK(item_attn_bwd(d, g, P, ws, W.meta, qi, ki, vi, oi, doi, lsei, Dq, dq, dk, dv, s));
-  CHK(G.run(dq, 3 * E, h1, E, ROWS_COMPACT, o.Wqkv_i, o.bqkv_i, dk, dv));
+  CHK(G.run(dq, 3 * E, xh1, E, ROWS_COMPACT, o.Wqkv_i, o.bqkv_i, dk, dv, ROWS_COMPACT,
+            prm + o.g1, prm + o.be1));
   // dZ1 = LN1'(dZ2 + dQKV_i Wqkv_i), the gradients read head-major in place
   a = gemm_base(g, N, E, 3 * E, EPI_LN_BWD);
   a.A = dq; a.A2 = dk; a.A3 = dv; a.amode = ROWS_ITEM_HM; a.lda = 3 * E;
   a.Bt = f.wt + f.wo.qkv_i; a.resid = dz2;
-  a.aux = (const T*)(sv + S.xh1); a.rstd_in = (const float*)(sv + S.rs1); a.gamma = prm + o.g1;
+  a.aux = xh1; a.rstd_in = (const float*)(sv + S.rs1); a.gamma = prm + o.g1;
   a.out = dz1; a.part = f.lnpart;
   STEP("item_qkv_dx_ln1/mfma", launch_gemm(a, s));
   STEP("reduce/hbm", launch_reduce_z(tiles, 2 * E, 2 * E, f.lnpart, grads + o.g1, accumulate, s));
@@ -805,7 +825,7 @@ int fwd_pre(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* p
   const POff o = param_offsets(d.E, d.H, d.block);
   const int E = d.E, H = d.H;
   const int64_t N = g.N;
-  STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, s));
+  STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, nullptr, s));
   // x' = decay X, r1 = RMS1(x')
   STEP("rms_in/hbm", launch_rms_in(g, X, d.decay, prm + o.g1, kRmsEps, b.xs, b.r1, b.rs1, s));
   STEP_ERR(feat_fwd(g, b.r1, ROWS_COMPACT, prm + o.bqkv_f, b, f, s));
@@ -854,7 +874,7 @@ int bwd_pre(const Dims& d, const tfm::Geo& g, const Plan& P, const float* prm, c
   const int64_t N = g.N;
   const int tiles = (int)tfm::gemm_tiles(tfm::EPI_RMS_BWD, E, N);
   FastGrads G{f, g, grads, accumulate, s};
-  STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, s));
+  STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, nullptr, s));
   T* dh2 = (T*)(ws + W.te);
   T* dh1 = (T*)(ws + W.tf);
   T* dgb = (T*)(ws + W.th1);
