@@ -88,8 +88,9 @@ int64_t gemm_tiles(int epi, int BN, int64_t M);
 // Wqkv_f, Wo_f, Wqkv_i, Wo_i, W1, W2.
 // bf16 weight copies (element offsets); fb: float32 folded biases (3E item Q|K|V, then H MLP
 // up), at element fb of the bf16 buffer
+// ms: the weight stream of the fused MLP forward (mlp_fwd_stream_elems elements)
 struct WOff {
-  int64_t qkv_f, o_f, qkv_i, o_i, w1, w2, fb, total;
+  int64_t qkv_f, o_f, qkv_i, o_i, w1, w2, fb, ms, total;
 };
 WOff weight_offsets(int E, int H);
 // LayerNorm affines folded into the products that consume the normalised rows: the item Q|K|V
@@ -168,6 +169,32 @@ hipError_t launch_thinking_bwd(const Geo& g, int T, const TT* dX, float* dtable,
 hipError_t launch_ln_out_bwd(const Geo& g, const bf16* dY, const bf16* xhat, const float* rstd,
                              const float* gamma, bf16* dz, float* part, int* nblocks,
                              hipStream_t s);
+
+// The MLP half of the post-norm block, forward, in one kernel (csrc/mlp.hip): item
+// out-projection + residual + LN2, MLP up-projection, GELU and down-projection with the hidden
+// layer in registers, residual + LN3.  Reads the weight stream that launch_mlp_fwd_stream
+// builds (mlp_fwd_stream_elems(E, H) bf16 elements).
+struct MlpFwdArgs {
+  int64_t M;            // active cells
+  const bf16* oi;       // [M][E] item attention output
+  const bf16* xh1;      // [M][E] x-hat of LN1
+  const bf16* ws;       // weight stream
+  const float *bo, *g1, *be1, *g2, *be2, *b2, *g3, *be3;  // [E] each
+  const float* fb1;     // [H] folded up-projection bias b1 + W1 be2
+  bf16* xh2;            // [M][E] x-hat of LN2
+  float* rs2;           // [M]
+  bf16* gout;           // [M][H] pre-activation (optional)
+  bf16* uout;           // [M][H] GELU of it (optional)
+  bf16* y;              // native [B][R][S][E]
+  bf16* xh3;            // [M][E] x-hat of LN3 (optional)
+  float* rs3;           // [M]
+  Geo g;
+};
+bool mlp_fused_ok(int E, int H);
+int64_t mlp_fwd_stream_elems(int E, int H);
+hipError_t launch_mlp_fwd_stream(const float* wo, const float* w1, const float* g2,
+                                 const float* w2, int E, int H, bf16* out, hipStream_t s);
+hipError_t launch_mlp_fwd(const MlpFwdArgs& a, hipStream_t s);
 
 // Scratch bytes that the MFMA path needs inside the workspace.
 size_t fast_workspace_bytes(int B, int R, int S, int E, int heads, int H, bool bf16);

@@ -14,6 +14,7 @@ WOff weight_offsets(int E, int H) {
   o.w1 = x; x += (int64_t)H * E;
   o.w2 = x; x += (int64_t)E * H;
   o.fb = (x + 7) / 8 * 8; x = o.fb + 2 * (3LL * E + H);
+  o.ms = (x + 127) / 128 * 128; x = o.ms + (mlp_fused_ok(E, H) ? mlp_fwd_stream_elems(E, H) : 0);
   o.total = x;
   return o;
 }

@@ -11,6 +11,7 @@
 #include <math.h>
 
 #include "fast.h"
+#include "gelu.h"
 #include "mfma.h"
 
 namespace tfm {
@@ -27,44 +28,6 @@ __device__ __attribute__((aligned(16))) const uint4 kZeroChunk = {0u, 0u, 0u, 0u
 // makes those reads free of bank conflicts on this LDS (measured: rotating by bits 2 and 3
 // instead costs about 3 conflict cycles per read).
 __device__ __forceinline__ int kslot(int r, int kc) { return kc ^ ((r >> 1) & 3); }
-
-// 16 bytes per lane from global memory into LDS at lds_dst + 16 * lane (lds_dst wave-uniform).
-// Issued through inline assembly so that the compiler does not add its own conservative
-// vmcnt waits before later LDS reads: the pipeline waits for these loads explicitly.
-__device__ __forceinline__ void lds_dma16(const void* src, bf16* lds_dst) {
-  const uint32_t m0v = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds_dst);
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
-               :
-               : "s"(m0v), "v"(src)
-               : "memory", "m0");
-}
-
-// Normal CDF Phi(x) = (1 + erf(x / sqrt 2)) / 2 with erf from Abramowitz & Stegun 7.1.26
-// (|error| <= 1.5e-7): erf(z) = 1 - t (a1 + t (a2 + ... + t a5)) exp(-z^2), t = 1 / (1 + p z)
-// for z >= 0, odd in z.  *e returns exp(-x^2 / 2), which the normal density shares.
-__device__ __forceinline__ float norm_cdf(float x, float* e) {
-  const float az = fabsf(x) * 0.70710678118654752f;
-  *e = __builtin_amdgcn_exp2f(-0.72134752044448170f * x * x);  // exp(-x^2/2) = 2^(-x^2 log2e / 2)
-  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, az, 1.0f));
-  float poly = fmaf(t, 1.061405429f, -1.453152027f);
-  poly = fmaf(t, poly, 1.421413741f);
-  poly = fmaf(t, poly, -0.284496736f);
-  poly = fmaf(t, poly, 0.254829592f);
-  const float h = 0.5f * t * poly * *e;  // (1 - erf(|z|)) / 2
-  return x >= 0.f ? 1.0f - h : h;
-}
-// GELU(x) = x Phi(x)
-__device__ __forceinline__ float gelu_f(float x) {
-  float e;
-  return x * norm_cdf(x, &e);
-}
-// GELU'(x) = Phi(x) + x phi(x), phi(x) = exp(-x^2 / 2) / sqrt(2 pi)
-__device__ __forceinline__ float gelu_grad_f(float x) {
-  float e;
-  const float cdf = norm_cdf(x, &e);
-  return fmaf(x * 0.39894228040143268f, e, cdf);
-}
 
 __device__ __forceinline__ int64_t row_addr(const Geo& g, int mode, int64_t m, int64_t ld) {
   return mode == ROWS_NATIVE ? native_cell(g, m) * g.E : m * ld;

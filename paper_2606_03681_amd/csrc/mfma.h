@@ -102,6 +102,18 @@ __device__ __forceinline__ float bloadf(rsrc_t r, uint32_t off) {
   return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
 
+// 16 bytes per lane from global memory into LDS at lds_dst + 16 * lane (lds_dst wave-uniform).
+// Issued through inline assembly so that the compiler does not add its own conservative
+// vmcnt waits before later LDS reads: the pipeline waits for these loads explicitly.
+__device__ __forceinline__ void lds_dma16(const void* src, bf16* lds_dst) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds_dst);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(m0v), "v"(src)
+               : "memory", "m0");
+}
+
 // Workgroup barrier that waits only for this wave's LDS traffic (lgkmcnt), not for global
 // loads still in flight, so that prefetches issued before it keep overlapping compute.
 // The memory clobber keeps the compiler from moving memory accesses across it.

@@ -1,0 +1,323 @@
+// The MLP half of the post-norm block in one kernel per direction, with the hidden layer kept in
+// registers (paper Sec. 4.1 and the Fig. 3 caption: after the item-axis attention come a norm,
+// the MLP and a norm).  Forward, per active cell:
+//
+//   z2  = O_i Wo_i^T + bo_i + (g1 xh1 + be1)      item out-projection + residual (H1 from x-hat1)
+//   xh2 = (z2 - mean z2) rstd2                     LN2 (x-hat saved, its affine folded onward)
+//   G   = xh2 W1'^T + b1'                          W1' = W1 diag(g2), b1' = b1 + W1 be2
+//   z3  = GELU(G) W2^T + b2 + (g2 xh2 + be2)
+//   xh3 = (z3 - mean z3) rstd3,  Y = g3 xh3 + be3  LN3
+//
+// Layout (v_mfma_f32_16x16x32_bf16; lane L = 16 g + c):
+// * A workgroup is 4 waves, a wave owns 32 cells (two 16-cell blocks that share every weight
+//   fragment read); every product is computed transposed,
+//   out^T = W x^T, so the weights are the A operand (rows = output features) and the cells the
+//   B operand: lane (g, c) holds 8 k values of cell c, and receives output features
+//   16 b + 4 g .. + 3 of cell c.
+// * The activations never leave registers between the products: two output blocks b, b + 1 of
+//   a product give lane (g, c) the features {4 g .. + 3, 16 + 4 g .. + 3} of a 32-block, which
+//   is a B fragment of the next product once its k positions are taken in that order; the
+//   weights read in the next product carry the same permutation of their input columns
+//   (applied when the weight stream is built), so no shuffle or LDS round trip is needed.
+// * Weights stream from L2 through a 2-slot LDS ring (global_load_lds, 16 bytes per lane) in
+//   stages of 2 E/16 fragments, each fragment 1 KB in lane order (one conflict-free 16-byte
+//   read per lane): first Wo_i (two k steps per stage), then per 32 hidden units the 2 E/32
+//   W1' fragments of the unit block pair and the E/16 W2 fragments of those units.
+#include <math.h>
+
+#include "fast.h"
+#include "gelu.h"
+#include "mfma.h"
+
+namespace tfm {
+
+namespace {
+
+// k position of slot j (0..7) of lane group g in a B fragment that two D blocks form:
+// values 4 g .. 4 g + 3 of the first block, then of the second (16 + ...).
+__device__ __forceinline__ int perm_k(int g, int j) { return j < 4 ? 4 * g + j : 16 + 4 * g + (j - 4); }
+
+__device__ __forceinline__ f32x4 unpack4(uint32_t lo, uint32_t hi) {
+  f32x4 r;
+  r[0] = __uint_as_float(lo << 16);
+  r[1] = __uint_as_float(lo & 0xffff0000u);
+  r[2] = __uint_as_float(hi << 16);
+  r[3] = __uint_as_float(hi & 0xffff0000u);
+  return r;
+}
+
+__device__ __forceinline__ f32x4 lds4(const float* p) {
+  const float4 f = *reinterpret_cast<const float4*>(p);
+  f32x4 r;
+  r[0] = f.x; r[1] = f.y; r[2] = f.z; r[3] = f.w;
+  return r;
+}
+
+__device__ __forceinline__ float sum4(const f32x4& v) { return (v[0] + v[1]) + (v[2] + v[3]); }
+
+}  // namespace
+
+// ----------------------------------------------------------------------------- weight stream
+// One thread per bf16 element of the stream (see the file comment for the order).
+__global__ void k_mlp_fwd_stream(const float* __restrict__ wo, const float* __restrict__ w1,
+                                 const float* __restrict__ g2, const float* __restrict__ w2,
+                                 int E, int H, bf16* __restrict__ out) {
+  const int NE = E / 16, NK = E / 32, FPS = 2 * NE;  // fragments per stage
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t total = (int64_t)(NK / 2 + H / 32) * FPS * 512;
+  if (t >= total) return;
+  const int j = (int)(t & 7), lane = (int)((t >> 3) & 63);
+  const int64_t f = t >> 9;  // fragment index in the stream
+  const int st = (int)(f / FPS), fi = (int)(f % FPS);
+  const int g = lane >> 4, r = lane & 15;
+  float v;
+  if (st < NK / 2) {  // Wo_i: rows = output features, k = input features (natural order)
+    const int kk = fi / NE, eb = fi % NE;
+    const int row = eb * 16 + r, k = (2 * st + kk) * 32 + 8 * g + j;
+    v = wo[(int64_t)row * E + k];
+  } else {
+    const int c = st - NK / 2;
+    if (fi < 2 * NK) {  // W1' = W1 diag(g2): rows = hidden units, k = features (permuted)
+      const int hb = fi / NK, ks = fi % NK;
+      const int row = c * 32 + hb * 16 + r, k = ks * 32 + perm_k(g, j);
+      v = w1[(int64_t)row * E + k] * g2[k];
+    } else {  // W2: rows = output features, k = the chunk's hidden units (permuted)
+      const int eb = fi - 2 * NK;
+      const int row = eb * 16 + r, k = c * 32 + perm_k(g, j);
+      v = w2[(int64_t)row * H + k];
+    }
+  }
+  out[t] = f2bf(v);
+}
+
+int64_t mlp_fwd_stream_elems(int E, int H) { return (int64_t)(E / 64 + H / 32) * (E / 8) * 512; }
+
+hipError_t launch_mlp_fwd_stream(const float* wo, const float* w1, const float* g2,
+                                 const float* w2, int E, int H, bf16* out, hipStream_t s) {
+  const int64_t n = mlp_fwd_stream_elems(E, H);
+  k_mlp_fwd_stream<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(wo, w1, g2, w2, E, H, out);
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------------------------------- forward
+// A workgroup: NW waves of CB 16-cell blocks each (every weight fragment read from LDS feeds CB
+// products), TILE = NW * CB * 16 cells.
+constexpr int MLP_NW = 4, MLP_CB = 2, MLP_TILE = MLP_NW * MLP_CB * 16;
+
+template <int E, int H>
+__global__ __launch_bounds__(MLP_NW * 64, 2) void k_mlp_fwd(MlpFwdArgs a) {
+  constexpr int NW = MLP_NW, CB = MLP_CB, NT = NW * 64;
+  constexpr int NE = E / 16, NK = E / 32;  // 16-feature output blocks, 32-wide k steps
+  constexpr int FPS = 2 * NE;              // fragments per stage
+  constexpr int SEL = FPS * 512;           // elements per stage
+  constexpr int NP1 = NK / 2;              // stages of the out-projection
+  constexpr int NST = NP1 + H / 32;        // stages in all
+  constexpr int DPT = FPS * 64 / NT;       // 16-byte DMA pieces per thread and stage
+  static_assert(NK % 2 == 0 && H % 32 == 0 && DPT >= 1 && FPS * 64 % NT == 0, "shape");
+  constexpr int NSLOT = 2;                 // LDS ring slots
+  __shared__ __attribute__((aligned(16))) bf16 ring[NSLOT * SEL];
+  // per-feature parameters: bo_i, g1, be1, g2, be2, b2, g3, be3; then b1' per hidden unit
+  __shared__ __attribute__((aligned(16))) float pe[8][E];
+  __shared__ __attribute__((aligned(16))) float pfb[H];
+
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
+  const int c = lane & 15, g = lane >> 4;
+  const int64_t m0 = (int64_t)blockIdx.x * MLP_TILE;
+  int64_t cell[CB], crow[CB];
+  bool valid[CB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    cell[cb] = m0 + (w * CB + cb) * 16 + c;
+    valid[cb] = cell[cb] < a.M;
+    crow[cb] = valid[cb] ? cell[cb] : a.M - 1;  // past the end: read the last cell, store nothing
+  }
+
+  auto issue = [&](int st) {
+    const bf16* src = a.ws + (int64_t)st * SEL;
+    bf16* dst = ring + (st % NSLOT) * SEL;
+#pragma unroll
+    for (int i = 0; i < DPT; ++i) {
+      const int piece = i * NT + w * 64;
+      lds_dma16(src + (int64_t)(piece + lane) * 8, dst + piece * 8);
+    }
+  };
+  issue(0);
+
+  // activations of the out-projection: O_i as B fragments, the residual x-hat1 in the D layout
+  bf16x8 ob[CB][NK];
+  uint2 xr[CB][NE];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+#pragma unroll
+    for (int ks = 0; ks < NK; ++ks) ob[cb][ks] = ld8(a.oi + crow[cb] * E + ks * 32 + 8 * g);
+#pragma unroll
+    for (int eb = 0; eb < NE; ++eb)
+      xr[cb][eb] = *reinterpret_cast<const uint2*>(a.xh1 + crow[cb] * E + eb * 16 + 4 * g);
+  }
+  for (int i = tid; i < E; i += NT) {
+    pe[0][i] = a.bo[i]; pe[1][i] = a.g1[i]; pe[2][i] = a.be1[i]; pe[3][i] = a.g2[i];
+    pe[4][i] = a.be2[i]; pe[5][i] = a.b2[i]; pe[6][i] = a.g3[i]; pe[7][i] = a.be3[i];
+  }
+  for (int i = tid; i < H; i += NT) pfb[i] = a.fb1[i];
+
+  f32x4 acc[CB][NE];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+    for (int eb = 0; eb < NE; ++eb) acc[cb][eb] = zero4();
+  bf16x8 xf[CB][NK];  // x-hat2 as B fragments (k order perm_k within each 32-block)
+
+  // Stage st waits for its own pieces (issued when stage st - 1 began), then the barrier
+  // publishes every wave's pieces and frees the slot of stage st - 1, which stage st + 1 refills
+  // while stage st computes.
+  auto stage_begin = [&](int st) -> const bf16* {
+    asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+    if (st + 1 < NST) issue(st + 1);
+    return ring + (st % NSLOT) * SEL + lane * 8;
+  };
+
+  // out-projection, two k steps per stage
+#pragma unroll
+  for (int st = 0; st < NP1; ++st) {
+    const bf16* sl = stage_begin(st);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int eb = 0; eb < NE; ++eb) {
+        const bf16x8 af = ld8(sl + (kk * NE + eb) * 512);
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+          acc[cb][eb] = mfma16(af, ob[cb][2 * st + kk], acc[cb][eb]);
+      }
+  }
+  // z2 = acc + bo_i + g1 xh1 + be1, LN2 -> x-hat2 (saved, and the B fragments of W1')
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    float s = 0.f;
+#pragma unroll
+    for (int eb = 0; eb < NE; ++eb) {
+      const int e0 = eb * 16 + 4 * g;
+      acc[cb][eb] += lds4(&pe[0][e0]) +
+                     lds4(&pe[1][e0]) * unpack4(xr[cb][eb].x, xr[cb][eb].y) + lds4(&pe[2][e0]);
+      s += sum4(acc[cb][eb]);
+    }
+    const float mean = rows4_sum(s) * (1.0f / E);
+    float v = 0.f;
+#pragma unroll
+    for (int eb = 0; eb < NE; ++eb) {
+      acc[cb][eb] -= mean;
+      v += sum4(acc[cb][eb] * acc[cb][eb]);
+    }
+    const float rs = 1.0f / sqrtf(rows4_sum(v) * (1.0f / E) + 1e-5f);
+#pragma unroll
+    for (int ks = 0; ks < NK; ++ks) {
+      const f32x4 lo = acc[cb][2 * ks] * rs, hi = acc[cb][2 * ks + 1] * rs;
+      uint4 u = make_uint4(pack2(lo[0], lo[1]), pack2(lo[2], lo[3]), pack2(hi[0], hi[1]),
+                           pack2(hi[2], hi[3]));
+      xf[cb][ks] = *reinterpret_cast<bf16x8*>(&u);
+      if (valid[cb]) {
+        bf16* row = a.xh2 + cell[cb] * E + ks * 32 + 4 * g;
+        *reinterpret_cast<uint2*>(row) = make_uint2(u.x, u.y);
+        *reinterpret_cast<uint2*>(row + 16) = make_uint2(u.z, u.w);
+      }
+    }
+    if (valid[cb] && g == 0) a.rs2[cell[cb]] = rs;
+#pragma unroll
+    for (int eb = 0; eb < NE; ++eb) acc[cb][eb] = zero4();  // now the down-projection sums
+  }
+
+  // hidden units [32 hc, 32 hc + 32): G^T = W1' xh2^T + b1', U = GELU(G), acc += W2 U^T
+#pragma unroll 1
+  for (int hc = 0; hc < H / 32; ++hc) {
+    const bf16* sl = stage_begin(NP1 + hc);
+    f32x4 gacc[CB][2];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) gacc[cb][0] = gacc[cb][1] = zero4();
+#pragma unroll
+    for (int ks = 0; ks < NK; ++ks)
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb) {
+        const bf16x8 af = ld8(sl + (hb * NK + ks) * 512);
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) gacc[cb][hb] = mfma16(af, xf[cb][ks], gacc[cb][hb]);
+      }
+    bf16x8 uf[CB];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+      uint32_t up[4];
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb) {
+        const int u0 = hc * 32 + hb * 16 + 4 * g;
+        const f32x4 gv = gacc[cb][hb] + lds4(&pfb[u0]);
+        f32x4 uv;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) uv[q] = gelu_f(gv[q]);
+        up[2 * hb] = pack2(uv[0], uv[1]);
+        up[2 * hb + 1] = pack2(uv[2], uv[3]);
+        if (valid[cb] && a.gout)
+          *reinterpret_cast<uint2*>(a.gout + cell[cb] * H + u0) =
+              make_uint2(pack2(gv[0], gv[1]), pack2(gv[2], gv[3]));
+        if (valid[cb] && a.uout)
+          *reinterpret_cast<uint2*>(a.uout + cell[cb] * H + u0) =
+              make_uint2(up[2 * hb], up[2 * hb + 1]);
+      }
+      uint4 uu = make_uint4(up[0], up[1], up[2], up[3]);
+      uf[cb] = *reinterpret_cast<bf16x8*>(&uu);
+    }
+#pragma unroll
+    for (int eb = 0; eb < NE; ++eb) {
+      const bf16x8 af = ld8(sl + (2 * NK + eb) * 512);
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) acc[cb][eb] = mfma16(af, uf[cb], acc[cb][eb]);
+    }
+  }
+
+  // z3 = acc + b2 + g2 xh2 + be2 (x-hat2 as rounded to bf16), LN3 -> x-hat3, Y = g3 xh3 + be3
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    float s = 0.f;
+#pragma unroll
+    for (int eb = 0; eb < NE; ++eb) {
+      const int e0 = eb * 16 + 4 * g;
+      const uint4 u = *reinterpret_cast<const uint4*>(&xf[cb][eb / 2]);
+      const f32x4 xv = (eb & 1) ? unpack4(u.z, u.w) : unpack4(u.x, u.y);
+      acc[cb][eb] += lds4(&pe[5][e0]) + lds4(&pe[3][e0]) * xv + lds4(&pe[4][e0]);
+      s += sum4(acc[cb][eb]);
+    }
+    const float mean = rows4_sum(s) * (1.0f / E);
+    float v = 0.f;
+#pragma unroll
+    for (int eb = 0; eb < NE; ++eb) {
+      acc[cb][eb] -= mean;
+      v += sum4(acc[cb][eb] * acc[cb][eb]);
+    }
+    const float rs = 1.0f / sqrtf(rows4_sum(v) * (1.0f / E) + 1e-5f);
+    if (!valid[cb]) continue;
+    if (g == 0) a.rs3[cell[cb]] = rs;
+    bf16* yrow = a.y + native_cell(a.g, cell[cb]) * E;
+#pragma unroll
+    for (int eb = 0; eb < NE; ++eb) {
+      const int e0 = eb * 16 + 4 * g;
+      const f32x4 xh = acc[cb][eb] * rs;
+      const f32x4 yv = lds4(&pe[6][e0]) * xh + lds4(&pe[7][e0]);
+      *reinterpret_cast<uint2*>(yrow + e0) = make_uint2(pack2(yv[0], yv[1]), pack2(yv[2], yv[3]));
+      if (a.xh3)
+        *reinterpret_cast<uint2*>(a.xh3 + cell[cb] * E + e0) =
+            make_uint2(pack2(xh[0], xh[1]), pack2(xh[2], xh[3]));
+    }
+  }
+}
+
+bool mlp_fused_ok(int E, int H) { return E == 192 && H == 384; }
+
+hipError_t launch_mlp_fwd(const MlpFwdArgs& a, hipStream_t s) {
+  if (a.M <= 0) return hipSuccess;
+  const unsigned grid = (unsigned)((a.M + MLP_TILE - 1) / MLP_TILE);
+  if (a.g.E == 192 && a.g.H == 384)
+    k_mlp_fwd<192, 384><<<grid, MLP_NW * 64, 0, s>>>(a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace tfm

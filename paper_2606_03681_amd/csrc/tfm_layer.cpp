@@ -661,6 +661,22 @@ int fwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
   STEP("item_qkv/mfma", launch_gemm(a, s));
   STEP("item_attn_fwd/mfma",
        launch_item_attn_fwd(g, b.qi, b.ki, b.vi, b.oi, b.lsei, s, b.kR));
+  if (mlp_fused_ok(E, H)) {
+    // out-projection + LN2, MLP and LN3 in one kernel, the hidden layer in registers
+    bf16* ms = f.w + f.wo.ms;
+    STEP("mlp_stream/hbm",
+         launch_mlp_fwd_stream(prm + o.Wo_i, prm + o.W1, prm + o.g2, prm + o.W2, E, H, ms, s));
+    MlpFwdArgs m{};
+    m.M = N; m.oi = b.oi; m.xh1 = b.h1; m.ws = ms;
+    m.bo = prm + o.bo_i; m.g1 = prm + o.g1; m.be1 = prm + o.be1; m.g2 = prm + o.g2;
+    m.be2 = prm + o.be2; m.b2 = prm + o.b2; m.g3 = prm + o.g3; m.be3 = prm + o.be3;
+    m.fb1 = fb + 3 * E;
+    m.xh2 = b.h2; m.rs2 = b.rs2; m.gout = b.g; m.uout = b.g ? b.u : nullptr;
+    m.y = Y; m.xh3 = b.xh3; m.rs3 = b.rs3; m.g = g;
+    STEP("mlp_fused/mfma", launch_mlp_fwd(m, s));
+    STEP("zero_inactive/hbm", launch_zero_inactive(g, Y, s));
+    return TFM_OK;
+  }
   // x-hat2 of H2 = LN2(H1 + O_i Wo_i^T + bo_i), H1 = g1 x-hat1 + be1
   a = gemm_base(g, N, E, E, EPI_LN);
   a.A = b.oi; a.lda = E; a.Bt = f.w + f.wo.o_i; a.bias = prm + o.bo_i;
