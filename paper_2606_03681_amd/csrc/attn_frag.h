@@ -89,6 +89,16 @@ struct HF<64> {
   }
 };
 
+// An empty use of a fragment's registers: the compiler waits for the loads that fill them here,
+// so no wait for them is left pending at the head of a later loop.
+template <int D>
+__device__ __forceinline__ void hf_touch(const typename HF<D>::frag& f) {
+  if constexpr (D == 64)
+    asm volatile("" ::"v"(f.lo), "v"(f.hi));
+  else
+    asm volatile("" ::"v"(f));
+}
+
 // Sum over the lane's values of a * b (one lane's share of a row dot product).
 template <int D>
 __device__ __forceinline__ float hf_dot(const typename HF<D>::frag& a,

@@ -33,7 +33,7 @@ __device__ __forceinline__ uint32_t pk_bf16(float a, float b) { return pack2(a, 
 }  // namespace
 
 template <int D>
-__global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __restrict__ q,
+__global__ __launch_bounds__(256, D == 64 ? 3 : 5) void k_item_attn_fwd(Geo g, const bf16* __restrict__ q,
                                                        const bf16* __restrict__ k,
                                                        const bf16* __restrict__ v,
                                                        bf16* __restrict__ o,
@@ -66,13 +66,17 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
   const int c = lane & 15, lg = lane >> 4;
   const int qw0 = qt * QWG + wave * QWV;
 
+  // Buffer resources of the problem: loads past the end (queries past R, keys past n) return 0
+  // without an exec-masked branch, so the compiler's wait counts stay exact and the prefetch of
+  // the next key tile is not waited for before the current tile's products.
+  const rsrc_t rQ = make_rsrc(Qp, (uint32_t)R * D * 2);
+  const rsrc_t rK = make_rsrc(Kp, (uint32_t)n * D * 2);
+  const rsrc_t rV = make_rsrc(Vp, (uint32_t)n * D * 2);
+
   // Q^T fragments (B operand): lane holds query qw0 + qb*16 + c
   typename HF<D>::frag qf[2];
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    int qq = qw0 + qb * 16 + c;
-    qf[qb] = qq < R ? HF<D>::glob(Qp + (int64_t)qq * D, lg) : HF<D>::zero();
-  }
+  for (int qb = 0; qb < 2; ++qb) qf[qb] = HF<D>::buf(rQ, (uint32_t)(qw0 + qb * 16 + c) * D * 2, lg);
 
   // staging: item it = tid + 256 i -> (key, 16-byte chunk of its dims): key it / CPR, chunk
   // it % CPR; at d = 32 key (it % 16) + 16 (it / 64), chunk (it / 16) % 4, so that each store
@@ -86,9 +90,10 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
     for (int i = 0; i < NSI; ++i) {
       const int it = tid + 256 * i;
       const int t = t0 + item_key(it), ch = item_ch(it) * 8;
-      const bool ok = it < KT * CPR && t < n;
-      rk[i] = ok ? ldu4(Kp + (int64_t)t * D + ch) : make_uint4(0, 0, 0, 0);
-      rv[i] = ok ? ldu4(Vp + (int64_t)t * D + ch) : make_uint4(0, 0, 0, 0);
+      // items past the tile (d = 16) name an offset past the range and read 0
+      const uint32_t off = it < KT * CPR ? (uint32_t)(t * D + ch) * 2 : 0xfffffff0u;
+      rk[i] = bload16(rK, off);
+      rv[i] = bload16(rV, off);
     }
   };
   auto sstore = [&](int buf) {
@@ -214,6 +219,9 @@ __global__ __launch_bounds__(256) void k_item_attn_fwd(Geo g, const bf16* __rest
   const int NF = n / KT;  // full tiles; a partial tail tile follows if NT > NF
   gload(0);
   sstore(0);
+  // the Q fragments have arrived before the loop (no load is pending at its head)
+  hf_touch<D>(qf[0]);
+  hf_touch<D>(qf[1]);
   lds_barrier();
   for (int it = 0; it < NF; ++it) {
     const int cur = it & 1;
