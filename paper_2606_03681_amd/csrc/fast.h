@@ -196,6 +196,36 @@ hipError_t launch_mlp_fwd_stream(const float* wo, const float* w1, const float* 
                                  const float* w2, int E, int H, bf16* out, hipStream_t s);
 hipError_t launch_mlp_fwd(const MlpFwdArgs& a, hipStream_t s);
 
+// Backward of the same sub-block in one kernel (csrc/mlp.hip): LN3' from the native dY, the MLP
+// backward with G recomputed from x-hat2, LN2'.  Writes dz3, dz2, dG and U (the weight
+// gradients' operands) and per-tile column sums [mlp_bwd_tiles(M)][4 E]: dY xh3, dY, dh2 xh2,
+// dh2 (the LN3 and LN2 weight and bias gradients).
+struct MlpBwdArgs {
+  int64_t M;
+  const bf16* dy;       // native upstream gradient
+  const bf16* xh3;      // [M][E]
+  const float* rs3;     // [M]
+  const bf16* xh2;      // [M][E]
+  const float* rs2;     // [M]
+  const bf16* ws;       // backward weight stream (mlp_bwd_stream_elems)
+  const float *g3, *g2; // [E]
+  const float* fb1;     // [H] folded up-projection bias
+  bf16* dz3;            // [M][E]
+  bf16* dz2;            // [M][E]
+  bf16* dg;             // [M][H]
+  bf16* u;              // [M][H]
+  float* part;          // [mlp_bwd_tiles(M)][4 E]
+  Geo g;
+};
+int64_t mlp_bwd_stream_elems(int E, int H);
+int64_t mlp_bwd_tiles(int64_t M);
+hipError_t launch_mlp_bwd_stream(const float* w1, const float* g2, const float* w2, int E, int H,
+                                 bf16* out, hipStream_t s);
+hipError_t launch_mlp_bwd(const MlpBwdArgs& a, hipStream_t s);
+
+// Bytes of the LayerNorm-backward column partials for up to `cells` cells.
+size_t ln_partial_bytes(int64_t cells, int E);
+
 // Scratch bytes that the MFMA path needs inside the workspace.
 size_t fast_workspace_bytes(int B, int R, int S, int E, int heads, int H, bool bf16);
 

@@ -14,7 +14,12 @@ WOff weight_offsets(int E, int H) {
   o.w1 = x; x += (int64_t)H * E;
   o.w2 = x; x += (int64_t)E * H;
   o.fb = (x + 7) / 8 * 8; x = o.fb + 2 * (3LL * E + H);
-  o.ms = (x + 127) / 128 * 128; x = o.ms + (mlp_fused_ok(E, H) ? mlp_fwd_stream_elems(E, H) : 0);
+  // the forward and the backward stream of the fused MLP share one region
+  int64_t msz = 0;
+  if (mlp_fused_ok(E, H))
+    msz = mlp_fwd_stream_elems(E, H) > mlp_bwd_stream_elems(E, H) ? mlp_fwd_stream_elems(E, H)
+                                                                   : mlp_bwd_stream_elems(E, H);
+  o.ms = (x + 127) / 128 * 128; x = o.ms + msz;
   o.total = x;
   return o;
 }
@@ -367,13 +372,21 @@ template hipError_t launch_thinking_bwd<float>(const Geo&, int, const float*, fl
 template hipError_t launch_thinking_bwd<bf16>(const Geo&, int, const bf16*, float*, int,
                                               hipStream_t);
 
+size_t ln_partial_bytes(int64_t cells, int E) {
+  // LN-backward GEMM epilogues: [64-cell tiles][2 E]; fused MLP backward: [tiles][4 E]
+  const size_t a = (size_t)gemm_row_tiles(cells) * 2 * E * 4;
+  const size_t b = (size_t)mlp_bwd_tiles(cells) * 4 * E * 4;
+  return (a > b ? a : b) + 256;
+}
+
 size_t fast_workspace_bytes(int B, int R, int S, int E, int heads, int H, bool bf16) {
   (void)heads;
   if (!bf16) return 0;
   WOff wo = weight_offsets(E, H);
   const int64_t tiles = gemm_row_tiles((int64_t)B * R * S);
   size_t bytes = 2 * (size_t)wo.total * 2 + 1024;   // w and wt
-  bytes += (size_t)tiles * 2 * E * 4 + 256;         // LN-backward column partials
+  (void)tiles;
+  bytes += ln_partial_bytes((int64_t)B * R * S, E);  // LN-backward column partials
   const int64_t cells = (int64_t)B * R * S;
   const int64_t zw = wgrad_max_chunks(cells);
   const int64_t maxw = 3LL * E * E > (int64_t)H * E ? 3LL * E * E : (int64_t)H * E;

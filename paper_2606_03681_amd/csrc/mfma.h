@@ -114,6 +114,17 @@ __device__ __forceinline__ void lds_dma16(const void* src, bf16* lds_dst) {
                : "memory", "m0");
 }
 
+// The same DMA from a wave-uniform base address (SGPRs) plus a per-lane byte offset: lane L's 16
+// bytes come from sbase + voff and land at lds_dst + 16 * L.  One VGPR of address per lane.
+__device__ __forceinline__ void lds_dma16_s(const void* sbase, uint32_t voff, bf16* lds_dst) {
+  const uint32_t m0v = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds_dst);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :
+               : "s"(m0v), "v"(voff), "s"(sbase)
+               : "memory", "m0");
+}
+
 // Workgroup barrier that waits only for this wave's LDS traffic (lgkmcnt), not for global
 // loads still in flight, so that prefetches issued before it keep overlapping compute.
 // The memory clobber keeps the compiler from moving memory accesses across it.

@@ -138,7 +138,7 @@ __global__ __launch_bounds__(MLP_NW * 64, 2) void k_mlp_fwd(MlpFwdArgs a) {
 #pragma unroll
     for (int i = 0; i < DPT; ++i) {
       const int piece = i * NT + w * 64;
-      lds_dma16(src + (int64_t)(piece + lane) * 8, dst + piece * 8);
+      lds_dma16_s(src + piece * 8, (uint32_t)lane * 16, dst + piece * 8);
     }
   };
   issue(0);
@@ -306,6 +306,272 @@ __global__ __launch_bounds__(MLP_NW * 64, 2) void k_mlp_fwd(MlpFwdArgs a) {
             make_uint2(pack2(xh[0], xh[1]), pack2(xh[2], xh[3]));
     }
   }
+}
+
+// ----------------------------------------------------------------------------- backward
+// Backward of the same sub-block, from the native upstream gradient dY:
+//
+//   dz3 = rstd3 (g - mean g - xh3 mean(g xh3)),  g = dY g3         LN3'   (dz3 saved for dW2)
+//   G   = xh2 W1'^T + b1' (recomputed),  U = GELU(G)               (U saved for dW2)
+//   dG  = (dz3 W2) GELU'(G)                                        (saved for dW1, db1)
+//   dh2 = dz3 + dG W1
+//   dz2 = rstd2 (g - mean g - xh2 mean(g xh2)),  g = dh2 g2        LN2'
+//
+// plus per-tile column sums of dY xh3, dY (the LN3 weight and bias gradients) and dh2 xh2, dh2
+// (LN2).  A workgroup is 12 waves of 16 cells; the inputs of a cell are loaded in the order that
+// two D blocks give (features {4 g .. + 3, 16 + 4 g .. + 3} of each 32-block), which serves both
+// as B fragments and as the per-feature operands of the norms.  Weight stream per 32 hidden
+// units: W1' (units x features), W2^T (units x features), both with permuted feature columns,
+// then W1^T (features x the chunk's units, permuted unit columns).
+__global__ void k_mlp_bwd_stream(const float* __restrict__ w1, const float* __restrict__ g2,
+                                 const float* __restrict__ w2, int E, int H,
+                                 bf16* __restrict__ out) {
+  const int NE = E / 16, NK = E / 32, FPS = 4 * NK + NE;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t total = (int64_t)(H / 32) * FPS * 512;
+  if (t >= total) return;
+  const int j = (int)(t & 7), lane = (int)((t >> 3) & 63);
+  const int64_t f = t >> 9;
+  const int c = (int)(f / FPS), fi = (int)(f % FPS);
+  const int g = lane >> 4, r = lane & 15;
+  float v;
+  if (fi < 4 * NK) {
+    const int part = fi / (2 * NK), hb = (fi % (2 * NK)) / NK, ks = fi % NK;
+    const int u = c * 32 + hb * 16 + r, k = ks * 32 + perm_k(g, j);
+    v = part == 0 ? w1[(int64_t)u * E + k] * g2[k] : w2[(int64_t)k * H + u];
+  } else {
+    const int eb = fi - 4 * NK;
+    const int e = eb * 16 + r, u = c * 32 + perm_k(g, j);
+    v = w1[(int64_t)u * E + e];
+  }
+  out[t] = f2bf(v);
+}
+
+int64_t mlp_bwd_stream_elems(int E, int H) { return (int64_t)(H / 32) * (3 * E / 16) * 512; }
+
+hipError_t launch_mlp_bwd_stream(const float* w1, const float* g2, const float* w2, int E, int H,
+                                 bf16* out, hipStream_t s) {
+  const int64_t n = mlp_bwd_stream_elems(E, H);
+  k_mlp_bwd_stream<<<(unsigned)((n + 255) / 256), 256, 0, s>>>(w1, g2, w2, E, H, out);
+  return hipGetLastError();
+}
+
+constexpr int MB_NW = 12, MB_TILE = MB_NW * 16;
+
+int64_t mlp_bwd_tiles(int64_t M) { return (M + MB_TILE - 1) / MB_TILE; }
+
+template <int E, int H>
+__global__ __launch_bounds__(MB_NW * 64, 3) void k_mlp_bwd(MlpBwdArgs a) {
+  constexpr int NW = MB_NW, NT = NW * 64;
+  constexpr int NE = E / 16, NK = E / 32;
+  constexpr int FPS = 4 * NK + NE;         // fragments per stage (one 32-unit chunk)
+  constexpr int SEL = FPS * 512;
+  constexpr int NST = H / 32;
+  constexpr int DPT = FPS * 64 / NT;
+  static_assert(H % 32 == 0 && DPT >= 1 && FPS * 64 % NT == 0, "shape");
+  __shared__ __attribute__((aligned(16))) bf16 ring[2 * SEL];
+  __shared__ __attribute__((aligned(16))) float pe[2][E];   // g3, g2
+  __shared__ __attribute__((aligned(16))) float pfb[H];     // b1'
+
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
+  const int c = lane & 15, g = lane >> 4;
+  const int64_t tile = blockIdx.x;
+  const int64_t cell = tile * MB_TILE + w * 16 + c;
+  const bool valid = cell < a.M;
+  const int64_t crow = valid ? cell : a.M - 1;
+
+  auto issue = [&](int st) {
+    const bf16* src = a.ws + (int64_t)st * SEL;
+    bf16* dst = ring + (st & 1) * SEL;
+#pragma unroll
+    for (int i = 0; i < DPT; ++i) {
+      const int piece = i * NT + w * 64;
+      lds_dma16_s(src + piece * 8, (uint32_t)lane * 16, dst + piece * 8);
+    }
+  };
+  issue(0);
+
+  // the cell's inputs, features {32 ks + 4 g .. + 3} (h = 0) and {32 ks + 16 + 4 g .. + 3}
+  uint2 dyl[NK][2], x3l[NK][2];
+  {
+    const bf16* dyr = a.dy + native_cell(a.g, crow) * E;
+    const bf16* x3r = a.xh3 + crow * E;
+#pragma unroll
+    for (int ks = 0; ks < NK; ++ks)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int e0 = ks * 32 + h * 16 + 4 * g;
+        dyl[ks][h] = *reinterpret_cast<const uint2*>(dyr + e0);
+        x3l[ks][h] = *reinterpret_cast<const uint2*>(x3r + e0);
+      }
+  }
+  const float rs3 = valid ? a.rs3[crow] : 0.f, rs2 = valid ? a.rs2[crow] : 0.f;
+  for (int i = tid; i < E; i += NT) {
+    pe[0][i] = a.g3[i];
+    pe[1][i] = a.g2[i];
+  }
+  for (int i = tid; i < H; i += NT) pfb[i] = a.fb1[i];
+  __syncthreads();
+
+  // column sums over the wave's 16 cells into red[w][which]: every lane of a 16-lane row ends
+  // with the same sums and stores them (same address, same value)
+  // [NW][2][E] per-wave sums: LN3's in the ring's second slot (free until the first stage
+  // begins), LN2's in its first slot (after the last stage)
+  float* red = reinterpret_cast<float*>(ring + SEL);
+  float* red2 = reinterpret_cast<float*>(ring);
+  static_assert(NW * 2 * E * 4 <= SEL * 2, "column sums fit a ring slot");
+  auto colsum = [&](int which, int eb, f32x4 v) {
+    f32x4 t;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) t[q] = row16_sum(v[q]);
+    float* dst = which < 2 ? red + (w * 2 + which) * E : red2 + (w * 2 + which - 2) * E;
+    *reinterpret_cast<f32x4*>(dst + eb * 16 + 4 * g) = t;
+  };
+  // the tile's sums of one norm (waves added in order) -> part[tile][off .. off + 2E)
+  auto flush = [&](const float* src, int off) {
+    __syncthreads();
+    for (int i = tid; i < 2 * E; i += NT) {
+      float sm = 0.f;
+#pragma unroll
+      for (int ww = 0; ww < NW; ++ww) sm += src[ww * 2 * E + i];
+      a.part[tile * 4 * E + off + i] = sm;
+    }
+  };
+
+  // LN3': dz3 = rs3 (dY g3 - mean(dY g3) - xh3 mean(dY g3 xh3)); invalid cells contribute 0
+  bf16x8 dzf[NK];
+  {
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int eb = 0; eb < NE; ++eb) {
+      const int ks = eb >> 1, h = eb & 1;
+      const f32x4 dy = valid ? unpack4(dyl[ks][h].x, dyl[ks][h].y) : zero4();
+      const f32x4 x3 = unpack4(x3l[ks][h].x, x3l[ks][h].y);
+      const f32x4 gy = dy * lds4(&pe[0][eb * 16 + 4 * g]);
+      s1 += sum4(gy);
+      s2 += sum4(gy * x3);
+      colsum(0, eb, dy * x3);
+      colsum(1, eb, dy);
+    }
+    const float m1 = rows4_sum(s1) * (1.0f / E), m2 = rows4_sum(s2) * (1.0f / E);
+#pragma unroll
+    for (int ks = 0; ks < NK; ++ks) {
+      uint32_t pk[4];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int eb = 2 * ks + h;
+        const f32x4 dy = valid ? unpack4(dyl[ks][h].x, dyl[ks][h].y) : zero4();
+        const f32x4 x3 = unpack4(x3l[ks][h].x, x3l[ks][h].y);
+        const f32x4 dz = rs3 * (dy * lds4(&pe[0][eb * 16 + 4 * g]) - m1 - x3 * m2);
+        pk[2 * h] = pack2(dz[0], dz[1]);
+        pk[2 * h + 1] = pack2(dz[2], dz[3]);
+        if (valid)
+          *reinterpret_cast<uint2*>(a.dz3 + cell * E + ks * 32 + h * 16 + 4 * g) =
+              make_uint2(pk[2 * h], pk[2 * h + 1]);
+      }
+      uint4 u = make_uint4(pk[0], pk[1], pk[2], pk[3]);
+      dzf[ks] = *reinterpret_cast<bf16x8*>(&u);
+    }
+  }
+  flush(red, 0);
+  // x-hat2 as B fragments (loaded once LN3' no longer holds its inputs)
+  bf16x8 xf[NK];
+#pragma unroll
+  for (int ks = 0; ks < NK; ++ks) {
+    const bf16* x2r = a.xh2 + crow * E + ks * 32 + 4 * g;
+    const uint2 lo = *reinterpret_cast<const uint2*>(x2r);
+    const uint2 hi = *reinterpret_cast<const uint2*>(x2r + 16);
+    uint4 u = make_uint4(lo.x, lo.y, hi.x, hi.y);
+    xf[ks] = *reinterpret_cast<bf16x8*>(&u);
+  }
+
+  auto stage_begin = [&](int st) -> const bf16* {
+    asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+    if (st + 1 < NST) issue(st + 1);
+    return ring + (st & 1) * SEL + lane * 8;
+  };
+
+  f32x4 acc[NE];  // dh2^T - dz3, features 16 eb + 4 g .. + 3 of the lane's cell
+#pragma unroll
+  for (int eb = 0; eb < NE; ++eb) acc[eb] = zero4();
+#pragma unroll 1
+  for (int hc = 0; hc < NST; ++hc) {
+    const bf16* sl = stage_begin(hc);
+    f32x4 gacc[2] = {zero4(), zero4()}, dacc[2] = {zero4(), zero4()};
+#pragma unroll
+    for (int ks = 0; ks < NK; ++ks)
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb) {
+        gacc[hb] = mfma16(ld8(sl + (hb * NK + ks) * 512), xf[ks], gacc[hb]);
+        dacc[hb] = mfma16(ld8(sl + ((2 + hb) * NK + ks) * 512), dzf[ks], dacc[hb]);
+      }
+    uint32_t dp[4];
+#pragma unroll
+    for (int hb = 0; hb < 2; ++hb) {
+      const int u0 = hc * 32 + hb * 16 + 4 * g;
+      const f32x4 gv = gacc[hb] + lds4(&pfb[u0]);
+      f32x4 uv, dv;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float e;
+        const float cdf = norm_cdf(gv[q], &e);
+        uv[q] = gv[q] * cdf;
+        dv[q] = dacc[hb][q] * fmaf(gv[q] * 0.39894228040143268f, e, cdf);
+      }
+      dp[2 * hb] = pack2(dv[0], dv[1]);
+      dp[2 * hb + 1] = pack2(dv[2], dv[3]);
+      if (valid) {
+        *reinterpret_cast<uint2*>(a.u + cell * H + u0) =
+            make_uint2(pack2(uv[0], uv[1]), pack2(uv[2], uv[3]));
+        *reinterpret_cast<uint2*>(a.dg + cell * H + u0) = make_uint2(dp[2 * hb], dp[2 * hb + 1]);
+      }
+    }
+    uint4 du = make_uint4(dp[0], dp[1], dp[2], dp[3]);
+    const bf16x8 dgf = *reinterpret_cast<bf16x8*>(&du);
+#pragma unroll
+    for (int eb = 0; eb < NE; ++eb) acc[eb] = mfma16(ld8(sl + (4 * NK + eb) * 512), dgf, acc[eb]);
+  }
+
+  // LN2': dh2 = acc + dz3 (as rounded to bf16), dz2 = rs2 (g - mean g - xh2 mean(g xh2))
+  __syncthreads();  // every wave is done with the ring
+  {
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int eb = 0; eb < NE; ++eb) {
+      const uint4 dzu = *reinterpret_cast<const uint4*>(&dzf[eb >> 1]);
+      const uint4 xu = *reinterpret_cast<const uint4*>(&xf[eb >> 1]);
+      const f32x4 dz = (eb & 1) ? unpack4(dzu.z, dzu.w) : unpack4(dzu.x, dzu.y);
+      const f32x4 x2 = (eb & 1) ? unpack4(xu.z, xu.w) : unpack4(xu.x, xu.y);
+      acc[eb] += dz;
+      const f32x4 dh = valid ? acc[eb] : zero4();
+      const f32x4 gg = acc[eb] * lds4(&pe[1][eb * 16 + 4 * g]);
+      s1 += sum4(gg);
+      s2 += sum4(gg * x2);
+      colsum(2, eb, dh * x2);
+      colsum(3, eb, dh);
+    }
+    const float m1 = rows4_sum(s1) * (1.0f / E), m2 = rows4_sum(s2) * (1.0f / E);
+#pragma unroll
+    for (int eb = 0; eb < NE; ++eb) {
+      const uint4 xu = *reinterpret_cast<const uint4*>(&xf[eb >> 1]);
+      const f32x4 x2 = (eb & 1) ? unpack4(xu.z, xu.w) : unpack4(xu.x, xu.y);
+      const f32x4 dz = rs2 * (acc[eb] * lds4(&pe[1][eb * 16 + 4 * g]) - m1 - x2 * m2);
+      if (valid)
+        *reinterpret_cast<uint2*>(a.dz2 + cell * E + eb * 16 + 4 * g) =
+            make_uint2(pack2(dz[0], dz[1]), pack2(dz[2], dz[3]));
+    }
+  }
+  flush(red2, 2 * E);
+}
+
+hipError_t launch_mlp_bwd(const MlpBwdArgs& a, hipStream_t s) {
+  if (a.M <= 0) return hipSuccess;
+  const unsigned grid = (unsigned)mlp_bwd_tiles(a.M);
+  if (a.g.E == 192 && a.g.H == 384)
+    k_mlp_bwd<192, 384><<<grid, MB_NW * 64, 0, s>>>(a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
 }
 
 bool mlp_fused_ok(int E, int H) { return E == 192 && H == 384; }

@@ -173,8 +173,10 @@ SavedLayout saved_layout(const Dims& d) {
   L.h2 = a.take(N * E * t);
   L.xh2 = a.take(xhn);
   L.rs2 = a.take(N * 4);
-  L.g = a.take(N * d.H * t);
-  L.u = a.take(N * d.H * t);
+  // the fused MLP backward recomputes G and U: no saved copies
+  const size_t gun = d.dtype == TFM_BF16 && tfm::mlp_fused_ok(d.E, d.H) ? 0 : N * d.H * t;
+  L.g = a.take(gun);
+  L.u = a.take(gun);
   L.xh3 = a.take(N * E * t);
   L.rs3 = a.take(N * 4);
   L.total = a.off;
@@ -571,7 +573,7 @@ FastWs fast_ws(const Dims& d, char* ws, const WsLayout& W) {
   f.wt = (tfm::bf16*)p;
   p += align_up((size_t)f.wo.total * 2);
   f.lnpart = (float*)p;
-  p += align_up((size_t)tfm::gemm_row_tiles(d.Nmax) * 2 * d.E * 4 + 256);
+  p += align_up(tfm::ln_partial_bytes(d.Nmax, d.E));
   const int64_t zw = tfm::wgrad_max_chunks(d.Nmax);
   const int64_t maxw = 3LL * d.E * d.E > (int64_t)d.H * d.E ? 3LL * d.E * d.E : (int64_t)d.H * d.E;
   f.wpart = (float*)p;
@@ -671,7 +673,7 @@ int fwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
     m.bo = prm + o.bo_i; m.g1 = prm + o.g1; m.be1 = prm + o.be1; m.g2 = prm + o.g2;
     m.be2 = prm + o.be2; m.b2 = prm + o.b2; m.g3 = prm + o.g3; m.be3 = prm + o.be3;
     m.fb1 = fb + 3 * E;
-    m.xh2 = b.h2; m.rs2 = b.rs2; m.gout = b.g; m.uout = b.g ? b.u : nullptr;
+    m.xh2 = b.h2; m.rs2 = b.rs2;  // G and U are recomputed by the fused backward
     m.y = Y; m.xh3 = b.xh3; m.rs3 = b.rs3; m.g = g;
     STEP("mlp_fused/mfma", launch_mlp_fwd(m, s));
     STEP("zero_inactive/hbm", launch_zero_inactive(g, Y, s));
@@ -742,7 +744,11 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const Plan& P, const tfm::bf16* X
   const int64_t N = g.N;
   const int tiles = (int)tfm::gemm_tiles(tfm::EPI_LN_BWD, E, N);
   FastGrads G{f, g, grads, accumulate, s};
-  STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, nullptr, s));
+  const bool fused_mlp = mlp_fused_ok(E, H);
+  // the backward reads the transposed copies only; the fold (x-hat2's affine in W1 and b1)
+  // gives the fused MLP backward the folded up-projection bias it recomputes G with
+  const WFold fold{prm + o.g1, prm + o.be1, prm + o.bqkv_i, prm + o.g2, prm + o.be2, prm + o.b1};
+  STEP("weight_prep/hbm", launch_weight_prep(prm, E, H, f.w, f.wt, fused_mlp ? &fold : nullptr, s));
   T* dz3 = (T*)(ws + W.tb);
   T* dz2 = (T*)(ws + W.te);
   T* dz1 = (T*)(ws + W.tf);
@@ -750,26 +756,51 @@ int bwd_fast(const Dims& d, const tfm::Geo& g, const Plan& P, const tfm::bf16* X
   T* dqkv = (T*)(ws + W.tqkv);
   const T* xh1 = (const T*)(sv + S.h1);  // the forward keeps x-hat1 and x-hat2 only
   const T* xh2 = (const T*)(sv + S.h2);
-  // LN3 (from the native dY), with its gamma/beta column sums
-  int nb = 0;
-  STEP("ln3_bwd/hbm", launch_ln_out_bwd(g, dY, (const T*)(sv + S.xh3), (const float*)(sv + S.rs3),
-                                        prm + o.g3, dz3, f.lnpart, &nb, s));
-  // gamma and beta gradients are adjacent in the packed order: one sum over 2E columns
-  STEP("reduce/hbm", launch_reduce_z(nb, 2 * E, 2 * E, f.lnpart, grads + o.g3, accumulate, s));
-  // MLP: dG = (dZ3 W2) * GELU'(G)
-  GemmArgs a = gemm_base(g, N, H, E, EPI_GELU_BWD);
-  a.A = dz3; a.lda = E; a.Bt = f.wt + f.wo.w2; a.out = dgb; a.ldo = H;
-  a.aux = (const T*)(sv + S.g);
-  STEP("mlp_down_dx/mfma", launch_gemm(a, s));
-  CHK(G.run(dz3, E, (const T*)(sv + S.u), H, ROWS_COMPACT, o.W2, o.b2));
-  CHK(G.run(dgb, H, xh2, E, ROWS_COMPACT, o.W1, o.b1, nullptr, nullptr, ROWS_COMPACT,
-            prm + o.g2, prm + o.be2));
-  // dZ2 = LN2'(dZ3 + dG W1)
-  a = gemm_base(g, N, E, H, EPI_LN_BWD);
-  a.A = dgb; a.lda = H; a.Bt = f.wt + f.wo.w1; a.resid = dz3; a.aux = xh2;
-  a.rstd_in = (const float*)(sv + S.rs2); a.gamma = prm + o.g2; a.out = dz2; a.part = f.lnpart;
-  STEP("mlp_up_dx_ln2/mfma", launch_gemm(a, s));
-  STEP("reduce/hbm", launch_reduce_z(tiles, 2 * E, 2 * E, f.lnpart, grads + o.g2, accumulate, s));
+  if (fused_mlp) {
+    // LN3', the MLP backward with G recomputed, LN2' in one kernel; its column sums give the
+    // LN3 and LN2 weight and bias gradients (each pair adjacent in the packed order)
+    T* ub = (T*)(ws + W.th2);
+    bf16* ms = f.w + f.wo.ms;
+    STEP("mlp_stream/hbm",
+         launch_mlp_bwd_stream(prm + o.W1, prm + o.g2, prm + o.W2, E, H, ms, s));
+    MlpBwdArgs m{};
+    m.M = N; m.dy = dY; m.xh3 = (const T*)(sv + S.xh3); m.rs3 = (const float*)(sv + S.rs3);
+    m.xh2 = xh2; m.rs2 = (const float*)(sv + S.rs2); m.ws = ms;
+    m.g3 = prm + o.g3; m.g2 = prm + o.g2;
+    m.fb1 = reinterpret_cast<const float*>(f.w + f.wo.fb) + 3 * E;
+    m.dz3 = dz3; m.dz2 = dz2; m.dg = dgb; m.u = ub; m.part = f.lnpart; m.g = g;
+    STEP("mlp_bwd_fused/mfma", launch_mlp_bwd(m, s));
+    const int nt = (int)mlp_bwd_tiles(N);
+    STEP("reduce/hbm", launch_reduce_z(nt, 2 * E, 4 * E, f.lnpart, grads + o.g3, accumulate, s));
+    STEP("reduce/hbm",
+         launch_reduce_z(nt, 2 * E, 4 * E, f.lnpart + 2 * E, grads + o.g2, accumulate, s));
+    CHK(G.run(dz3, E, ub, H, ROWS_COMPACT, o.W2, o.b2));
+    CHK(G.run(dgb, H, xh2, E, ROWS_COMPACT, o.W1, o.b1, nullptr, nullptr, ROWS_COMPACT,
+              prm + o.g2, prm + o.be2));
+  } else {
+    // LN3 (from the native dY), with its gamma/beta column sums
+    int nb = 0;
+    STEP("ln3_bwd/hbm", launch_ln_out_bwd(g, dY, (const T*)(sv + S.xh3),
+                                          (const float*)(sv + S.rs3), prm + o.g3, dz3, f.lnpart,
+                                          &nb, s));
+    // gamma and beta gradients are adjacent in the packed order: one sum over 2E columns
+    STEP("reduce/hbm", launch_reduce_z(nb, 2 * E, 2 * E, f.lnpart, grads + o.g3, accumulate, s));
+    // MLP: dG = (dZ3 W2) * GELU'(G)
+    GemmArgs a = gemm_base(g, N, H, E, EPI_GELU_BWD);
+    a.A = dz3; a.lda = E; a.Bt = f.wt + f.wo.w2; a.out = dgb; a.ldo = H;
+    a.aux = (const T*)(sv + S.g);
+    STEP("mlp_down_dx/mfma", launch_gemm(a, s));
+    CHK(G.run(dz3, E, (const T*)(sv + S.u), H, ROWS_COMPACT, o.W2, o.b2));
+    CHK(G.run(dgb, H, xh2, E, ROWS_COMPACT, o.W1, o.b1, nullptr, nullptr, ROWS_COMPACT,
+              prm + o.g2, prm + o.be2));
+    // dZ2 = LN2'(dZ3 + dG W1)
+    a = gemm_base(g, N, E, H, EPI_LN_BWD);
+    a.A = dgb; a.lda = H; a.Bt = f.wt + f.wo.w1; a.resid = dz3; a.aux = xh2;
+    a.rstd_in = (const float*)(sv + S.rs2); a.gamma = prm + o.g2; a.out = dz2; a.part = f.lnpart;
+    STEP("mlp_up_dx_ln2/mfma", launch_gemm(a, s));
+    STEP("reduce/hbm", launch_reduce_z(tiles, 2 * E, 2 * E, f.lnpart, grads + o.g2, accumulate, s));
+  }
+  GemmArgs a;
   // item attention
   T* doi = (T*)(ws + W.tc);
   a = gemm_base(g, N, E, E, EPI_BIAS);
