@@ -439,13 +439,15 @@ __global__ __launch_bounds__(MB_NW * 64, 3) void k_mlp_bwd(MlpBwdArgs a) {
   };
 
   // LN3': dz3 = rs3 (dY g3 - mean(dY g3) - xh3 mean(dY g3 xh3)); invalid cells contribute 0
+  // (their dY is scaled by 0, without a branch)
+  const float vmask = valid ? 1.f : 0.f;
   bf16x8 dzf[NK];
   {
     float s1 = 0.f, s2 = 0.f;
 #pragma unroll
     for (int eb = 0; eb < NE; ++eb) {
       const int ks = eb >> 1, h = eb & 1;
-      const f32x4 dy = valid ? unpack4(dyl[ks][h].x, dyl[ks][h].y) : zero4();
+      const f32x4 dy = unpack4(dyl[ks][h].x, dyl[ks][h].y) * vmask;
       const f32x4 x3 = unpack4(x3l[ks][h].x, x3l[ks][h].y);
       const f32x4 gy = dy * lds4(&pe[0][eb * 16 + 4 * g]);
       s1 += sum4(gy);
@@ -460,7 +462,7 @@ __global__ __launch_bounds__(MB_NW * 64, 3) void k_mlp_bwd(MlpBwdArgs a) {
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int eb = 2 * ks + h;
-        const f32x4 dy = valid ? unpack4(dyl[ks][h].x, dyl[ks][h].y) : zero4();
+        const f32x4 dy = unpack4(dyl[ks][h].x, dyl[ks][h].y) * vmask;
         const f32x4 x3 = unpack4(x3l[ks][h].x, x3l[ks][h].y);
         const f32x4 dz = rs3 * (dy * lds4(&pe[0][eb * 16 + 4 * g]) - m1 - x3 * m2);
         pk[2 * h] = pack2(dz[0], dz[1]);
@@ -491,9 +493,14 @@ __global__ __launch_bounds__(MB_NW * 64, 3) void k_mlp_bwd(MlpBwdArgs a) {
     return ring + (st & 1) * SEL + lane * 8;
   };
 
-  f32x4 acc[NE];  // dh2^T - dz3, features 16 eb + 4 g .. + 3 of the lane's cell
+  // dh2 = dz3 (as rounded to bf16) + dG W1, features 16 eb + 4 g .. + 3 of the lane's cell:
+  // seeded with dz3 so that the fragments of dz3 are dead after the loop
+  f32x4 acc[NE];
 #pragma unroll
-  for (int eb = 0; eb < NE; ++eb) acc[eb] = zero4();
+  for (int eb = 0; eb < NE; ++eb) {
+    const uint4 dzu = *reinterpret_cast<const uint4*>(&dzf[eb >> 1]);
+    acc[eb] = (eb & 1) ? unpack4(dzu.z, dzu.w) : unpack4(dzu.x, dzu.y);
+  }
 #pragma unroll 1
   for (int hc = 0; hc < NST; ++hc) {
     const bf16* sl = stage_begin(hc);
@@ -532,17 +539,14 @@ __global__ __launch_bounds__(MB_NW * 64, 3) void k_mlp_bwd(MlpBwdArgs a) {
     for (int eb = 0; eb < NE; ++eb) acc[eb] = mfma16(ld8(sl + (4 * NK + eb) * 512), dgf, acc[eb]);
   }
 
-  // LN2': dh2 = acc + dz3 (as rounded to bf16), dz2 = rs2 (g - mean g - xh2 mean(g xh2))
+  // LN2': dz2 = rs2 (g - mean g - xh2 mean(g xh2)), g = dh2 g2
   __syncthreads();  // every wave is done with the ring
   {
     float s1 = 0.f, s2 = 0.f;
 #pragma unroll
     for (int eb = 0; eb < NE; ++eb) {
-      const uint4 dzu = *reinterpret_cast<const uint4*>(&dzf[eb >> 1]);
       const uint4 xu = *reinterpret_cast<const uint4*>(&xf[eb >> 1]);
-      const f32x4 dz = (eb & 1) ? unpack4(dzu.z, dzu.w) : unpack4(dzu.x, dzu.y);
       const f32x4 x2 = (eb & 1) ? unpack4(xu.z, xu.w) : unpack4(xu.x, xu.y);
-      acc[eb] += dz;
       const f32x4 dh = valid ? acc[eb] : zero4();
       const f32x4 gg = acc[eb] * lds4(&pe[1][eb * 16 + 4 * g]);
       s1 += sum4(gg);
