@@ -106,8 +106,10 @@ hipError_t launch_weight_prep(const float* params, int E, int H, bf16* w, bf16* 
 
 // Weight gradient of a product whose input was the folded x-hat (see WFold): with
 // h = gamma o x-hat + beta, dW[n][k] = (sum_z wpart)[n][k] gamma[k] + (sum_z bpart)[n] beta[k];
-// grad (N x K) = (accumulate ? grad : 0) + that, z ascending
-hipError_t launch_reduce_wfold(int Z, int N, int K, const float* wpart, const float* bpart,
+// grad (N x K) = (accumulate ? grad : 0) + that, in the fixed summation order of
+// launch_reduce_z.  The bias sums are left in the first row of bpart (the other rows are
+// scratch afterwards): the bias gradient is then a one-row reduce of bpart.
+hipError_t launch_reduce_wfold(int Z, int N, int K, float* wpart, float* bpart,
                                const float* gamma, const float* beta, float* grad,
                                int accumulate, hipStream_t s);
 // grad[i] = (accumulate ? grad[i] : 0) + sum_z part[z * stride + i], z ascending

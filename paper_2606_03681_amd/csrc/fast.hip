@@ -81,31 +81,6 @@ hipError_t launch_weight_prep(const float* params, int E, int H, bf16* w, bf16* 
   return hipGetLastError();
 }
 
-__global__ void k_reduce_wfold(int Z, int N, int K, const float* __restrict__ wpart,
-                               const float* __restrict__ bpart, const float* __restrict__ gamma,
-                               const float* __restrict__ beta, float* __restrict__ grad,
-                               int accumulate) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t NK = (int64_t)N * K;
-  if (i >= NK) return;
-  const int n = (int)(i / K), k = (int)(i - (int64_t)n * K);
-  float sw = 0.f, sb = 0.f;
-  for (int z = 0; z < Z; ++z) {
-    sw += wpart[(int64_t)z * NK + i];
-    sb += bpart[(int64_t)z * N + n];
-  }
-  grad[i] = (accumulate ? grad[i] : 0.f) + fmaf(sw, gamma[k], sb * beta[k]);
-}
-
-hipError_t launch_reduce_wfold(int Z, int N, int K, const float* wpart, const float* bpart,
-                               const float* gamma, const float* beta, float* grad,
-                               int accumulate, hipStream_t s) {
-  const int64_t NK = (int64_t)N * K;
-  k_reduce_wfold<<<(unsigned)((NK + 255) / 256), 256, 0, s>>>(Z, N, K, wpart, bpart, gamma, beta,
-                                                              grad, accumulate);
-  return hipGetLastError();
-}
-
 __global__ void k_reduce_strided(int Z, int64_t count, int64_t stride,
                                  const float* __restrict__ part, float* __restrict__ grad,
                                  int accumulate) {

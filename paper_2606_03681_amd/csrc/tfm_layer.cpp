@@ -721,13 +721,16 @@ struct FastGrads {
     a.part = f.wpart; a.bpart = f.bpart; a.g = g;
     const int Z = tfm::wgrad_chunks(g.N);
     STEP("wgrad/mfma", tfm::launch_wgrad_mfma(a, s));
-    if (xg)
+    if (xg) {
+      // leaves the bias sums in the first row of bpart
       STEP("reduce/hbm", tfm::launch_reduce_wfold(Z, N, K, f.wpart, f.bpart, xg, xb,
                                                   grads + offW, accumulate, s));
-    else
+      STEP("reduce/hbm", tfm::launch_reduce_z(1, N, N, f.bpart, grads + offb, accumulate, s));
+    } else {
       STEP("reduce/hbm", tfm::launch_reduce_z(Z, (int64_t)N * K, (int64_t)N * K, f.wpart,
                                               grads + offW, accumulate, s));
-    STEP("reduce/hbm", tfm::launch_reduce_z(Z, N, N, f.bpart, grads + offb, accumulate, s));
+      STEP("reduce/hbm", tfm::launch_reduce_z(Z, N, N, f.bpart, grads + offb, accumulate, s));
+    }
     return TFM_OK;
   }
 };

@@ -299,10 +299,14 @@ __global__ __launch_bounds__(512) void k_wgrad(WgradArgs a) {
 // z0 + zg + 8, ... with four independent accumulators, combined in a fixed order (bitwise
 // reproducible).  out may be the first partial row of the block's own range (the first pass of
 // a two-pass sum): every read of the range precedes the barrier, every write follows it, and no
-// other block touches the range.
+// other block touches the range.  With fg given, output i = n K + k receives
+// sum * fg[k] + sb[n] * fb[k] instead of the sum (the folded LayerNorm affine of the product's
+// input; sb holds the bias-gradient sums).
 __global__ __launch_bounds__(256) void k_reduce_z(int Z, int zc, int64_t count, int64_t stride,
                                                   const float* part, float* out,
-                                                  int64_t out_ystride, int accumulate) {
+                                                  int64_t out_ystride, int accumulate,
+                                                  const float* fg, const float* fb,
+                                                  const float* sb, int fK) {
   __shared__ float4 red[8][32];
   const int o = threadIdx.x & 31, zg = threadIdx.x >> 5;
   const int64_t i4 = ((int64_t)blockIdx.x * 32 + o) * 4;
@@ -347,7 +351,15 @@ __global__ __launch_bounds__(256) void k_reduce_z(int Z, int zc, int64_t count, 
     for (int k = 1; k < 8; ++k) {
       t.x += red[k][o].x; t.y += red[k][o].y; t.z += red[k][o].z; t.w += red[k][o].w;
     }
-    const float tv[4] = {t.x, t.y, t.z, t.w};
+    float tv[4] = {t.x, t.y, t.z, t.w};
+    if (fg) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int64_t i = i4 + k;
+        const int n = (int)(i / fK), kk = (int)(i - (int64_t)n * fK);
+        if (i < count) tv[k] = fmaf(tv[k], fg[kk], sb[n] * fb[kk]);
+      }
+    }
 #pragma unroll
     for (int k = 0; k < 4; ++k)
       if (i4 + k < count) out[i4 + k] = (accumulate ? out[i4 + k] : 0.f) + tv[k];
@@ -415,8 +427,9 @@ hipError_t launch_wgrad_mfma(const WgradArgs& a, hipStream_t s) {
   }
 }
 
-hipError_t launch_reduce_z(int Z, int64_t count, int64_t stride, float* part, float* out,
-                           int accumulate, hipStream_t s) {
+static hipError_t reduce_z(int Z, int64_t count, int64_t stride, float* part, float* out,
+                           int accumulate, const float* fg, const float* fb, const float* sb,
+                           int fK, hipStream_t s) {
   if (Z <= 0 || count <= 0) return hipSuccess;
   const unsigned bx = (unsigned)((count + 127) / 128);
   // Few output blocks and many partials: first fold groups of ZC partials into the first row
@@ -425,12 +438,31 @@ hipError_t launch_reduce_z(int Z, int64_t count, int64_t stride, float* part, fl
   if (bx < 512 && Z > 2 * ZC) {
     const unsigned groups = (unsigned)((Z + ZC - 1) / ZC);
     k_reduce_z<<<dim3(bx, groups), 256, 0, s>>>(Z, ZC, count, stride, part, part,
-                                                 (int64_t)ZC * stride, 0);
+                                                 (int64_t)ZC * stride, 0, nullptr, nullptr,
+                                                 nullptr, 1);
     Z = (int)groups;
     stride *= ZC;
   }
-  k_reduce_z<<<dim3(bx, 1), 256, 0, s>>>(Z, Z, count, stride, part, out, 0, accumulate);
+  k_reduce_z<<<dim3(bx, 1), 256, 0, s>>>(Z, Z, count, stride, part, out, 0, accumulate, fg, fb,
+                                         sb, fK);
   return hipGetLastError();
+}
+
+hipError_t launch_reduce_z(int Z, int64_t count, int64_t stride, float* part, float* out,
+                           int accumulate, hipStream_t s) {
+  return reduce_z(Z, count, stride, part, out, accumulate, nullptr, nullptr, nullptr, 1, s);
+}
+
+hipError_t launch_reduce_wfold(int Z, int N, int K, float* wpart, float* bpart,
+                               const float* gamma, const float* beta, float* grad,
+                               int accumulate, hipStream_t s) {
+  if (Z <= 0 || N <= 0 || K <= 0) return hipSuccess;
+  // the bias sums first, into the first partial row of bpart (in place), which the folded
+  // weight sums then read
+  hipError_t e = reduce_z(Z, N, N, bpart, bpart, 0, nullptr, nullptr, nullptr, 1, s);
+  if (e != hipSuccess) return e;
+  return reduce_z(Z, (int64_t)N * K, (int64_t)N * K, wpart, grad, accumulate, gamma, beta, bpart,
+                  K, s);
 }
 
 }  // namespace tfm
