@@ -704,6 +704,14 @@ __global__ __launch_bounds__(256, (gemm_half_tile<EPI, BN>() ? 3 : 2)) void k_ge
 // (EPI_ITEM_QKV).  The products and the epilogue arithmetic are those of k_gemm (same MFMA
 // order), so both kernels give identical results.  (The GELU epilogues stay on k_gemm: their
 // VALU work needs the overlap of several workgroups per CU.)
+// 16-byte store marked non-temporal (streamed past the caches' retention), for outputs that
+// no later access of the same kernel reads
+__device__ __forceinline__ void stu4_nt(bf16* p, uint4 v) {
+  typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+  const u32x4_t x = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(x, reinterpret_cast<u32x4_t*>(p));
+}
+
 template <int BN>
 struct WrShape {
   static constexpr int WN = 4;                  // column waves
@@ -858,7 +866,12 @@ __global__ __launch_bounds__(512, 1) void k_gemm_wr(GemmArgs a) {
         const int head = (pc0 + cc) / g.d, jd = pc0 + cc - head * g.d;
         o = off + (int64_t)head * g.R * g.d + jd;
       }
-      stu4(dst + o, ldu4(&tile[row * TS + cc]));
+      // saved tensors read only by later kernels (the Q|K|V projections) stream past the caches;
+      // the single-tile products' outputs, which the next kernel reads, do not
+      if (EPI == EPI_ITEM_QKV || NY > 1)
+        stu4_nt(dst + o, ldu4(&tile[row * TS + cc]));
+      else
+        stu4(dst + o, ldu4(&tile[row * TS + cc]));
     }
   }
 }
