@@ -102,6 +102,10 @@ TEST_CONFIGS = {
                                n_train=(1, 200), C=20, active=(0, 20), mask="random", E=64,
                                heads=2, H=192, layers=2, cells="normal", weights="xavier_bias",
                                block="pre"),
+    # fewer active cells (2 x 9 x 3 = 54) than one tile of the fused MLP kernels (128 cells
+    # forward, 192 backward): every workgroup of those kernels has clamped, masked cells
+    "tiny-mlp-bf16": dict(name="tiny-mlp-bf16", dtype="bf16", B=2, R=9, n_train=5, C=2, E=192,
+                          heads=6, H=384, layers=2, cells="normal", weights="xavier_bias"),
     # train prefixes on both sides of the one-kernel item-attention backward's limit (768
     # rows): its columns and those of the two-kernel form run in separate launches
     "mixed-prefix-bf16": dict(name="mixed-prefix-bf16", dtype="bf16", B=5, R=1000,

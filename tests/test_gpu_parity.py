@@ -39,7 +39,7 @@ def _gpu():
 @pytest.mark.parametrize("name", [0, "ragged-small-f32", "ragged-small-bf16", "d16-bf16",
                                   "d64-bf16", "d64-f32", "prenorm-small-bf16",
                                   "prenorm-d64-bf16", "wide-d32-bf16", "wide-d64-bf16",
-                                  "wide-prenorm-d64-bf16", "mixed-prefix-bf16"])
+                                  "wide-prenorm-d64-bf16", "mixed-prefix-bf16", "tiny-mlp-bf16"])
 def test_parity_full(name):
     w = wl.make_workload(name)
     _say(f"[parity] {w.cfg['name']} seed={w.seed}")
