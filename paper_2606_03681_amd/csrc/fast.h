@@ -112,9 +112,6 @@ hipError_t launch_weight_prep(const float* params, int E, int H, bf16* w, bf16* 
 hipError_t launch_reduce_wfold(int Z, int N, int K, float* wpart, float* bpart,
                                const float* gamma, const float* beta, float* grad,
                                int accumulate, hipStream_t s);
-// grad[i] = (accumulate ? grad[i] : 0) + sum_z part[z * stride + i], z ascending
-hipError_t launch_reduce_strided(int Z, int64_t count, int64_t stride, const float* part,
-                                 float* grad, int accumulate, hipStream_t s);
 
 // Writes 0 to every element of the native tensor that lies in an inactive cell.
 hipError_t launch_zero_inactive(const Geo& g, bf16* native, hipStream_t s);

@@ -52,20 +52,23 @@ __global__ void k_weight_prep(const float* __restrict__ p, int E, int H, WOff wo
   }
 }
 
-// Folded biases, one thread per output: bqkv_i[n] + sum_k Wqkv_i[n][k] be1[k] for n < 3E, then
-// b1[m] + sum_k W1[m][k] be2[k]; float32, k ascending.
+// Folded biases, one wave per output: bqkv_i[n] + sum_k Wqkv_i[n][k] be1[k] for n < 3E, then
+// b1[m] + sum_k W1[m][k] be2[k]; float32, lane l summing k = l, l + 64, ... (a coalesced read of
+// the weight row), then the lanes' sums added in a fixed butterfly.
 __global__ void k_fold_bias(const float* __restrict__ p, int E, int H, WFold fold,
                             float* __restrict__ fb) {
-  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+  const int n = blockIdx.x * 4 + wave_id();
   if (n >= 3 * E + H) return;
+  const int lane = threadIdx.x & 63;
   const int64_t E2 = (int64_t)E * E;
   const bool q = n < 3 * E;
   const int m = q ? n : n - 3 * E;
   const float* row = p + (q ? 4 * E2 + 4 * E : 8 * E2 + 8 * E) + (int64_t)m * E;
   const float* be = q ? fold.be1 : fold.be2;
-  float acc = (q ? fold.bqkv_i : fold.b1)[m];
-  for (int k = 0; k < E; ++k) acc = fmaf(row[k], be[k], acc);
-  fb[n] = acc;
+  float acc = 0.f;
+  for (int k = lane; k < E; k += 64) acc = fmaf(row[k], be[k], acc);
+  acc = wave_reduce_sum(acc);
+  if (lane == 0) fb[n] = (q ? fold.bqkv_i : fold.b1)[m] + acc;
 }
 
 hipError_t launch_weight_prep(const float* params, int E, int H, bf16* w, bf16* wt,
@@ -75,26 +78,9 @@ hipError_t launch_weight_prep(const float* params, int E, int H, bf16* w, bf16* 
   k_weight_prep<<<grid, 256, 0, s>>>(params, E, H, wo, w, wt, fold ? *fold : WFold{}, fold != nullptr);
   if (fold) {
     const int n = 3 * E + H;
-    k_fold_bias<<<(n + 255) / 256, 256, 0, s>>>(params, E, H, *fold,
+    k_fold_bias<<<(n + 3) / 4, 256, 0, s>>>(params, E, H, *fold,
                                                 reinterpret_cast<float*>(w + wo.fb));
   }
-  return hipGetLastError();
-}
-
-__global__ void k_reduce_strided(int Z, int64_t count, int64_t stride,
-                                 const float* __restrict__ part, float* __restrict__ grad,
-                                 int accumulate) {
-  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= count) return;
-  float s = 0.f;
-  for (int z = 0; z < Z; ++z) s += part[(int64_t)z * stride + i];
-  grad[i] = (accumulate ? grad[i] : 0.f) + s;
-}
-
-hipError_t launch_reduce_strided(int Z, int64_t count, int64_t stride, const float* part,
-                                 float* grad, int accumulate, hipStream_t s) {
-  k_reduce_strided<<<(unsigned)((count + 255) / 256), 256, 0, s>>>(Z, count, stride, part, grad,
-                                                                   accumulate);
   return hipGetLastError();
 }
 
