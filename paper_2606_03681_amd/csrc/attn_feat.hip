@@ -109,7 +109,7 @@ __device__ __forceinline__ bf16x8 get_cols(const bf16* tile, int ks, int db, int
 
 // ================================================================================ forward
 template <int D, int SM>
-__global__ __launch_bounds__(256) void k_feat_attn_fwd(Geo g, const bf16* __restrict__ qkv,
+__global__ __launch_bounds__(256, D <= 32 ? 4 : 1) void k_feat_attn_fwd(Geo g, const bf16* __restrict__ qkv,
                                                        bf16* __restrict__ o,
                                                        float* __restrict__ lse) {
   constexpr int DB = D / 16;
