@@ -369,7 +369,7 @@ __global__ __launch_bounds__(MB_NW * 64, 3) void k_mlp_bwd(MlpBwdArgs a) {
   constexpr int NST = H / 32;
   constexpr int DPT = FPS * 64 / NT;
   static_assert(H % 32 == 0 && DPT >= 1 && FPS * 64 % NT == 0, "shape");
-  __shared__ __attribute__((aligned(16))) bf16 ring[2 * SEL];
+  __shared__ __attribute__((aligned(16))) bf16 ring[3 * SEL];  // three stages: two in flight
   __shared__ __attribute__((aligned(16))) float pe[2][E];   // g3, g2
   __shared__ __attribute__((aligned(16))) float pfb[H];     // b1'
 
@@ -382,7 +382,7 @@ __global__ __launch_bounds__(MB_NW * 64, 3) void k_mlp_bwd(MlpBwdArgs a) {
 
   auto issue = [&](int st) {
     const bf16* src = a.ws + (int64_t)st * SEL;
-    bf16* dst = ring + (st & 1) * SEL;
+    bf16* dst = ring + (st % 3) * SEL;
 #pragma unroll
     for (int i = 0; i < DPT; ++i) {
       const int piece = i * NT + w * 64;
@@ -390,6 +390,7 @@ __global__ __launch_bounds__(MB_NW * 64, 3) void k_mlp_bwd(MlpBwdArgs a) {
     }
   };
   issue(0);
+  issue(1);
 
   // the cell's inputs, features {32 ks + 4 g .. + 3} (h = 0) and {32 ks + 16 + 4 g .. + 3}
   uint2 dyl[NK][2], x3l[NK][2];
@@ -415,9 +416,9 @@ __global__ __launch_bounds__(MB_NW * 64, 3) void k_mlp_bwd(MlpBwdArgs a) {
 
   // column sums over the wave's 16 cells into red[w][which]: every lane of a 16-lane row ends
   // with the same sums and stores them (same address, same value)
-  // [NW][2][E] per-wave sums: LN3's in the ring's second slot (free until the first stage
+  // [NW][2][E] per-wave sums: LN3's in the ring's third slot (free until the first stage
   // begins), LN2's in its first slot (after the last stage)
-  float* red = reinterpret_cast<float*>(ring + SEL);
+  float* red = reinterpret_cast<float*>(ring + 2 * SEL);
   float* red2 = reinterpret_cast<float*>(ring);
   static_assert(NW * 2 * E * 4 <= SEL * 2, "column sums fit a ring slot");
   auto colsum = [&](int which, int eb, f32x4 v) {
@@ -487,10 +488,17 @@ __global__ __launch_bounds__(MB_NW * 64, 3) void k_mlp_bwd(MlpBwdArgs a) {
     xf[ks] = *reinterpret_cast<bf16x8*>(&u);
   }
 
+  // Stage st waits for its own pieces only: loads complete in issue order, so with the DPT
+  // pieces of stage st + 1 issued after them, at most DPT outstanding vector-memory operations
+  // means stage st has landed (stores in flight do not change that).  The barrier publishes
+  // every wave's pieces and frees the slot of stage st - 1, which stage st + 2 then refills.
   auto stage_begin = [&](int st) -> const bf16* {
-    asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
-    if (st + 1 < NST) issue(st + 1);
-    return ring + (st & 1) * SEL + lane * 8;
+    if (st + 1 < NST)
+      asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(DPT) : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory");
+    if (st + 2 < NST) issue(st + 2);
+    return ring + (st % 3) * SEL + lane * 8;
   };
 
   // dh2 = dz3 (as rounded to bf16) + dG W1, features 16 eb + 4 g .. + 3 of the lane's cell:
