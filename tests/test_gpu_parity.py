@@ -90,6 +90,31 @@ def test_bitwise_deterministic():
         assert np.array_equal(x, y)
 
 
+@pytest.mark.parametrize("name", ["tiny-mlp-bf16", "ragged-small-f32", "prenorm-small-bf16",
+                                  "mixed-prefix-bf16"])
+def test_gradient_accumulation_is_exact(name):
+    """A second backward with accumulate != 0 adds its gradients to the first call's: with a
+    bitwise-reproducible backward the result is exactly twice the one-call gradients, on every
+    reduction path (split-z sums, the folded LayerNorm affines, the LayerNorm column sums);
+    dX is written, not accumulated."""
+    import torch
+    from paper_2606_03681_amd import tfm
+    from paper_2606_03681_amd.stack import Stack, to_device
+    w = wl.make_workload(name)
+    dims = tfm.make_dims(dtype=w.dtype, block=w.block,
+                         **{k: v for k, v in w.dims.items() if k != "dtype"})
+    st = Stack(dims, w.n_train, w.cell_mask, w.params)
+    st.forward(to_device(w.X, w.dtype))
+    dY = to_device(w.dY, w.dtype)
+    dx1 = st.backward(dY).clone()
+    once = [g.clone() for g in st.grads]
+    dx2 = st.backward(dY, accumulate=True)
+    torch.cuda.synchronize()
+    assert torch.equal(dx1, dx2)
+    for g1, g2 in zip(once, st.grads):
+        assert torch.equal(g2, 2 * g1)
+
+
 def test_test_rows_do_not_change_train_outputs():
     """Changing every test row leaves the train rows' outputs bit-identical on the GPU."""
     w = wl.make_workload(1, datasets=[0, 1])
