@@ -4,9 +4,9 @@
 // first n_train rows (the train prefix).  The prefix is a loop bound over key tiles — scores
 // are never materialised and the only masking is inside the last, partial key tile.
 //
-// One workgroup = 4 waves = 128 queries of one problem; each wave owns 32 queries (two 16-query
-// MFMA blocks).  Key tiles of 64 keys are staged in LDS (K and V as [key][d]; V is read back
-// transposed) with double buffering and shared by the 4 waves.  Per tile a wave computes S^T = K Q^T
+// One workgroup = 4 waves of one problem; each wave owns 64 queries (four 16-query MFMA blocks)
+// at d <= 32 and 32 at d = 64.  Key tiles of 64 keys are staged in LDS (K and V as [key][d]; V
+// is read back transposed) with double buffering and shared by the 4 waves.  Per tile a wave computes S^T = K Q^T
 // (keys x queries, so that a lane holds 4 keys of one query), the online softmax in the exp2
 // domain with the scale folded into one FMA, and O^T += V^T P^T where the D tile of S^T is
 // reused directly as the B operand (the k positions of V^T are permuted to match).
@@ -25,15 +25,21 @@ namespace tfm {
 namespace {
 
 constexpr int KT = 64;   // keys per tile
-constexpr int QWV = 32;  // queries per wave
-constexpr int QWG = 128; // queries per workgroup
+// 16-query blocks per wave: four at d <= 32 (every K and V fragment read from LDS serves 64
+// queries; 163 VGPRs, three waves per SIMD), two at d = 64 (its fragments are twice as wide)
+template <int D>
+constexpr int qblocks() { return D == 64 ? 2 : 4; }
+template <int D>
+constexpr int qwave() { return 16 * qblocks<D>(); }   // queries per wave
+template <int D>
+constexpr int qgroup() { return 4 * qwave<D>(); }     // queries per workgroup (4 waves)
 
 __device__ __forceinline__ uint32_t pk_bf16(float a, float b) { return pack2(a, b); }
 
 }  // namespace
 
 template <int D>
-__global__ __launch_bounds__(256, D == 64 ? 3 : 5) void k_item_attn_fwd(Geo g, const bf16* __restrict__ q,
+__global__ __launch_bounds__(256, 3) void k_item_attn_fwd(Geo g, const bf16* __restrict__ q,
                                                        const bf16* __restrict__ k,
                                                        const bf16* __restrict__ v,
                                                        bf16* __restrict__ o,
@@ -46,6 +52,7 @@ __global__ __launch_bounds__(256, D == 64 ? 3 : 5) void k_item_attn_fwd(Geo g, c
   constexpr int KS = SW ? 32 : (D == 64 ? tr_stride<D>() : D + 8);
   constexpr int VS = SW ? 32 : tr_stride<D>();     // LDS row stride of V
   constexpr int DB = D / 16;  // 16-wide dim blocks
+  constexpr int QB = qblocks<D>();
   constexpr int CPR = D / 8;  // 16-byte chunks per key row
   __shared__ __attribute__((aligned(16))) bf16 Ks[2][KT * KS];
   __shared__ __attribute__((aligned(16))) bf16 Vs[2][KT * VS];
@@ -64,7 +71,7 @@ __global__ __launch_bounds__(256, D == 64 ? 3 : 5) void k_item_attn_fwd(Geo g, c
 
   const int tid = threadIdx.x, lane = tid & 63, wave = wave_id();
   const int c = lane & 15, lg = lane >> 4;
-  const int qw0 = qt * QWG + wave * QWV;
+  const int qw0 = qt * qgroup<D>() + wave * qwave<D>();
 
   // Buffer resources of the problem: loads past the end (queries past R, keys past n) return 0
   // without an exec-masked branch, so the compiler's wait counts stay exact and the prefetch of
@@ -74,9 +81,9 @@ __global__ __launch_bounds__(256, D == 64 ? 3 : 5) void k_item_attn_fwd(Geo g, c
   const rsrc_t rV = make_rsrc(Vp, (uint32_t)n * D * 2);
 
   // Q^T fragments (B operand): lane holds query qw0 + qb*16 + c
-  typename HF<D>::frag qf[2];
+  typename HF<D>::frag qf[QB];
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) qf[qb] = HF<D>::buf(rQ, (uint32_t)(qw0 + qb * 16 + c) * D * 2, lg);
+  for (int qb = 0; qb < QB; ++qb) qf[qb] = HF<D>::buf(rQ, (uint32_t)(qw0 + qb * 16 + c) * D * 2, lg);
 
   // staging: item it = tid + 256 i -> (key, 16-byte chunk of its dims): key it / CPR, chunk
   // it % CPR; at d = 32 key (it % 16) + 16 (it / 64), chunk (it / 16) % 4, so that each store
@@ -124,15 +131,17 @@ __global__ __launch_bounds__(256, D == 64 ? 3 : 5) void k_item_attn_fwd(Geo g, c
   // S^T - ref and p = exp2(acc) needs no further arithmetic.  The reference is set by the first
   // tile and raised only when a tile's maximum exceeds it by more than 8, which keeps every p
   // below 2^8 and makes the shift-and-rescale rare.
-  float ref[2] = {-INFINITY, -INFINITY};
+  float ref[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) ref[qb] = -INFINITY;
   constexpr float slack = 8.0f;
   // O^T accumulators: DB blocks of V^T rows plus one block whose first row is all ones, so
   // that row accumulates the softmax denominator with the same rescaling as O.
-  f32x4 oacc[DB + 1][2];
+  f32x4 oacc[DB + 1][QB];
 #pragma unroll
   for (int db = 0; db <= DB; ++db)
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) oacc[db][qb] = zero4();
+    for (int qb = 0; qb < QB; ++qb) oacc[db][qb] = zero4();
   bf16x8 ones;
   {
     const uint32_t w = c == 0 ? 0x3f803f80u : 0u;  // bf16 1.0 pairs in row 0 only
@@ -142,10 +151,10 @@ __global__ __launch_bounds__(256, D == 64 ? 3 : 5) void k_item_attn_fwd(Geo g, c
 
   auto tile = [&](const int cur, const int t0, const bool tail) {
     // S^T - ref for 4 key blocks x 2 query blocks
-    f32x4 sc[4][2];
-    f32x4 init[2];
+    f32x4 sc[4][QB];
+    f32x4 init[QB];
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
       const float r0 = ref[qb] == -INFINITY ? 0.f : -ref[qb];
       init[qb][0] = init[qb][1] = init[qb][2] = init[qb][3] = r0;
     }
@@ -157,7 +166,7 @@ __global__ __launch_bounds__(256, D == 64 ? 3 : 5) void k_item_attn_fwd(Geo g, c
       else
         kf = HF<D>::lds(&Ks[cur][(kb * 16 + c) * KS], lg);
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) sc[kb][qb] = HF<D>::mma(kf, qf[qb], init[qb]);
+      for (int qb = 0; qb < QB; ++qb) sc[kb][qb] = HF<D>::mma(kf, qf[qb], init[qb]);
     }
     if (tail) {
 #pragma unroll
@@ -165,13 +174,13 @@ __global__ __launch_bounds__(256, D == 64 ? 3 : 5) void k_item_attn_fwd(Geo g, c
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           if (t0 + kb * 16 + lg * 4 + i >= n) {
-            sc[kb][0][i] = -INFINITY;
-            sc[kb][1][i] = -INFINITY;
+#pragma unroll
+            for (int qb = 0; qb < QB; ++qb) sc[kb][qb][i] = -INFINITY;
           }
     }
-    bf16x8 pf[2][2];
+    bf16x8 pf[QB][2];
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
       float mx = fmaxf(fmaxf(sc[0][qb][0], sc[0][qb][1]), fmaxf(sc[0][qb][2], sc[0][qb][3]));
 #pragma unroll
       for (int kb = 1; kb < 4; ++kb)
@@ -208,10 +217,10 @@ __global__ __launch_bounds__(256, D == 64 ? 3 : 5) void k_item_attn_fwd(Geo g, c
         const bf16x8 vf = SW ? tr8_row64(&Vs[cur][ks * 32 * 32], voff[db])
                              : ld_tr8(&Vs[cur][ks * 32 * VS], VS, db * 16, lane);
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) oacc[db][qb] = mfma16(vf, pf[qb][ks], oacc[db][qb]);
+        for (int qb = 0; qb < QB; ++qb) oacc[db][qb] = mfma16(vf, pf[qb][ks], oacc[db][qb]);
       }
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) oacc[DB][qb] = mfma16(ones, pf[qb][ks], oacc[DB][qb]);
+      for (int qb = 0; qb < QB; ++qb) oacc[DB][qb] = mfma16(ones, pf[qb][ks], oacc[DB][qb]);
     }
   };
 
@@ -220,8 +229,8 @@ __global__ __launch_bounds__(256, D == 64 ? 3 : 5) void k_item_attn_fwd(Geo g, c
   gload(0);
   sstore(0);
   // the Q fragments have arrived before the loop (no load is pending at its head)
-  hf_touch<D>(qf[0]);
-  hf_touch<D>(qf[1]);
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) hf_touch<D>(qf[qb]);
   lds_barrier();
   for (int it = 0; it < NF; ++it) {
     const int cur = it & 1;
@@ -234,7 +243,7 @@ __global__ __launch_bounds__(256, D == 64 ? 3 : 5) void k_item_attn_fwd(Geo g, c
 
   // normalise and write O (cell-major) and the natural-log LSE = ln 2 * (ref + log2 l)
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
+  for (int qb = 0; qb < QB; ++qb) {
     const float lt = __shfl(oacc[DB][qb][0], c, 64);  // row 0 of the ones block, lane (0, c)
     const int qq = qw0 + qb * 16 + c;
     if (qq >= R) continue;
@@ -254,17 +263,20 @@ __global__ __launch_bounds__(256, D == 64 ? 3 : 5) void k_item_attn_fwd(Geo g, c
 hipError_t launch_item_attn_fwd(const Geo& g, const bf16* q, const bf16* k, const bf16* v,
                                 bf16* o, float* lse, hipStream_t s, int kR) {
   if (kR <= 0) kR = g.R;
-  const int QT = (g.R + QWG - 1) / QWG;
   const int64_t P = (int64_t)g.NC * g.heads;
-  const int64_t grid = (P + 7) / 8 * 8 * QT;
-  if (g.d == 16)
-    k_item_attn_fwd<16><<<(unsigned)grid, 256, 0, s>>>(g, q, k, v, o, lse, QT, kR);
-  else if (g.d == 32)
-    k_item_attn_fwd<32><<<(unsigned)grid, 256, 0, s>>>(g, q, k, v, o, lse, QT, kR);
-  else if (g.d == 64)
-    k_item_attn_fwd<64><<<(unsigned)grid, 256, 0, s>>>(g, q, k, v, o, lse, QT, kR);
-  else
+  auto grid = [&](int QT) { return (unsigned)((P + 7) / 8 * 8 * QT); };
+  if (g.d == 16) {
+    const int QT = (g.R + qgroup<16>() - 1) / qgroup<16>();
+    k_item_attn_fwd<16><<<grid(QT), 256, 0, s>>>(g, q, k, v, o, lse, QT, kR);
+  } else if (g.d == 32) {
+    const int QT = (g.R + qgroup<32>() - 1) / qgroup<32>();
+    k_item_attn_fwd<32><<<grid(QT), 256, 0, s>>>(g, q, k, v, o, lse, QT, kR);
+  } else if (g.d == 64) {
+    const int QT = (g.R + qgroup<64>() - 1) / qgroup<64>();
+    k_item_attn_fwd<64><<<grid(QT), 256, 0, s>>>(g, q, k, v, o, lse, QT, kR);
+  } else {
     return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
