@@ -180,13 +180,13 @@ struct MlpFwdArgs {
   const bf16* ws;       // weight stream
   const float *bo, *g1, *be1, *g2, *be2, *b2, *g3, *be3;  // [E] each
   const float* fb1;     // [H] folded up-projection bias b1 + W1 be2
-  bf16* xh2;            // [M][E] x-hat of LN2
-  float* rs2;           // [M]
+  bf16* xh2;            // [M][E] x-hat of LN2 (null: not stored)
+  float* rs2;           // [M] (null: not stored)
   bf16* gout;           // [M][H] pre-activation (optional)
   bf16* uout;           // [M][H] GELU of it (optional)
   bf16* y;              // native [B][R][S][E]
-  bf16* xh3;            // [M][E] x-hat of LN3 (optional)
-  float* rs3;           // [M]
+  bf16* xh3;            // [M][E] x-hat of LN3 (null: not stored)
+  float* rs3;           // [M] (null: not stored)
   Geo g;
 };
 bool mlp_fused_ok(int E, int H);

@@ -215,13 +215,13 @@ __global__ __launch_bounds__(MLP_NW * 64, 2) void k_mlp_fwd(MlpFwdArgs a) {
       uint4 u = make_uint4(pack2(lo[0], lo[1]), pack2(lo[2], lo[3]), pack2(hi[0], hi[1]),
                            pack2(hi[2], hi[3]));
       xf[cb][ks] = *reinterpret_cast<bf16x8*>(&u);
-      if (valid[cb]) {
+      if (valid[cb] && a.xh2) {
         bf16* row = a.xh2 + cell[cb] * E + ks * 32 + 4 * g;
         *reinterpret_cast<uint2*>(row) = make_uint2(u.x, u.y);
         *reinterpret_cast<uint2*>(row + 16) = make_uint2(u.z, u.w);
       }
     }
-    if (valid[cb] && g == 0) a.rs2[cell[cb]] = rs;
+    if (valid[cb] && g == 0 && a.rs2) a.rs2[cell[cb]] = rs;
 #pragma unroll
     for (int eb = 0; eb < NE; ++eb) acc[cb][eb] = zero4();  // now the down-projection sums
   }
@@ -293,7 +293,7 @@ __global__ __launch_bounds__(MLP_NW * 64, 2) void k_mlp_fwd(MlpFwdArgs a) {
     }
     const float rs = 1.0f / sqrtf(rows4_sum(v) * (1.0f / E) + 1e-5f);
     if (!valid[cb]) continue;
-    if (g == 0) a.rs3[cell[cb]] = rs;
+    if (g == 0 && a.rs3) a.rs3[cell[cb]] = rs;
     bf16* yrow = a.y + native_cell(a.g, cell[cb]) * E;
 #pragma unroll
     for (int eb = 0; eb < NE; ++eb) {

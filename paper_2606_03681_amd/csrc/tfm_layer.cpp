@@ -606,6 +606,7 @@ struct FwdBufs {
   float *lsef = nullptr, *lsei = nullptr, *rs1 = nullptr, *rs2 = nullptr, *rs3 = nullptr;
   bool query = false;  // ki / vi hold the keys and values of a context call: project Q only
   int kR = 0;          // rows per (column, head) of ki / vi; 0: R
+  bool save = true;    // the forward keeps what its backward reads (false: forward-only calls)
 };
 
 FwdBufs bufs_from_saved(char* sv, const SavedLayout& S) {
@@ -673,8 +674,9 @@ int fwd_fast(const Dims& d, const tfm::Geo& g, const tfm::bf16* X, const float* 
     m.bo = prm + o.bo_i; m.g1 = prm + o.g1; m.be1 = prm + o.be1; m.g2 = prm + o.g2;
     m.be2 = prm + o.be2; m.b2 = prm + o.b2; m.g3 = prm + o.g3; m.be3 = prm + o.be3;
     m.fb1 = fb + 3 * E;
-    m.xh2 = b.h2; m.rs2 = b.rs2;  // G and U are recomputed by the fused backward
-    m.y = Y; m.xh3 = b.xh3; m.rs3 = b.rs3; m.g = g;
+    // saved for the backward only (G and U are recomputed by the fused backward)
+    m.xh2 = b.save ? b.h2 : nullptr; m.rs2 = b.save ? b.rs2 : nullptr;
+    m.y = Y; m.xh3 = b.save ? b.xh3 : nullptr; m.rs3 = b.save ? b.rs3 : nullptr; m.g = g;
     STEP("mlp_fused/mfma", launch_mlp_fwd(m, s));
     STEP("zero_inactive/hbm", launch_zero_inactive(g, Y, s));
     return TFM_OK;
@@ -1064,6 +1066,7 @@ FwdBufs infer_bufs(const Dims& d, char* ws, const InferLayout& L, tfm::bf16* kc,
   }
   b.query = query;
   b.kR = kR;
+  b.save = false;
   return b;
 }
 
